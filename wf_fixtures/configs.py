@@ -1,0 +1,71 @@
+"""Model shapes used by the tests and the benchmark.
+
+``LARGE_V3`` is the target of the paper's experiments (Section 4: Whisper
+large-v3; 32 decoder blocks of width 1280 with 20 heads of 64, a 5120-wide
+GELU MLP and a 51866-token vocabulary).  ``TINY`` is a 4-block, width-384
+Whisper-shaped decoder with fp32 weights used as the correctness workload.
+``MICRO`` and ``VOCAB64`` are small shapes for brute-force and statistical
+tests on the CPU (the 64-token vocabulary is the one the sampling
+equivalence check runs on).
+
+The drafter always has two blocks of the target's width (Section 3.2,
+"a two-layer drafter") and a block of K = 8 mask positions (Eq. 2).
+"""
+from dataclasses import dataclass, field, replace
+
+
+@dataclass(frozen=True)
+class ModelConfig:
+    name: str
+    n_layer: int          # target decoder blocks
+    d_model: int          # residual width
+    n_head: int           # attention heads (head width is d_model // n_head)
+    d_ff: int             # MLP hidden width
+    n_vocab: int          # vocabulary size (tied embedding / output head)
+    taps: tuple           # zero-based target blocks whose outputs feed the history memory
+    dtype: str            # "f32" or "bf16": storage type of weights, memory and caches
+    n_ctx: int = 448      # learned text positions
+    n_frames: int = 1500  # acoustic memory length (30 s window)
+    n_draft_layer: int = 2
+    block_k: int = 8      # mask positions per draft block
+    eos_id: int = 50257   # end-of-transcript token id
+
+    @property
+    def head_dim(self) -> int:
+        return self.d_model // self.n_head
+
+    @property
+    def n_tap(self) -> int:
+        return len(self.taps)
+
+    def with_(self, **kw) -> "ModelConfig":
+        return replace(self, **kw)
+
+
+# Whisper large-v3 decoder shapes; drafter taps from Appendix A.2.
+LARGE_V3 = ModelConfig(name="large-v3", n_layer=32, d_model=1280, n_head=20, d_ff=5120,
+                       n_vocab=51866, taps=(1, 8, 15, 22, 29), dtype="bf16")
+
+# Whisper-tiny-shaped decoder with fp32 weights: every block is tapped.
+TINY = ModelConfig(name="tiny", n_layer=4, d_model=384, n_head=6, d_ff=1536,
+                   n_vocab=51865, taps=(0, 1, 2, 3), dtype="f32")
+
+# Small shapes for brute-force CPU tests.  Head width stays 64.
+MICRO = ModelConfig(name="micro", n_layer=2, d_model=128, n_head=2, d_ff=256,
+                    n_vocab=512, taps=(0, 1), dtype="f32", n_ctx=64, n_frames=48,
+                    eos_id=7)
+
+# The 64-token vocabulary variant for the sampling distribution check.
+VOCAB64 = ModelConfig(name="vocab64", n_layer=2, d_model=128, n_head=2, d_ff=256,
+                      n_vocab=64, taps=(0, 1), dtype="f32", n_ctx=64, n_frames=48,
+                      eos_id=-1)
+
+_BY_NAME = {c.name: c for c in (LARGE_V3, TINY, MICRO, VOCAB64)}
+
+
+def config_by_name(name: str) -> ModelConfig:
+    return _BY_NAME[name]
+
+
+# Philox stream purposes (counter word 0 carries purpose << 32 | slot).
+PURPOSE = {"PREFILL": 1, "PLAIN": 2, "DRAFT": 3, "ACC": 4, "RES": 5, "BON": 6}
