@@ -1,0 +1,8 @@
+"""Whisper-Flash draft-and-verify step on MI355X (gfx950).
+
+The step runs in the HIP kernels of ``libwf.so`` behind the C ABI of
+``include/wf.h``; ``binding`` marshals arguments from Python.
+"""
+from .binding import WhisperFlash, WfError, load_library, make_config, to_device_storage, EXPORTS, LIB_PATH
+
+__all__ = ["WhisperFlash", "WfError", "load_library", "make_config", "to_device_storage", "EXPORTS", "LIB_PATH"]

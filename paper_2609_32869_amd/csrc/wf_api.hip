@@ -1,0 +1,671 @@
+// Host runtime of libwf: configuration checks, workspace carve-up, parameter
+// copy, and the enqueue sequences of encode / prefill / draft / verify / step.
+// Every device buffer lives in the caller's workspace; nothing here allocates
+// device memory.
+#include <algorithm>
+#include <cmath>
+#include <type_traits>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <vector>
+
+#include "wf_internal.h"
+
+using namespace wf;
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(Handle* h, int code, const std::string& msg) {
+  if (h) h->err = msg;
+  g_err = msg;
+  return code;
+}
+
+#define HIPCK(h, x)                                                                 \
+  do {                                                                              \
+    hipError_t e_ = (x);                                                            \
+    if (e_ != hipSuccess) return fail(h, WF_EHIP, std::string(#x ": ") + hipGetErrorString(e_)); \
+  } while (0)
+
+size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+size_t elt_bytes(const wf_config& c) { return c.dtype == WF_BF16 ? 2 : 4; }
+
+int check_config(const wf_config* c, std::string& why) {
+  if (!c) { why = "null config"; return WF_EINVAL; }
+  if (c->dtype != WF_F32 && c->dtype != WF_BF16) { why = "dtype must be WF_F32 or WF_BF16"; return WF_EINVAL; }
+  if (c->n_head <= 0 || c->d_model != c->n_head * kHeadDim) { why = "head width must be 64"; return WF_EINVAL; }
+  if (c->n_layer <= 0 || c->n_draft_layer <= 0) { why = "layer counts must be positive"; return WF_EINVAL; }
+  if (c->d_ff <= 0 || c->d_ff % 16) { why = "d_ff must be a positive multiple of 16"; return WF_EINVAL; }
+  if (c->n_vocab < 2) { why = "n_vocab must be >= 2"; return WF_EINVAL; }
+  if (c->n_ctx < 16 || c->n_ctx > kMaxCtx || c->n_ctx % kPage) { why = "n_ctx must be a multiple of 16 in [16, 448]"; return WF_EINVAL; }
+  if (c->n_frames < 1) { why = "n_frames must be positive"; return WF_EINVAL; }
+  if (c->block_k != kRows - 1) { why = "block_k must be 8"; return WF_EINVAL; }
+  if (c->n_tap < 1 || c->n_tap > WF_MAX_TAPS) { why = "n_tap must be in [1, 8]"; return WF_EINVAL; }
+  for (int i = 0; i < c->n_tap; ++i) {
+    if (c->taps[i] < 0 || c->taps[i] >= c->n_layer || (i && c->taps[i] <= c->taps[i - 1])) {
+      why = "taps must be strictly increasing block indices";
+      return WF_EINVAL;
+    }
+  }
+  if (c->max_batch < 1 || c->max_batch > 4096) { why = "max_batch must be in [1, 4096]"; return WF_EINVAL; }
+  if (c->eos_id < -1 || c->eos_id >= c->n_vocab) { why = "eos_id out of range"; return WF_EINVAL; }
+  return WF_OK;
+}
+
+// manifest entry -> (numel, destination element offset in the weight region)
+struct ManEntry {
+  size_t numel, dst;
+};
+
+std::vector<ManEntry> manifest(const wf_config& c, const Layout& L) {
+  const size_t d = c.d_model, F = c.d_ff;
+  std::vector<ManEntry> m;
+  m.push_back({(size_t)c.n_vocab * d, L.tok_emb});
+  m.push_back({(size_t)c.n_ctx * d, L.pos_emb});
+  auto block = [&](const BlockW& b) {
+    m.push_back({d, b.ln1_g}); m.push_back({d, b.ln1_b});
+    m.push_back({d * d, b.w_qkv}); m.push_back({d, b.b_qkv});
+    m.push_back({d * d, b.w_qkv + d * d});
+    m.push_back({d * d, b.w_qkv + 2 * d * d}); m.push_back({d, b.b_qkv + 2 * d});
+    m.push_back({d * d, b.w_o}); m.push_back({d, b.b_o});
+    m.push_back({d, b.ln2_g}); m.push_back({d, b.ln2_b});
+    m.push_back({d * d, b.w_q2}); m.push_back({d, b.b_q2});
+    m.push_back({d * d, b.w_kv2});
+    m.push_back({d * d, b.w_kv2 + d * d}); m.push_back({d, b.b_kv2 + d});
+    m.push_back({d * d, b.w_o2}); m.push_back({d, b.b_o2});
+    m.push_back({d, b.ln3_g}); m.push_back({d, b.ln3_b});
+    m.push_back({F * d, b.w_fc1}); m.push_back({F, b.b_fc1});
+    m.push_back({d * F, b.w_fc2}); m.push_back({d, b.b_fc2});
+  };
+  for (auto& b : L.tb) block(b);
+  m.push_back({d, L.lnf_g}); m.push_back({d, L.lnf_b});
+  m.push_back({d * c.n_tap * d, L.hproj_w}); m.push_back({d, L.hproj_b}); m.push_back({d, L.mask});
+  for (auto& b : L.db) block(b);
+  m.push_back({d, L.dlnf_g}); m.push_back({d, L.dlnf_b});
+  return m;
+}
+
+}  // namespace
+
+namespace wf {
+
+int compute_layout(const wf_config& c, Layout& L) {
+  const size_t d = c.d_model, F = c.d_ff, V = c.n_vocab, B = c.max_batch, H = c.n_head;
+  const size_t R9 = B * kRows;
+  const size_t eb = elt_bytes(c);
+  // weight region (element offsets, 128-element aligned)
+  size_t w = 0;
+  auto take = [&](size_t n) { size_t o = w; w = align_up(w + n, 128); return o; };
+  L.tok_emb = take(V * d);
+  L.pos_emb = take((size_t)c.n_ctx * d);
+  auto block = [&]() {
+    BlockW b;
+    b.ln1_g = take(d); b.ln1_b = take(d);
+    b.w_qkv = take(3 * d * d); b.b_qkv = take(3 * d);
+    b.w_o = take(d * d); b.b_o = take(d);
+    b.ln2_g = take(d); b.ln2_b = take(d);
+    b.w_q2 = take(d * d); b.b_q2 = take(d);
+    b.w_kv2 = take(2 * d * d); b.b_kv2 = take(2 * d);
+    b.w_o2 = take(d * d); b.b_o2 = take(d);
+    b.ln3_g = take(d); b.ln3_b = take(d);
+    b.w_fc1 = take(F * d); b.b_fc1 = take(F);
+    b.w_fc2 = take(d * F); b.b_fc2 = take(d);
+    return b;
+  };
+  L.tb.clear();
+  L.db.clear();
+  for (int l = 0; l < c.n_layer; ++l) L.tb.push_back(block());
+  L.lnf_g = take(d); L.lnf_b = take(d);
+  L.hproj_w = take(d * c.n_tap * d); L.hproj_b = take(d); L.mask = take(d);
+  for (int l = 0; l < c.n_draft_layer; ++l) L.db.push_back(block());
+  L.dlnf_g = take(d); L.dlnf_b = take(d);
+  L.weight_elems = w;
+  L.pages_per_slot = c.n_ctx / kPage;
+  L.nsplit = (c.n_frames + kFrameSplit - 1) / kFrameSplit;
+  L.head_blocks = (int)((V + 15) / 16);
+  // byte regions
+  size_t o = 0;
+  auto region = [&](size_t bytes) { size_t r = o; o = align_up(o + bytes, 256); return r; };
+  L.state = region(B * kStateInts * 4);
+  L.page_table = region(B * L.pages_per_slot * 4);
+  L.rope = region((size_t)(c.n_ctx + kRows + 1) * 32 * 2 * 4);
+  L.status = region(256);
+  L.aux = region(4 * B * 4);
+  L.weights = region(w * eb);
+  L.xkv = region((size_t)(c.n_layer + c.n_draft_layer) * B * 2 * c.n_frames * d * eb);
+  L.skv = region((size_t)c.n_layer * 2 * B * L.pages_per_slot * H * kPage * kHeadDim * eb);
+  L.hkv = region((size_t)c.n_draft_layer * 2 * B * H * c.n_ctx * kHeadDim * eb);
+  L.h = region(R9 * d * 4);
+  L.xn = region(R9 * d * 4);
+  L.qkv = region(R9 * 3 * d * 4);
+  L.attn = region(R9 * d * 4);
+  L.act = region(R9 * F * 4);
+  L.hp = region(R9 * d * 4);
+  L.kvh = region(R9 * 2 * d * 4);
+  L.taps = region(R9 * c.n_tap * d * 4);
+  L.xm = region(R9 * H * L.nsplit * 4);
+  L.xl = region(R9 * H * L.nsplit * 4);
+  L.xo = region(R9 * H * L.nsplit * kHeadDim * 4);
+  L.hv = region(R9 * L.head_blocks * 4);
+  L.hi = region(R9 * L.head_blocks * 4);
+  L.tok = region(R9 * 4);
+  L.g = region(R9 * 4);
+  L.gmax = region(R9 * 4);
+  L.draft = region(B * c.block_k * 4);
+  L.lasth = region(R9 * d * 4);
+  L.logits = region(R9 * V * 4);
+  L.dlogits = region(R9 * V * 4);
+  L.total = o;
+  return WF_OK;
+}
+
+}  // namespace wf
+
+namespace {
+
+template <typename S>
+struct Runner {
+  Handle* h;
+  hipStream_t st;
+  const wf_config& c;
+  const Layout& L;
+  Runner(Handle* h_, hipStream_t s) : h(h_), st(s), c(h_->cfg), L(h_->lay) {}
+
+  const S* W(size_t off) const { return h->at<const S>(L.weights) + off; }
+  float* F32(size_t off) const { return h->at<float>(off); }
+  int* I32(size_t off) const { return h->at<int>(off); }
+  S* xkv_layer(int l) const { return h->at<S>(L.xkv) + (size_t)l * c.max_batch * 2 * c.n_frames * c.d_model; }
+  S* skv_layer(int l) const {
+    return h->at<S>(L.skv) + (size_t)l * 2 * kv_stride();
+  }
+  size_t kv_stride() const { return (size_t)c.max_batch * L.pages_per_slot * c.n_head * kPage * kHeadDim; }
+  S* hkv(int dl, int kv) const {
+    return h->at<S>(L.hkv) + ((size_t)dl * 2 + kv) * c.max_batch * c.n_head * c.n_ctx * kHeadDim;
+  }
+
+  GemvArgs gemv_base(int slot0, int n) const {
+    GemvArgs a{};
+    a.slot0 = slot0;
+    a.nslots = n;
+    a.tap = -1;
+    a.n_tap = c.n_tap;
+    a.state = I32(L.state);
+    a.page_table = I32(L.page_table);
+    a.d = c.d_model;
+    a.n_head = c.n_head;
+    a.n_ctx = c.n_ctx;
+    a.pages_per_slot = L.pages_per_slot;
+    return a;
+  }
+
+  void gemv(int epi, int slot0, int n, const float* x, int ldx, size_t w, size_t b, int K, int N, float* y, int ldy,
+            int tap = -1) {
+    GemvArgs a = gemv_base(slot0, n);
+    a.x = x;
+    a.ldx = ldx;
+    a.w = W(w);
+    a.bias = W(b);
+    a.K = K;
+    a.N = N;
+    a.y = y;
+    a.ldy = ldy;
+    a.tap = tap;
+    a.taps = F32(L.taps);
+    Ops<S>::gemv(epi, a, st);
+  }
+
+  void ln(int slot0, int n, const float* x, size_t g, size_t b, float* y) {
+    Ops<S>::layernorm(x, W(g), W(b), y, c.d_model, slot0 * kRows, n * kRows, st);
+  }
+
+  void cross(int slot0, int n, int layer) {
+    CrossArgs a{};
+    a.q = F32(L.qkv);
+    a.ldq = 3 * c.d_model;
+    a.kv = xkv_layer(layer);
+    a.pm = F32(L.xm);
+    a.pl = F32(L.xl);
+    a.po = F32(L.xo);
+    a.out = F32(L.attn);
+    a.slot0 = slot0;
+    a.d = c.d_model;
+    a.n_head = c.n_head;
+    a.n_frames = c.n_frames;
+    a.nsplit = L.nsplit;
+    Ops<S>::attn_cross(a, n, st);
+  }
+
+  // second half of a decoder block shared by target and drafter: cross-attention and MLP
+  void block_tail(int slot0, int n, const BlockW& b, int xlayer, int tap) {
+    const int d = c.d_model;
+    float *h_ = F32(L.h), *xn = F32(L.xn), *qkv = F32(L.qkv), *attn = F32(L.attn), *act = F32(L.act);
+    ln(slot0, n, h_, b.ln2_g, b.ln2_b, xn);
+    gemv(EPI_STORE, slot0, n, xn, d, b.w_q2, b.b_q2, d, d, qkv, 3 * d);
+    cross(slot0, n, xlayer);
+    gemv(EPI_RESID, slot0, n, attn, d, b.w_o2, b.b_o2, d, d, h_, d);
+    ln(slot0, n, h_, b.ln3_g, b.ln3_b, xn);
+    gemv(EPI_GELU, slot0, n, xn, d, b.w_fc1, b.b_fc1, d, c.d_ff, act, c.d_ff);
+    gemv(EPI_RESID, slot0, n, act, c.d_ff, b.w_fc2, b.b_fc2, c.d_ff, d, h_, d, tap);
+  }
+
+  void target_forward(int slot0, int n) {
+    const int d = c.d_model;
+    float *h_ = F32(L.h), *xn = F32(L.xn), *qkv = F32(L.qkv), *attn = F32(L.attn);
+    for (int l = 0; l < c.n_layer; ++l) {
+      const BlockW& b = L.tb[l];
+      int tap = -1;
+      for (int i = 0; i < c.n_tap; ++i)
+        if (c.taps[i] == l) tap = i;
+      ln(slot0, n, h_, b.ln1_g, b.ln1_b, xn);
+      GemvArgs a = gemv_base(slot0, n);
+      a.x = xn; a.ldx = d; a.w = W(b.w_qkv); a.bias = W(b.b_qkv); a.K = d; a.N = 3 * d;
+      a.y = qkv; a.ldy = 3 * d; a.cache = skv_layer(l); a.kv_stride = kv_stride();
+      Ops<S>::gemv(EPI_QKV, a, st);
+      AttnArgs at{};
+      at.q = qkv; at.ldq = 3 * d; at.kcache = skv_layer(l); at.vcache = skv_layer(l) + kv_stride();
+      at.state = I32(L.state); at.page_table = I32(L.page_table); at.rope = F32(L.rope); at.out = attn;
+      at.slot0 = slot0; at.d = d; at.n_head = c.n_head; at.n_ctx = c.n_ctx; at.pages_per_slot = L.pages_per_slot;
+      Ops<S>::attn_self(at, n, st);
+      gemv(EPI_RESID, slot0, n, attn, d, b.w_o, b.b_o, d, d, h_, d);
+      block_tail(slot0, n, b, l, tap);
+    }
+  }
+
+  // vocabulary head over rows of x: logits = x @ tok_emb^T, per-row argmax into g
+  void head(int slot0, int n, const float* x, float* logits) {
+    GemvArgs a = gemv_base(slot0, n);
+    a.x = x; a.ldx = c.d_model; a.w = W(L.tok_emb); a.bias = nullptr; a.K = c.d_model; a.N = c.n_vocab;
+    a.y = logits; a.ldy = c.n_vocab; a.hv = F32(L.hv); a.hi = I32(L.hi); a.nblk = L.head_blocks;
+    Ops<S>::gemv(EPI_ARGMAX, a, st);
+    argmax_final(F32(L.hv), I32(L.hi), L.head_blocks, slot0 * kRows, n * kRows, I32(L.g), F32(L.gmax),
+                 h->at<unsigned>(L.status), st);
+  }
+
+  // drafter history for pending rows (Appendix A.2): taps -> W_h -> per-block LN, k (RoPE), v
+  void history_apply(int slot0, int n) {
+    const int d = c.d_model;
+    float *hp = F32(L.hp), *xn = F32(L.xn), *kvh = F32(L.kvh);
+    gemv(EPI_STORE, slot0, n, F32(L.taps), c.n_tap * d, L.hproj_w, L.hproj_b, c.n_tap * d, d, hp, d);
+    for (int dl = 0; dl < c.n_draft_layer; ++dl) {
+      const BlockW& b = L.db[dl];
+      ln(slot0, n, hp, b.ln1_g, b.ln1_b, xn);
+      gemv(EPI_STORE, slot0, n, xn, d, b.w_qkv + (size_t)d * d, b.b_qkv + d, d, 2 * d, kvh, 2 * d);
+      HistArgs ha{};
+      ha.kv = kvh; ha.kcache = hkv(dl, 0); ha.vcache = hkv(dl, 1); ha.state = I32(L.state); ha.rope = F32(L.rope);
+      ha.slot0 = slot0; ha.d = d; ha.n_head = c.n_head; ha.n_ctx = c.n_ctx;
+      Ops<S>::hist_write(ha, n, st);
+    }
+  }
+
+  void drafter_forward(int slot0, int n, int* dst) {
+    const int d = c.d_model;
+    float *h_ = F32(L.h), *xn = F32(L.xn), *qkv = F32(L.qkv), *attn = F32(L.attn);
+    BeginArgs ba{};
+    ba.state = I32(L.state); ba.emb = W(L.tok_emb); ba.pos = W(L.mask); ba.h = h_;
+    ba.slot0 = slot0; ba.d = d; ba.n_vocab = c.n_vocab; ba.n_ctx = c.n_ctx; ba.block_k = c.block_k;
+    Ops<S>::draft_begin(ba, n, st);
+    for (int dl = 0; dl < c.n_draft_layer; ++dl) {
+      const BlockW& b = L.db[dl];
+      ln(slot0, n, h_, b.ln1_g, b.ln1_b, xn);
+      gemv(EPI_STORE, slot0, n, xn, d, b.w_qkv, b.b_qkv, d, 3 * d, qkv, 3 * d);
+      AttnArgs at{};
+      at.q = qkv; at.ldq = 3 * d; at.kcache = hkv(dl, 0); at.vcache = hkv(dl, 1);
+      at.state = I32(L.state); at.rope = F32(L.rope); at.out = attn;
+      at.slot0 = slot0; at.d = d; at.n_head = c.n_head; at.n_ctx = c.n_ctx;
+      Ops<S>::attn_draft(at, n, st);
+      gemv(EPI_RESID, slot0, n, attn, d, b.w_o, b.b_o, d, d, h_, d);
+      block_tail(slot0, n, b, c.n_layer + dl, -1);
+    }
+    ln(slot0, n, h_, L.dlnf_g, L.dlnf_b, xn);
+    head(slot0, n, xn, h->debug ? F32(L.dlogits) : nullptr);
+    draft_tokens(I32(L.g), dst, I32(L.draft), slot0, n, c.block_k, st);
+  }
+
+  void verify(int slot0, int n, const int* draft, int k_max, int* out, int* n_out, int* n_acc, int* done) {
+    BeginArgs ba{};
+    ba.state = I32(L.state); ba.draft = draft; ba.tok = I32(L.tok); ba.emb = W(L.tok_emb); ba.pos = W(L.pos_emb);
+    ba.h = F32(L.h); ba.slot0 = slot0; ba.d = c.d_model; ba.n_vocab = c.n_vocab; ba.n_ctx = c.n_ctx;
+    ba.block_k = c.block_k; ba.k_max = k_max;
+    Ops<S>::verify_begin(ba, n, st);
+    target_forward(slot0, n);
+    ln(slot0, n, F32(L.h), L.lnf_g, L.lnf_b, F32(L.xn));
+    head(slot0, n, F32(L.xn), h->debug ? F32(L.logits) : nullptr);
+    AcceptArgs aa{};
+    aa.state = I32(L.state); aa.tok = I32(L.tok); aa.g = I32(L.g); aa.out = out; aa.n_out = n_out; aa.n_acc = n_acc;
+    aa.done = done; aa.slot0 = slot0; aa.n = n; aa.block_k = c.block_k; aa.eos = c.eos_id; aa.n_ctx = c.n_ctx;
+    accept_greedy(aa, st);
+  }
+
+  void draft(int slot0, int n, int* dst) {
+    history_apply(slot0, n);
+    hist_done(I32(L.state), slot0, n, st);
+    drafter_forward(slot0, n, dst);
+  }
+
+  void encode(int slot0, int n, const void* mem) {
+    const size_t per = (size_t)c.n_frames * c.d_model;
+    for (int s = 0; s < n; ++s) {
+      const int slot = slot0 + s;
+      for (int l = 0; l < c.n_layer + c.n_draft_layer; ++l) {
+        const BlockW& b = l < c.n_layer ? L.tb[l] : L.db[l - c.n_layer];
+        XkvArgs a{};
+        a.mem = reinterpret_cast<const S*>(mem) + s * per;
+        a.w = W(b.w_kv2);
+        a.bias = W(b.b_kv2);
+        a.out = xkv_layer(l) + (size_t)slot * 2 * c.n_frames * c.d_model;
+        a.d = c.d_model;
+        a.n_head = c.n_head;
+        a.n_frames = c.n_frames;
+        Ops<S>::gemm_xkv(a, st);
+      }
+    }
+  }
+
+  void prefill(int slot0, int n, const int* tokens, int pmax, int max_len, int* first) {
+    const int nchunks = (max_len + kRows - 1) / kRows;
+    BeginArgs ba{};
+    ba.state = I32(L.state); ba.draft = tokens; ba.tok = I32(L.tok); ba.emb = W(L.tok_emb); ba.pos = W(L.pos_emb);
+    ba.h = F32(L.h); ba.slot0 = slot0; ba.d = c.d_model; ba.n_vocab = c.n_vocab; ba.n_ctx = c.n_ctx;
+    ba.block_k = c.block_k; ba.pmax = pmax;
+    for (int ch = 0; ch < nchunks; ++ch) {
+      ba.chunk = ch;
+      Ops<S>::prefill_begin(ba, n, st);
+      target_forward(slot0, n);
+      save_last(F32(L.h), F32(L.lasth), I32(L.state), slot0, n, c.d_model, ch, st);
+      history_apply(slot0, n);
+    }
+    ln(slot0, n, F32(L.lasth), L.lnf_g, L.lnf_b, F32(L.xn));
+    head(slot0, n, F32(L.xn), nullptr);
+    prefill_finish(I32(L.state), I32(L.g), slot0, n, c.eos_id, c.n_ctx, first, st);
+  }
+};
+
+template <typename Fn>
+int dispatch(Handle* h, Fn&& fn) {
+  if (h->cfg.dtype == WF_BF16) {
+    fn(static_cast<bf16*>(nullptr));
+  } else {
+    fn(static_cast<float*>(nullptr));
+  }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return fail(h, WF_EHIP, std::string("kernel launch: ") + hipGetErrorString(e));
+  return WF_OK;
+}
+
+int check_batch(Handle* h, int slot0, int n, bool need_live) {
+  if (!h) return fail(nullptr, WF_EINVAL, "null handle");
+  if (n < 1 || slot0 < 0 || slot0 + n > h->cfg.max_batch) return fail(h, WF_EINVAL, "slot range out of bounds");
+  if (need_live)
+    for (int s = slot0; s < slot0 + n; ++s)
+      if (!h->live[s]) return fail(h, WF_ESTATE, "slot not prefilled");
+  return WF_OK;
+}
+
+std::vector<float> rope_table(int n_pos) {
+  std::vector<float> t((size_t)n_pos * 32 * 2);
+  for (int p = 0; p < n_pos; ++p)
+    for (int i = 0; i < 32; ++i) {
+      const float omega = (float)std::pow(10000.0, -2.0 * i / 64.0);
+      const float theta = (float)p * omega;  // fp32 product
+      t[((size_t)p * 32 + i) * 2] = (float)std::cos((double)theta);
+      t[((size_t)p * 32 + i) * 2 + 1] = (float)std::sin((double)theta);
+    }
+  return t;
+}
+
+}  // namespace
+
+extern "C" {
+
+int wf_workspace_bytes(const wf_config* cfg, size_t* bytes) {
+  std::string why;
+  if (int r = check_config(cfg, why)) return fail(nullptr, r, why);
+  if (!bytes) return fail(nullptr, WF_EINVAL, "null bytes");
+  Layout L;
+  compute_layout(*cfg, L);
+  *bytes = L.total;
+  return WF_OK;
+}
+
+int wf_weight_count(const wf_config* cfg, int* n) {
+  std::string why;
+  if (int r = check_config(cfg, why)) return fail(nullptr, r, why);
+  if (!n) return fail(nullptr, WF_EINVAL, "null n");
+  Layout L;
+  compute_layout(*cfg, L);
+  *n = (int)manifest(*cfg, L).size();
+  return WF_OK;
+}
+
+int wf_weight_numel(const wf_config* cfg, int i, int64_t* numel) {
+  std::string why;
+  if (int r = check_config(cfg, why)) return fail(nullptr, r, why);
+  Layout L;
+  compute_layout(*cfg, L);
+  auto m = manifest(*cfg, L);
+  if (!numel || i < 0 || i >= (int)m.size()) return fail(nullptr, WF_EINVAL, "index out of range");
+  *numel = (int64_t)m[i].numel;
+  return WF_OK;
+}
+
+int wf_init_weights(wf_handle** out, const wf_config* cfg, const void* const* weights, int n_weights, void* workspace,
+                    size_t ws_bytes, void* stream) {
+  std::string why;
+  if (!out) return fail(nullptr, WF_EINVAL, "null handle pointer");
+  if (int r = check_config(cfg, why)) return fail(nullptr, r, why);
+  if (!workspace || (reinterpret_cast<uintptr_t>(workspace) & 255)) return fail(nullptr, WF_EINVAL, "workspace must be 256-byte aligned");
+  Layout L;
+  compute_layout(*cfg, L);
+  if (ws_bytes < L.total) return fail(nullptr, WF_ESIZE, "workspace too small");
+  auto man = manifest(*cfg, L);
+  if (!weights || n_weights != (int)man.size()) return fail(nullptr, WF_EINVAL, "wrong number of weight tensors");
+  for (int i = 0; i < n_weights; ++i)
+    if (!weights[i]) return fail(nullptr, WF_EINVAL, "null weight pointer");
+  Handle* h = new (std::nothrow) Handle();
+  if (!h) return fail(nullptr, WF_EINVAL, "out of host memory");
+  h->cfg = *cfg;
+  h->lay = L;
+  h->ws = static_cast<char*>(workspace);
+  h->ws_bytes = ws_bytes;
+  h->live.assign(cfg->max_batch, 0);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  auto cleanup = [&](int code, const std::string& msg) { delete h; return fail(nullptr, code, msg); };
+  hipError_t e = hipMemsetAsync(workspace, 0, L.total, st);
+  if (e != hipSuccess) return cleanup(WF_EHIP, std::string("hipMemsetAsync: ") + hipGetErrorString(e));
+  const size_t eb = elt_bytes(*cfg);
+  char* wbase = h->at<char>(L.weights);
+  for (int i = 0; i < n_weights; ++i) {
+    e = hipMemcpyAsync(wbase + man[i].dst * eb, weights[i], man[i].numel * eb, hipMemcpyDeviceToDevice, st);
+    if (e != hipSuccess) return cleanup(WF_EHIP, std::string("hipMemcpyAsync: ") + hipGetErrorString(e));
+  }
+  // page table: logical page j of slot s -> physical page j * max_batch + s
+  std::vector<int> pt((size_t)cfg->max_batch * L.pages_per_slot);
+  for (int s = 0; s < cfg->max_batch; ++s)
+    for (int j = 0; j < L.pages_per_slot; ++j) pt[(size_t)s * L.pages_per_slot + j] = j * cfg->max_batch + s;
+  std::vector<float> rope = rope_table(cfg->n_ctx + kRows + 1);
+  e = hipMemcpyAsync(h->at<char>(L.page_table), pt.data(), pt.size() * 4, hipMemcpyHostToDevice, st);
+  if (e == hipSuccess) e = hipMemcpyAsync(h->at<char>(L.rope), rope.data(), rope.size() * 4, hipMemcpyHostToDevice, st);
+  if (e == hipSuccess) e = hipStreamSynchronize(st);
+  if (e != hipSuccess) return cleanup(WF_EHIP, std::string("init copy: ") + hipGetErrorString(e));
+  *out = reinterpret_cast<wf_handle*>(h);
+  return WF_OK;
+}
+
+int wf_encode_memory_set(wf_handle* hh, int slot0, int n, const void* mem, void* stream) {
+  Handle* h = reinterpret_cast<Handle*>(hh);
+  if (int r = check_batch(h, slot0, n, false)) return r;
+  if (!mem) return fail(h, WF_EINVAL, "null memory");
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  return dispatch(h, [&](auto* tag) {
+    using S = std::remove_pointer_t<decltype(tag)>;
+    Runner<S>(h, st).encode(slot0, n, mem);
+  });
+}
+
+int wf_prefill(wf_handle* hh, int slot0, int n, const int32_t* tokens, int pmax, const int32_t* lens,
+               const int32_t* max_new, int32_t* first, void* stream) {
+  Handle* h = reinterpret_cast<Handle*>(hh);
+  if (int r = check_batch(h, slot0, n, false)) return r;
+  if (!tokens || !lens || !max_new || pmax < 1) return fail(h, WF_EINVAL, "null argument");
+  if (h->temperature > 0.f) return fail(h, WF_EINVAL, "sampling is not available in this build");
+  int max_len = 0;
+  for (int s = 0; s < n; ++s) {
+    if (lens[s] < 1 || lens[s] > pmax || lens[s] > h->cfg.n_ctx) return fail(h, WF_EINVAL, "prompt length out of range");
+    if (max_new[s] < 1) return fail(h, WF_EINVAL, "max_new must be >= 1");
+    max_len = std::max(max_len, (int)lens[s]);
+  }
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  std::vector<int> init((size_t)n * kStateInts, 0);
+  for (int s = 0; s < n; ++s) {
+    init[(size_t)s * kStateInts + ST_LEN] = lens[s];
+    init[(size_t)s * kStateInts + ST_MAX_NEW] = max_new[s];
+  }
+  HIPCK(h, hipMemcpyAsync(h->at<int>(h->lay.state) + (size_t)slot0 * kStateInts, init.data(), init.size() * 4,
+                          hipMemcpyHostToDevice, st));
+  int r = dispatch(h, [&](auto* tag) {
+    using S = std::remove_pointer_t<decltype(tag)>;
+    Runner<S>(h, st).prefill(slot0, n, tokens, pmax, max_len, first);
+  });
+  if (r) return r;
+  HIPCK(h, hipStreamSynchronize(st));
+  for (int s = slot0; s < slot0 + n; ++s) h->live[s] = 1;
+  return WF_OK;
+}
+
+int wf_set_sampling(wf_handle* hh, float temperature, uint64_t seed, const uint8_t* suppress) {
+  Handle* h = reinterpret_cast<Handle*>(hh);
+  if (!h) return fail(nullptr, WF_EINVAL, "null handle");
+  if (!(temperature >= 0.f) || std::isinf(temperature)) return fail(h, WF_EINVAL, "temperature must be finite and >= 0");
+  if (temperature > 0.f) return fail(h, WF_EINVAL, "sampling is not available in this build");
+  h->temperature = temperature;
+  h->seed = seed;
+  h->suppress = suppress;
+  return WF_OK;
+}
+
+int wf_draft(wf_handle* hh, int slot0, int n, int32_t* draft, void* stream) {
+  Handle* h = reinterpret_cast<Handle*>(hh);
+  if (int r = check_batch(h, slot0, n, true)) return r;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  return dispatch(h, [&](auto* tag) {
+    using S = std::remove_pointer_t<decltype(tag)>;
+    Runner<S>(h, st).draft(slot0, n, draft);
+  });
+}
+
+int wf_verify_accept(wf_handle* hh, int slot0, int n, const int32_t* draft, int k_max, int32_t* out, int32_t* n_out,
+                     int32_t* n_acc, int32_t* done, void* stream) {
+  Handle* h = reinterpret_cast<Handle*>(hh);
+  if (int r = check_batch(h, slot0, n, true)) return r;
+  if (!draft) return fail(h, WF_EINVAL, "null draft");
+  if (k_max < 0 || k_max > h->cfg.block_k) return fail(h, WF_EINVAL, "k_max out of range");
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  return dispatch(h, [&](auto* tag) {
+    using S = std::remove_pointer_t<decltype(tag)>;
+    Runner<S>(h, st).verify(slot0, n, draft, k_max, out, n_out, n_acc, done);
+  });
+}
+
+static int step_enqueue(Handle* h, int slot0, int n, int k_max, const int32_t* ovr, int32_t* out, int32_t* n_out,
+                        int32_t* n_acc, int32_t* done, hipStream_t st) {
+  return dispatch(h, [&](auto* tag) {
+    using S = std::remove_pointer_t<decltype(tag)>;
+    Runner<S> R(h, st);
+    R.draft(slot0, n, nullptr);
+    const int* d = ovr ? ovr : h->at<int>(h->lay.draft) + (size_t)slot0 * h->cfg.block_k;
+    R.verify(slot0, n, d, k_max, out, n_out, n_acc, done);
+  });
+}
+
+int wf_step(wf_handle* hh, int slot0, int n, int k_max, const int32_t* ovr, int32_t* out, int32_t* n_out,
+            int32_t* n_acc, int32_t* done, int use_graph, void* stream) {
+  Handle* h = reinterpret_cast<Handle*>(hh);
+  if (int r = check_batch(h, slot0, n, true)) return r;
+  if (k_max < 0 || k_max > h->cfg.block_k) return fail(h, WF_EINVAL, "k_max out of range");
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (!use_graph) return step_enqueue(h, slot0, n, k_max, ovr, out, n_out, n_acc, done, st);
+  if (!st) return fail(h, WF_EINVAL, "graph replay needs a non-null stream");
+  GraphKey key{slot0, n, k_max, ovr, out, n_out, n_acc, done};
+  auto it = h->graphs.find(key);
+  if (it == h->graphs.end()) {
+    HIPCK(h, hipStreamBeginCapture(st, hipStreamCaptureModeThreadLocal));
+    int r = step_enqueue(h, slot0, n, k_max, ovr, out, n_out, n_acc, done, st);
+    hipGraph_t g = nullptr;
+    hipError_t e = hipStreamEndCapture(st, &g);
+    if (r) { if (g) (void)hipGraphDestroy(g); return r; }
+    if (e != hipSuccess) return fail(h, WF_EHIP, std::string("hipStreamEndCapture: ") + hipGetErrorString(e));
+    hipGraphExec_t ex = nullptr;
+    e = hipGraphInstantiate(&ex, g, nullptr, nullptr, 0);
+    (void)hipGraphDestroy(g);
+    if (e != hipSuccess) return fail(h, WF_EHIP, std::string("hipGraphInstantiate: ") + hipGetErrorString(e));
+    it = h->graphs.emplace(key, ex).first;
+  }
+  HIPCK(h, hipGraphLaunch(it->second, st));
+  return WF_OK;
+}
+
+int wf_debug_ptr(wf_handle* hh, int which, void** ptr) {
+  Handle* h = reinterpret_cast<Handle*>(hh);
+  if (!h || !ptr) return fail(h, WF_EINVAL, "null argument");
+  switch (which) {
+    case 0: *ptr = h->at<void>(h->lay.logits); break;
+    case 1: *ptr = h->at<void>(h->lay.dlogits); break;
+    case 2: *ptr = h->at<void>(h->lay.state); break;
+    case 3: *ptr = h->at<void>(h->lay.draft); break;
+    default: return fail(h, WF_EINVAL, "unknown debug view");
+  }
+  return WF_OK;
+}
+
+int wf_set_debug(wf_handle* hh, int enable) {
+  Handle* h = reinterpret_cast<Handle*>(hh);
+  if (!h) return fail(nullptr, WF_EINVAL, "null handle");
+  if (h->debug != (enable != 0)) {
+    for (auto& kv : h->graphs) (void)hipGraphExecDestroy(kv.second);
+    h->graphs.clear();
+  }
+  h->debug = enable != 0;
+  return WF_OK;
+}
+
+int wf_status(wf_handle* hh, uint32_t* flags, void* stream) {
+  Handle* h = reinterpret_cast<Handle*>(hh);
+  if (!h || !flags) return fail(h, WF_EINVAL, "null argument");
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  uint32_t v = 0;
+  HIPCK(h, hipMemcpyAsync(&v, h->at<char>(h->lay.status), 4, hipMemcpyDeviceToHost, st));
+  HIPCK(h, hipStreamSynchronize(st));
+  *flags = v;
+  if (v) HIPCK(h, hipMemsetAsync(h->at<char>(h->lay.status), 0, 4, st));
+  return WF_OK;
+}
+
+int wf_release(wf_handle* hh) {
+  Handle* h = reinterpret_cast<Handle*>(hh);
+  if (!h) return fail(nullptr, WF_EINVAL, "null handle");
+  for (auto& kv : h->graphs) (void)hipGraphExecDestroy(kv.second);
+  delete h;
+  return WF_OK;
+}
+
+const char* wf_strerror(int code) {
+  switch (code) {
+    case WF_OK: return "ok";
+    case WF_EINVAL: return "invalid argument";
+    case WF_ESTATE: return "invalid state";
+    case WF_ESIZE: return "workspace too small";
+    case WF_EHIP: return "HIP runtime error";
+    default: return "unknown error";
+  }
+}
+
+const char* wf_last_error(wf_handle* hh) {
+  Handle* h = reinterpret_cast<Handle*>(hh);
+  return h ? h->err.c_str() : g_err.c_str();
+}
+
+}  // extern "C"

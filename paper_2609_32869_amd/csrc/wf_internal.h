@@ -1,0 +1,67 @@
+// Internal runtime structures of libwf: workspace carve-up, parameter views and
+// kernel launchers.  Not part of the ABI.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <map>
+#include <string>
+#include <tuple>
+#include <vector>
+
+#include "../../include/wf.h"
+#include "wf_common.h"
+#include "wf_kernels.h"
+
+namespace wf {
+
+// Offsets (in elements of the storage type) of one decoder block's parameters
+// inside the weight region.  q/k/v are stored concatenated ([3d, d] and [3d]
+// bias with a zero key bias), as are the cross-attention k/v ([2d, d], [2d]).
+struct BlockW {
+  size_t ln1_g, ln1_b, w_qkv, b_qkv, w_o, b_o;
+  size_t ln2_g, ln2_b, w_q2, b_q2, w_kv2, b_kv2, w_o2, b_o2;
+  size_t ln3_g, ln3_b, w_fc1, b_fc1, w_fc2, b_fc2;
+};
+
+struct Layout {
+  // byte offsets into the workspace
+  size_t state, page_table, rope, status, aux, weights, xkv, skv, hkv;
+  size_t h, xn, qkv, attn, act, hp, kvh, taps, xm, xl, xo, hv, hi, tok, g, gmax, draft, lasth, logits, dlogits;
+  size_t total;
+  // element offsets inside the weight region
+  size_t tok_emb, pos_emb, lnf_g, lnf_b, hproj_w, hproj_b, mask, dlnf_g, dlnf_b;
+  std::vector<BlockW> tb, db;
+  size_t weight_elems;
+  int pages_per_slot, nsplit, head_blocks;
+};
+
+struct Handle;
+
+struct GraphKey {
+  int slot0, n, k_max;
+  const void *ovr, *out, *nout, *nacc, *done;
+  bool operator<(const GraphKey& o) const {
+    return std::tie(slot0, n, k_max, ovr, out, nout, nacc, done) <
+           std::tie(o.slot0, o.n, o.k_max, o.ovr, o.out, o.nout, o.nacc, o.done);
+  }
+};
+
+struct Handle {
+  wf_config cfg;
+  Layout lay;
+  char* ws;
+  size_t ws_bytes;
+  float temperature = 0.f;
+  uint64_t seed = 0;
+  const uint8_t* suppress = nullptr;
+  bool debug = false;
+  std::string err;
+  std::vector<int> live;  // host mirror: slot prefilled
+  std::map<GraphKey, hipGraphExec_t> graphs;
+
+  template <typename T>
+  T* at(size_t off) const { return reinterpret_cast<T*>(ws + off); }
+};
+
+int compute_layout(const wf_config& c, Layout& L);
+
+}  // namespace wf

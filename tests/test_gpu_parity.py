@@ -1,0 +1,109 @@
+"""Parity of the HIP path (called through the C ABI) with the oracle.
+
+Bar: token ids and accepted lengths identical wherever the oracle's top-2
+margin exceeds the logit tolerance; logits within max |delta| <= 2e-2 for bf16
+storage (bf16 caches against fp32 oracle arithmetic on the same bf16
+weights) and <= 1e-3 for fp32 storage.
+"""
+import numpy as np
+import pytest
+import torch
+
+from wf_fixtures import MICRO, TINY, LARGE_V3, make_weights, make_memory, make_prefix, make_prefix_lengths, plant_drafts
+from oracle import OracleOpts, Target, plain_greedy
+
+pytestmark = pytest.mark.gpu
+
+TOL_F32 = 1e-3
+TOL_BF16 = 2e-2
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+
+
+def _planted(ls, refs, rng):
+    K = ls.cfg.block_k
+    ov = np.zeros((ls.n, K), np.int32)
+    for i, s in enumerate(ls.sess):
+        cont = (list(refs[i]) + [0] * (K + 1))[s.emitted:s.emitted + K]
+        ov[i] = plant_drafts(cont, int(rng.integers(0, K + 1)), ls.cfg.n_vocab, rng)
+    return ov
+
+
+def test_micro_lockstep_natural_and_planted():
+    from lockstep import Lockstep
+    cfg = MICRO
+    W = make_weights(cfg)
+    prompts = [make_prefix(cfg, 0, 5), make_prefix(cfg, 1, 13), make_prefix(cfg, 2, 27)]
+    max_new = [30, 12, 40]
+    ls = Lockstep(cfg, W, prompts, max_new, TOL_F32)
+    for _ in range(3):
+        ls.step()
+    T = Target(cfg, W.values, OracleOpts())
+    refs = [plain_greedy(T, make_memory(cfg, i), prompts[i], max_new[i]) for i in range(3)]
+    rng = np.random.default_rng(0)
+    for _ in range(12):
+        ls.step(override=_planted(ls, refs, rng))
+    # the whole transcript equals plain greedy decoding
+    for i, s in enumerate(ls.sess):
+        if ls.live[i]:
+            assert s.out == refs[i][:len(s.out)]
+    assert max(ls.accepted) > 0
+    ls.close()
+
+
+def test_micro_k_max_and_budget_edges():
+    from lockstep import Lockstep
+    cfg = MICRO
+    W = make_weights(cfg)
+    # prompt ending near the context limit: budget caps k at n_ctx - L - 1
+    prompts = [make_prefix(cfg, 3, cfg.n_ctx - 6), make_prefix(cfg, 4, 1)]
+    ls = Lockstep(cfg, W, prompts, [100, 3], TOL_F32)
+    T = Target(cfg, W.values, OracleOpts())
+    refs = [plain_greedy(T, make_memory(cfg, i), prompts[i], m) for i, m in enumerate([100, 3])]
+    rng = np.random.default_rng(1)
+    for k_max in (0, 3, 8, 8, 8, 8):
+        ls.step(k_max=k_max, override=_planted(ls, refs, rng))
+    for i, s in enumerate(ls.sess):
+        assert s.done
+    ls.close()
+
+
+def test_tiny_greedy_64_tokens_equal_plain_greedy():
+    """Tiny Whisper-shaped decoder, fp32 weights, prefix 32, 64 greedy tokens."""
+    from lockstep import Lockstep
+    cfg = TINY
+    W = make_weights(cfg)
+    prompt = make_prefix(cfg, 0, 32)
+    ls = Lockstep(cfg, W, [prompt], [64], TOL_F32)
+    T = Target(cfg, W.values, OracleOpts())
+    ref = plain_greedy(T, make_memory(cfg, 0), prompt, 64)
+    rng = np.random.default_rng(2)
+    n = 0
+    while not ls.sess[0].done and n < 70:
+        ov = _planted(ls, [ref], rng) if n % 2 else None
+        ls.step(override=ov)
+        n += 1
+    assert ls.live[0], ls.near_ties
+    assert ls.sess[0].out == ref
+    ls.close()
+
+
+@pytest.mark.timeout(900)
+def test_large_v3_bf16_lockstep_b1():
+    """Whisper-large-v3 shapes, bf16 weights/caches, one slot, prefix in [20, 200]."""
+    from lockstep import Lockstep
+    cfg = LARGE_V3
+    W = make_weights(cfg)
+    L = int(make_prefix_lengths(1, 20, 200)[0])
+    prompt = make_prefix(cfg, 0, L)
+    ls = Lockstep(cfg, W, [prompt], [448], TOL_BF16)
+    for _ in range(2):
+        ls.step()
+    # planted acceptance using the GPU's own argmax continuation is checked
+    # through the oracle inside the step comparison
+    print(f"large-v3: max |dlogit| draft {ls.max_dlogit:.3e} target {ls.max_tlogit:.3e}, near ties {ls.near_ties}")
+    ls.close()
