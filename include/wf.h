@@ -187,6 +187,18 @@ int wf_step(wf_handle* h, int slot0, int n, int k_max, const int32_t* draft_over
 int wf_debug_ptr(wf_handle* h, int which, void** ptr);
 int wf_set_debug(wf_handle* h, int enable);
 
+/*
+ * Profiling of eager calls: when enabled, every kernel launch of later
+ * non-graph calls is bracketed by HIP events on the call's stream.
+ * wf_profile_summary synchronises those events and writes a JSON object
+ * {"<kernel class>": {"launches": n, "ms": total, "bytes": algorithmic bytes}}
+ * into buf (len bytes, including the terminating NUL), then forgets them.
+ * Algorithmic bytes count parameters, caches and activations each launch must
+ * move once.  Graph replays are never instrumented.
+ */
+int wf_profile_enable(wf_handle* h, int enable);
+int wf_profile_summary(wf_handle* h, char* buf, size_t len);
+
 /* Read and clear the sticky device status word (synchronises `stream`). */
 int wf_status(wf_handle* h, uint32_t* flags, void* stream);
 

@@ -23,8 +23,8 @@ WF_STATUS_POSITION_OVERFLOW = 0x2
 # symbols declared in include/wf.h
 EXPORTS = ["wf_workspace_bytes", "wf_weight_count", "wf_weight_numel", "wf_init_weights",
            "wf_encode_memory_set", "wf_prefill", "wf_set_sampling", "wf_draft", "wf_verify_accept",
-           "wf_step", "wf_debug_ptr", "wf_set_debug", "wf_status", "wf_release", "wf_strerror",
-           "wf_last_error"]
+           "wf_step", "wf_debug_ptr", "wf_set_debug", "wf_profile_enable", "wf_profile_summary", "wf_status",
+           "wf_release", "wf_strerror", "wf_last_error"]
 
 
 class WfConfig(ctypes.Structure):
@@ -65,6 +65,8 @@ def load_library(path=LIB_PATH):
         "wf_step": [P, I, I, I, P, P, P, P, P, I, P],
         "wf_debug_ptr": [P, I, ctypes.POINTER(P)],
         "wf_set_debug": [P, I],
+        "wf_profile_enable": [P, I],
+        "wf_profile_summary": [P, ctypes.c_char_p, Z],
         "wf_status": [P, ctypes.POINTER(ctypes.c_uint32), P],
         "wf_release": [P],
         "wf_strerror": [I],
@@ -223,6 +225,15 @@ class WhisperFlash:
 
     def last_draft(self):
         return self._view(3, (self.max_batch, self.K), torch.int32)
+
+    def profile(self, on):
+        self._check(self.lib.wf_profile_enable(self.h, 1 if on else 0))
+
+    def profile_summary(self):
+        import json
+        buf = ctypes.create_string_buffer(1 << 16)
+        self._check(self.lib.wf_profile_summary(self.h, buf, len(buf)))
+        return json.loads(buf.value.decode())
 
     def status(self, stream=None):
         f = ctypes.c_uint32()

@@ -175,6 +175,31 @@ struct Runner {
   const Layout& L;
   Runner(Handle* h_, hipStream_t s) : h(h_), st(s), c(h_->cfg), L(h_->lay) {}
 
+  // Run one launch; when profiling (eager calls only) bracket it with events.
+  template <typename F>
+  void launch(const char* tag, double bytes, F&& f) {
+    if (!h->prof || h->capturing) {
+      f();
+      return;
+    }
+    ProfRec r{tag, bytes, nullptr, nullptr};
+    for (hipEvent_t* e : {&r.a, &r.b}) {
+      if (!h->ev_pool.empty()) {
+        *e = h->ev_pool.back();
+        h->ev_pool.pop_back();
+      } else if (hipEventCreate(e) != hipSuccess) {
+        *e = nullptr;
+      }
+    }
+    if (r.a && r.b) (void)hipEventRecord(r.a, st);
+    f();
+    if (r.a && r.b) {
+      (void)hipEventRecord(r.b, st);
+      h->prof_recs.push_back(r);
+    }
+  }
+  double eb() const { return c.dtype == WF_BF16 ? 2.0 : 4.0; }
+
   const S* W(size_t off) const { return h->at<const S>(L.weights) + off; }
   float* F32(size_t off) const { return h->at<float>(off); }
   int* I32(size_t off) const { return h->at<int>(off); }
@@ -215,11 +240,14 @@ struct Runner {
     a.ldy = ldy;
     a.tap = tap;
     a.taps = F32(L.taps);
-    Ops<S>::gemv(epi, a, st);
+    const double rows = (double)kRows * n;
+    const double bytes = (double)N * K * eb() + N * eb() + rows * K * 4 + rows * N * 4 * (epi == EPI_RESID ? 2 : 1);
+    launch("gemv", bytes, [&] { Ops<S>::gemv(epi, a, st); });
   }
 
   void ln(int slot0, int n, const float* x, size_t g, size_t b, float* y) {
-    Ops<S>::layernorm(x, W(g), W(b), y, c.d_model, slot0 * kRows, n * kRows, st);
+    launch("layernorm", 8.0 * kRows * n * c.d_model,
+           [&] { Ops<S>::layernorm(x, W(g), W(b), y, c.d_model, slot0 * kRows, n * kRows, st); });
   }
 
   void cross(int slot0, int n, int layer) {
@@ -236,7 +264,7 @@ struct Runner {
     a.n_head = c.n_head;
     a.n_frames = c.n_frames;
     a.nsplit = L.nsplit;
-    Ops<S>::attn_cross(a, n, st);
+    launch("attn_cross", 2.0 * c.n_head * c.n_frames * kHeadDim * eb() * n, [&] { Ops<S>::attn_cross(a, n, st); });
   }
 
   // second half of a decoder block shared by target and drafter: cross-attention and MLP
@@ -264,12 +292,12 @@ struct Runner {
       GemvArgs a = gemv_base(slot0, n);
       a.x = xn; a.ldx = d; a.w = W(b.w_qkv); a.bias = W(b.b_qkv); a.K = d; a.N = 3 * d;
       a.y = qkv; a.ldy = 3 * d; a.cache = skv_layer(l); a.kv_stride = kv_stride();
-      Ops<S>::gemv(EPI_QKV, a, st);
+      launch("gemv", 3.0 * d * d * eb() + 3.0 * d * eb() + kRows * n * d * 4.0 * 4, [&] { Ops<S>::gemv(EPI_QKV, a, st); });
       AttnArgs at{};
       at.q = qkv; at.ldq = 3 * d; at.kcache = skv_layer(l); at.vcache = skv_layer(l) + kv_stride();
       at.state = I32(L.state); at.page_table = I32(L.page_table); at.rope = F32(L.rope); at.out = attn;
       at.slot0 = slot0; at.d = d; at.n_head = c.n_head; at.n_ctx = c.n_ctx; at.pages_per_slot = L.pages_per_slot;
-      Ops<S>::attn_self(at, n, st);
+      launch("attn_self", 0, [&] { Ops<S>::attn_self(at, n, st); });
       gemv(EPI_RESID, slot0, n, attn, d, b.w_o, b.b_o, d, d, h_, d);
       block_tail(slot0, n, b, l, tap);
     }
@@ -280,9 +308,12 @@ struct Runner {
     GemvArgs a = gemv_base(slot0, n);
     a.x = x; a.ldx = c.d_model; a.w = W(L.tok_emb); a.bias = nullptr; a.K = c.d_model; a.N = c.n_vocab;
     a.y = logits; a.ldy = c.n_vocab; a.hv = F32(L.hv); a.hi = I32(L.hi); a.nblk = L.head_blocks;
-    Ops<S>::gemv(EPI_ARGMAX, a, st);
-    argmax_final(F32(L.hv), I32(L.hi), L.head_blocks, slot0 * kRows, n * kRows, I32(L.g), F32(L.gmax),
-                 h->at<unsigned>(L.status), st);
+    launch("gemv", (double)c.n_vocab * c.d_model * eb() + kRows * n * c.d_model * 4.0 + kRows * n * L.head_blocks * 8.0,
+           [&] { Ops<S>::gemv(EPI_ARGMAX, a, st); });
+    launch("argmax_final", kRows * n * L.head_blocks * 8.0, [&] {
+      argmax_final(F32(L.hv), I32(L.hi), L.head_blocks, slot0 * kRows, n * kRows, I32(L.g), F32(L.gmax),
+                   h->at<unsigned>(L.status), st);
+    });
   }
 
   // drafter history for pending rows (Appendix A.2): taps -> W_h -> per-block LN, k (RoPE), v
@@ -297,7 +328,7 @@ struct Runner {
       HistArgs ha{};
       ha.kv = kvh; ha.kcache = hkv(dl, 0); ha.vcache = hkv(dl, 1); ha.state = I32(L.state); ha.rope = F32(L.rope);
       ha.slot0 = slot0; ha.d = d; ha.n_head = c.n_head; ha.n_ctx = c.n_ctx;
-      Ops<S>::hist_write(ha, n, st);
+      launch("hist_write", 0, [&] { Ops<S>::hist_write(ha, n, st); });
     }
   }
 
@@ -307,7 +338,7 @@ struct Runner {
     BeginArgs ba{};
     ba.state = I32(L.state); ba.emb = W(L.tok_emb); ba.pos = W(L.mask); ba.h = h_;
     ba.slot0 = slot0; ba.d = d; ba.n_vocab = c.n_vocab; ba.n_ctx = c.n_ctx; ba.block_k = c.block_k;
-    Ops<S>::draft_begin(ba, n, st);
+    launch("begin", 0, [&] { Ops<S>::draft_begin(ba, n, st); });
     for (int dl = 0; dl < c.n_draft_layer; ++dl) {
       const BlockW& b = L.db[dl];
       ln(slot0, n, h_, b.ln1_g, b.ln1_b, xn);
@@ -316,13 +347,13 @@ struct Runner {
       at.q = qkv; at.ldq = 3 * d; at.kcache = hkv(dl, 0); at.vcache = hkv(dl, 1);
       at.state = I32(L.state); at.rope = F32(L.rope); at.out = attn;
       at.slot0 = slot0; at.d = d; at.n_head = c.n_head; at.n_ctx = c.n_ctx;
-      Ops<S>::attn_draft(at, n, st);
+      launch("attn_draft", 0, [&] { Ops<S>::attn_draft(at, n, st); });
       gemv(EPI_RESID, slot0, n, attn, d, b.w_o, b.b_o, d, d, h_, d);
       block_tail(slot0, n, b, c.n_layer + dl, -1);
     }
     ln(slot0, n, h_, L.dlnf_g, L.dlnf_b, xn);
     head(slot0, n, xn, h->debug ? F32(L.dlogits) : nullptr);
-    draft_tokens(I32(L.g), dst, I32(L.draft), slot0, n, c.block_k, st);
+    launch("misc", 0, [&] { draft_tokens(I32(L.g), dst, I32(L.draft), slot0, n, c.block_k, st); });
   }
 
   void verify(int slot0, int n, const int* draft, int k_max, int* out, int* n_out, int* n_acc, int* done) {
@@ -330,19 +361,19 @@ struct Runner {
     ba.state = I32(L.state); ba.draft = draft; ba.tok = I32(L.tok); ba.emb = W(L.tok_emb); ba.pos = W(L.pos_emb);
     ba.h = F32(L.h); ba.slot0 = slot0; ba.d = c.d_model; ba.n_vocab = c.n_vocab; ba.n_ctx = c.n_ctx;
     ba.block_k = c.block_k; ba.k_max = k_max;
-    Ops<S>::verify_begin(ba, n, st);
+    launch("begin", 0, [&] { Ops<S>::verify_begin(ba, n, st); });
     target_forward(slot0, n);
     ln(slot0, n, F32(L.h), L.lnf_g, L.lnf_b, F32(L.xn));
     head(slot0, n, F32(L.xn), h->debug ? F32(L.logits) : nullptr);
     AcceptArgs aa{};
     aa.state = I32(L.state); aa.tok = I32(L.tok); aa.g = I32(L.g); aa.out = out; aa.n_out = n_out; aa.n_acc = n_acc;
     aa.done = done; aa.slot0 = slot0; aa.n = n; aa.block_k = c.block_k; aa.eos = c.eos_id; aa.n_ctx = c.n_ctx;
-    accept_greedy(aa, st);
+    launch("accept", 0, [&] { accept_greedy(aa, st); });
   }
 
   void draft(int slot0, int n, int* dst) {
     history_apply(slot0, n);
-    hist_done(I32(L.state), slot0, n, st);
+    launch("misc", 0, [&] { hist_done(I32(L.state), slot0, n, st); });
     drafter_forward(slot0, n, dst);
   }
 
@@ -593,7 +624,9 @@ int wf_step(wf_handle* hh, int slot0, int n, int k_max, const int32_t* ovr, int3
   auto it = h->graphs.find(key);
   if (it == h->graphs.end()) {
     HIPCK(h, hipStreamBeginCapture(st, hipStreamCaptureModeThreadLocal));
+    h->capturing = true;
     int r = step_enqueue(h, slot0, n, k_max, ovr, out, n_out, n_acc, done, st);
+    h->capturing = false;
     hipGraph_t g = nullptr;
     hipError_t e = hipStreamEndCapture(st, &g);
     if (r) { if (g) (void)hipGraphDestroy(g); return r; }
@@ -632,6 +665,48 @@ int wf_set_debug(wf_handle* hh, int enable) {
   return WF_OK;
 }
 
+int wf_profile_enable(wf_handle* hh, int enable) {
+  Handle* h = reinterpret_cast<Handle*>(hh);
+  if (!h) return fail(nullptr, WF_EINVAL, "null handle");
+  h->prof = enable != 0;
+  return WF_OK;
+}
+
+int wf_profile_summary(wf_handle* hh, char* buf, size_t len) {
+  Handle* h = reinterpret_cast<Handle*>(hh);
+  if (!h || !buf || len == 0) return fail(h, WF_EINVAL, "null argument");
+  struct Agg {
+    double ms = 0, bytes = 0;
+    long n = 0;
+  };
+  std::map<std::string, Agg> agg;
+  for (auto& r : h->prof_recs) {
+    HIPCK(h, hipEventSynchronize(r.b));
+    float ms = 0.f;
+    HIPCK(h, hipEventElapsedTime(&ms, r.a, r.b));
+    Agg& a = agg[r.tag];
+    a.ms += ms;
+    a.bytes += r.bytes;
+    a.n += 1;
+    h->ev_pool.push_back(r.a);
+    h->ev_pool.push_back(r.b);
+  }
+  h->prof_recs.clear();
+  std::string js = "{";
+  bool first = true;
+  for (auto& kv : agg) {
+    char item[256];
+    snprintf(item, sizeof(item), "%s\"%s\": {\"launches\": %ld, \"ms\": %.6f, \"bytes\": %.1f}", first ? "" : ", ",
+             kv.first.c_str(), kv.second.n, kv.second.ms, kv.second.bytes);
+    js += item;
+    first = false;
+  }
+  js += "}";
+  if (js.size() + 1 > len) return fail(h, WF_ESIZE, "summary buffer too small");
+  memcpy(buf, js.c_str(), js.size() + 1);
+  return WF_OK;
+}
+
 int wf_status(wf_handle* hh, uint32_t* flags, void* stream) {
   Handle* h = reinterpret_cast<Handle*>(hh);
   if (!h || !flags) return fail(h, WF_EINVAL, "null argument");
@@ -648,6 +723,8 @@ int wf_release(wf_handle* hh) {
   Handle* h = reinterpret_cast<Handle*>(hh);
   if (!h) return fail(nullptr, WF_EINVAL, "null handle");
   for (auto& kv : h->graphs) (void)hipGraphExecDestroy(kv.second);
+  for (auto& r : h->prof_recs) { (void)hipEventDestroy(r.a); (void)hipEventDestroy(r.b); }
+  for (auto e : h->ev_pool) (void)hipEventDestroy(e);
   delete h;
   return WF_OK;
 }

@@ -45,6 +45,12 @@ struct GraphKey {
   }
 };
 
+struct ProfRec {
+  const char* tag;
+  double bytes;
+  hipEvent_t a, b;
+};
+
 struct Handle {
   wf_config cfg;
   Layout lay;
@@ -57,6 +63,10 @@ struct Handle {
   std::string err;
   std::vector<int> live;  // host mirror: slot prefilled
   std::map<GraphKey, hipGraphExec_t> graphs;
+  bool prof = false;       // record events around eager launches
+  bool capturing = false;  // inside graph capture: never record events
+  std::vector<ProfRec> prof_recs;
+  std::vector<hipEvent_t> ev_pool;
 
   template <typename T>
   T* at(size_t off) const { return reinterpret_cast<T*>(ws + off); }
