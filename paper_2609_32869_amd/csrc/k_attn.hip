@@ -1,0 +1,366 @@
+// Attention kernels (gfx950): one block per (head, query row).
+//
+// A block owns one query row of one head and all of that row's keys, so no
+// partial results are merged across blocks.  Keys and values are read eight rows
+// at a time: lane l takes dims 8*(l%8)..+7 of key l/8, so one wave load is eight
+// consecutive 64-wide rows (1 KB of bf16).  Scores of all keys stay in LDS; the
+// softmax is exact (max, then sum) in fp32.  The nine row-blocks of a head are
+// numbered so they share blockIdx % 8 and therefore one XCD and its L2, which
+// serves the key/value rows to the other eight after the first reads them.
+#include "../../include/wf.h"
+#include "wf_operand.h"
+
+namespace wf {
+
+__device__ __forceinline__ bool head_row(int b, int H, int& head, int& row) {
+  const int x = b & 7, i = b >> 3;
+  head = x + 8 * (i / kRows);
+  row = i % kRows;
+  return head < H;
+}
+
+template <int NT>
+__device__ __forceinline__ float block_max(float v, float* red) {
+  v = wave_max(v);
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  __syncthreads();
+  if (lane == 0) red[w] = v;
+  __syncthreads();
+  float m = red[0];
+#pragma unroll
+  for (int i = 1; i < NT / 64; ++i) m = fmaxf(m, red[i]);
+  return m;
+}
+template <int NT>
+__device__ __forceinline__ float block_sum(float v, float* red) {
+  v = wave_sum(v);
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  __syncthreads();
+  if (lane == 0) red[w] = v;
+  __syncthreads();
+  float s = 0.f;
+#pragma unroll
+  for (int i = 0; i < NT / 64; ++i) s += red[i];
+  return s;
+}
+
+// sum over the 8 lanes of one key (lane bits 0..2)
+__device__ __forceinline__ float key_sum(float s) {
+  s += __shfl_xor(s, 1, 64);
+  s += __shfl_xor(s, 2, 64);
+  s += __shfl_xor(s, 4, 64);
+  return s;
+}
+
+// Eight consecutive storage elements of a key/value row, kept packed until used.
+template <typename S>
+struct Raw8;
+template <>
+struct Raw8<bf16> {
+  uint4 v;
+  __device__ __forceinline__ void load(const bf16* p) { v = *reinterpret_cast<const uint4*>(p); }
+  __device__ __forceinline__ void zero() { v = make_uint4(0u, 0u, 0u, 0u); }
+  __device__ __forceinline__ void unpack(float* o) const {
+    o[0] = __uint_as_float(v.x << 16); o[1] = __uint_as_float(v.x & 0xffff0000u);
+    o[2] = __uint_as_float(v.y << 16); o[3] = __uint_as_float(v.y & 0xffff0000u);
+    o[4] = __uint_as_float(v.z << 16); o[5] = __uint_as_float(v.z & 0xffff0000u);
+    o[6] = __uint_as_float(v.w << 16); o[7] = __uint_as_float(v.w & 0xffff0000u);
+  }
+};
+template <>
+struct Raw8<float> {
+  float4 a, b;
+  __device__ __forceinline__ void load(const float* p) {
+    a = *reinterpret_cast<const float4*>(p);
+    b = *reinterpret_cast<const float4*>(p + 4);
+  }
+  __device__ __forceinline__ void zero() { a = b = make_float4(0.f, 0.f, 0.f, 0.f); }
+  __device__ __forceinline__ void unpack(float* o) const {
+    o[0] = a.x; o[1] = a.y; o[2] = a.z; o[3] = a.w;
+    o[4] = b.x; o[5] = b.y; o[6] = b.z; o[7] = b.w;
+  }
+};
+
+// Scores of keys [0, nk) whose rows are at rowptr(j) (64 storage elements each,
+// eight consecutive keys contiguous) into sc[]; q8 = this lane's 8 query dims.
+// A wave issues the loads of B key octets before the first use.
+template <typename S, int NT, int B, typename RowPtr>
+__device__ __forceinline__ void score_pass(const float* q8, int nk, RowPtr rowptr, float* sc) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, g = lane & 7, kl = lane >> 3;
+  constexpr int NW = NT / 64;
+  const int noct = (nk + 7) >> 3;
+  for (int o0 = w; o0 < noct; o0 += NW * B) {
+    Raw8<S> kv[B];
+#pragma unroll
+    for (int b = 0; b < B; ++b) {
+      const int key = (o0 + NW * b) * 8 + kl;
+      if (key < nk) kv[b].load(rowptr(key) + 8 * g);
+      else kv[b].zero();
+    }
+#pragma unroll
+    for (int b = 0; b < B; ++b) {
+      float k8[8];
+      kv[b].unpack(k8);
+      float s = 0.f;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) s = fmaf(q8[e], k8[e], s);
+      s = key_sum(s);
+      const int key = (o0 + NW * b) * 8 + kl;
+      if (g == 0 && key < nk) sc[key] = s;
+    }
+  }
+}
+
+// acc[8] += p[key] * V[key][8g..8g+7] over keys [0, nk) (per-lane partials)
+template <typename S, int NT, int B, typename RowPtr>
+__device__ __forceinline__ void value_pass(float* acc, int nk, RowPtr rowptr, const float* p) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, g = lane & 7, kl = lane >> 3;
+  constexpr int NW = NT / 64;
+  const int noct = (nk + 7) >> 3;
+  for (int o0 = w; o0 < noct; o0 += NW * B) {
+    Raw8<S> vv[B];
+#pragma unroll
+    for (int b = 0; b < B; ++b) {
+      const int key = (o0 + NW * b) * 8 + kl;
+      if (key < nk) vv[b].load(rowptr(key) + 8 * g);
+      else vv[b].zero();
+    }
+#pragma unroll
+    for (int b = 0; b < B; ++b) {
+      const int key = (o0 + NW * b) * 8 + kl;
+      const float pk = key < nk ? p[key] : 0.f;
+      float v8[8];
+      vv[b].unpack(v8);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) acc[e] = fmaf(pk, v8[e], acc[e]);
+    }
+  }
+}
+
+// reduce acc over the 8 key lanes (bits 3..5) and the waves; returns the 64-wide
+// unnormalised output in part[0][*]
+template <int NT>
+__device__ __forceinline__ void reduce_out(float* acc, float (*part)[64]) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, g = lane & 7;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    acc[e] += __shfl_xor(acc[e], 8, 64);
+    acc[e] += __shfl_xor(acc[e], 16, 64);
+    acc[e] += __shfl_xor(acc[e], 32, 64);
+  }
+  if (lane < 8) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) part[w][8 * g + e] = acc[e];
+  }
+  __syncthreads();
+}
+
+// softmax in place over sc[0, nk): exp(s - max); returns the sum
+template <int NT>
+__device__ __forceinline__ float softmax_pass(float* sc, int nk, float* red) {
+  float m = -INFINITY;
+  for (int j = threadIdx.x; j < nk; j += NT) m = fmaxf(m, sc[j]);
+  m = block_max<NT>(m, red);
+  float l = 0.f;
+  for (int j = threadIdx.x; j < nk; j += NT) {
+    const float e = __expf(sc[j] - m);
+    sc[j] = e;
+    l += e;
+  }
+  return block_sum<NT>(l, red);
+}
+
+// ---------------------------------------------------------------- cross-attention
+// Query row i of slot s against all acoustic frames of one head (no mask).
+constexpr int kCrossThreads = 1024;
+template <typename S>
+constexpr int kCrossB = sizeof(S) == 2 ? 12 : 6;  // key octets in flight per wave
+template <typename S>
+__global__ void __launch_bounds__(kCrossThreads) k_attn_cross(CrossArgs a) {
+  constexpr int NT = kCrossThreads, NW = NT / 64;
+  __shared__ float sc[kMaxFrames];
+  __shared__ float part[NW][64];
+  __shared__ float red[NW];
+  int head, row;
+  if (!head_row(blockIdx.x, a.n_head, head, row)) return;
+  const int slot = a.slot0 + blockIdx.y;
+  const int lane = threadIdx.x & 63, g = lane & 7;
+  const float* qr = a.q + (size_t)(slot * kRows + row) * a.ldq + head * kHeadDim + 8 * g;
+  float q8[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) q8[e] = qr[e] * 0.125f;
+  const S* Kx = reinterpret_cast<const S*>(a.kv) + ((size_t)slot * 2 * a.n_head + head) * a.n_frames * kHeadDim;
+  const S* Vx = Kx + (size_t)a.n_head * a.n_frames * kHeadDim;
+  const int F = a.n_frames;
+  score_pass<S, NT, kCrossB<S>>(q8, F, [&](int j) { return Kx + (size_t)j * kHeadDim; }, sc);
+  __syncthreads();
+  const float L = softmax_pass<NT>(sc, F, red);
+  __syncthreads();
+  float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  value_pass<S, NT, kCrossB<S>>(acc, F, [&](int j) { return Vx + (size_t)j * kHeadDim; }, sc);
+  reduce_out<NT>(acc, part);
+  if (threadIdx.x < kHeadDim) {
+    float o = 0.f;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) o += part[w][threadIdx.x];
+    put_op<S>(a.out, a.nsplit, a.R9, slot * kRows + row, head * kHeadDim + threadIdx.x, o / L);
+  }
+}
+
+// ---------------------------------------------------------------- causal self-attention
+// Verify pass: row i < nv of slot s sits at position pos0 + i and attends to cached
+// positions 0..pos0 + i (Section 3.1: one causal pass).  Rows i >= nv are padding
+// and get zeros.
+constexpr int kSelfThreads = 256;
+template <typename S>
+__global__ void __launch_bounds__(kSelfThreads) k_attn_self(AttnArgs a) {
+  constexpr int NT = kSelfThreads, NW = NT / 64;
+  __shared__ float sc[kMaxCtx];
+  __shared__ float part[NW][64];
+  __shared__ float red[NW];
+  int head, row;
+  if (!head_row(blockIdx.x, a.n_head, head, row)) return;
+  const int slot = a.slot0 + blockIdx.y;
+  const int* st = a.state + slot * kStateInts;
+  const int pos0 = st[ST_POS0], nv = st[ST_NV];
+  if (row >= nv) {
+    if (threadIdx.x < kHeadDim) put_op<S>(a.out, a.nsplit, a.R9, slot * kRows + row, head * kHeadDim + threadIdx.x, 0.f);
+    return;
+  }
+  const int nk = pos0 + row + 1;
+  const int lane = threadIdx.x & 63, g = lane & 7;
+  const float* qr = a.q + (size_t)(slot * kRows + row) * a.ldq + head * kHeadDim + 8 * g;
+  float q8[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) q8[e] = qr[e] * 0.125f;
+  const S* Kc = reinterpret_cast<const S*>(a.kcache);
+  const S* Vc = reinterpret_cast<const S*>(a.vcache);
+  const int* pt = a.page_table + slot * a.pages_per_slot;
+  const int H = a.n_head;
+  auto krow = [&](int j) { return Kc + (((size_t)pt[j >> 4] * H + head) * kPage + (j & 15)) * kHeadDim; };
+  auto vrow = [&](int j) { return Vc + (((size_t)pt[j >> 4] * H + head) * kPage + (j & 15)) * kHeadDim; };
+  score_pass<S, NT, 14>(q8, nk, krow, sc);
+  __syncthreads();
+  const float L = softmax_pass<NT>(sc, nk, red);
+  __syncthreads();
+  float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  value_pass<S, NT, 14>(acc, nk, vrow, sc);
+  reduce_out<NT>(acc, part);
+  if (threadIdx.x < kHeadDim) {
+    const float o = (part[0][threadIdx.x] + part[1][threadIdx.x]) + (part[2][threadIdx.x] + part[3][threadIdx.x]);
+    put_op<S>(a.out, a.nsplit, a.R9, slot * kRows + row, head * kHeadDim + threadIdx.x, o / L);
+  }
+}
+
+// ---------------------------------------------------------------- drafter attention
+// Block row i (position t+i, t = anchor position) attends in one softmax to the
+// history keys at positions 0..t-1 and to all nine block keys (Section 3.2:
+// bidirectional inside the block).  The query and the block keys get RoPE here
+// (rotate-half, pairs (j, j+32)); history keys were stored with RoPE at their own
+// positions.
+template <typename S>
+__global__ void __launch_bounds__(kSelfThreads) k_attn_draft(AttnArgs a) {
+  constexpr int NT = kSelfThreads, NW = NT / 64;
+  __shared__ float sc[kMaxCtx + 16];
+  __shared__ float part[NW][64];
+  __shared__ float red[NW];
+  __shared__ float kb[kRows][kHeadDim];
+  __shared__ float vb[kRows][kHeadDim];
+  int head, row;
+  if (!head_row(blockIdx.x, a.n_head, head, row)) return;
+  const int slot = a.slot0 + blockIdx.y;
+  const int t0 = a.state[slot * kStateInts + ST_L];
+  const int d = a.d;
+  const int lane = threadIdx.x & 63, g = lane & 7;
+  // rotated block keys and their values
+  for (int t = threadIdx.x; t < kRows * 32; t += NT) {
+    const int jb = t >> 5, j = t & 31;
+    const int pos = t0 + jb;
+    const float c = a.rope[(pos * 32 + j) * 2], sn = a.rope[(pos * 32 + j) * 2 + 1];
+    const float* kr = a.q + (size_t)(slot * kRows + jb) * a.ldq + d + head * kHeadDim;
+    const float* vr = kr + d;
+    const float k1 = kr[j], k2 = kr[j + 32];
+    kb[jb][j] = k1 * c - k2 * sn;
+    kb[jb][j + 32] = k1 * sn + k2 * c;
+    vb[jb][j] = vr[j];
+    vb[jb][j + 32] = vr[j + 32];
+  }
+  // this lane's 8 rotated query dims
+  float q8[8];
+  {
+    const float* qr = a.q + (size_t)(slot * kRows + row) * a.ldq + head * kHeadDim;
+    const int pos = t0 + row;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int dim = 8 * g + e, j = dim & 31;
+      const float c = a.rope[(pos * 32 + j) * 2], sn = a.rope[(pos * 32 + j) * 2 + 1];
+      const float u1 = qr[j], u2 = qr[j + 32];
+      q8[e] = (dim < 32 ? u1 * c - u2 * sn : u1 * sn + u2 * c) * 0.125f;
+    }
+  }
+  const S* Kh = reinterpret_cast<const S*>(a.kcache) + ((size_t)slot * a.n_head + head) * a.n_ctx * kHeadDim;
+  const S* Vh = reinterpret_cast<const S*>(a.vcache) + ((size_t)slot * a.n_head + head) * a.n_ctx * kHeadDim;
+  score_pass<S, NT, 14>(q8, t0, [&](int j) { return Kh + (size_t)j * kHeadDim; }, sc);
+  __syncthreads();
+  // the nine block keys: one wave, lane (key kl, dims 8g..), keys 0..7 then key 8
+  if (threadIdx.x < 64) {
+    const int kl = lane >> 3;
+    for (int half = 0; half < 2; ++half) {
+      const int jb = half * 8 + kl;
+      float s = 0.f;
+      if (jb < kRows) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) s = fmaf(q8[e], kb[jb][8 * g + e], s);
+      }
+      s = key_sum(s);
+      if (g == 0 && jb < kRows) sc[t0 + jb] = s;
+    }
+  }
+  __syncthreads();
+  const int nk = t0 + kRows;
+  const float L = softmax_pass<NT>(sc, nk, red);
+  __syncthreads();
+  float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  value_pass<S, NT, 14>(acc, t0, [&](int j) { return Vh + (size_t)j * kHeadDim; }, sc);
+  if (threadIdx.x < 64) {
+    const int kl = lane >> 3;
+    for (int half = 0; half < 2; ++half) {
+      const int jb = half * 8 + kl;
+      if (jb < kRows) {
+        const float pk = sc[t0 + jb];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc[e] = fmaf(pk, vb[jb][8 * g + e], acc[e]);
+      }
+    }
+  }
+  reduce_out<NT>(acc, part);
+  if (threadIdx.x < kHeadDim) {
+    const float o = (part[0][threadIdx.x] + part[1][threadIdx.x]) + (part[2][threadIdx.x] + part[3][threadIdx.x]);
+    put_op<S>(a.out, a.nsplit, a.R9, slot * kRows + row, head * kHeadDim + threadIdx.x, o / L);
+  }
+}
+
+// ---------------------------------------------------------------- launchers
+static inline unsigned row_blocks(int H) { return (unsigned)(8 * ((H + 7) / 8) * kRows); }
+
+template <typename S>
+void Ops<S>::attn_self(const AttnArgs& a, int n, hipStream_t st) {
+  k_attn_self<S><<<dim3(row_blocks(a.n_head), n), kSelfThreads, 0, st>>>(a);
+}
+template <typename S>
+void Ops<S>::attn_draft(const AttnArgs& a, int n, hipStream_t st) {
+  k_attn_draft<S><<<dim3(row_blocks(a.n_head), n), kSelfThreads, 0, st>>>(a);
+}
+template <typename S>
+void Ops<S>::attn_cross(const CrossArgs& a, int n, hipStream_t st) {
+  k_attn_cross<S><<<dim3(row_blocks(a.n_head), n), kCrossThreads, 0, st>>>(a);
+}
+
+template void Ops<float>::attn_self(const AttnArgs&, int, hipStream_t);
+template void Ops<bf16>::attn_self(const AttnArgs&, int, hipStream_t);
+template void Ops<float>::attn_draft(const AttnArgs&, int, hipStream_t);
+template void Ops<bf16>::attn_draft(const AttnArgs&, int, hipStream_t);
+template void Ops<float>::attn_cross(const CrossArgs&, int, hipStream_t);
+template void Ops<bf16>::attn_cross(const CrossArgs&, int, hipStream_t);
+
+}  // namespace wf

@@ -1,0 +1,340 @@
+// Weight-streaming matrix products Y = X W^T for the 9 rows of each slot
+// (gfx950).  Every parameter byte is read once per pass; the activation operand
+// is tiny and stays in L2.
+//
+// bf16 storage: weights and operands are stored in matrix-core fragment order
+// (wf_common.h) so every wave load is 1 KB of contiguous memory.  Two shapes:
+//  * 16-column tiles, v_mfma_f32_16x16x32_bf16, two 16-row operand tiles per pass
+//    (narrow matrices: more tiles, more blocks);
+//  * 32-column tiles, v_mfma_f32_32x32x16_bf16, one 32-row operand tile per pass
+//    (wide matrices: half the operand traffic per weight byte).
+// A block streams one column tile; its waves split the k-steps and issue the loads
+// of up to U steps before the first matrix instruction that consumes them; the
+// wave partials are summed in LDS in a fixed order.
+//
+// fp32 storage (the small correctness configuration): row-major weights and
+// operand, v_mfma_f32_16x16x4f32.
+#include "../../include/wf.h"
+#include "wf_operand.h"
+
+namespace wf {
+
+constexpr int kU = 10;  // k-steps whose loads a wave issues together (16-wave blocks: 5)
+
+// ---------------------------------------------------------------- epilogue
+// sv holds the wave-summed tile: TM operand rows (split terms) x TC columns.
+template <typename S, int EPI, int TM, int TC, int NT>
+__device__ void finish_tile(const GemvArgs& a, float (*sv)[TC + 1], float (*ov)[TC], int m0, int nb) {
+  const bool split3 = a.nsplit == 3;
+  const int R = a.slot0 * kRows, Rend = (a.slot0 + a.nslots) * kRows;
+  const int nrows = split3 ? kRows : TM;
+  const S* bias = reinterpret_cast<const S*>(a.bias);
+  for (int idx = threadIdx.x; idx < nrows * TC; idx += NT) {
+    const int ml = idx / TC, c = idx % TC;
+    const int row = split3 ? ml : m0 + ml;
+    float v = split3 ? (sv[ml][c] + sv[ml + 9][c]) + sv[ml + 18][c] : sv[ml][c];
+    const int n = nb + c;
+    const bool act = row >= R && row < Rend && n < a.N;
+    if (act && bias != nullptr) v += to_f(bias[n]);
+    const int slot = row / kRows, r = row - slot * kRows;
+    if constexpr (EPI == EPI_STORE) {
+      if (act) a.y[(size_t)row * a.ldy + n] = v;
+    } else if constexpr (EPI == EPI_GELU) {
+      if (act) put_op<S>(a.aout, a.nsplit, a.R9, row, n, gelu_erf(v));
+    } else if constexpr (EPI == EPI_RESID) {
+      if (act) {
+        float* p = a.y + (size_t)row * a.ldy + n;
+        const float hn = *p + v;
+        *p = hn;
+        if (a.tap >= 0) put_op<S>(a.aout, a.nsplit, a.R9, row, a.tap * a.N + n, hn);
+      }
+    } else if constexpr (EPI == EPI_QKV) {
+      if (act) {
+        const int d = a.d;
+        if (n < d) {
+          a.y[(size_t)row * a.ldy + n] = v;
+        } else {
+          const int* st = a.state + slot * kStateInts;
+          const int nv = st[ST_NV], pos = st[ST_POS0] + r;
+          if (r < nv && pos < a.n_ctx) {
+            const int kv = n >= 2 * d;
+            const int cc = n - d - kv * d, head = cc >> 6, dim = cc & 63;
+            const int page = a.page_table[slot * a.pages_per_slot + (pos >> 4)];
+            S* cache = reinterpret_cast<S*>(a.cache) + (size_t)kv * a.kv_stride;
+            cache[(((size_t)page * a.n_head + head) * kPage + (pos & 15)) * kHeadDim + dim] = from_f<S>(v);
+          }
+        }
+      }
+    } else if constexpr (EPI == EPI_ARGMAX) {
+      if (act && a.y != nullptr) a.y[(size_t)row * a.ldy + n] = v;
+      ov[ml][c] = act ? v : -INFINITY;
+    }
+  }
+  if constexpr (EPI == EPI_ARGMAX) {
+    __syncthreads();
+    for (int ml = threadIdx.x; ml < nrows; ml += NT) {
+      const int row = split3 ? ml : m0 + ml;
+      if (row < R || row >= Rend) continue;
+      float bv = ov[ml][0];
+      int bi = nb;
+      for (int j = 1; j < TC; ++j) {
+        if (nb + j >= a.N) break;
+        if (better(ov[ml][j], nb + j, bv, bi)) { bv = ov[ml][j]; bi = nb + j; }
+      }
+      const size_t o = (size_t)row * a.nblk + blockIdx.x;
+      a.hv[o] = bv;
+      a.hi[o] = bi;
+    }
+  }
+}
+
+// ---------------------------------------------------------------- bf16, 16-column tiles
+template <int EPI, int NW>
+__global__ void __launch_bounds__(NW * 64) k_gemv16(GemvArgs a) {
+  constexpr int U = NW >= 16 ? kU / 2 : kU;
+  __shared__ float red[NW][32][17];
+  __shared__ float sv[32][17];
+  __shared__ float ov[32][16];
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const int col = lane & 15, kg = lane >> 4;
+  const int KS = a.K / 32;
+  const int spw = (KS + NW - 1) / NW;
+  const int s0 = min(KS, wv * spw), s1 = min(KS, s0 + spw);
+  const bf16x8* Wt = reinterpret_cast<const bf16x8*>(a.w) + (size_t)blockIdx.x * KS * 64 + lane;
+  const bf16x8* Ab = reinterpret_cast<const bf16x8*>(a.a.p) + lane;
+  const int MT = a.a.mt;
+  for (int tile0 = a.mt0; tile0 < a.mt1; tile0 += 2) {
+    const bool two = tile0 + 1 < a.mt1;
+    floatx4 acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
+    for (int st = s0; st < s1; st += U) {
+      bf16x8 bw[U], a0[U], a1[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int ss = min(st + u, s1 - 1);
+        bw[u] = Wt[(size_t)ss * 64];
+        a0[u] = Ab[((size_t)ss * MT + tile0) * 64];
+        if (two) a1[u] = Ab[((size_t)ss * MT + tile0 + 1) * 64];
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+        if (st + u < s1) {
+          acc0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0[u], bw[u], acc0, 0, 0, 0);
+          if (two) acc1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1[u], bw[u], acc1, 0, 0, 0);
+        }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      red[wv][kg * 4 + v][col] = acc0[v];
+      red[wv][16 + kg * 4 + v][col] = acc1[v];
+    }
+    __syncthreads();
+    for (int idx = threadIdx.x; idx < 32 * 16; idx += NW * 64) {
+      const int ml = idx >> 4, c = idx & 15;
+      float s = 0.f;
+#pragma unroll
+      for (int w = 0; w < NW; ++w) s += red[w][ml][c];
+      sv[ml][c] = s;
+    }
+    __syncthreads();
+    finish_tile<bf16, EPI, 32, 16, NW * 64>(a, sv, ov, tile0 * 16, blockIdx.x * 16);
+    if (a.nsplit == 3) break;
+  }
+}
+
+// ---------------------------------------------------------------- bf16, 32-column tiles
+template <int EPI, int NW>
+__global__ void __launch_bounds__(NW * 64) k_gemv32(GemvArgs a) {
+  constexpr int U = NW >= 16 ? kU / 2 : kU;
+  __shared__ float red[NW][32][33];
+  __shared__ float sv[32][33];
+  __shared__ float ov[32][32];
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const int col = lane & 31, kg = lane >> 5;
+  const int KS = a.K / 16;
+  const int spw = (KS + NW - 1) / NW;
+  const int s0 = min(KS, wv * spw), s1 = min(KS, s0 + spw);
+  const bf16x8* Wt = reinterpret_cast<const bf16x8*>(a.w) + (size_t)blockIdx.x * KS * 64 + lane;
+  const bf16x8* Ab = reinterpret_cast<const bf16x8*>(a.a.p) + lane;
+  const int MT = a.a.mt;
+  for (int tile0 = a.mt0; tile0 < a.mt1; ++tile0) {
+    floatx16 acc = {};
+    for (int st = s0; st < s1; st += U) {
+      bf16x8 bw[U], av[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int ss = min(st + u, s1 - 1);
+        bw[u] = Wt[(size_t)ss * 64];
+        av[u] = Ab[((size_t)ss * MT + tile0) * 64];
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+        if (st + u < s1) acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[u], bw[u], acc, 0, 0, 0);
+    }
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) red[wv][8 * i + 4 * kg + j][col] = acc[4 * i + j];
+    __syncthreads();
+    for (int idx = threadIdx.x; idx < 32 * 32; idx += NW * 64) {
+      const int ml = idx >> 5, c = idx & 31;
+      float s = 0.f;
+#pragma unroll
+      for (int w = 0; w < NW; ++w) s += red[w][ml][c];
+      sv[ml][c] = s;
+    }
+    __syncthreads();
+    finish_tile<bf16, EPI, 32, 32, NW * 64>(a, sv, ov, tile0 * 32, blockIdx.x * 32);
+    if (a.nsplit == 3) break;
+  }
+}
+
+// ---------------------------------------------------------------- fp32, row-major
+// Lane group kg supplies k = kg*4 + e at step e of each 16-wide slice (the sum over
+// k does not depend on the order in which k is visited).
+template <int EPI, int NW>
+__global__ void __launch_bounds__(NW * 64) k_gemv_f32(GemvArgs a) {
+  constexpr int U = NW >= 16 ? kU / 2 : kU;
+  __shared__ float red[NW][32][17];
+  __shared__ float sv[32][17];
+  __shared__ float ov[32][16];
+  const float* __restrict__ W = reinterpret_cast<const float*>(a.w);
+  const float* __restrict__ A = reinterpret_cast<const float*>(a.a.p);
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const int col = lane & 15, kg = lane >> 4;
+  const int nb = blockIdx.x * 16;
+  const int K = a.K, lda = a.a.ld;
+  const int KS = K / 16;
+  const int spw = (KS + NW - 1) / NW;
+  const int s0 = min(KS, wv * spw), s1 = min(KS, s0 + spw);
+  const float* wp = W + (size_t)min(nb + col, a.N - 1) * K + kg * 4;
+  for (int tile0 = a.mt0; tile0 < a.mt1; tile0 += 2) {
+    const bool two = tile0 + 1 < a.mt1;
+    const float* ap0 = A + (size_t)(tile0 * 16 + col) * lda + kg * 4;
+    const float* ap1 = ap0 + (size_t)16 * lda;
+    floatx4 acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
+    for (int st = s0; st < s1; st += U) {
+      float4 bw[U], a0[U], a1[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int k = min(st + u, s1 - 1) * 16;
+        bw[u] = *reinterpret_cast<const float4*>(wp + k);
+        a0[u] = *reinterpret_cast<const float4*>(ap0 + k);
+        if (two) a1[u] = *reinterpret_cast<const float4*>(ap1 + k);
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+        if (st + u < s1) {
+          acc0 = __builtin_amdgcn_mfma_f32_16x16x4f32(a0[u].x, bw[u].x, acc0, 0, 0, 0);
+          acc0 = __builtin_amdgcn_mfma_f32_16x16x4f32(a0[u].y, bw[u].y, acc0, 0, 0, 0);
+          acc0 = __builtin_amdgcn_mfma_f32_16x16x4f32(a0[u].z, bw[u].z, acc0, 0, 0, 0);
+          acc0 = __builtin_amdgcn_mfma_f32_16x16x4f32(a0[u].w, bw[u].w, acc0, 0, 0, 0);
+          if (two) {
+            acc1 = __builtin_amdgcn_mfma_f32_16x16x4f32(a1[u].x, bw[u].x, acc1, 0, 0, 0);
+            acc1 = __builtin_amdgcn_mfma_f32_16x16x4f32(a1[u].y, bw[u].y, acc1, 0, 0, 0);
+            acc1 = __builtin_amdgcn_mfma_f32_16x16x4f32(a1[u].z, bw[u].z, acc1, 0, 0, 0);
+            acc1 = __builtin_amdgcn_mfma_f32_16x16x4f32(a1[u].w, bw[u].w, acc1, 0, 0, 0);
+          }
+        }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      red[wv][kg * 4 + v][col] = acc0[v];
+      red[wv][16 + kg * 4 + v][col] = acc1[v];
+    }
+    __syncthreads();
+    for (int idx = threadIdx.x; idx < 32 * 16; idx += NW * 64) {
+      const int ml = idx >> 4, c = idx & 15;
+      float s = 0.f;
+#pragma unroll
+      for (int w = 0; w < NW; ++w) s += red[w][ml][c];
+      sv[ml][c] = s;
+    }
+    __syncthreads();
+    finish_tile<float, EPI, 32, 16, NW * 64>(a, sv, ov, tile0 * 16, nb);
+  }
+}
+
+// ---------------------------------------------------------------- weight repack
+// Row-major [N][K] bf16 -> fragment order; columns beyond N are zero.
+__global__ void __launch_bounds__(256) k_repack(const bf16* __restrict__ src, bf16* __restrict__ dst, int N, int K,
+                                                int kind, size_t chunks) {
+  const size_t c = (size_t)blockIdx.x * 256 + threadIdx.x;
+  if (c >= chunks) return;
+  const int lane = (int)(c & 63);
+  size_t rest = c >> 6;
+  int n, k;
+  if (kind == W_F16) {
+    const int KS = K / 32;
+    const int ks = (int)(rest % KS), tile = (int)(rest / KS);
+    n = tile * 16 + (lane & 15);
+    k = ks * 32 + 8 * (lane >> 4);
+  } else {
+    const int KS = K / 16;
+    const int ks = (int)(rest % KS), tile = (int)(rest / KS);
+    n = tile * 32 + (lane & 31);
+    k = ks * 16 + 8 * (lane >> 5);
+  }
+  uint4 v = make_uint4(0u, 0u, 0u, 0u);
+  if (n < N) v = *reinterpret_cast<const uint4*>(src + (size_t)n * K + k);
+  *reinterpret_cast<uint4*>(dst + c * 8) = v;
+}
+
+// ---------------------------------------------------------------- launchers
+template <int EPI, int NW>
+static void launch_bf16(const GemvArgs& a, hipStream_t st) {
+  if (a.wkind == W_F32) {
+    k_gemv32<EPI, NW><<<(a.N + 31) / 32, NW * 64, 0, st>>>(a);
+  } else {
+    k_gemv16<EPI, NW><<<(a.N + 15) / 16, NW * 64, 0, st>>>(a);
+  }
+}
+template <int EPI, int NW>
+static void launch_f32(const GemvArgs& a, hipStream_t st) {
+  k_gemv_f32<EPI, NW><<<(a.N + 15) / 16, NW * 64, 0, st>>>(a);
+}
+
+template <typename S, int EPI>
+static void launch_epi(const GemvArgs& a, hipStream_t st) {
+  // waves per block: enough that each wave's share of the k-steps fits one batch
+  const int kstep = sizeof(S) == 4 ? 16 : (a.wkind == W_F32 ? 16 : 32);
+  const int steps = a.K / kstep;
+  if constexpr (sizeof(S) == 4) {
+    if (steps <= 4 * kU) launch_f32<EPI, 4>(a, st);
+    else if (steps <= 8 * kU) launch_f32<EPI, 8>(a, st);
+    else launch_f32<EPI, 16>(a, st);
+  } else {
+    if (steps <= 4 * kU) launch_bf16<EPI, 4>(a, st);
+    else if (steps <= 8 * kU) launch_bf16<EPI, 8>(a, st);
+    else launch_bf16<EPI, 16>(a, st);
+  }
+}
+
+template <typename S>
+void Ops<S>::gemv(int epi, const GemvArgs& a, hipStream_t st) {
+  switch (epi) {
+    case EPI_STORE: launch_epi<S, EPI_STORE>(a, st); break;
+    case EPI_GELU: launch_epi<S, EPI_GELU>(a, st); break;
+    case EPI_RESID: launch_epi<S, EPI_RESID>(a, st); break;
+    case EPI_QKV: launch_epi<S, EPI_QKV>(a, st); break;
+    case EPI_ARGMAX: launch_epi<S, EPI_ARGMAX>(a, st); break;
+  }
+}
+
+template <>
+void repack<bf16>(const void* src, void* dst, int N, int K, int wkind, hipStream_t st) {
+  const int tile = wkind == W_F32 ? 32 : 16;
+  const size_t npad = (size_t)(N + tile - 1) / tile * tile;
+  const size_t chunks = npad * K / 8;
+  k_repack<<<(unsigned)((chunks + 255) / 256), 256, 0, st>>>(reinterpret_cast<const bf16*>(src),
+                                                                reinterpret_cast<bf16*>(dst), N, K, wkind, chunks);
+}
+template <>
+void repack<float>(const void*, void*, int, int, int, hipStream_t) {}
+
+template void Ops<float>::gemv(int, const GemvArgs&, hipStream_t);
+template void Ops<bf16>::gemv(int, const GemvArgs&, hipStream_t);
+
+}  // namespace wf

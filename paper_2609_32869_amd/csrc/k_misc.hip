@@ -1,0 +1,414 @@
+// Small kernels of the draft-and-verify step (gfx950, wave64): LayerNorm into a
+// matrix operand, pass set-up, argmax, acceptance, drafter-history write and the
+// encode-time cross K/V product.
+//
+// Rows: a pass over slot s uses activation rows s*9 + i, i = 0..8 (anchor plus
+// eight candidates, or eight masks for the drafter).  Every kernel computes a
+// row's result the same way however many rows or slots share the launch, so a
+// token's logits never depend on the batch composition.
+#include "../../include/wf.h"
+#include "wf_operand.h"
+
+namespace wf {
+
+// ---------------------------------------------------------------- LayerNorm -> operand
+// y = g * (x - mean) / sqrt(var + 1e-5) + b over the d columns of a row (Whisper's
+// pre-LN blocks and final LN), written as the operand of the next product.  One
+// block of 256 threads per row; the row stays in registers (d <= 2048).
+template <typename S>
+__global__ void __launch_bounds__(256) k_ln_operand(LnArgs a) {
+  __shared__ float red[8];
+  const int row = a.row0 + blockIdx.x;
+  const float* xr = a.x + (size_t)row * a.d;
+  const S* g = reinterpret_cast<const S*>(a.g);
+  const S* b = reinterpret_cast<const S*>(a.b);
+  float v[8];
+  float s = 0.f;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const int i = threadIdx.x + j * 256;
+    v[j] = i < a.d ? xr[i] : 0.f;
+    s += v[j];
+  }
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  s = wave_sum(s);
+  if (lane == 0) red[w] = s;
+  __syncthreads();
+  const float mean = ((red[0] + red[1]) + (red[2] + red[3])) / (float)a.d;
+  float q = 0.f;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const int i = threadIdx.x + j * 256;
+    const float c = v[j] - mean;
+    q += i < a.d ? c * c : 0.f;
+  }
+  q = wave_sum(q);
+  if (lane == 0) red[4 + w] = q;
+  __syncthreads();
+  const float var = ((red[4] + red[5]) + (red[6] + red[7])) / (float)a.d;
+  const float inv = 1.0f / sqrtf(var + 1e-5f);
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const int i = threadIdx.x + j * 256;
+    if (i < a.d) put_op<S>(a.out, a.nsplit, a.R9, row, i, (v[j] - mean) * inv * to_f(g[i]) + to_f(b[i]));
+  }
+}
+
+// ---------------------------------------------------------------- streamed matrix-core GEMV
+// Y[row, n] = sum_k X[row, k] W[n, k] for the 9 rows of each slot of the batch.
+// Block = 4 waves and 16 output columns; wave w takes a contiguous quarter of K.
+// Lane (col = lane % 16, kg = lane / 16) streams 16-byte chunks of weight row
+// n0 + col (8 per round in flight) as the B operand of v_mfma_f32_16x16x32_bf16
+
+// final argmax over the per-block partials of each row; flags non-finite maxima
+__global__ void __launch_bounds__(256) k_argmax_final(const float* __restrict__ hv, const int* __restrict__ hi,
+                                                      int nblk, int row0, int* __restrict__ g,
+                                                      float* __restrict__ gmax, unsigned* status) {
+  __shared__ float bvs[4];
+  __shared__ int bis[4];
+  const int row = row0 + blockIdx.x;
+  float bv = -INFINITY;
+  int bi = 0x7fffffff;
+  for (int j = threadIdx.x; j < nblk; j += 256) {
+    float v = hv[(size_t)row * nblk + j];
+    int i = hi[(size_t)row * nblk + j];
+    if (better(v, i, bv, bi)) { bv = v; bi = i; }
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    float ov = __shfl_xor(bv, o, 64);
+    int oi = __shfl_xor(bi, o, 64);
+    if (better(ov, oi, bv, bi)) { bv = ov; bi = oi; }
+  }
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  if (lane == 0) { bvs[w] = bv; bis[w] = bi; }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    for (int j = 1; j < 4; ++j)
+      if (better(bvs[j], bis[j], bvs[0], bis[0])) { bvs[0] = bvs[j]; bis[0] = bis[j]; }
+    g[row] = bis[0];
+    gmax[row] = bvs[0];
+    if (!isfinite(bvs[0])) atomicOr(status, WF_STATUS_NONFINITE_LOGITS);
+  }
+}
+
+// ---------------------------------------------------------------- attention helpers
+
+// Row `tok`, column c of the token embedding, stored in the order the vocabulary
+// head streams it (32-column fragment order for bf16, row-major for fp32).
+template <typename S>
+__device__ __forceinline__ float emb_at(const BeginArgs& a, int tok, int c) {
+  const S* E = reinterpret_cast<const S*>(a.emb);
+  if (a.emb_kind == W_F32) return to_f(E[wfrag32_index(tok, c, a.d / 16)]);
+  return to_f(E[(size_t)tok * a.d + c]);
+}
+
+// ---------------------------------------------------------------- pass set-up
+// Verify rows: [anchor, c_1..c_k] at positions L..L+k with the budget rule
+// k = min(K, k_max, max_new - emitted - 1, n_ctx - L - 1) (Appendix A.1).
+template <typename S>
+__global__ void __launch_bounds__(256) k_verify_begin(BeginArgs a) {
+  __shared__ int toks[kRows];
+  __shared__ int pos0s, nvs;
+  const int slot = a.slot0 + blockIdx.x;
+  int* st = a.state + slot * kStateInts;
+  if (threadIdx.x == 0) {
+    const int L = st[ST_L], left = st[ST_MAX_NEW] - st[ST_EMITTED];
+    int nv = 0;
+    if (st[ST_LIVE] && !st[ST_DONE] && left > 0 && L < a.n_ctx) {
+      int k = min(min(a.block_k, a.k_max), min(left - 1, a.n_ctx - L - 1));
+      nv = k + 1;
+    }
+    st[ST_POS0] = L;
+    st[ST_NV] = nv;
+    pos0s = L;
+    nvs = nv;
+    const int anchor = st[ST_ANCHOR];
+    for (int i = 0; i < kRows; ++i) {
+      int t = (i == 0 || i >= nv) ? anchor : a.draft[(size_t)blockIdx.x * a.block_k + i - 1];
+      t = min(max(t, 0), a.n_vocab - 1);
+      toks[i] = t;
+      a.tok[slot * kRows + i] = t;
+    }
+  }
+  __syncthreads();
+  const S* P = reinterpret_cast<const S*>(a.pos);
+  for (int i = 0; i < kRows; ++i) {
+    const int p = min(pos0s + i, a.n_ctx - 1);
+    float* hr = a.h + (size_t)(slot * kRows + i) * a.d;
+    for (int c = threadIdx.x; c < a.d; c += 256) hr[c] = emb_at<S>(a, toks[i], c) + to_f(P[(size_t)p * a.d + c]);
+  }
+}
+
+// Draft block X_t = [Emb(y_t), m, ..., m] (Eq. 2).
+template <typename S>
+__global__ void __launch_bounds__(256) k_draft_begin(BeginArgs a) {
+  const int slot = a.slot0 + blockIdx.x;
+  const int* st = a.state + slot * kStateInts;
+  const int anchor = min(max(st[ST_ANCHOR], 0), a.n_vocab - 1);
+  const S* m = reinterpret_cast<const S*>(a.pos);
+  for (int i = 0; i < kRows; ++i) {
+    float* hr = a.h + (size_t)(slot * kRows + i) * a.d;
+    for (int c = threadIdx.x; c < a.d; c += 256) hr[c] = (i == 0) ? emb_at<S>(a, anchor, c) : to_f(m[c]);
+  }
+}
+
+// Prefill chunk c: prompt positions 9c..9c+8 of each slot.
+template <typename S>
+__global__ void __launch_bounds__(256) k_prefill_begin(BeginArgs a) {
+  __shared__ int toks[kRows];
+  __shared__ int pos0s;
+  const int slot = a.slot0 + blockIdx.x;
+  int* st = a.state + slot * kStateInts;
+  if (threadIdx.x == 0) {
+    const int len = st[ST_LEN];
+    const int pos0 = a.chunk * kRows;
+    const int nv = max(0, min(kRows, len - pos0));
+    st[ST_POS0] = pos0;
+    st[ST_NV] = nv;
+    st[ST_HPOS] = pos0;
+    st[ST_HN] = nv;
+    pos0s = pos0;
+    for (int i = 0; i < kRows; ++i) {
+      int t = (i < nv) ? a.draft[(size_t)blockIdx.x * a.pmax + pos0 + i] : 0;
+      t = min(max(t, 0), a.n_vocab - 1);
+      toks[i] = t;
+      a.tok[slot * kRows + i] = t;
+    }
+  }
+  __syncthreads();
+  const S* P = reinterpret_cast<const S*>(a.pos);
+  for (int i = 0; i < kRows; ++i) {
+    const int p = min(pos0s + i, a.n_ctx - 1);
+    float* hr = a.h + (size_t)(slot * kRows + i) * a.d;
+    for (int c = threadIdx.x; c < a.d; c += 256) hr[c] = emb_at<S>(a, toks[i], c) + to_f(P[(size_t)p * a.d + c]);
+  }
+}
+
+// keep the final hidden row of each slot's last prompt position (row 0 of lasth)
+__global__ void __launch_bounds__(256) k_save_last(const float* __restrict__ h, float* __restrict__ lasth,
+                                                   const int* __restrict__ state, int slot0, int d, int chunk) {
+  const int slot = slot0 + blockIdx.x;
+  const int len = state[slot * kStateInts + ST_LEN];
+  const int last = len - 1;
+  if (last / kRows != chunk) return;
+  const int r = last % kRows;
+  for (int c = threadIdx.x; c < d; c += 256)
+    lasth[(size_t)slot * kRows * d + c] = h[(size_t)(slot * kRows + r) * d + c];
+}
+
+// first anchor from the argmax of the last prompt row
+__global__ void k_prefill_finish(int* __restrict__ state, const int* __restrict__ g, int slot0, int n, int eos,
+                                 int n_ctx, int* __restrict__ first) {
+  const int s = blockIdx.x * blockDim.x + threadIdx.x;
+  if (s >= n) return;
+  const int slot = slot0 + s;
+  int* st = state + slot * kStateInts;
+  const int tok = g[slot * kRows];
+  st[ST_ANCHOR] = tok;
+  st[ST_L] = st[ST_LEN];
+  st[ST_EMITTED] = 1;
+  st[ST_STEP] = 0;
+  st[ST_HN] = 0;
+  st[ST_DONE] = (tok == eos) || st[ST_MAX_NEW] <= 1 || st[ST_LEN] >= n_ctx;
+  st[ST_LIVE] = 1;
+  if (first) first[s] = tok;
+}
+
+// ---------------------------------------------------------------- history update
+// Write the drafter history of pending rows: k gets RoPE at its own position, both
+// k and v are rounded to the storage type (Appendix A.2).
+template <typename S>
+__global__ void __launch_bounds__(256) k_hist_write(HistArgs a) {
+  const int slot = a.slot0 + blockIdx.y, r = blockIdx.x;
+  const int* st = a.state + slot * kStateInts;
+  const int hn = st[ST_HN], pos = st[ST_HPOS] + r;
+  if (r >= hn || pos >= a.n_ctx) return;
+  const float* kr = a.kv + (size_t)(slot * kRows + r) * 2 * a.d;
+  const float* vr = kr + a.d;
+  S* Kh = reinterpret_cast<S*>(a.kcache);
+  S* Vh = reinterpret_cast<S*>(a.vcache);
+  for (int t = threadIdx.x; t < a.n_head * 32; t += 256) {
+    const int head = t >> 5, j = t & 31;
+    const float c = a.rope[(pos * 32 + j) * 2], sn = a.rope[(pos * 32 + j) * 2 + 1];
+    const float k1 = kr[head * kHeadDim + j], k2 = kr[head * kHeadDim + j + 32];
+    const size_t base = (((size_t)slot * a.n_head + head) * a.n_ctx + pos) * kHeadDim;
+    Kh[base + j] = from_f<S>(k1 * c - k2 * sn);
+    Kh[base + j + 32] = from_f<S>(k1 * sn + k2 * c);
+    Vh[base + j] = from_f<S>(vr[head * kHeadDim + j]);
+    Vh[base + j + 32] = from_f<S>(vr[head * kHeadDim + j + 32]);
+  }
+}
+
+__global__ void k_hist_done(int* state, int slot0, int n) {
+  const int s = blockIdx.x * blockDim.x + threadIdx.x;
+  if (s < n) state[(slot0 + s) * kStateInts + ST_HN] = 0;
+}
+
+// ---------------------------------------------------------------- acceptance
+// Greedy longest-prefix rule (Section 3.1) with the end-of-transcript rule and
+// the cache/anchor update of Appendix A.1.  One thread per slot.
+__global__ void k_accept_greedy(AcceptArgs a) {
+  const int s = blockIdx.x * blockDim.x + threadIdx.x;
+  if (s >= a.n) return;
+  const int slot = a.slot0 + s;
+  int* st = a.state + slot * kStateInts;
+  const int nv = st[ST_NV];
+  const int K = a.block_k;
+  int* out = a.out ? a.out + (size_t)s * (K + 1) : nullptr;
+  if (nv == 0) {
+    if (a.n_out) a.n_out[s] = 0;
+    if (a.n_acc) a.n_acc[s] = 0;
+    if (a.done) a.done[s] = st[ST_LIVE] ? 1 : 0;
+    if (st[ST_LIVE]) st[ST_DONE] = 1;
+    return;
+  }
+  const int k = nv - 1;
+  const int* tok = a.tok + slot * kRows;
+  const int* g = a.g + slot * kRows;
+  int acc = 0;
+  while (acc < k && tok[acc + 1] == g[acc]) ++acc;
+  int nemit = 0;
+  bool fin = false;
+  for (int e = 0; e < acc; ++e) {
+    const int c = tok[e + 1];
+    if (out) out[nemit] = c;
+    ++nemit;
+    if (c == a.eos) { fin = true; break; }
+  }
+  int last;
+  if (!fin) {
+    last = g[acc];
+    if (out) out[nemit] = last;
+    ++nemit;
+    fin = (last == a.eos);
+  } else {
+    last = tok[nemit];
+    acc = nemit;
+  }
+  const int L = st[ST_L];
+  st[ST_HPOS] = L;
+  st[ST_HN] = nv;
+  st[ST_L] = L + 1 + acc;
+  st[ST_ANCHOR] = last;
+  st[ST_EMITTED] += nemit;
+  st[ST_STEP] += 1;
+  st[ST_K] = k;
+  st[ST_A] = acc;
+  const bool done = fin || st[ST_EMITTED] >= st[ST_MAX_NEW] || st[ST_L] >= a.n_ctx;
+  st[ST_DONE] = done;
+  if (out)
+    for (int j = nemit; j <= K; ++j) out[j] = -1;
+  if (a.n_out) a.n_out[s] = nemit;
+  if (a.n_acc) a.n_acc[s] = acc;
+  if (a.done) a.done[s] = done;
+}
+
+// drafted tokens = argmax of mask rows 1..K
+__global__ void k_draft_tokens(const int* __restrict__ g, int* __restrict__ dst, int* __restrict__ keep, int slot0,
+                               int n, int K) {
+  const int t = blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= n * K) return;
+  const int s = t / K, j = t % K;
+  const int v = g[(slot0 + s) * kRows + 1 + j];
+  if (dst) dst[t] = v;
+  keep[(size_t)(slot0 + s) * K + j] = v;
+}
+
+// ---------------------------------------------------------------- encode: cross K/V
+// C[f, n] = sum_k A[f, k] W[n, k] + b[n] for the 2d key/value columns of one
+// block, written to the per-head frame-major cross cache.  64x64 tiles, fp32
+// accumulation.
+template <typename S>
+__global__ void __launch_bounds__(256) k_gemm_xkv(XkvArgs a) {
+  __shared__ float As[16][64 + 4];
+  __shared__ float Bs[16][64 + 4];
+  const S* A = reinterpret_cast<const S*>(a.mem);
+  const S* W = reinterpret_cast<const S*>(a.w);
+  const S* bias = reinterpret_cast<const S*>(a.bias);
+  const int m0 = blockIdx.x * 64, n0 = blockIdx.y * 64;
+  const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
+  const int K = a.d, M = a.n_frames, N = 2 * a.d;
+  float acc[4][4] = {};
+  for (int k0 = 0; k0 < K; k0 += 16) {
+    for (int t = threadIdx.x; t < 64 * 16; t += 256) {
+      const int mm = t >> 4, kk = t & 15;
+      As[kk][mm] = (m0 + mm < M) ? to_f(A[(size_t)(m0 + mm) * K + k0 + kk]) : 0.f;
+      Bs[kk][mm] = to_f(W[(size_t)(n0 + mm) * K + k0 + kk]);
+    }
+    __syncthreads();
+#pragma unroll
+    for (int kk = 0; kk < 16; ++kk) {
+      float av[4], bv[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) av[i] = As[kk][ty * 4 + i];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) bv[j] = Bs[kk][tx * 4 + j];
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = fmaf(av[i], bv[j], acc[i][j]);
+    }
+    __syncthreads();
+  }
+  S* out = reinterpret_cast<S*>(a.out);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int f = m0 + ty * 4 + i;
+    if (f >= M) continue;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int n = n0 + tx * 4 + j;
+      const int kv = n >= a.d, col = n - kv * a.d, head = col >> 6, dim = col & 63;
+      const float v = acc[i][j] + to_f(bias[n]);
+      out[(((size_t)kv * a.n_head + head) * M + f) * kHeadDim + dim] = from_f<S>(v);
+    }
+  }
+}
+
+
+// ---------------------------------------------------------------- launchers
+template <typename S>
+void Ops<S>::ln_operand(const LnArgs& a, int rows, hipStream_t st) {
+  k_ln_operand<S><<<rows, 256, 0, st>>>(a);
+}
+template <typename S>
+void Ops<S>::verify_begin(const BeginArgs& a, int n, hipStream_t st) { k_verify_begin<S><<<n, 256, 0, st>>>(a); }
+template <typename S>
+void Ops<S>::draft_begin(const BeginArgs& a, int n, hipStream_t st) { k_draft_begin<S><<<n, 256, 0, st>>>(a); }
+template <typename S>
+void Ops<S>::prefill_begin(const BeginArgs& a, int n, hipStream_t st) { k_prefill_begin<S><<<n, 256, 0, st>>>(a); }
+template <typename S>
+void Ops<S>::hist_write(const HistArgs& a, int n, hipStream_t st) { k_hist_write<S><<<dim3(kRows, n), 256, 0, st>>>(a); }
+template <typename S>
+void Ops<S>::gemm_xkv(const XkvArgs& a, hipStream_t st) {
+  k_gemm_xkv<S><<<dim3((a.n_frames + 63) / 64, 2 * a.d / 64), 256, 0, st>>>(a);
+}
+
+void argmax_final(const float* hv, const int* hi, int nblk, int row0, int rows, int* g, float* gmax,
+                  unsigned* status, hipStream_t st) {
+  k_argmax_final<<<rows, 256, 0, st>>>(hv, hi, nblk, row0, g, gmax, status);
+}
+void save_last(const float* h, float* lasth, const int* state, int slot0, int n, int d, int chunk, hipStream_t st) {
+  k_save_last<<<n, 256, 0, st>>>(h, lasth, state, slot0, d, chunk);
+}
+void prefill_finish(int* state, const int* g, int slot0, int n, int eos, int n_ctx, int* first, hipStream_t st) {
+  k_prefill_finish<<<(n + 63) / 64, 64, 0, st>>>(state, g, slot0, n, eos, n_ctx, first);
+}
+void hist_done(int* state, int slot0, int n, hipStream_t st) { k_hist_done<<<(n + 63) / 64, 64, 0, st>>>(state, slot0, n); }
+void accept_greedy(const AcceptArgs& a, hipStream_t st) { k_accept_greedy<<<(a.n + 63) / 64, 64, 0, st>>>(a); }
+void draft_tokens(const int* g, int* dst, int* keep, int slot0, int n, int K, hipStream_t st) {
+  k_draft_tokens<<<(n * K + 255) / 256, 256, 0, st>>>(g, dst, keep, slot0, n, K);
+}
+
+#define WF_MISC_INST(S)                                                     \
+  template void Ops<S>::ln_operand(const LnArgs&, int, hipStream_t);        \
+  template void Ops<S>::verify_begin(const BeginArgs&, int, hipStream_t);   \
+  template void Ops<S>::draft_begin(const BeginArgs&, int, hipStream_t);    \
+  template void Ops<S>::prefill_begin(const BeginArgs&, int, hipStream_t);  \
+  template void Ops<S>::hist_write(const HistArgs&, int, hipStream_t);      \
+  template void Ops<S>::gemm_xkv(const XkvArgs&, hipStream_t);
+WF_MISC_INST(float)
+WF_MISC_INST(bf16)
+
+}  // namespace wf

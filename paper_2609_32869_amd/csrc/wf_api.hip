@@ -39,10 +39,10 @@ int check_config(const wf_config* c, std::string& why) {
   if (c->dtype != WF_F32 && c->dtype != WF_BF16) { why = "dtype must be WF_F32 or WF_BF16"; return WF_EINVAL; }
   if (c->n_head <= 0 || c->d_model != c->n_head * kHeadDim) { why = "head width must be 64"; return WF_EINVAL; }
   if (c->n_layer <= 0 || c->n_draft_layer <= 0) { why = "layer counts must be positive"; return WF_EINVAL; }
-  if (c->d_ff <= 0 || c->d_ff % 16) { why = "d_ff must be a positive multiple of 16"; return WF_EINVAL; }
+  if (c->d_ff <= 0 || c->d_ff % 32) { why = "d_ff must be a positive multiple of 32"; return WF_EINVAL; }
   if (c->n_vocab < 2) { why = "n_vocab must be >= 2"; return WF_EINVAL; }
   if (c->n_ctx < 16 || c->n_ctx > kMaxCtx || c->n_ctx % kPage) { why = "n_ctx must be a multiple of 16 in [16, 448]"; return WF_EINVAL; }
-  if (c->n_frames < 1) { why = "n_frames must be positive"; return WF_EINVAL; }
+  if (c->n_frames < 1 || c->n_frames > kMaxFrames) { why = "n_frames must be in [1, 2048]"; return WF_EINVAL; }
   if (c->block_k != kRows - 1) { why = "block_k must be 8"; return WF_EINVAL; }
   if (c->n_tap < 1 || c->n_tap > WF_MAX_TAPS) { why = "n_tap must be in [1, 8]"; return WF_EINVAL; }
   for (int i = 0; i < c->n_tap; ++i) {
@@ -56,36 +56,58 @@ int check_config(const wf_config* c, std::string& why) {
   return WF_OK;
 }
 
-// manifest entry -> (numel, destination element offset in the weight region)
+// manifest entry -> (numel, destination element offset in the weight region, the
+// streamed matrix it belongs to or -1)
 struct ManEntry {
   size_t numel, dst;
+  int mat;
 };
 
-std::vector<ManEntry> manifest(const wf_config& c, const Layout& L) {
+// A streamed weight matrix [N][K]: with bf16 storage it is kept in matrix-core
+// fragment order (kind W_F16 or W_F32); entries of the manifest that make it up
+// are consecutive and hold consecutive row ranges.
+struct Mat {
+  size_t dst;
+  int N, K, kind;
+};
+
+std::vector<ManEntry> manifest(const wf_config& c, const Layout& L, std::vector<Mat>* mats = nullptr) {
   const size_t d = c.d_model, F = c.d_ff;
+  const bool frag = c.dtype == WF_BF16;
   std::vector<ManEntry> m;
-  m.push_back({(size_t)c.n_vocab * d, L.tok_emb});
-  m.push_back({(size_t)c.n_ctx * d, L.pos_emb});
+  std::vector<Mat> mm;
+  // start a streamed matrix (bf16 storage only); returns its index for the entries
+  auto mat = [&](size_t dst, size_t N, size_t K, int kind) {
+    if (!frag) return -1;
+    mm.push_back({dst, (int)N, (int)K, kind});
+    return (int)mm.size() - 1;
+  };
+  const int emb = mat(L.tok_emb, c.n_vocab, d, W_F32);
+  m.push_back({(size_t)c.n_vocab * d, L.tok_emb, emb});
+  m.push_back({(size_t)c.n_ctx * d, L.pos_emb, -1});
   auto block = [&](const BlockW& b) {
-    m.push_back({d, b.ln1_g}); m.push_back({d, b.ln1_b});
-    m.push_back({d * d, b.w_qkv}); m.push_back({d, b.b_qkv});
-    m.push_back({d * d, b.w_qkv + d * d});
-    m.push_back({d * d, b.w_qkv + 2 * d * d}); m.push_back({d, b.b_qkv + 2 * d});
-    m.push_back({d * d, b.w_o}); m.push_back({d, b.b_o});
-    m.push_back({d, b.ln2_g}); m.push_back({d, b.ln2_b});
-    m.push_back({d * d, b.w_q2}); m.push_back({d, b.b_q2});
-    m.push_back({d * d, b.w_kv2});
-    m.push_back({d * d, b.w_kv2 + d * d}); m.push_back({d, b.b_kv2 + d});
-    m.push_back({d * d, b.w_o2}); m.push_back({d, b.b_o2});
-    m.push_back({d, b.ln3_g}); m.push_back({d, b.ln3_b});
-    m.push_back({F * d, b.w_fc1}); m.push_back({F, b.b_fc1});
-    m.push_back({d * F, b.w_fc2}); m.push_back({d, b.b_fc2});
+    m.push_back({d, b.ln1_g, -1}); m.push_back({d, b.ln1_b, -1});
+    const int qkv = mat(b.w_qkv, 3 * d, d, W_F16);
+    m.push_back({d * d, b.w_qkv, qkv}); m.push_back({d, b.b_qkv, -1});
+    m.push_back({d * d, b.w_qkv + d * d, qkv});
+    m.push_back({d * d, b.w_qkv + 2 * d * d, qkv}); m.push_back({d, b.b_qkv + 2 * d, -1});
+    m.push_back({d * d, b.w_o, mat(b.w_o, d, d, W_F16)}); m.push_back({d, b.b_o, -1});
+    m.push_back({d, b.ln2_g, -1}); m.push_back({d, b.ln2_b, -1});
+    m.push_back({d * d, b.w_q2, mat(b.w_q2, d, d, W_F16)}); m.push_back({d, b.b_q2, -1});
+    m.push_back({d * d, b.w_kv2, -1});  // encode-time product: row-major
+    m.push_back({d * d, b.w_kv2 + d * d, -1}); m.push_back({d, b.b_kv2 + d, -1});
+    m.push_back({d * d, b.w_o2, mat(b.w_o2, d, d, W_F16)}); m.push_back({d, b.b_o2, -1});
+    m.push_back({d, b.ln3_g, -1}); m.push_back({d, b.ln3_b, -1});
+    m.push_back({F * d, b.w_fc1, mat(b.w_fc1, F, d, W_F32)}); m.push_back({F, b.b_fc1, -1});
+    m.push_back({d * F, b.w_fc2, mat(b.w_fc2, d, F, W_F16)}); m.push_back({d, b.b_fc2, -1});
   };
   for (auto& b : L.tb) block(b);
-  m.push_back({d, L.lnf_g}); m.push_back({d, L.lnf_b});
-  m.push_back({d * c.n_tap * d, L.hproj_w}); m.push_back({d, L.hproj_b}); m.push_back({d, L.mask});
+  m.push_back({d, L.lnf_g, -1}); m.push_back({d, L.lnf_b, -1});
+  m.push_back({d * c.n_tap * d, L.hproj_w, mat(L.hproj_w, d, c.n_tap * d, W_F16)});
+  m.push_back({d, L.hproj_b, -1}); m.push_back({d, L.mask, -1});
   for (auto& b : L.db) block(b);
-  m.push_back({d, L.dlnf_g}); m.push_back({d, L.dlnf_b});
+  m.push_back({d, L.dlnf_g, -1}); m.push_back({d, L.dlnf_b, -1});
+  if (mats) *mats = mm;
   return m;
 }
 
@@ -100,7 +122,7 @@ int compute_layout(const wf_config& c, Layout& L) {
   // weight region (element offsets, 128-element aligned)
   size_t w = 0;
   auto take = [&](size_t n) { size_t o = w; w = align_up(w + n, 128); return o; };
-  L.tok_emb = take(V * d);
+  L.tok_emb = take(align_up(V, 32) * d);  // padded to whole 32-column tiles
   L.pos_emb = take((size_t)c.n_ctx * d);
   auto block = [&]() {
     BlockW b;
@@ -125,8 +147,14 @@ int compute_layout(const wf_config& c, Layout& L) {
   L.dlnf_g = take(d); L.dlnf_b = take(d);
   L.weight_elems = w;
   L.pages_per_slot = c.n_ctx / kPage;
-  L.nsplit = (c.n_frames + kFrameSplit - 1) / kFrameSplit;
-  L.head_blocks = (int)((V + 15) / 16);
+  // the vocabulary head streams 32-column tiles (bf16) or 16-column tiles (fp32)
+  L.head_blocks = c.dtype == WF_BF16 ? (int)((V + 31) / 32) : (int)((V + 15) / 16);
+  // raw bf16 matrices are staged at init in the cross K/V region before reordering
+  L.stage_bytes = 0;
+  if (c.dtype == WF_BF16) {
+    const size_t big = std::max({V * d, 3 * d * d, F * d, (size_t)c.n_tap * d * d});
+    L.stage_bytes = big * eb;
+  }
   // byte regions
   size_t o = 0;
   auto region = [&](size_t bytes) { size_t r = o; o = align_up(o + bytes, 256); return r; };
@@ -136,20 +164,23 @@ int compute_layout(const wf_config& c, Layout& L) {
   L.status = region(256);
   L.aux = region(4 * B * 4);
   L.weights = region(w * eb);
-  L.xkv = region((size_t)(c.n_layer + c.n_draft_layer) * B * 2 * c.n_frames * d * eb);
+  L.xkv = region(std::max((size_t)(c.n_layer + c.n_draft_layer) * B * 2 * c.n_frames * d * eb, L.stage_bytes));
   L.skv = region((size_t)c.n_layer * 2 * B * L.pages_per_slot * H * kPage * kHeadDim * eb);
   L.hkv = region((size_t)c.n_draft_layer * 2 * B * H * c.n_ctx * kHeadDim * eb);
+  // matrix operands: 3 bf16 terms per fp32 value at batch 1 with bf16 storage
+  L.nsplit_op = (c.dtype == WF_BF16 && c.max_batch == 1) ? 3 : 1;
+  const size_t rows = L.nsplit_op * R9;
+  L.mt16 = (int)((rows + 15) / 16);
+  L.mt32 = (int)((rows + 31) / 32);
+  const size_t M16 = (size_t)L.mt16 * 16, M32 = std::max((size_t)L.mt32 * 32, M16);
+  L.a_d16 = region(M16 * d * eb);
+  L.a_d32 = region(M32 * d * eb);
+  L.a_f16 = region(M16 * F * eb);
+  L.a_tap16 = region(M16 * c.n_tap * d * eb);
   L.h = region(R9 * d * 4);
-  L.xn = region(R9 * d * 4);
   L.qkv = region(R9 * 3 * d * 4);
-  L.attn = region(R9 * d * 4);
-  L.act = region(R9 * F * 4);
   L.hp = region(R9 * d * 4);
   L.kvh = region(R9 * 2 * d * 4);
-  L.taps = region(R9 * c.n_tap * d * 4);
-  L.xm = region(R9 * H * L.nsplit * 4);
-  L.xl = region(R9 * H * L.nsplit * 4);
-  L.xo = region(R9 * H * L.nsplit * kHeadDim * 4);
   L.hv = region(R9 * L.head_blocks * 4);
   L.hi = region(R9 * L.head_blocks * 4);
   L.tok = region(R9 * 4);
@@ -212,12 +243,36 @@ struct Runner {
     return h->at<S>(L.hkv) + ((size_t)dl * 2 + kv) * c.max_batch * c.n_head * c.n_ctx * kHeadDim;
   }
 
-  GemvArgs gemv_base(int slot0, int n) const {
+  bool frag() const { return c.dtype == WF_BF16; }
+  // Operand buffer at `off` with row length K, in the order read by products whose
+  // weights have 32-column (wide) or 16-column tiles.
+  Operand op(size_t off, int K, bool wide) const {
+    if (!frag()) return Operand{h->at<void>(off), K, OP_ROW, L.mt16};
+    return wide ? Operand{h->at<void>(off), K, OP_F32, L.mt32} : Operand{h->at<void>(off), K, OP_F16, L.mt16};
+  }
+  Operand Ad16() const { return op(L.a_d16, c.d_model, false); }
+  Operand Ad32() const { return op(L.a_d32, c.d_model, true); }
+  Operand Af16() const { return op(L.a_f16, c.d_ff, false); }
+  Operand Atap16() const { return op(L.a_tap16, c.n_tap * c.d_model, false); }
+  int wk(bool wide) const { return frag() ? (wide ? W_F32 : W_F16) : W_ROW; }
+  int R9() const { return c.max_batch * kRows; }
+
+  GemvArgs gemv_base(int slot0, int n, int wkind) const {
     GemvArgs a{};
     a.slot0 = slot0;
     a.nslots = n;
+    a.nsplit = L.nsplit_op;
+    a.R9 = R9();
+    a.wkind = wkind;
+    const int T = wkind == W_F32 ? 32 : 16;  // operand rows per tile
+    if (L.nsplit_op == 3) {
+      a.mt0 = 0;
+      a.mt1 = (3 * R9() + T - 1) / T;
+    } else {
+      a.mt0 = slot0 * kRows / T;
+      a.mt1 = ((slot0 + n) * kRows + T - 1) / T;
+    }
     a.tap = -1;
-    a.n_tap = c.n_tap;
     a.state = I32(L.state);
     a.page_table = I32(L.page_table);
     a.d = c.d_model;
@@ -227,27 +282,34 @@ struct Runner {
     return a;
   }
 
-  void gemv(int epi, int slot0, int n, const float* x, int ldx, size_t w, size_t b, int K, int N, float* y, int ldy,
-            int tap = -1) {
-    GemvArgs a = gemv_base(slot0, n);
-    a.x = x;
-    a.ldx = ldx;
+  // bytes a GEMV launch must move: weights + bias once, operand rows, outputs
+  double gemv_bytes(int n, int K, int N, int epi) const {
+    const double rows = (double)kRows * n;
+    return (double)N * K * eb() + N * eb() + L.nsplit_op * rows * K * eb() +
+           rows * N * 4.0 * (epi == EPI_RESID ? 2 : 1);
+  }
+
+  void gemv(int epi, int slot0, int n, Operand x, size_t w, size_t b, int K, int N, float* y, int ldy,
+            Operand aout = Operand{nullptr, 0, OP_ROW, 0}, int tap = -1) {
+    GemvArgs a = gemv_base(slot0, n, wk(x.kind == OP_F32));
+    a.a = x;
     a.w = W(w);
     a.bias = W(b);
     a.K = K;
     a.N = N;
     a.y = y;
     a.ldy = ldy;
+    a.aout = aout;
     a.tap = tap;
-    a.taps = F32(L.taps);
-    const double rows = (double)kRows * n;
-    const double bytes = (double)N * K * eb() + N * eb() + rows * K * 4 + rows * N * 4 * (epi == EPI_RESID ? 2 : 1);
-    launch("gemv", bytes, [&] { Ops<S>::gemv(epi, a, st); });
+    launch("gemv", gemv_bytes(n, K, N, epi), [&] { Ops<S>::gemv(epi, a, st); });
   }
 
-  void ln(int slot0, int n, const float* x, size_t g, size_t b, float* y) {
-    launch("layernorm", 8.0 * kRows * n * c.d_model,
-           [&] { Ops<S>::layernorm(x, W(g), W(b), y, c.d_model, slot0 * kRows, n * kRows, st); });
+  void ln(int slot0, int n, const float* x, size_t g, size_t b, Operand out) {
+    LnArgs la{};
+    la.x = x; la.g = W(g); la.b = W(b); la.out = out; la.d = c.d_model; la.row0 = slot0 * kRows;
+    la.nsplit = L.nsplit_op; la.R9 = R9();
+    launch("layernorm", 4.0 * kRows * n * c.d_model * (1 + L.nsplit_op * eb() / 4.0),
+           [&] { Ops<S>::ln_operand(la, n * kRows, st); });
   }
 
   void cross(int slot0, int n, int layer) {
@@ -255,61 +317,59 @@ struct Runner {
     a.q = F32(L.qkv);
     a.ldq = 3 * c.d_model;
     a.kv = xkv_layer(layer);
-    a.pm = F32(L.xm);
-    a.pl = F32(L.xl);
-    a.po = F32(L.xo);
-    a.out = F32(L.attn);
+    a.out = Ad16();
     a.slot0 = slot0;
     a.d = c.d_model;
     a.n_head = c.n_head;
     a.n_frames = c.n_frames;
-    a.nsplit = L.nsplit;
+    a.nsplit = L.nsplit_op;
+    a.R9 = R9();
     launch("attn_cross", 2.0 * c.n_head * c.n_frames * kHeadDim * eb() * n, [&] { Ops<S>::attn_cross(a, n, st); });
   }
 
   // second half of a decoder block shared by target and drafter: cross-attention and MLP
   void block_tail(int slot0, int n, const BlockW& b, int xlayer, int tap) {
     const int d = c.d_model;
-    float *h_ = F32(L.h), *xn = F32(L.xn), *qkv = F32(L.qkv), *attn = F32(L.attn), *act = F32(L.act);
-    ln(slot0, n, h_, b.ln2_g, b.ln2_b, xn);
-    gemv(EPI_STORE, slot0, n, xn, d, b.w_q2, b.b_q2, d, d, qkv, 3 * d);
+    float *h_ = F32(L.h), *qkv = F32(L.qkv);
+    ln(slot0, n, h_, b.ln2_g, b.ln2_b, Ad16());
+    gemv(EPI_STORE, slot0, n, Ad16(), b.w_q2, b.b_q2, d, d, qkv, 3 * d);
     cross(slot0, n, xlayer);
-    gemv(EPI_RESID, slot0, n, attn, d, b.w_o2, b.b_o2, d, d, h_, d);
-    ln(slot0, n, h_, b.ln3_g, b.ln3_b, xn);
-    gemv(EPI_GELU, slot0, n, xn, d, b.w_fc1, b.b_fc1, d, c.d_ff, act, c.d_ff);
-    gemv(EPI_RESID, slot0, n, act, c.d_ff, b.w_fc2, b.b_fc2, c.d_ff, d, h_, d, tap);
+    gemv(EPI_RESID, slot0, n, Ad16(), b.w_o2, b.b_o2, d, d, h_, d);
+    ln(slot0, n, h_, b.ln3_g, b.ln3_b, Ad32());
+    gemv(EPI_GELU, slot0, n, Ad32(), b.w_fc1, b.b_fc1, d, c.d_ff, nullptr, 0, Af16());
+    gemv(EPI_RESID, slot0, n, Af16(), b.w_fc2, b.b_fc2, c.d_ff, d, h_, d, Atap16(), tap);
   }
 
   void target_forward(int slot0, int n) {
     const int d = c.d_model;
-    float *h_ = F32(L.h), *xn = F32(L.xn), *qkv = F32(L.qkv), *attn = F32(L.attn);
+    float *h_ = F32(L.h), *qkv = F32(L.qkv);
     for (int l = 0; l < c.n_layer; ++l) {
       const BlockW& b = L.tb[l];
       int tap = -1;
       for (int i = 0; i < c.n_tap; ++i)
         if (c.taps[i] == l) tap = i;
-      ln(slot0, n, h_, b.ln1_g, b.ln1_b, xn);
-      GemvArgs a = gemv_base(slot0, n);
-      a.x = xn; a.ldx = d; a.w = W(b.w_qkv); a.bias = W(b.b_qkv); a.K = d; a.N = 3 * d;
+      ln(slot0, n, h_, b.ln1_g, b.ln1_b, Ad16());
+      GemvArgs a = gemv_base(slot0, n, wk(false));
+      a.a = Ad16(); a.w = W(b.w_qkv); a.bias = W(b.b_qkv); a.K = d; a.N = 3 * d;
       a.y = qkv; a.ldy = 3 * d; a.cache = skv_layer(l); a.kv_stride = kv_stride();
-      launch("gemv", 3.0 * d * d * eb() + 3.0 * d * eb() + kRows * n * d * 4.0 * 4, [&] { Ops<S>::gemv(EPI_QKV, a, st); });
+      launch("gemv", gemv_bytes(n, d, 3 * d, EPI_QKV), [&] { Ops<S>::gemv(EPI_QKV, a, st); });
       AttnArgs at{};
       at.q = qkv; at.ldq = 3 * d; at.kcache = skv_layer(l); at.vcache = skv_layer(l) + kv_stride();
-      at.state = I32(L.state); at.page_table = I32(L.page_table); at.rope = F32(L.rope); at.out = attn;
+      at.state = I32(L.state); at.page_table = I32(L.page_table); at.rope = F32(L.rope); at.out = Ad16();
       at.slot0 = slot0; at.d = d; at.n_head = c.n_head; at.n_ctx = c.n_ctx; at.pages_per_slot = L.pages_per_slot;
+      at.nsplit = L.nsplit_op; at.R9 = R9();
       launch("attn_self", 0, [&] { Ops<S>::attn_self(at, n, st); });
-      gemv(EPI_RESID, slot0, n, attn, d, b.w_o, b.b_o, d, d, h_, d);
+      gemv(EPI_RESID, slot0, n, Ad16(), b.w_o, b.b_o, d, d, h_, d);
       block_tail(slot0, n, b, l, tap);
     }
   }
 
-  // vocabulary head over rows of x: logits = x @ tok_emb^T, per-row argmax into g
-  void head(int slot0, int n, const float* x, float* logits) {
-    GemvArgs a = gemv_base(slot0, n);
-    a.x = x; a.ldx = c.d_model; a.w = W(L.tok_emb); a.bias = nullptr; a.K = c.d_model; a.N = c.n_vocab;
+  // vocabulary head over the operand rows in A_d32: logits = x @ tok_emb^T, per-row argmax into g
+  void head(int slot0, int n, float* logits) {
+    GemvArgs a = gemv_base(slot0, n, wk(true));
+    a.a = Ad32(); a.w = W(L.tok_emb); a.bias = nullptr; a.K = c.d_model; a.N = c.n_vocab;
     a.y = logits; a.ldy = c.n_vocab; a.hv = F32(L.hv); a.hi = I32(L.hi); a.nblk = L.head_blocks;
-    launch("gemv", (double)c.n_vocab * c.d_model * eb() + kRows * n * c.d_model * 4.0 + kRows * n * L.head_blocks * 8.0,
-           [&] { Ops<S>::gemv(EPI_ARGMAX, a, st); });
+    launch("gemv", gemv_bytes(n, c.d_model, c.n_vocab, EPI_ARGMAX), [&] { Ops<S>::gemv(EPI_ARGMAX, a, st); });
     launch("argmax_final", kRows * n * L.head_blocks * 8.0, [&] {
       argmax_final(F32(L.hv), I32(L.hi), L.head_blocks, slot0 * kRows, n * kRows, I32(L.g), F32(L.gmax),
                    h->at<unsigned>(L.status), st);
@@ -319,12 +379,13 @@ struct Runner {
   // drafter history for pending rows (Appendix A.2): taps -> W_h -> per-block LN, k (RoPE), v
   void history_apply(int slot0, int n) {
     const int d = c.d_model;
-    float *hp = F32(L.hp), *xn = F32(L.xn), *kvh = F32(L.kvh);
-    gemv(EPI_STORE, slot0, n, F32(L.taps), c.n_tap * d, L.hproj_w, L.hproj_b, c.n_tap * d, d, hp, d);
+    float *hp = F32(L.hp), *kvh = F32(L.kvh);
+    gemv(EPI_STORE, slot0, n, Atap16(), L.hproj_w, L.hproj_b, c.n_tap * d, d, hp, d);
     for (int dl = 0; dl < c.n_draft_layer; ++dl) {
       const BlockW& b = L.db[dl];
-      ln(slot0, n, hp, b.ln1_g, b.ln1_b, xn);
-      gemv(EPI_STORE, slot0, n, xn, d, b.w_qkv + (size_t)d * d, b.b_qkv + d, d, 2 * d, kvh, 2 * d);
+      ln(slot0, n, hp, b.ln1_g, b.ln1_b, Ad16());
+      // rows d..3d of the concatenated q|k|v matrix start d*d elements in, in either order
+      gemv(EPI_STORE, slot0, n, Ad16(), b.w_qkv + (size_t)d * d, b.b_qkv + d, d, 2 * d, kvh, 2 * d);
       HistArgs ha{};
       ha.kv = kvh; ha.kcache = hkv(dl, 0); ha.vcache = hkv(dl, 1); ha.state = I32(L.state); ha.rope = F32(L.rope);
       ha.slot0 = slot0; ha.d = d; ha.n_head = c.n_head; ha.n_ctx = c.n_ctx;
@@ -334,37 +395,38 @@ struct Runner {
 
   void drafter_forward(int slot0, int n, int* dst) {
     const int d = c.d_model;
-    float *h_ = F32(L.h), *xn = F32(L.xn), *qkv = F32(L.qkv), *attn = F32(L.attn);
+    float *h_ = F32(L.h), *qkv = F32(L.qkv);
     BeginArgs ba{};
-    ba.state = I32(L.state); ba.emb = W(L.tok_emb); ba.pos = W(L.mask); ba.h = h_;
+    ba.state = I32(L.state); ba.emb = W(L.tok_emb); ba.emb_kind = wk(true); ba.pos = W(L.mask); ba.h = h_;
     ba.slot0 = slot0; ba.d = d; ba.n_vocab = c.n_vocab; ba.n_ctx = c.n_ctx; ba.block_k = c.block_k;
     launch("begin", 0, [&] { Ops<S>::draft_begin(ba, n, st); });
     for (int dl = 0; dl < c.n_draft_layer; ++dl) {
       const BlockW& b = L.db[dl];
-      ln(slot0, n, h_, b.ln1_g, b.ln1_b, xn);
-      gemv(EPI_STORE, slot0, n, xn, d, b.w_qkv, b.b_qkv, d, 3 * d, qkv, 3 * d);
+      ln(slot0, n, h_, b.ln1_g, b.ln1_b, Ad16());
+      gemv(EPI_STORE, slot0, n, Ad16(), b.w_qkv, b.b_qkv, d, 3 * d, qkv, 3 * d);
       AttnArgs at{};
       at.q = qkv; at.ldq = 3 * d; at.kcache = hkv(dl, 0); at.vcache = hkv(dl, 1);
-      at.state = I32(L.state); at.rope = F32(L.rope); at.out = attn;
+      at.state = I32(L.state); at.rope = F32(L.rope); at.out = Ad16();
       at.slot0 = slot0; at.d = d; at.n_head = c.n_head; at.n_ctx = c.n_ctx;
+      at.nsplit = L.nsplit_op; at.R9 = R9();
       launch("attn_draft", 0, [&] { Ops<S>::attn_draft(at, n, st); });
-      gemv(EPI_RESID, slot0, n, attn, d, b.w_o, b.b_o, d, d, h_, d);
+      gemv(EPI_RESID, slot0, n, Ad16(), b.w_o, b.b_o, d, d, h_, d);
       block_tail(slot0, n, b, c.n_layer + dl, -1);
     }
-    ln(slot0, n, h_, L.dlnf_g, L.dlnf_b, xn);
-    head(slot0, n, xn, h->debug ? F32(L.dlogits) : nullptr);
+    ln(slot0, n, h_, L.dlnf_g, L.dlnf_b, Ad32());
+    head(slot0, n, h->debug ? F32(L.dlogits) : nullptr);
     launch("misc", 0, [&] { draft_tokens(I32(L.g), dst, I32(L.draft), slot0, n, c.block_k, st); });
   }
 
   void verify(int slot0, int n, const int* draft, int k_max, int* out, int* n_out, int* n_acc, int* done) {
     BeginArgs ba{};
-    ba.state = I32(L.state); ba.draft = draft; ba.tok = I32(L.tok); ba.emb = W(L.tok_emb); ba.pos = W(L.pos_emb);
+    ba.state = I32(L.state); ba.draft = draft; ba.tok = I32(L.tok); ba.emb = W(L.tok_emb); ba.emb_kind = wk(true); ba.pos = W(L.pos_emb);
     ba.h = F32(L.h); ba.slot0 = slot0; ba.d = c.d_model; ba.n_vocab = c.n_vocab; ba.n_ctx = c.n_ctx;
     ba.block_k = c.block_k; ba.k_max = k_max;
     launch("begin", 0, [&] { Ops<S>::verify_begin(ba, n, st); });
     target_forward(slot0, n);
-    ln(slot0, n, F32(L.h), L.lnf_g, L.lnf_b, F32(L.xn));
-    head(slot0, n, F32(L.xn), h->debug ? F32(L.logits) : nullptr);
+    ln(slot0, n, F32(L.h), L.lnf_g, L.lnf_b, Ad32());
+    head(slot0, n, h->debug ? F32(L.logits) : nullptr);
     AcceptArgs aa{};
     aa.state = I32(L.state); aa.tok = I32(L.tok); aa.g = I32(L.g); aa.out = out; aa.n_out = n_out; aa.n_acc = n_acc;
     aa.done = done; aa.slot0 = slot0; aa.n = n; aa.block_k = c.block_k; aa.eos = c.eos_id; aa.n_ctx = c.n_ctx;
@@ -399,7 +461,7 @@ struct Runner {
   void prefill(int slot0, int n, const int* tokens, int pmax, int max_len, int* first) {
     const int nchunks = (max_len + kRows - 1) / kRows;
     BeginArgs ba{};
-    ba.state = I32(L.state); ba.draft = tokens; ba.tok = I32(L.tok); ba.emb = W(L.tok_emb); ba.pos = W(L.pos_emb);
+    ba.state = I32(L.state); ba.draft = tokens; ba.tok = I32(L.tok); ba.emb = W(L.tok_emb); ba.emb_kind = wk(true); ba.pos = W(L.pos_emb);
     ba.h = F32(L.h); ba.slot0 = slot0; ba.d = c.d_model; ba.n_vocab = c.n_vocab; ba.n_ctx = c.n_ctx;
     ba.block_k = c.block_k; ba.pmax = pmax;
     for (int ch = 0; ch < nchunks; ++ch) {
@@ -409,8 +471,8 @@ struct Runner {
       save_last(F32(L.h), F32(L.lasth), I32(L.state), slot0, n, c.d_model, ch, st);
       history_apply(slot0, n);
     }
-    ln(slot0, n, F32(L.lasth), L.lnf_g, L.lnf_b, F32(L.xn));
-    head(slot0, n, F32(L.xn), nullptr);
+    ln(slot0, n, F32(L.lasth), L.lnf_g, L.lnf_b, Ad32());
+    head(slot0, n, nullptr);
     prefill_finish(I32(L.state), I32(L.g), slot0, n, c.eos_id, c.n_ctx, first, st);
   }
 };
@@ -509,9 +571,28 @@ int wf_init_weights(wf_handle** out, const wf_config* cfg, const void* const* we
   if (e != hipSuccess) return cleanup(WF_EHIP, std::string("hipMemsetAsync: ") + hipGetErrorString(e));
   const size_t eb = elt_bytes(*cfg);
   char* wbase = h->at<char>(L.weights);
+  char* stage = h->at<char>(L.xkv);
+  std::vector<Mat> mats;
+  manifest(*cfg, L, &mats);
+  std::vector<int> last(mats.size(), -1);  // last manifest entry of each matrix
+  for (int i = 0; i < n_weights; ++i)
+    if (man[i].mat >= 0) last[man[i].mat] = i;
   for (int i = 0; i < n_weights; ++i) {
-    e = hipMemcpyAsync(wbase + man[i].dst * eb, weights[i], man[i].numel * eb, hipMemcpyDeviceToDevice, st);
+    const int mi = man[i].mat;
+    char* dst = mi < 0 ? wbase + man[i].dst * eb : stage + (man[i].dst - mats[mi].dst) * eb;
+    e = hipMemcpyAsync(dst, weights[i], man[i].numel * eb, hipMemcpyDeviceToDevice, st);
     if (e != hipSuccess) return cleanup(WF_EHIP, std::string("hipMemcpyAsync: ") + hipGetErrorString(e));
+    if (mi >= 0 && last[mi] == i) {
+      // the whole matrix is staged: reorder it into its place
+      const Mat& m = mats[mi];
+      repack<bf16>(stage, wbase + m.dst * eb, m.N, m.K, m.kind, st);
+      e = hipGetLastError();
+      if (e != hipSuccess) return cleanup(WF_EHIP, std::string("repack: ") + hipGetErrorString(e));
+    }
+  }
+  if (!mats.empty()) {
+    e = hipMemsetAsync(stage, 0, L.stage_bytes, st);
+    if (e != hipSuccess) return cleanup(WF_EHIP, std::string("hipMemsetAsync: ") + hipGetErrorString(e));
   }
   // page table: logical page j of slot s -> physical page j * max_batch + s
   std::vector<int> pt((size_t)cfg->max_batch * L.pages_per_slot);

@@ -9,7 +9,7 @@ constexpr int kRows = 9;          // rows per slot in a verify / draft pass (anc
 constexpr int kHeadDim = 64;
 constexpr int kPage = 16;         // tokens per self-attention KV page
 constexpr int kStateInts = 16;    // per-slot state words
-constexpr int kFrameSplit = 128;  // acoustic frames per cross-attention split
+constexpr int kMaxFrames = 2048;  // largest supported number of acoustic frames
 constexpr int kMaxCtx = 448;      // largest supported text context
 
 // per-slot state word indices
@@ -29,6 +29,25 @@ enum {
   ST_LEN = 12,     // prompt length
   ST_LIVE = 13,    // slot has been prefilled
 };
+
+// Matrix-core fragment orders.  v_mfma_f32_16x16x32_bf16 reads, per lane l, 8
+// consecutive k of row (or column) l % 16 starting at k = 8 * (l / 16);
+// v_mfma_f32_32x32x16_bf16 reads 8 consecutive k of row l % 32 starting at
+// k = 8 * (l / 32).  Weights are stored tile by tile ([tile][k-step][lane][8]) and
+// activation operands k-step by k-step ([k-step][tile][lane][8]), so that one
+// wave's fragment load is 1 KB of contiguous memory.
+__host__ __device__ __forceinline__ size_t wfrag16_index(int n, int k, int ksteps) {
+  return ((size_t)((n >> 4) * ksteps + (k >> 5)) * 64 + (n & 15) + 16 * ((k & 31) >> 3)) * 8 + (k & 7);
+}
+__host__ __device__ __forceinline__ size_t wfrag32_index(int n, int k, int ksteps) {
+  return ((size_t)((n >> 5) * ksteps + (k >> 4)) * 64 + (n & 31) + 32 * ((k & 15) >> 3)) * 8 + (k & 7);
+}
+__host__ __device__ __forceinline__ size_t afrag16_index(int m, int k, int mtiles) {
+  return ((size_t)((k >> 5) * mtiles + (m >> 4)) * 64 + (m & 15) + 16 * ((k & 31) >> 3)) * 8 + (k & 7);
+}
+__host__ __device__ __forceinline__ size_t afrag32_index(int m, int k, int mtiles) {
+  return ((size_t)((k >> 4) * mtiles + (m >> 5)) * 64 + (m & 31) + 32 * ((k & 15) >> 3)) * 8 + (k & 7);
+}
 
 // bf16 storage element: the upper 16 bits of an fp32 value.
 struct bf16 {

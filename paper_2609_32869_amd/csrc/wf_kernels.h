@@ -8,25 +8,43 @@ namespace wf {
 
 enum { EPI_STORE = 0, EPI_GELU = 1, EPI_RESID = 2, EPI_QKV = 3, EPI_ARGMAX = 4 };
 
+// Matrix-operand rows: the activation rows of a pass are stored once per split
+// term, row m = s * R9 + slot * 9 + i, s < nsplit (R9 = 9 * max_batch).  With
+// bf16 storage and nsplit = 3 the three bf16 terms of an fp32 value sum to it
+// (24 significant bits), so bf16 matrix cores reproduce fp32 products exactly;
+// with nsplit = 1 the operand is the value rounded to the storage type.
+// Operand orders: row-major [rows][ld] (fp32 storage), or bf16 fragment order for
+// 16x16x32 (OP_F16) or 32x32x16 (OP_F32) matrix instructions with `mt` row tiles.
+enum { OP_ROW = 0, OP_F16 = 1, OP_F32 = 2 };
+struct Operand {
+  void* p;
+  int ld;    // row length K
+  int kind;  // OP_ROW / OP_F16 / OP_F32
+  int mt;    // row tiles held by the buffer (fragment orders)
+};
+
+// Weight orders: row-major [N][K] or bf16 fragment order (16- or 32-column tiles).
+enum { W_ROW = 0, W_F16 = 1, W_F32 = 2 };
+
 struct GemvArgs {
-  const float* x;  // input rows [slot*9 + i][ldx], fp32
-  int ldx;
-  const void* w;     // [N, K] storage type
+  Operand a;         // input operand
+  const void* w;     // [N, K] storage type, order wkind
+  int wkind;
   const void* bias;  // [N] storage type or null
   int K, N;
-  int slot0, nslots;
-  float* y;  // output rows (EPI_STORE/GELU: out; RESID: residual stream; QKV: q; ARGMAX: optional logits)
+  int slot0, nslots, nsplit, R9;
+  int mt0, mt1;      // 16-row tiles of the operand covering the batch (all split terms)
+  float* y;          // STORE: out; RESID: residual stream; QKV: q; ARGMAX: optional logits
   int ldy;
-  // EPI_RESID tap copy
-  float* taps;
-  int tap, n_tap;
-  // EPI_QKV cache append
+  Operand aout;      // GELU: operand of the next product; RESID: tap operand (column offset tap * N)
+  int tap;
+  // QKV cache append
   const int* state;
   const int* page_table;
   void* cache;
   size_t kv_stride;
   int d, n_head, n_ctx, pages_per_slot;
-  // EPI_ARGMAX partials
+  // ARGMAX partials
   float* hv;
   int* hi;
   int nblk;
@@ -40,24 +58,32 @@ struct AttnArgs {
   const int* state;
   const int* page_table;
   const float* rope;  // [pos][32][cos, sin]
-  float* out;         // [rows][d]
-  int slot0, d, n_head, n_ctx, pages_per_slot;
+  Operand out;        // operand rows of the following product
+  int slot0, d, n_head, n_ctx, pages_per_slot, nsplit, R9;
 };
 
 struct CrossArgs {
   const float* q;
   int ldq;
-  const void* kv;  // layer base of [slot][2][head][frame][64]
-  float *pm, *pl, *po;
-  float* out;
-  int slot0, d, n_head, n_frames, nsplit;
+  const void* kv;  // block base of [slot][2][head][frame][64]
+  Operand out;
+  int slot0, d, n_head, n_frames, nsplit, R9;
+};
+
+struct LnArgs {
+  const float* x;  // [rows][d]
+  const void* g;
+  const void* b;
+  Operand out;
+  int d, row0, nsplit, R9;
 };
 
 struct BeginArgs {
   int* state;
   const int* draft;  // verify: draft [n][block_k]; prefill: tokens [n][pmax]
   int* tok;
-  const void* emb;
+  const void* emb;  // token embedding, order emb_kind (W_ROW or W_F32)
+  int emb_kind;
   const void* pos;  // positional table (target) or mask vector (drafter)
   float* h;
   int slot0, d, n_vocab, n_ctx, block_k, k_max, chunk, pmax;
@@ -65,7 +91,7 @@ struct BeginArgs {
 
 struct HistArgs {
   const float* kv;  // [rows][2d]: k (no RoPE yet) | v
-  void* kcache;     // layer base [slot][head][n_ctx][64]
+  void* kcache;     // drafter block base [slot][head][n_ctx][64]
   void* vcache;
   const int* state;
   const float* rope;
@@ -87,13 +113,13 @@ struct XkvArgs {
   const void* mem;  // [n_frames][d] of one slot
   const void* w;    // [2d][d]
   const void* bias; // [2d]
-  void* out;        // layer base + slot offset
+  void* out;        // block base + slot offset
   int d, n_head, n_frames;
 };
 
 template <typename S>
 struct Ops {
-  static void layernorm(const float* x, const void* g, const void* b, float* y, int d, int row0, int rows, hipStream_t st);
+  static void ln_operand(const LnArgs& a, int rows, hipStream_t st);
   static void gemv(int epi, const GemvArgs& a, hipStream_t st);
   static void attn_self(const AttnArgs& a, int n, hipStream_t st);
   static void attn_draft(const AttnArgs& a, int n, hipStream_t st);
@@ -104,6 +130,9 @@ struct Ops {
   static void hist_write(const HistArgs& a, int n, hipStream_t st);
   static void gemm_xkv(const XkvArgs& a, hipStream_t st);
 };
+
+template <typename S>
+void repack(const void* src, void* dst, int N, int K, int wkind, hipStream_t st);
 
 void argmax_final(const float* hv, const int* hi, int nblk, int row0, int rows, int* g, float* gmax, unsigned* status,
                   hipStream_t st);

@@ -92,6 +92,52 @@ def test_tiny_greedy_64_tokens_equal_plain_greedy():
     ls.close()
 
 
+# bf16 storage at micro scale with a ragged vocabulary (501: a partial last column
+# tile of the head) and a ragged frame count (45: a partial last key octet).
+MICRO_BF16 = MICRO.with_(name="micro-bf16", dtype="bf16", n_vocab=501, n_frames=45)
+TOL_MICRO_BF16 = 2e-3
+
+
+def _run_planted(ls, refs, rng, steps, natural_every=3):
+    for n in range(steps):
+        ls.step(override=None if n % natural_every == 0 else _planted(ls, refs, rng))
+
+
+def test_micro_bf16_b1_split_operands():
+    """Batch 1, bf16: operands split into three bf16 terms (fp32-exact products)."""
+    from lockstep import Lockstep
+    cfg = MICRO_BF16
+    W = make_weights(cfg)
+    prompts = [make_prefix(cfg, 0, 11)]
+    ls = Lockstep(cfg, W, prompts, [48], TOL_MICRO_BF16)
+    opts = OracleOpts(dtype=np.float32, kv_bf16=True)
+    T = Target(cfg, W.values, opts)
+    refs = [plain_greedy(T, make_memory(cfg, 0), prompts[0], 48)]
+    _run_planted(ls, refs, np.random.default_rng(5), 12)
+    print(f"micro-bf16 b1: max |dlogit| draft {ls.max_dlogit:.3e} target {ls.max_tlogit:.3e}, near ties {ls.near_ties}")
+    assert ls.steps == 12
+    ls.close()
+
+
+def test_micro_bf16_b3_bf16_operands():
+    """Batch 3, bf16: operands rounded to bf16 (the oracle rounds them the same way)."""
+    from lockstep import Lockstep
+    cfg = MICRO_BF16
+    W = make_weights(cfg)
+    prompts = [make_prefix(cfg, 0, 4), make_prefix(cfg, 1, 20), make_prefix(cfg, 2, 9)]
+    max_new = [40, 9, 30]
+    opts = OracleOpts(dtype=np.float32, kv_bf16=True, gemm_bf16=True)
+    # Rounding every product input to bf16 makes the result sensitive to the fp32
+    # summation order: the oracle in fp32 and in fp64 (same rounding points)
+    # already differ by 3e-3 in the draft logits here, so the bf16 bar applies.
+    ls = Lockstep(cfg, W, prompts, max_new, TOL_BF16, opts=opts)
+    T = Target(cfg, W.values, opts)
+    refs = [plain_greedy(T, make_memory(cfg, i), prompts[i], max_new[i]) for i in range(3)]
+    _run_planted(ls, refs, np.random.default_rng(6), 10)
+    print(f"micro-bf16 b3: max |dlogit| draft {ls.max_dlogit:.3e} target {ls.max_tlogit:.3e}, near ties {ls.near_ties}")
+    ls.close()
+
+
 @pytest.mark.timeout(900)
 def test_large_v3_bf16_lockstep_b1():
     """Whisper-large-v3 shapes, bf16 weights/caches, one slot, prefix in [20, 200]."""
