@@ -45,12 +45,7 @@ __device__ __forceinline__ float block_sum(float v, float* red) {
 }
 
 // sum over the 8 lanes of one key (lane bits 0..2)
-__device__ __forceinline__ float key_sum(float s) {
-  s += __shfl_xor(s, 1, 64);
-  s += __shfl_xor(s, 2, 64);
-  s += __shfl_xor(s, 4, 64);
-  return s;
-}
+__device__ __forceinline__ float key_sum(float s) { return sum8(s); }
 
 // Eight consecutive storage elements of a key/value row, kept packed until used.
 template <typename S>
@@ -170,17 +165,113 @@ __device__ __forceinline__ float softmax_pass(float* sc, int nk, float* red) {
   return block_sum<NT>(l, red);
 }
 
+// ---------------------------------------------------------------- one query row, all keys
+// Attention of one query row over keys [0, nk) whose rows start roff(j) elements
+// into Kb and Vb (eight consecutive keys contiguous).  Wave w takes key octets w, w + NW, ... in
+// batches of B, with the key and value loads of a batch issued together.  The
+// wave keeps a running maximum m, a running sum l of exp(s - m) and the weighted
+// value sums acc (lane dims 8g..8g+7, partial over the lane's keys); the waves'
+// states are merged once at the end (softmax is exact: every key is seen).
+template <typename S, int NW, int B, typename RowOff>
+__device__ __forceinline__ void attend_wave(const float* q8, int nk, const S* __restrict__ Kb, const S* __restrict__ Vb,
+                                            RowOff roff, float& m, float& l, float* acc) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, g = lane & 7, kl = lane >> 3;
+  const int noct = (nk + 7) >> 3;
+  m = -INFINITY;
+  l = 0.f;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) acc[e] = 0.f;
+  for (int o0 = w; o0 < noct; o0 += NW * B) {
+    Raw8<S> kr[B], vr[B];
+#pragma unroll
+    for (int b = 0; b < B; ++b) {
+      const int key = (o0 + NW * b) * 8 + kl;
+      if (key < nk) {
+        const uint32_t o = roff(key) + 8 * g;
+        kr[b].load(Kb + o);
+        vr[b].load(Vb + o);
+      } else {
+        kr[b].zero();
+        vr[b].zero();
+      }
+    }
+    float sc[B];
+    float bm = -INFINITY;
+#pragma unroll
+    for (int b = 0; b < B; ++b) {
+      float k8[8];
+      kr[b].unpack(k8);
+      float t = 0.f;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) t = fmaf(q8[e], k8[e], t);
+      t = key_sum(t);
+      sc[b] = (o0 + NW * b) * 8 + kl < nk ? t : -INFINITY;
+      bm = fmaxf(bm, sc[b]);
+    }
+    // key o0 * 8 < nk is in this batch, so mn is finite
+    const float mn = fmaxf(m, wave_max(bm));
+    const float f = __expf(m - mn);
+    l *= f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc[e] *= f;
+#pragma unroll
+    for (int b = 0; b < B; ++b) {
+      const float p = __expf(sc[b] - mn);  // 0 for keys past nk
+      l += g == 0 ? p : 0.f;
+      float v8[8];
+      vr[b].unpack(v8);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) acc[e] = fmaf(p, v8[e], acc[e]);
+    }
+    m = mn;
+  }
+}
+
+// Merge the NW wave states; threads 0..63 return output dim threadIdx.x.
+// part holds, per wave and 16-lane row, the row's value sums (after folding key
+// lanes 8..15 of the row onto 0..7).
+template <int NW>
+__device__ __forceinline__ float merge_waves(float m, float l, float* acc, float (*part)[4][64], float* pm, float* pl) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, g = lane & 7;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) acc[e] += dpp<kDppRor8>(acc[e]);
+  l = wave_sum(l);
+  if ((lane & 8) == 0) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) part[w][lane >> 4][8 * g + e] = acc[e];
+  }
+  if (lane == 0) {
+    pm[w] = m;
+    pl[w] = l;
+  }
+  __syncthreads();
+  float o = 0.f;
+  if (threadIdx.x < kHeadDim) {
+    float M = pm[0];
+#pragma unroll
+    for (int i = 1; i < NW; ++i) M = fmaxf(M, pm[i]);
+    float L = 0.f;
+#pragma unroll
+    for (int i = 0; i < NW; ++i) {
+      const float f = __expf(pm[i] - M);  // 0 for a wave without keys
+      L += pl[i] * f;
+      o += ((part[i][0][threadIdx.x] + part[i][1][threadIdx.x]) + (part[i][2][threadIdx.x] + part[i][3][threadIdx.x])) * f;
+    }
+    o /= L;
+  }
+  return o;
+}
+
 // ---------------------------------------------------------------- cross-attention
 // Query row i of slot s against all acoustic frames of one head (no mask).
-constexpr int kCrossThreads = 1024;
+constexpr int kCrossThreads = 512;
 template <typename S>
-constexpr int kCrossB = sizeof(S) == 2 ? 12 : 6;  // key octets in flight per wave
+constexpr int kCrossB = sizeof(S) == 2 ? 24 : 12;  // key octets in flight per wave
 template <typename S>
 __global__ void __launch_bounds__(kCrossThreads) k_attn_cross(CrossArgs a) {
-  constexpr int NT = kCrossThreads, NW = NT / 64;
-  __shared__ float sc[kMaxFrames];
-  __shared__ float part[NW][64];
-  __shared__ float red[NW];
+  constexpr int NW = kCrossThreads / 64;
+  __shared__ float part[NW][4][64];
+  __shared__ float pm[NW], pl[NW];
   int head, row;
   if (!head_row(blockIdx.x, a.n_head, head, row)) return;
   const int slot = a.slot0 + blockIdx.y;
@@ -191,65 +282,200 @@ __global__ void __launch_bounds__(kCrossThreads) k_attn_cross(CrossArgs a) {
   for (int e = 0; e < 8; ++e) q8[e] = qr[e] * 0.125f;
   const S* Kx = reinterpret_cast<const S*>(a.kv) + ((size_t)slot * 2 * a.n_head + head) * a.n_frames * kHeadDim;
   const S* Vx = Kx + (size_t)a.n_head * a.n_frames * kHeadDim;
-  const int F = a.n_frames;
-  score_pass<S, NT, kCrossB<S>>(q8, F, [&](int j) { return Kx + (size_t)j * kHeadDim; }, sc);
-  __syncthreads();
-  const float L = softmax_pass<NT>(sc, F, red);
-  __syncthreads();
-  float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-  value_pass<S, NT, kCrossB<S>>(acc, F, [&](int j) { return Vx + (size_t)j * kHeadDim; }, sc);
-  reduce_out<NT>(acc, part);
-  if (threadIdx.x < kHeadDim) {
-    float o = 0.f;
+  float m, l, acc[8];
+  attend_wave<S, NW, kCrossB<S>>(q8, a.n_frames, Kx, Vx, [](int j) { return (uint32_t)j * kHeadDim; }, m, l, acc);
+  const float o = merge_waves<NW>(m, l, acc, part, pm, pl);
+  if (threadIdx.x < kHeadDim)
+    put_op<S>(a.out, a.nsplit, a.R9, slot * kRows + row, head * kHeadDim + threadIdx.x, o);
+}
+
+// ---------------------------------------------------------------- cross-attention over key chunks
+// Block (head, chunk) of slot s: all nine query rows against frames
+// [chunk * cs, chunk * cs + cs), so every key/value byte is read by one block.
+// Wave w takes key octets w, w + NW, ...; each row keeps a running max, sum and
+// weighted value sums; the waves' states are merged in LDS and the chunk's state
+// {m, l, 0, 0, acc[64]} is stored for the combine.
+constexpr int kXpThreads = 512;
+constexpr int kXpStride = 68;  // floats per (chunk, row) state
+template <typename S>
+__global__ void __launch_bounds__(kXpThreads) k_xattn_part(XpartArgs a) {
+  constexpr int NW = kXpThreads / 64, B = 2;
+  __shared__ float wacc[NW][kRows][64];
+  __shared__ float wm[NW][kRows], wl[NW][kRows];
+  const int head = blockIdx.x / a.nchunk, chunk = blockIdx.x % a.nchunk;
+  const int slot = a.slot0 + blockIdx.y;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, g = lane & 7, kl = lane >> 3;
+  const int cs = (a.n_frames + a.nchunk - 1) / a.nchunk;
+  const int f0 = min(a.n_frames, chunk * cs), nk = min(a.n_frames, f0 + cs) - f0;
+  float q8[kRows][8];
 #pragma unroll
-    for (int w = 0; w < NW; ++w) o += part[w][threadIdx.x];
-    put_op<S>(a.out, a.nsplit, a.R9, slot * kRows + row, head * kHeadDim + threadIdx.x, o / L);
+  for (int r = 0; r < kRows; ++r) {
+    const float* qr = a.q + (size_t)(slot * kRows + r) * a.ldq + head * kHeadDim + 8 * g;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) q8[r][e] = qr[e] * 0.125f;
   }
+  const S* Kx = reinterpret_cast<const S*>(a.kv) + (((size_t)slot * 2 * a.n_head + head) * a.n_frames + f0) * kHeadDim;
+  const S* Vx = Kx + (size_t)a.n_head * a.n_frames * kHeadDim;
+  float m[kRows], l[kRows], acc[kRows][8];
+#pragma unroll
+  for (int r = 0; r < kRows; ++r) {
+    m[r] = -INFINITY;
+    l[r] = 0.f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc[r][e] = 0.f;
+  }
+  const int noct = (nk + 7) >> 3;
+  for (int o0 = w; o0 < noct; o0 += NW * B) {
+    Raw8<S> kr[B], vr[B];
+#pragma unroll
+    for (int b = 0; b < B; ++b) {
+      const int key = (o0 + NW * b) * 8 + kl;
+      if (key < nk) {
+        kr[b].load(Kx + (uint32_t)key * kHeadDim + 8 * g);
+        vr[b].load(Vx + (uint32_t)key * kHeadDim + 8 * g);
+      } else {
+        kr[b].zero();
+        vr[b].zero();
+      }
+    }
+    float sc[kRows][B];
+#pragma unroll
+    for (int b = 0; b < B; ++b) {
+      float k8[8];
+      kr[b].unpack(k8);
+      const bool ok = (o0 + NW * b) * 8 + kl < nk;
+#pragma unroll
+      for (int r = 0; r < kRows; ++r) {
+        float t = 0.f;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) t = fmaf(q8[r][e], k8[e], t);
+        t = sum8(t);
+        sc[r][b] = ok ? t : -INFINITY;
+      }
+    }
+    float v8[B][8];
+#pragma unroll
+    for (int b = 0; b < B; ++b) vr[b].unpack(v8[b]);
+#pragma unroll
+    for (int r = 0; r < kRows; ++r) {
+      float bm = sc[r][0];
+#pragma unroll
+      for (int b = 1; b < B; ++b) bm = fmaxf(bm, sc[r][b]);
+      const float mn = fmaxf(m[r], wave_max(bm));  // key o0 * 8 < nk is in this batch
+      const float f = __expf(m[r] - mn);
+      l[r] *= f;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) acc[r][e] *= f;
+#pragma unroll
+      for (int b = 0; b < B; ++b) {
+        const float p = __expf(sc[r][b] - mn);
+        l[r] += g == 0 ? p : 0.f;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc[r][e] = fmaf(p, v8[b][e], acc[r][e]);
+      }
+      m[r] = mn;
+    }
+  }
+  // fold the 8 key lanes (bits 3..5) of each dim group, then publish per wave
+#pragma unroll
+  for (int r = 0; r < kRows; ++r) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      float t = acc[r][e] + dpp<kDppRor8>(acc[r][e]);
+      t += __shfl_xor(t, 16, 64);
+      t += __shfl_xor(t, 32, 64);
+      acc[r][e] = t;
+    }
+    const float lr = wave_sum(l[r]);
+    if (lane < 8) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) wacc[w][r][8 * g + e] = acc[r][e];
+    }
+    if (lane == 0) {
+      wm[w][r] = m[r];
+      wl[w][r] = lr;
+    }
+  }
+  __syncthreads();
+  float* out = a.part + (((size_t)slot * a.n_head + head) * a.nchunk + chunk) * kRows * kXpStride;
+  for (int t = threadIdx.x; t < kRows * 64; t += kXpThreads) {
+    const int r = t >> 6, dim = t & 63;
+    float M = wm[0][r];
+#pragma unroll
+    for (int i = 1; i < NW; ++i) M = fmaxf(M, wm[i][r]);
+    float L = 0.f, o = 0.f;
+#pragma unroll
+    for (int i = 0; i < NW; ++i) {
+      const float f = __expf(wm[i][r] - M);  // 0 for a wave without keys
+      L += wl[i][r] * f;
+      o += wacc[i][r][dim] * f;
+    }
+    out[r * kXpStride + 4 + dim] = o;
+    if (dim == 0) {
+      out[r * kXpStride] = M;
+      out[r * kXpStride + 1] = L;
+    }
+  }
+}
+
+// Merge the chunk states of (slot, head): thread (row, dim).
+template <typename S>
+__global__ void __launch_bounds__(kRows * 64) k_xattn_combine(XpartArgs a) {
+  const int head = blockIdx.x, slot = a.slot0 + blockIdx.y;
+  const int r = threadIdx.x >> 6, dim = threadIdx.x & 63;
+  const float* in = a.part + ((size_t)slot * a.n_head + head) * a.nchunk * kRows * kXpStride + r * kXpStride;
+  float M = -INFINITY;
+  for (int c = 0; c < a.nchunk; ++c) M = fmaxf(M, in[(size_t)c * kRows * kXpStride]);
+  float L = 0.f, o = 0.f;
+  for (int c = 0; c < a.nchunk; ++c) {
+    const float* p = in + (size_t)c * kRows * kXpStride;
+    const float f = __expf(p[0] - M);
+    L += p[1] * f;
+    o += p[4 + dim] * f;
+  }
+  put_op<S>(a.out, a.nsplit, a.R9, slot * kRows + r, head * kHeadDim + dim, o / L);
 }
 
 // ---------------------------------------------------------------- causal self-attention
 // Verify pass: row i < nv of slot s sits at position pos0 + i and attends to cached
 // positions 0..pos0 + i (Section 3.1: one causal pass).  Rows i >= nv are padding
-// and get zeros.
+// and get zeros.  All keys of a row fit one batch (4 waves x 14 octets = 448).
 constexpr int kSelfThreads = 256;
 template <typename S>
 __global__ void __launch_bounds__(kSelfThreads) k_attn_self(AttnArgs a) {
-  constexpr int NT = kSelfThreads, NW = NT / 64;
-  __shared__ float sc[kMaxCtx];
-  __shared__ float part[NW][64];
-  __shared__ float red[NW];
+  constexpr int NW = kSelfThreads / 64;
+  static_assert(NW * 14 * 8 >= kMaxCtx, "one batch of key octets covers the context");
+  __shared__ float part[NW][4][64];
+  __shared__ float pm[NW], pl[NW];
+  __shared__ int pts[kMaxCtx / kPage];
   int head, row;
   if (!head_row(blockIdx.x, a.n_head, head, row)) return;
   const int slot = a.slot0 + blockIdx.y;
   const int* st = a.state + slot * kStateInts;
+  // state, page table and query are independent loads
+  if (threadIdx.x < a.pages_per_slot) pts[threadIdx.x] = a.page_table[slot * a.pages_per_slot + threadIdx.x];
   const int pos0 = st[ST_POS0], nv = st[ST_NV];
-  if (row >= nv) {
-    if (threadIdx.x < kHeadDim) put_op<S>(a.out, a.nsplit, a.R9, slot * kRows + row, head * kHeadDim + threadIdx.x, 0.f);
-    return;
-  }
-  const int nk = pos0 + row + 1;
   const int lane = threadIdx.x & 63, g = lane & 7;
   const float* qr = a.q + (size_t)(slot * kRows + row) * a.ldq + head * kHeadDim + 8 * g;
   float q8[8];
 #pragma unroll
   for (int e = 0; e < 8; ++e) q8[e] = qr[e] * 0.125f;
+  __syncthreads();
+  if (row >= nv) {
+    if (threadIdx.x < kHeadDim) put_op<S>(a.out, a.nsplit, a.R9, slot * kRows + row, head * kHeadDim + threadIdx.x, 0.f);
+    return;
+  }
+  const int nk = pos0 + row + 1;
   const S* Kc = reinterpret_cast<const S*>(a.kcache);
   const S* Vc = reinterpret_cast<const S*>(a.vcache);
-  const int* pt = a.page_table + slot * a.pages_per_slot;
   const int H = a.n_head;
-  auto krow = [&](int j) { return Kc + (((size_t)pt[j >> 4] * H + head) * kPage + (j & 15)) * kHeadDim; };
-  auto vrow = [&](int j) { return Vc + (((size_t)pt[j >> 4] * H + head) * kPage + (j & 15)) * kHeadDim; };
-  score_pass<S, NT, 14>(q8, nk, krow, sc);
-  __syncthreads();
-  const float L = softmax_pass<NT>(sc, nk, red);
-  __syncthreads();
-  float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-  value_pass<S, NT, 14>(acc, nk, vrow, sc);
-  reduce_out<NT>(acc, part);
-  if (threadIdx.x < kHeadDim) {
-    const float o = (part[0][threadIdx.x] + part[1][threadIdx.x]) + (part[2][threadIdx.x] + part[3][threadIdx.x]);
-    put_op<S>(a.out, a.nsplit, a.R9, slot * kRows + row, head * kHeadDim + threadIdx.x, o / L);
-  }
+  float m, l, acc[8];
+  attend_wave<S, NW, 14>(
+      q8, nk, Kc, Vc, [&](int j) { return (((uint32_t)pts[j >> 4] * H + head) * kPage + (j & 15)) * kHeadDim; }, m, l,
+      acc);
+  const float o = merge_waves<NW>(m, l, acc, part, pm, pl);
+  if (threadIdx.x < kHeadDim)
+    put_op<S>(a.out, a.nsplit, a.R9, slot * kRows + row, head * kHeadDim + threadIdx.x, o);
 }
 
 // ---------------------------------------------------------------- drafter attention
@@ -356,6 +582,19 @@ void Ops<S>::attn_cross(const CrossArgs& a, int n, hipStream_t st) {
   k_attn_cross<S><<<dim3(row_blocks(a.n_head), n), kCrossThreads, 0, st>>>(a);
 }
 
+template <typename S>
+void Ops<S>::xattn_part(const XpartArgs& a, int n, hipStream_t st) {
+  k_xattn_part<S><<<dim3(a.n_head * a.nchunk, n), kXpThreads, 0, st>>>(a);
+}
+template <typename S>
+void Ops<S>::xattn_combine(const XpartArgs& a, int n, hipStream_t st) {
+  k_xattn_combine<S><<<dim3(a.n_head, n), kRows * 64, 0, st>>>(a);
+}
+
+template void Ops<float>::xattn_part(const XpartArgs&, int, hipStream_t);
+template void Ops<bf16>::xattn_part(const XpartArgs&, int, hipStream_t);
+template void Ops<float>::xattn_combine(const XpartArgs&, int, hipStream_t);
+template void Ops<bf16>::xattn_combine(const XpartArgs&, int, hipStream_t);
 template void Ops<float>::attn_self(const AttnArgs&, int, hipStream_t);
 template void Ops<bf16>::attn_self(const AttnArgs&, int, hipStream_t);
 template void Ops<float>::attn_draft(const AttnArgs&, int, hipStream_t);

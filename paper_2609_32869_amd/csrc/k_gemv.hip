@@ -22,58 +22,96 @@ namespace wf {
 constexpr int kU = 10;  // k-steps whose loads a wave issues together (16-wave blocks: 5)
 
 // ---------------------------------------------------------------- epilogue
+// Bias and residual values of the batch-1 tile (9 rows x TC columns), loaded at
+// kernel start so the epilogue does not wait on a global read.  Element it of a
+// thread is tile entry threadIdx.x + it * NT, as in the epilogue loop.
+template <int TC, int NT>
+struct EpiPre {
+  static constexpr int P = (kRows * TC + NT - 1) / NT;
+  float b[P], r[P];
+
+  template <typename S, int EPI>
+  __device__ __forceinline__ void load(const GemvArgs& a, int nb) {
+    if (a.nsplit != 3) return;
+    const S* bias = reinterpret_cast<const S*>(a.bias);
+#pragma unroll
+    for (int it = 0; it < P; ++it) {
+      const int idx = threadIdx.x + it * NT, ml = idx / TC, n = nb + idx % TC;
+      const bool in = idx < kRows * TC && n < a.N;
+      b[it] = (in && bias != nullptr) ? to_f(bias[n]) : 0.f;
+      if constexpr (EPI == EPI_RESID) r[it] = in ? a.y[(size_t)(a.slot0 * kRows + ml) * a.ldy + n] : 0.f;
+    }
+  }
+};
+
+// Output value v of (row, column n); res = current residual value (EPI_RESID).
+template <typename S, int EPI>
+__device__ __forceinline__ void epi_one(const GemvArgs& a, int row, int n, float v, float res) {
+  const int slot = row / kRows, r = row - slot * kRows;
+  if constexpr (EPI == EPI_STORE) {
+    a.y[(size_t)row * a.ldy + n] = v;
+  } else if constexpr (EPI == EPI_GELU) {
+    put_op<S>(a.aout, a.nsplit, a.R9, row, n, gelu_erf(v));
+  } else if constexpr (EPI == EPI_RESID) {
+    const float hn = res + v;
+    a.y[(size_t)row * a.ldy + n] = hn;
+    if (a.tap >= 0) put_op<S>(a.aout, a.nsplit, a.R9, row, a.tap * a.N + n, hn);
+  } else if constexpr (EPI == EPI_QKV) {
+    const int d = a.d;
+    if (n < d) {
+      a.y[(size_t)row * a.ldy + n] = v;
+    } else {
+      const int* st = a.state + slot * kStateInts;
+      const int nv = st[ST_NV], pos = st[ST_POS0] + r;
+      if (r < nv && pos < a.n_ctx) {
+        const int kv = n >= 2 * d;
+        const int cc = n - d - kv * d, head = cc >> 6, dim = cc & 63;
+        const int page = a.page_table[slot * a.pages_per_slot + (pos >> 4)];
+        S* cache = reinterpret_cast<S*>(a.cache) + (size_t)kv * a.kv_stride;
+        cache[(((size_t)page * a.n_head + head) * kPage + (pos & 15)) * kHeadDim + dim] = from_f<S>(v);
+      }
+    }
+  } else if constexpr (EPI == EPI_ARGMAX) {
+    if (a.y != nullptr) a.y[(size_t)row * a.ldy + n] = v;
+  } else if constexpr (EPI == EPI_PART) {
+    a.y[blockIdx.y * a.pstride + (size_t)row * a.ldy + n] = v;
+  }
+}
+
 // sv holds the wave-summed tile: TM operand rows (split terms) x TC columns.
 template <typename S, int EPI, int TM, int TC, int NT>
-__device__ void finish_tile(const GemvArgs& a, float (*sv)[TC + 1], float (*ov)[TC], int m0, int nb) {
+__device__ void finish_tile(const GemvArgs& a, float (*sv)[TC + 1], float (*ov)[TC], int m0, int nb,
+                            const EpiPre<TC, NT>& pre) {
   const bool split3 = a.nsplit == 3;
   const int R = a.slot0 * kRows, Rend = (a.slot0 + a.nslots) * kRows;
   const int nrows = split3 ? kRows : TM;
-  const S* bias = reinterpret_cast<const S*>(a.bias);
-  for (int idx = threadIdx.x; idx < nrows * TC; idx += NT) {
-    const int ml = idx / TC, c = idx % TC;
-    const int row = split3 ? ml : m0 + ml;
-    float v = split3 ? (sv[ml][c] + sv[ml + 9][c]) + sv[ml + 18][c] : sv[ml][c];
-    const int n = nb + c;
-    const bool act = row >= R && row < Rend && n < a.N;
-    if (act && bias != nullptr) v += to_f(bias[n]);
-    const int slot = row / kRows, r = row - slot * kRows;
-    if constexpr (EPI == EPI_STORE) {
-      if (act) a.y[(size_t)row * a.ldy + n] = v;
-    } else if constexpr (EPI == EPI_GELU) {
-      if (act) put_op<S>(a.aout, a.nsplit, a.R9, row, n, gelu_erf(v));
-    } else if constexpr (EPI == EPI_RESID) {
-      if (act) {
-        float* p = a.y + (size_t)row * a.ldy + n;
-        const float hn = *p + v;
-        *p = hn;
-        if (a.tap >= 0) put_op<S>(a.aout, a.nsplit, a.R9, row, a.tap * a.N + n, hn);
-      }
-    } else if constexpr (EPI == EPI_QKV) {
-      if (act) {
-        const int d = a.d;
-        if (n < d) {
-          a.y[(size_t)row * a.ldy + n] = v;
-        } else {
-          const int* st = a.state + slot * kStateInts;
-          const int nv = st[ST_NV], pos = st[ST_POS0] + r;
-          if (r < nv && pos < a.n_ctx) {
-            const int kv = n >= 2 * d;
-            const int cc = n - d - kv * d, head = cc >> 6, dim = cc & 63;
-            const int page = a.page_table[slot * a.pages_per_slot + (pos >> 4)];
-            S* cache = reinterpret_cast<S*>(a.cache) + (size_t)kv * a.kv_stride;
-            cache[(((size_t)page * a.n_head + head) * kPage + (pos & 15)) * kHeadDim + dim] = from_f<S>(v);
-          }
-        }
-      }
-    } else if constexpr (EPI == EPI_ARGMAX) {
-      if (act && a.y != nullptr) a.y[(size_t)row * a.ldy + n] = v;
-      ov[ml][c] = act ? v : -INFINITY;
+  if (split3) {
+    // rows r, r + 9, r + 18 hold the three split terms of row r
+#pragma unroll
+    for (int it = 0; it < EpiPre<TC, NT>::P; ++it) {
+      const int idx = threadIdx.x + it * NT;
+      if (idx >= kRows * TC) break;
+      const int ml = idx / TC, c = idx % TC, n = nb + c, row = R + ml;
+      const bool act = n < a.N;
+      const float v = ((sv[ml][c] + sv[ml + 9][c]) + sv[ml + 18][c]) + pre.b[it];
+      if (act) epi_one<S, EPI>(a, row, n, v, pre.r[it]);
+      if constexpr (EPI == EPI_ARGMAX) ov[ml][c] = act ? v : -INFINITY;
+    }
+  } else {
+    const S* bias = reinterpret_cast<const S*>(a.bias);
+    for (int idx = threadIdx.x; idx < TM * TC; idx += NT) {
+      const int ml = idx / TC, c = idx % TC, row = m0 + ml, n = nb + c;
+      const bool act = row >= R && row < Rend && n < a.N;
+      float v = sv[ml][c];
+      if (act && bias != nullptr) v += to_f(bias[n]);
+      if (act) epi_one<S, EPI>(a, row, n, v, EPI == EPI_RESID ? a.y[(size_t)row * a.ldy + n] : 0.f);
+      if constexpr (EPI == EPI_ARGMAX) ov[ml][c] = act ? v : -INFINITY;
     }
   }
   if constexpr (EPI == EPI_ARGMAX) {
     __syncthreads();
     for (int ml = threadIdx.x; ml < nrows; ml += NT) {
-      const int row = split3 ? ml : m0 + ml;
+      const int row = split3 ? R + ml : m0 + ml;
       if (row < R || row >= Rend) continue;
       float bv = ov[ml][0];
       int bi = nb;
@@ -96,6 +134,8 @@ __global__ void __launch_bounds__(NW * 64) k_gemv16(GemvArgs a) {
   __shared__ float sv[32][17];
   __shared__ float ov[32][16];
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  EpiPre<16, NW * 64> pre;
+  pre.template load<bf16, EPI>(a, blockIdx.x * 16);
   const int col = lane & 15, kg = lane >> 4;
   const int KS = a.K / 32;
   const int spw = (KS + NW - 1) / NW;
@@ -137,7 +177,83 @@ __global__ void __launch_bounds__(NW * 64) k_gemv16(GemvArgs a) {
       sv[ml][c] = s;
     }
     __syncthreads();
-    finish_tile<bf16, EPI, 32, 16, NW * 64>(a, sv, ov, tile0 * 16, blockIdx.x * 16);
+    finish_tile<bf16, EPI, 32, 16, NW * 64>(a, sv, ov, tile0 * 16, blockIdx.x * 16, pre);
+    if (a.nsplit == 3) break;
+  }
+}
+
+// ---------------------------------------------------------------- bf16, CT 16-column tiles, split-K
+// A block covers CT adjacent 16-column tiles (the operand fragments loaded per
+// k-step serve CT weight fragments) and one of gridDim.y contiguous k-ranges;
+// with more than one k-range the epilogue must be EPI_PART.
+template <int EPI, int NW, int CT>
+__global__ void __launch_bounds__(NW * 64) k_gemv16w(GemvArgs a) {
+  constexpr int U = CT >= 4 ? 4 : 8;
+  constexpr int TC = 16 * CT;
+  __shared__ float red[NW][32][TC + 1];
+  __shared__ float sv[32][TC + 1];
+  __shared__ float ov[32][TC];
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  EpiPre<TC, NW * 64> pre;
+  pre.template load<bf16, EPI>(a, blockIdx.x * TC);
+  const int col = lane & 15, kg = lane >> 4;
+  const int KS = a.K / 32;
+  const int ntile = (a.N + 15) / 16;
+  const int kss = (KS + gridDim.y - 1) / gridDim.y;
+  const int k0 = min(KS, (int)blockIdx.y * kss), k1 = min(KS, k0 + kss);
+  const int spw = (k1 - k0 + NW - 1) / NW;
+  const int s0 = min(k1, k0 + wv * spw), s1 = min(k1, s0 + spw);
+  const bf16x8* Wt = reinterpret_cast<const bf16x8*>(a.w) + (size_t)blockIdx.x * CT * KS * 64 + lane;
+  const bf16x8* Ab = reinterpret_cast<const bf16x8*>(a.a.p) + lane;
+  const int MT = a.a.mt;
+  bool tv[CT];
+#pragma unroll
+  for (int c = 0; c < CT; ++c) tv[c] = (int)blockIdx.x * CT + c < ntile;
+  for (int tile0 = a.mt0; tile0 < a.mt1; tile0 += 2) {
+    const bool two = tile0 + 1 < a.mt1;
+    floatx4 acc0[CT], acc1[CT];
+#pragma unroll
+    for (int c = 0; c < CT; ++c) acc0[c] = acc1[c] = floatx4{0.f, 0.f, 0.f, 0.f};
+    for (int st = s0; st < s1; st += U) {
+      bf16x8 bw[U][CT], a0[U], a1[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int ss = min(st + u, s1 - 1);
+#pragma unroll
+        for (int c = 0; c < CT; ++c)
+          if (tv[c]) bw[u][c] = Wt[((size_t)c * KS + ss) * 64];
+        a0[u] = Ab[((size_t)ss * MT + tile0) * 64];
+        if (two) a1[u] = Ab[((size_t)ss * MT + tile0 + 1) * 64];
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+        if (st + u < s1) {
+#pragma unroll
+          for (int c = 0; c < CT; ++c)
+            if (tv[c]) {
+              acc0[c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0[u], bw[u][c], acc0[c], 0, 0, 0);
+              if (two) acc1[c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1[u], bw[u][c], acc1[c], 0, 0, 0);
+            }
+        }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int c = 0; c < CT; ++c)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        red[wv][kg * 4 + v][16 * c + col] = acc0[c][v];
+        red[wv][16 + kg * 4 + v][16 * c + col] = acc1[c][v];
+      }
+    __syncthreads();
+    for (int idx = threadIdx.x; idx < 32 * TC; idx += NW * 64) {
+      const int ml = idx / TC, c = idx % TC;
+      float s = 0.f;
+#pragma unroll
+      for (int w = 0; w < NW; ++w) s += red[w][ml][c];
+      sv[ml][c] = s;
+    }
+    __syncthreads();
+    finish_tile<bf16, EPI, 32, TC, NW * 64>(a, sv, ov, tile0 * 16, blockIdx.x * TC, pre);
     if (a.nsplit == 3) break;
   }
 }
@@ -150,6 +266,8 @@ __global__ void __launch_bounds__(NW * 64) k_gemv32(GemvArgs a) {
   __shared__ float sv[32][33];
   __shared__ float ov[32][32];
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  EpiPre<32, NW * 64> pre;
+  pre.template load<bf16, EPI>(a, blockIdx.x * 32);
   const int col = lane & 31, kg = lane >> 5;
   const int KS = a.K / 16;
   const int spw = (KS + NW - 1) / NW;
@@ -185,9 +303,216 @@ __global__ void __launch_bounds__(NW * 64) k_gemv32(GemvArgs a) {
       sv[ml][c] = s;
     }
     __syncthreads();
-    finish_tile<bf16, EPI, 32, 32, NW * 64>(a, sv, ov, tile0 * 32, blockIdx.x * 32);
+    finish_tile<bf16, EPI, 32, 32, NW * 64>(a, sv, ov, tile0 * 32, blockIdx.x * 32, pre);
     if (a.nsplit == 3) break;
   }
+}
+
+// ---------------------------------------------------------------- LayerNorm folded in (bf16, batch 1)
+// The block normalises the 9 rows of the pass itself (two-pass mean and variance
+// over K, then gain and bias, as a separate LayerNorm would) and writes their
+// three bf16 split terms (rows r, 9 + r, 18 + r; rows 27..31 zero) into LDS in
+// the fragment order of its tile shape.  Each wave handles rows wv, wv + NW, ...
+// with every load of its rows in flight at once.
+__device__ __forceinline__ uint4 pack8(const uint32_t* h) {
+  return make_uint4(h[0] | ((uint32_t)h[1] << 16), h[2] | ((uint32_t)h[3] << 16), h[4] | ((uint32_t)h[5] << 16),
+                    h[6] | ((uint32_t)h[7] << 16));
+}
+
+// LDS slot of operand chunk (row m, k..k+7): fragment order with the 16-byte slot
+// inside each 256-byte group XOR-swizzled by the group index, so that both the
+// staging writes (one row, many k) and the fragment reads (64 consecutive slots)
+// spread over the banks.
+__device__ __forceinline__ int lds_swz(int i) { return i ^ ((i >> 4) & 15); }
+template <int TILE>
+__device__ __forceinline__ int lds_frag(int m, int k) {
+  if constexpr (TILE == 16) return lds_swz(((k >> 5) * 2 + (m >> 4)) * 64 + (m & 15) + 16 * ((k & 31) >> 3));
+  else return lds_swz((k >> 4) * 64 + (m & 31) + 32 * ((k & 15) >> 3));
+}
+
+// The rows, gains and biases a wave needs, loaded before the weights so the
+// normalisation only waits for them.
+template <int NW>
+struct LnRows {
+  static constexpr int RPW = (kRows + NW - 1) / NW;
+  static constexpr int J = (kLnFoldMaxK / 8 + 63) / 64;
+  float x[RPW][J][8];
+  uint4 gr[J], br[J];
+
+  __device__ __forceinline__ void load(const GemvArgs& a) {
+    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+    const int nch = a.K >> 3;
+    const uint4* G = reinterpret_cast<const uint4*>(a.lng);
+    const uint4* B = reinterpret_cast<const uint4*>(a.lnb);
+#pragma unroll
+    for (int j = 0; j < J; ++j) {
+      const int c = lane + 64 * j;
+      const bool ok = c < nch;
+#pragma unroll
+      for (int i = 0; i < RPW; ++i) {
+        const int r = wv + NW * i;
+        if (ok && r < kRows) {
+          ld8(a.lnx + (size_t)r * a.K + 8 * c, x[i][j]);
+        } else {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) x[i][j][e] = 0.f;
+        }
+      }
+      gr[j] = ok ? G[c] : make_uint4(0u, 0u, 0u, 0u);
+      br[j] = ok ? B[c] : make_uint4(0u, 0u, 0u, 0u);
+    }
+  }
+
+  template <int TILE>
+  __device__ __forceinline__ void stage(const GemvArgs& a, uint4* aop) {
+    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+    const int K = a.K, nch = K >> 3;
+    // statistics of all the wave's rows as independent chains (rows past the
+    // last are zeros and are not written)
+    float mean[RPW], inv[RPW];
+#pragma unroll
+    for (int i = 0; i < RPW; ++i) {
+      float s = 0.f;
+#pragma unroll
+      for (int j = 0; j < J; ++j)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) s += x[i][j][e];
+      mean[i] = wave_sum(s) / (float)K;
+    }
+#pragma unroll
+    for (int i = 0; i < RPW; ++i) {
+      float q = 0.f;
+#pragma unroll
+      for (int j = 0; j < J; ++j) {
+        if (lane + 64 * j < nch) {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const float cdev = x[i][j][e] - mean[i];
+            q += cdev * cdev;
+          }
+        }
+      }
+      inv[i] = 1.0f / sqrtf(wave_sum(q) / (float)K + 1e-5f);
+    }
+#pragma unroll
+    for (int i = 0; i < RPW; ++i) {
+      const int r = wv + NW * i;
+      if (r >= kRows) break;
+#pragma unroll
+      for (int j = 0; j < J; ++j) {
+        const int c = lane + 64 * j;
+        if (c >= nch) continue;
+        const uint32_t gw[4] = {gr[j].x, gr[j].y, gr[j].z, gr[j].w};
+        const uint32_t bw[4] = {br[j].x, br[j].y, br[j].z, br[j].w};
+        uint32_t th[8], tm[8], tl[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const float g = __uint_as_float(e & 1 ? gw[e >> 1] & 0xffff0000u : gw[e >> 1] << 16);
+          const float b = __uint_as_float(e & 1 ? bw[e >> 1] & 0xffff0000u : bw[e >> 1] << 16);
+          split3_bits((x[i][j][e] - mean[i]) * inv[i] * g + b, th[e], tm[e], tl[e]);
+        }
+        aop[lds_frag<TILE>(r, 8 * c)] = pack8(th);
+        aop[lds_frag<TILE>(kRows + r, 8 * c)] = pack8(tm);
+        aop[lds_frag<TILE>(2 * kRows + r, 8 * c)] = pack8(tl);
+      }
+    }
+    for (int t = threadIdx.x; t < (32 - 3 * kRows) * nch; t += NW * 64)
+      aop[lds_frag<TILE>(3 * kRows + t / nch, 8 * (t % nch))] = make_uint4(0u, 0u, 0u, 0u);
+  }
+};
+
+// 16-column tiles; every wave's k-steps fit one batch of loads (K <= kLnFoldMaxK).
+template <int EPI, int NW, int U>
+__global__ void __launch_bounds__(NW * 64) k_gemv16_ln(GemvArgs a) {
+  __shared__ uint4 aop[kLnFoldMaxK / 32 * 2 * 64];
+  __shared__ float red[NW][32][17];
+  __shared__ float sv[32][17];
+  __shared__ float ov[32][16];
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  EpiPre<16, NW * 64> pre;
+  pre.template load<bf16, EPI>(a, blockIdx.x * 16);
+  const int col = lane & 15, kg = lane >> 4;
+  const int KS = a.K / 32;
+  const int spw = (KS + NW - 1) / NW;
+  const int s0 = min(KS, wv * spw), s1 = min(KS, s0 + spw);
+  const bf16x8* Wt = reinterpret_cast<const bf16x8*>(a.w) + (size_t)blockIdx.x * KS * 64 + lane;
+  LnRows<NW> rows;
+  rows.load(a);
+  bf16x8 bw[U];
+#pragma unroll
+  for (int u = 0; u < U; ++u)
+    if (s0 + u < s1) bw[u] = Wt[(size_t)(s0 + u) * 64];
+  rows.template stage<16>(a, aop);
+  __syncthreads();
+  floatx4 acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int u = 0; u < U; ++u)
+    if (s0 + u < s1) {
+      const bf16x8 a0 = __builtin_bit_cast(bf16x8, aop[lds_swz(((s0 + u) * 2) * 64 + lane)]);
+      const bf16x8 a1 = __builtin_bit_cast(bf16x8, aop[lds_swz(((s0 + u) * 2 + 1) * 64 + lane)]);
+      acc0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0, bw[u], acc0, 0, 0, 0);
+      acc1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1, bw[u], acc1, 0, 0, 0);
+    }
+#pragma unroll
+  for (int v = 0; v < 4; ++v) {
+    red[wv][kg * 4 + v][col] = acc0[v];
+    red[wv][16 + kg * 4 + v][col] = acc1[v];
+  }
+  __syncthreads();
+  for (int idx = threadIdx.x; idx < 32 * 16; idx += NW * 64) {
+    const int ml = idx >> 4, c = idx & 15;
+    float s = 0.f;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) s += red[w][ml][c];
+    sv[ml][c] = s;
+  }
+  __syncthreads();
+  finish_tile<bf16, EPI, 32, 16, NW * 64>(a, sv, ov, 0, blockIdx.x * 16, pre);
+}
+
+// 32-column tiles; every wave's k-steps fit one batch of loads (K <= kLnFoldMaxK).
+template <int EPI, int NW, int U>
+__global__ void __launch_bounds__(NW * 64) k_gemv32_ln(GemvArgs a) {
+  __shared__ uint4 aop[kLnFoldMaxK / 16 * 64];
+  __shared__ float red[NW][32][33];
+  __shared__ float sv[32][33];
+  __shared__ float ov[32][32];
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  EpiPre<32, NW * 64> pre;
+  pre.template load<bf16, EPI>(a, blockIdx.x * 32);
+  const int col = lane & 31, kg = lane >> 5;
+  const int KS = a.K / 16;
+  const int spw = (KS + NW - 1) / NW;
+  const int s0 = min(KS, wv * spw), s1 = min(KS, s0 + spw);
+  const bf16x8* Wt = reinterpret_cast<const bf16x8*>(a.w) + (size_t)blockIdx.x * KS * 64 + lane;
+  LnRows<NW> rows;
+  rows.load(a);
+  bf16x8 bw[U];
+#pragma unroll
+  for (int u = 0; u < U; ++u)
+    if (s0 + u < s1) bw[u] = Wt[(size_t)(s0 + u) * 64];
+  rows.template stage<32>(a, aop);
+  __syncthreads();
+  floatx16 acc = {};
+#pragma unroll
+  for (int u = 0; u < U; ++u)
+    if (s0 + u < s1)
+      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, aop[lds_swz((s0 + u) * 64 + lane)]), bw[u],
+                                                     acc, 0, 0, 0);
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) red[wv][8 * i + 4 * kg + j][col] = acc[4 * i + j];
+  __syncthreads();
+  for (int idx = threadIdx.x; idx < 32 * 32; idx += NW * 64) {
+    const int ml = idx >> 5, c = idx & 31;
+    float s = 0.f;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) s += red[w][ml][c];
+    sv[ml][c] = s;
+  }
+  __syncthreads();
+  finish_tile<bf16, EPI, 32, 32, NW * 64>(a, sv, ov, 0, blockIdx.x * 32, pre);
 }
 
 // ---------------------------------------------------------------- fp32, row-major
@@ -202,6 +527,8 @@ __global__ void __launch_bounds__(NW * 64) k_gemv_f32(GemvArgs a) {
   const float* __restrict__ W = reinterpret_cast<const float*>(a.w);
   const float* __restrict__ A = reinterpret_cast<const float*>(a.a.p);
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  EpiPre<16, NW * 64> pre;
+  pre.template load<float, EPI>(a, blockIdx.x * 16);
   const int col = lane & 15, kg = lane >> 4;
   const int nb = blockIdx.x * 16;
   const int K = a.K, lda = a.a.ld;
@@ -253,7 +580,7 @@ __global__ void __launch_bounds__(NW * 64) k_gemv_f32(GemvArgs a) {
       sv[ml][c] = s;
     }
     __syncthreads();
-    finish_tile<float, EPI, 32, 16, NW * 64>(a, sv, ov, tile0 * 16, nb);
+    finish_tile<float, EPI, 32, 16, NW * 64>(a, sv, ov, tile0 * 16, nb, pre);
   }
 }
 
@@ -296,8 +623,32 @@ static void launch_f32(const GemvArgs& a, hipStream_t st) {
   k_gemv_f32<EPI, NW><<<(a.N + 15) / 16, NW * 64, 0, st>>>(a);
 }
 
+// 16 waves: one row of the LayerNorm per wave; K <= kLnFoldMaxK gives at most
+// kLnFoldMaxK / 16 / 16 = 5 k-steps per wave.
+constexpr int kLnWaves = 16;
+constexpr int kLnSteps = kLnFoldMaxK / 16 / kLnWaves;
+template <int EPI>
+static void launch_ln(const GemvArgs& a, hipStream_t st) {
+  if (a.wkind == W_F32) {
+    k_gemv32_ln<EPI, kLnWaves, kLnSteps><<<(a.N + 31) / 32, kLnWaves * 64, 0, st>>>(a);
+  } else {
+    k_gemv16_ln<EPI, kLnWaves, kLnSteps><<<(a.N + 15) / 16, kLnWaves * 64, 0, st>>>(a);
+  }
+}
+
 template <typename S, int EPI>
 static void launch_epi(const GemvArgs& a, hipStream_t st) {
+  if constexpr (sizeof(S) == 2) {
+    if (a.lnx != nullptr) {
+      launch_ln<EPI>(a, st);
+      return;
+    }
+    if constexpr (EPI == EPI_PART) {  // 64-column blocks, k split over grid y
+      const int ntile = (a.N + 15) / 16;
+      k_gemv16w<EPI, 8, 4><<<dim3((ntile + 3) / 4, a.ksplit > 1 ? a.ksplit : 1), 512, 0, st>>>(a);
+      return;
+    }
+  }
   // waves per block: enough that each wave's share of the k-steps fits one batch
   const int kstep = sizeof(S) == 4 ? 16 : (a.wkind == W_F32 ? 16 : 32);
   const int steps = a.K / kstep;
@@ -320,6 +671,7 @@ void Ops<S>::gemv(int epi, const GemvArgs& a, hipStream_t st) {
     case EPI_RESID: launch_epi<S, EPI_RESID>(a, st); break;
     case EPI_QKV: launch_epi<S, EPI_QKV>(a, st); break;
     case EPI_ARGMAX: launch_epi<S, EPI_ARGMAX>(a, st); break;
+    case EPI_PART: launch_epi<S, EPI_PART>(a, st); break;
   }
 }
 

@@ -60,19 +60,31 @@ __global__ void __launch_bounds__(256) k_ln_operand(LnArgs a) {
 // Lane (col = lane % 16, kg = lane / 16) streams 16-byte chunks of weight row
 // n0 + col (8 per round in flight) as the B operand of v_mfma_f32_16x16x32_bf16
 
-// final argmax over the per-block partials of each row; flags non-finite maxima
+// final argmax over the per-block partials of each row; flags non-finite maxima.
+// Drafter pass (keep != null): rows 1..K of slot s are the drafted tokens, also
+// stored to keep[s * K + j] and, if given, dst[(s - slot0) * K + j].
+constexpr int kArgmaxLoads = 8;
 __global__ void __launch_bounds__(256) k_argmax_final(const float* __restrict__ hv, const int* __restrict__ hi,
                                                       int nblk, int row0, int* __restrict__ g,
-                                                      float* __restrict__ gmax, unsigned* status) {
+                                                      float* __restrict__ gmax, unsigned* status, int* keep, int* dst,
+                                                      int slot0, int K) {
   __shared__ float bvs[4];
   __shared__ int bis[4];
   const int row = row0 + blockIdx.x;
   float bv = -INFINITY;
   int bi = 0x7fffffff;
-  for (int j = threadIdx.x; j < nblk; j += 256) {
-    float v = hv[(size_t)row * nblk + j];
-    int i = hi[(size_t)row * nblk + j];
-    if (better(v, i, bv, bi)) { bv = v; bi = i; }
+  for (int j0 = threadIdx.x; j0 < nblk; j0 += 256 * kArgmaxLoads) {
+    float v[kArgmaxLoads];
+    int ix[kArgmaxLoads];
+#pragma unroll
+    for (int u = 0; u < kArgmaxLoads; ++u) {
+      const int j = j0 + 256 * u;
+      v[u] = j < nblk ? hv[(size_t)row * nblk + j] : -INFINITY;
+      ix[u] = j < nblk ? hi[(size_t)row * nblk + j] : 0x7fffffff;
+    }
+#pragma unroll
+    for (int u = 0; u < kArgmaxLoads; ++u)
+      if (better(v[u], ix[u], bv, bi)) { bv = v[u]; bi = ix[u]; }
   }
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) {
@@ -89,6 +101,11 @@ __global__ void __launch_bounds__(256) k_argmax_final(const float* __restrict__ 
     g[row] = bis[0];
     gmax[row] = bvs[0];
     if (!isfinite(bvs[0])) atomicOr(status, WF_STATUS_NONFINITE_LOGITS);
+    const int slot = row / kRows, i = row - slot * kRows;
+    if (keep != nullptr && i >= 1 && i <= K) {
+      keep[(size_t)slot * K + i - 1] = bis[0];
+      if (dst != nullptr) dst[(size_t)(slot - slot0) * K + i - 1] = bis[0];
+    }
   }
 }
 
@@ -104,85 +121,116 @@ __device__ __forceinline__ float emb_at(const BeginArgs& a, int tok, int c) {
 }
 
 // ---------------------------------------------------------------- pass set-up
+// Rows of a pass: h[slot * 9 + i] = E[toks[i]] + P[pos[i]] (target) or E[anchor] /
+// mask vector (drafter).  Work is split into 8-column chunks, every load of a
+// thread issued before the first add.
+constexpr int kBeginTasks = 9;  // chunk tasks per thread: 9 rows * 2048 / 8 / 256
+template <typename S>
+__device__ __forceinline__ void fill_rows(const BeginArgs& a, int slot, const int* toks, const int* poss, bool mask_rows) {
+  const S* E = reinterpret_cast<const S*>(a.emb);
+  const S* P = reinterpret_cast<const S*>(a.pos);
+  const int nch = a.d >> 3;
+  float e8[kBeginTasks][8], p8[kBeginTasks][8];
+#pragma unroll
+  for (int j = 0; j < kBeginTasks; ++j) {
+    const int t = threadIdx.x + 256 * j, i = t / nch, c = 8 * (t % nch);
+    if (i < kRows) {
+      const int tok = toks[i];
+      const bool from_mask = mask_rows && i > 0;
+      if (!from_mask) {
+        const size_t ei = a.emb_kind == W_F32 ? wfrag32_index(tok, c, a.d / 16) : (size_t)tok * a.d + c;
+        ld8(E + ei, e8[j]);
+      } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) e8[j][e] = 0.f;
+      }
+      if (mask_rows) {
+        if (from_mask) ld8(P + c, p8[j]);
+        else {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) p8[j][e] = 0.f;
+        }
+      } else {
+        ld8(P + (size_t)poss[i] * a.d + c, p8[j]);
+      }
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < kBeginTasks; ++j) {
+    const int t = threadIdx.x + 256 * j, i = t / nch, c = 8 * (t % nch);
+    if (i < kRows) {
+      float* hr = a.h + (size_t)(slot * kRows + i) * a.d + c;
+      *reinterpret_cast<float4*>(hr) = make_float4(e8[j][0] + p8[j][0], e8[j][1] + p8[j][1], e8[j][2] + p8[j][2], e8[j][3] + p8[j][3]);
+      *reinterpret_cast<float4*>(hr + 4) =
+          make_float4(e8[j][4] + p8[j][4], e8[j][5] + p8[j][5], e8[j][6] + p8[j][6], e8[j][7] + p8[j][7]);
+    }
+  }
+}
+
 // Verify rows: [anchor, c_1..c_k] at positions L..L+k with the budget rule
 // k = min(K, k_max, max_new - emitted - 1, n_ctx - L - 1) (Appendix A.1).
 template <typename S>
 __global__ void __launch_bounds__(256) k_verify_begin(BeginArgs a) {
-  __shared__ int toks[kRows];
-  __shared__ int pos0s, nvs;
+  __shared__ int toks[kRows], poss[kRows];
   const int slot = a.slot0 + blockIdx.x;
   int* st = a.state + slot * kStateInts;
+  const int L = st[ST_L], left = st[ST_MAX_NEW] - st[ST_EMITTED], anchor = st[ST_ANCHOR];
+  const bool go = st[ST_LIVE] && !st[ST_DONE] && left > 0 && L < a.n_ctx;
+  const int nv = go ? min(min(a.block_k, a.k_max), min(left - 1, a.n_ctx - L - 1)) + 1 : 0;
+  if (threadIdx.x < kRows) {
+    const int i = threadIdx.x;
+    int t = (i == 0 || i >= nv) ? anchor : a.draft[(size_t)blockIdx.x * a.block_k + i - 1];
+    t = min(max(t, 0), a.n_vocab - 1);
+    toks[i] = t;
+    poss[i] = min(L + i, a.n_ctx - 1);
+    a.tok[slot * kRows + i] = t;
+  }
   if (threadIdx.x == 0) {
-    const int L = st[ST_L], left = st[ST_MAX_NEW] - st[ST_EMITTED];
-    int nv = 0;
-    if (st[ST_LIVE] && !st[ST_DONE] && left > 0 && L < a.n_ctx) {
-      int k = min(min(a.block_k, a.k_max), min(left - 1, a.n_ctx - L - 1));
-      nv = k + 1;
-    }
     st[ST_POS0] = L;
     st[ST_NV] = nv;
-    pos0s = L;
-    nvs = nv;
-    const int anchor = st[ST_ANCHOR];
-    for (int i = 0; i < kRows; ++i) {
-      int t = (i == 0 || i >= nv) ? anchor : a.draft[(size_t)blockIdx.x * a.block_k + i - 1];
-      t = min(max(t, 0), a.n_vocab - 1);
-      toks[i] = t;
-      a.tok[slot * kRows + i] = t;
-    }
   }
   __syncthreads();
-  const S* P = reinterpret_cast<const S*>(a.pos);
-  for (int i = 0; i < kRows; ++i) {
-    const int p = min(pos0s + i, a.n_ctx - 1);
-    float* hr = a.h + (size_t)(slot * kRows + i) * a.d;
-    for (int c = threadIdx.x; c < a.d; c += 256) hr[c] = emb_at<S>(a, toks[i], c) + to_f(P[(size_t)p * a.d + c]);
-  }
+  fill_rows<S>(a, slot, toks, poss, false);
 }
 
-// Draft block X_t = [Emb(y_t), m, ..., m] (Eq. 2).
+// Draft block X_t = [Emb(y_t), m, ..., m] (Eq. 2).  The drafter history is up to
+// date at this point, so its pending-row count is cleared here.
 template <typename S>
 __global__ void __launch_bounds__(256) k_draft_begin(BeginArgs a) {
+  __shared__ int toks[kRows];
   const int slot = a.slot0 + blockIdx.x;
-  const int* st = a.state + slot * kStateInts;
-  const int anchor = min(max(st[ST_ANCHOR], 0), a.n_vocab - 1);
-  const S* m = reinterpret_cast<const S*>(a.pos);
-  for (int i = 0; i < kRows; ++i) {
-    float* hr = a.h + (size_t)(slot * kRows + i) * a.d;
-    for (int c = threadIdx.x; c < a.d; c += 256) hr[c] = (i == 0) ? emb_at<S>(a, anchor, c) : to_f(m[c]);
-  }
+  int* st = a.state + slot * kStateInts;
+  if (threadIdx.x < kRows) toks[threadIdx.x] = min(max(st[ST_ANCHOR], 0), a.n_vocab - 1);
+  __syncthreads();
+  if (threadIdx.x == 0) st[ST_HN] = 0;
+  fill_rows<S>(a, slot, toks, nullptr, true);
 }
 
 // Prefill chunk c: prompt positions 9c..9c+8 of each slot.
 template <typename S>
 __global__ void __launch_bounds__(256) k_prefill_begin(BeginArgs a) {
-  __shared__ int toks[kRows];
-  __shared__ int pos0s;
+  __shared__ int toks[kRows], poss[kRows];
   const int slot = a.slot0 + blockIdx.x;
   int* st = a.state + slot * kStateInts;
+  const int len = st[ST_LEN];
+  const int pos0 = a.chunk * kRows;
+  const int nv = max(0, min(kRows, len - pos0));
+  if (threadIdx.x < kRows) {
+    const int i = threadIdx.x;
+    int t = (i < nv) ? a.draft[(size_t)blockIdx.x * a.pmax + pos0 + i] : 0;
+    t = min(max(t, 0), a.n_vocab - 1);
+    toks[i] = t;
+    poss[i] = min(pos0 + i, a.n_ctx - 1);
+    a.tok[slot * kRows + i] = t;
+  }
   if (threadIdx.x == 0) {
-    const int len = st[ST_LEN];
-    const int pos0 = a.chunk * kRows;
-    const int nv = max(0, min(kRows, len - pos0));
     st[ST_POS0] = pos0;
     st[ST_NV] = nv;
     st[ST_HPOS] = pos0;
     st[ST_HN] = nv;
-    pos0s = pos0;
-    for (int i = 0; i < kRows; ++i) {
-      int t = (i < nv) ? a.draft[(size_t)blockIdx.x * a.pmax + pos0 + i] : 0;
-      t = min(max(t, 0), a.n_vocab - 1);
-      toks[i] = t;
-      a.tok[slot * kRows + i] = t;
-    }
   }
   __syncthreads();
-  const S* P = reinterpret_cast<const S*>(a.pos);
-  for (int i = 0; i < kRows; ++i) {
-    const int p = min(pos0s + i, a.n_ctx - 1);
-    float* hr = a.h + (size_t)(slot * kRows + i) * a.d;
-    for (int c = threadIdx.x; c < a.d; c += 256) hr[c] = emb_at<S>(a, toks[i], c) + to_f(P[(size_t)p * a.d + c]);
-  }
+  fill_rows<S>(a, slot, toks, poss, false);
 }
 
 // keep the final hidden row of each slot's last prompt position (row 0 of lasth)
@@ -240,11 +288,6 @@ __global__ void __launch_bounds__(256) k_hist_write(HistArgs a) {
   }
 }
 
-__global__ void k_hist_done(int* state, int slot0, int n) {
-  const int s = blockIdx.x * blockDim.x + threadIdx.x;
-  if (s < n) state[(slot0 + s) * kStateInts + ST_HN] = 0;
-}
-
 // ---------------------------------------------------------------- acceptance
 // Greedy longest-prefix rule (Section 3.1) with the end-of-transcript rule and
 // the cache/anchor update of Appendix A.1.  One thread per slot.
@@ -264,8 +307,12 @@ __global__ void k_accept_greedy(AcceptArgs a) {
     return;
   }
   const int k = nv - 1;
-  const int* tok = a.tok + slot * kRows;
-  const int* g = a.g + slot * kRows;
+  int tok[kRows], g[kRows];
+#pragma unroll
+  for (int i = 0; i < kRows; ++i) {
+    tok[i] = a.tok[slot * kRows + i];
+    g[i] = a.g[slot * kRows + i];
+  }
   int acc = 0;
   while (acc < k && tok[acc + 1] == g[acc]) ++acc;
   int nemit = 0;
@@ -302,17 +349,6 @@ __global__ void k_accept_greedy(AcceptArgs a) {
   if (a.n_out) a.n_out[s] = nemit;
   if (a.n_acc) a.n_acc[s] = acc;
   if (a.done) a.done[s] = done;
-}
-
-// drafted tokens = argmax of mask rows 1..K
-__global__ void k_draft_tokens(const int* __restrict__ g, int* __restrict__ dst, int* __restrict__ keep, int slot0,
-                               int n, int K) {
-  const int t = blockIdx.x * blockDim.x + threadIdx.x;
-  if (t >= n * K) return;
-  const int s = t / K, j = t % K;
-  const int v = g[(slot0 + s) * kRows + 1 + j];
-  if (dst) dst[t] = v;
-  keep[(size_t)(slot0 + s) * K + j] = v;
 }
 
 // ---------------------------------------------------------------- encode: cross K/V
@@ -367,10 +403,87 @@ __global__ void __launch_bounds__(256) k_gemm_xkv(XkvArgs a) {
 }
 
 
+// ---------------------------------------------------------------- split-K reduction + LayerNorm
+// h[row] += sum over the partial products (fixed order) + bias; the new h is also
+// written as the drafter tap operand when requested; then, if a gain is given,
+// LayerNorm(h[row]) as the operand of the next product (same formula as the
+// separate LayerNorm).  One block per row; column c of the row is thread c % 1024.
+constexpr int kRlnThreads = 1024;
+constexpr int kRlnMaxParts = 16;
+template <typename S>
+__global__ void __launch_bounds__(kRlnThreads) k_reduce_ln(RlnArgs a) {
+  constexpr int NW = kRlnThreads / 64;
+  constexpr int J = 2;  // d <= 2048
+  __shared__ float red[2][NW];
+  const int row = a.row0 + blockIdx.x;
+  const int d = a.d;
+  const S* bias = reinterpret_cast<const S*>(a.bias);
+  float* hr = a.h + (size_t)row * d;
+  float v[J];
+  // every load of the row is issued before the first add
+  float x[J], pv[J][kRlnMaxParts], bv[J];
+#pragma unroll
+  for (int j = 0; j < J; ++j) {
+    const int c = threadIdx.x + j * kRlnThreads;
+    const bool ok = c < d;
+    x[j] = ok ? hr[c] : 0.f;
+    bv[j] = (ok && bias != nullptr) ? to_f(bias[c]) : 0.f;
+#pragma unroll
+    for (int p = 0; p < kRlnMaxParts; ++p)
+      pv[j][p] = (ok && p < a.nparts) ? a.part[p * a.pstride + (size_t)row * d + c] : 0.f;
+  }
+#pragma unroll
+  for (int j = 0; j < J; ++j) {
+    const int c = threadIdx.x + j * kRlnThreads;
+    float sum = 0.f;
+#pragma unroll
+    for (int p = 0; p < kRlnMaxParts; ++p) sum += pv[j][p];
+    v[j] = x[j] + (sum + bv[j]);
+    if (c < d) {
+      hr[c] = v[j];
+      if (a.tapcol >= 0) put_op<S>(a.tap, a.nsplit, a.R9, row, a.tapcol + c, v[j]);
+    }
+  }
+  if (a.g == nullptr) return;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  float s = wave_sum(v[0] + v[1]);
+  if (lane == 0) red[0][w] = s;
+  __syncthreads();
+  float tot = 0.f;
+#pragma unroll
+  for (int i = 0; i < NW; ++i) tot += red[0][i];
+  const float mean = tot / (float)d;
+  float q = 0.f;
+#pragma unroll
+  for (int j = 0; j < J; ++j) {
+    const int c = threadIdx.x + j * kRlnThreads;
+    const float cdev = v[j] - mean;
+    q += c < d ? cdev * cdev : 0.f;
+  }
+  q = wave_sum(q);
+  if (lane == 0) red[1][w] = q;
+  __syncthreads();
+  float qt = 0.f;
+#pragma unroll
+  for (int i = 0; i < NW; ++i) qt += red[1][i];
+  const float inv = 1.0f / sqrtf(qt / (float)d + 1e-5f);
+  const S* g = reinterpret_cast<const S*>(a.g);
+  const S* b = reinterpret_cast<const S*>(a.b);
+#pragma unroll
+  for (int j = 0; j < J; ++j) {
+    const int c = threadIdx.x + j * kRlnThreads;
+    if (c < d) put_op<S>(a.out, a.nsplit, a.R9, row, c, (v[j] - mean) * inv * to_f(g[c]) + to_f(b[c]));
+  }
+}
+
 // ---------------------------------------------------------------- launchers
 template <typename S>
 void Ops<S>::ln_operand(const LnArgs& a, int rows, hipStream_t st) {
   k_ln_operand<S><<<rows, 256, 0, st>>>(a);
+}
+template <typename S>
+void Ops<S>::reduce_ln(const RlnArgs& a, int rows, hipStream_t st) {
+  k_reduce_ln<S><<<rows, kRlnThreads, 0, st>>>(a);
 }
 template <typename S>
 void Ops<S>::verify_begin(const BeginArgs& a, int n, hipStream_t st) { k_verify_begin<S><<<n, 256, 0, st>>>(a); }
@@ -386,8 +499,8 @@ void Ops<S>::gemm_xkv(const XkvArgs& a, hipStream_t st) {
 }
 
 void argmax_final(const float* hv, const int* hi, int nblk, int row0, int rows, int* g, float* gmax,
-                  unsigned* status, hipStream_t st) {
-  k_argmax_final<<<rows, 256, 0, st>>>(hv, hi, nblk, row0, g, gmax, status);
+                  unsigned* status, int* keep, int* dst, int slot0, int K, hipStream_t st) {
+  k_argmax_final<<<rows, 256, 0, st>>>(hv, hi, nblk, row0, g, gmax, status, keep, dst, slot0, K);
 }
 void save_last(const float* h, float* lasth, const int* state, int slot0, int n, int d, int chunk, hipStream_t st) {
   k_save_last<<<n, 256, 0, st>>>(h, lasth, state, slot0, d, chunk);
@@ -395,14 +508,11 @@ void save_last(const float* h, float* lasth, const int* state, int slot0, int n,
 void prefill_finish(int* state, const int* g, int slot0, int n, int eos, int n_ctx, int* first, hipStream_t st) {
   k_prefill_finish<<<(n + 63) / 64, 64, 0, st>>>(state, g, slot0, n, eos, n_ctx, first);
 }
-void hist_done(int* state, int slot0, int n, hipStream_t st) { k_hist_done<<<(n + 63) / 64, 64, 0, st>>>(state, slot0, n); }
 void accept_greedy(const AcceptArgs& a, hipStream_t st) { k_accept_greedy<<<(a.n + 63) / 64, 64, 0, st>>>(a); }
-void draft_tokens(const int* g, int* dst, int* keep, int slot0, int n, int K, hipStream_t st) {
-  k_draft_tokens<<<(n * K + 255) / 256, 256, 0, st>>>(g, dst, keep, slot0, n, K);
-}
 
 #define WF_MISC_INST(S)                                                     \
   template void Ops<S>::ln_operand(const LnArgs&, int, hipStream_t);        \
+  template void Ops<S>::reduce_ln(const RlnArgs&, int, hipStream_t);        \
   template void Ops<S>::verify_begin(const BeginArgs&, int, hipStream_t);   \
   template void Ops<S>::draft_begin(const BeginArgs&, int, hipStream_t);    \
   template void Ops<S>::prefill_begin(const BeginArgs&, int, hipStream_t);  \

@@ -38,6 +38,7 @@ int check_config(const wf_config* c, std::string& why) {
   if (!c) { why = "null config"; return WF_EINVAL; }
   if (c->dtype != WF_F32 && c->dtype != WF_BF16) { why = "dtype must be WF_F32 or WF_BF16"; return WF_EINVAL; }
   if (c->n_head <= 0 || c->d_model != c->n_head * kHeadDim) { why = "head width must be 64"; return WF_EINVAL; }
+  if (c->d_model > 2048) { why = "d_model must be <= 2048"; return WF_EINVAL; }
   if (c->n_layer <= 0 || c->n_draft_layer <= 0) { why = "layer counts must be positive"; return WF_EINVAL; }
   if (c->d_ff <= 0 || c->d_ff % 32) { why = "d_ff must be a positive multiple of 32"; return WF_EINVAL; }
   if (c->n_vocab < 2) { why = "n_vocab must be >= 2"; return WF_EINVAL; }
@@ -190,6 +191,14 @@ int compute_layout(const wf_config& c, Layout& L) {
   L.lasth = region(R9 * d * 4);
   L.logits = region(R9 * V * 4);
   L.dlogits = region(R9 * V * 4);
+  // batch 1 with bf16 storage: the second MLP product is split over k into
+  // partial sums that the residual update reduces (about 240 blocks of 64 columns)
+  L.fc2_split = 0;
+  if (c.dtype == WF_BF16 && L.nsplit_op == 3 && d <= (size_t)kLnFoldMaxK) {
+    const int tiles64 = (int)((d + 63) / 64), ksteps = (int)(F / 32);
+    L.fc2_split = std::max(1, std::min({kRlnMaxPartsHost, 240 / tiles64, ksteps}));
+  }
+  L.part = region((size_t)std::max(L.fc2_split, 1) * R9 * d * 4);
   L.total = o;
   return WF_OK;
 }
@@ -205,6 +214,17 @@ struct Runner {
   const wf_config& c;
   const Layout& L;
   Runner(Handle* h_, hipStream_t s) : h(h_), st(s), c(h_->cfg), L(h_->lay) {}
+
+  // The LayerNorm operand of the next product was already written by the
+  // residual reduction (Ad16 for a block's first product, Ad32 for the head).
+  bool ln_ready = false;
+
+  // The LayerNorm that follows a block: the next block's first one, or the final
+  // one before the vocabulary head (wide: its operand feeds 32-column tiles).
+  struct LnNext {
+    size_t g, b;
+    bool wide;
+  };
 
   // Run one launch; when profiling (eager calls only) bracket it with events.
   template <typename F>
@@ -289,8 +309,8 @@ struct Runner {
            rows * N * 4.0 * (epi == EPI_RESID ? 2 : 1);
   }
 
-  void gemv(int epi, int slot0, int n, Operand x, size_t w, size_t b, int K, int N, float* y, int ldy,
-            Operand aout = Operand{nullptr, 0, OP_ROW, 0}, int tap = -1) {
+  GemvArgs gemv_args(int slot0, int n, Operand x, size_t w, size_t b, int K, int N, float* y, int ldy,
+                     Operand aout, int tap) const {
     GemvArgs a = gemv_base(slot0, n, wk(x.kind == OP_F32));
     a.a = x;
     a.w = W(w);
@@ -301,7 +321,42 @@ struct Runner {
     a.ldy = ldy;
     a.aout = aout;
     a.tap = tap;
-    launch("gemv", gemv_bytes(n, K, N, epi), [&] { Ops<S>::gemv(epi, a, st); });
+    return a;
+  }
+  void run_gemv(int epi, int n, const GemvArgs& a) {
+    launch("gemv", gemv_bytes(n, a.K, a.N, epi), [&] { Ops<S>::gemv(epi, a, st); });
+  }
+
+  void gemv(int epi, int slot0, int n, Operand x, size_t w, size_t b, int K, int N, float* y, int ldy,
+            Operand aout = Operand{nullptr, 0, OP_ROW, 0}, int tap = -1) {
+    run_gemv(epi, n, gemv_args(slot0, n, x, w, b, K, N, y, ldy, aout, tap));
+  }
+
+  // LayerNorm folded into the product that consumes it: bf16 storage at batch 1
+  // (three split terms) with rows short enough to stage in LDS.
+  bool fold_ln() const { return frag() && L.nsplit_op == 3 && c.d_model <= kLnFoldMaxK; }
+
+  // Make LayerNorm(rows x; gain g, bias b) the operand of product a: folded into
+  // the product, or a separate launch that writes operand `op`.
+  // The fold repeats the normalisation in every block, so products with many
+  // column blocks (the vocabulary head) take the separate launch.
+  void ln_operand(GemvArgs& a, int slot0, int n, const float* x, size_t g, size_t b, Operand op, bool fold = true) {
+    if (fold && fold_ln()) {
+      a.lnx = x + (size_t)slot0 * kRows * c.d_model;
+      a.lng = W(g);
+      a.lnb = W(b);
+    } else {
+      ln(slot0, n, x, g, b, op);
+      a.a = op;
+    }
+  }
+
+  // y = LN(x) W^T + bias with the LayerNorm operand in `op` when not folded
+  void gemv_ln(int epi, int slot0, int n, const float* x, size_t g, size_t gb, Operand op, size_t w, size_t b, int K,
+               int N, float* y, int ldy, Operand aout = Operand{nullptr, 0, OP_ROW, 0}) {
+    GemvArgs a = gemv_args(slot0, n, op, w, b, K, N, y, ldy, aout, -1);
+    ln_operand(a, slot0, n, x, g, gb, op);
+    run_gemv(epi, n, a);
   }
 
   void ln(int slot0, int n, const float* x, size_t g, size_t b, Operand out) {
@@ -328,31 +383,48 @@ struct Runner {
   }
 
   // second half of a decoder block shared by target and drafter: cross-attention and MLP
-  void block_tail(int slot0, int n, const BlockW& b, int xlayer, int tap) {
+  void block_tail(int slot0, int n, const BlockW& b, int xlayer, int tap, const LnNext& nx) {
     const int d = c.d_model;
     float *h_ = F32(L.h), *qkv = F32(L.qkv);
-    ln(slot0, n, h_, b.ln2_g, b.ln2_b, Ad16());
-    gemv(EPI_STORE, slot0, n, Ad16(), b.w_q2, b.b_q2, d, d, qkv, 3 * d);
+    gemv_ln(EPI_STORE, slot0, n, h_, b.ln2_g, b.ln2_b, Ad16(), b.w_q2, b.b_q2, d, d, qkv, 3 * d);
     cross(slot0, n, xlayer);
     gemv(EPI_RESID, slot0, n, Ad16(), b.w_o2, b.b_o2, d, d, h_, d);
-    ln(slot0, n, h_, b.ln3_g, b.ln3_b, Ad32());
-    gemv(EPI_GELU, slot0, n, Ad32(), b.w_fc1, b.b_fc1, d, c.d_ff, nullptr, 0, Af16());
-    gemv(EPI_RESID, slot0, n, Af16(), b.w_fc2, b.b_fc2, c.d_ff, d, h_, d, Atap16(), tap);
+    gemv_ln(EPI_GELU, slot0, n, h_, b.ln3_g, b.ln3_b, Ad32(), b.w_fc1, b.b_fc1, d, c.d_ff, nullptr, 0, Af16());
+    if (L.fc2_split > 0) {
+      // k-split partial sums, then h += sum + bias, the tap, and the next LayerNorm
+      GemvArgs a = gemv_args(slot0, n, Af16(), b.w_fc2, b.b_fc2, c.d_ff, d, F32(L.part), d, Operand{nullptr, 0, OP_ROW, 0}, -1);
+      a.bias = nullptr;
+      a.ct = 4;
+      a.ksplit = L.fc2_split;
+      a.pstride = (size_t)R9() * d;
+      run_gemv(EPI_PART, n, a);
+      RlnArgs ra{};
+      ra.part = F32(L.part); ra.nparts = L.fc2_split; ra.pstride = (size_t)R9() * d; ra.bias = W(b.b_fc2); ra.h = h_;
+      ra.tap = Atap16(); ra.tapcol = tap >= 0 ? tap * d : -1; ra.g = W(nx.g); ra.b = W(nx.b); ra.out = nx.wide ? Ad32() : Ad16();
+      ra.d = d; ra.row0 = slot0 * kRows; ra.nsplit = L.nsplit_op; ra.R9 = R9();
+      launch("reduce_ln", 4.0 * kRows * n * d * (L.fc2_split + 3), [&] { Ops<S>::reduce_ln(ra, n * kRows, st); });
+      ln_ready = true;
+    } else {
+      gemv(EPI_RESID, slot0, n, Af16(), b.w_fc2, b.b_fc2, c.d_ff, d, h_, d, Atap16(), tap);
+    }
   }
 
   void target_forward(int slot0, int n) {
     const int d = c.d_model;
     float *h_ = F32(L.h), *qkv = F32(L.qkv);
+    ln_ready = false;
     for (int l = 0; l < c.n_layer; ++l) {
       const BlockW& b = L.tb[l];
       int tap = -1;
       for (int i = 0; i < c.n_tap; ++i)
         if (c.taps[i] == l) tap = i;
-      ln(slot0, n, h_, b.ln1_g, b.ln1_b, Ad16());
       GemvArgs a = gemv_base(slot0, n, wk(false));
-      a.a = Ad16(); a.w = W(b.w_qkv); a.bias = W(b.b_qkv); a.K = d; a.N = 3 * d;
+      a.w = W(b.w_qkv); a.bias = W(b.b_qkv); a.K = d; a.N = 3 * d;
       a.y = qkv; a.ldy = 3 * d; a.cache = skv_layer(l); a.kv_stride = kv_stride();
-      launch("gemv", gemv_bytes(n, d, 3 * d, EPI_QKV), [&] { Ops<S>::gemv(EPI_QKV, a, st); });
+      if (ln_ready) a.a = Ad16();
+      else ln_operand(a, slot0, n, h_, b.ln1_g, b.ln1_b, Ad16());
+      ln_ready = false;
+      run_gemv(EPI_QKV, n, a);
       AttnArgs at{};
       at.q = qkv; at.ldq = 3 * d; at.kcache = skv_layer(l); at.vcache = skv_layer(l) + kv_stride();
       at.state = I32(L.state); at.page_table = I32(L.page_table); at.rope = F32(L.rope); at.out = Ad16();
@@ -360,19 +432,26 @@ struct Runner {
       at.nsplit = L.nsplit_op; at.R9 = R9();
       launch("attn_self", 0, [&] { Ops<S>::attn_self(at, n, st); });
       gemv(EPI_RESID, slot0, n, Ad16(), b.w_o, b.b_o, d, d, h_, d);
-      block_tail(slot0, n, b, l, tap);
+      const LnNext nx = l + 1 < c.n_layer ? LnNext{L.tb[l + 1].ln1_g, L.tb[l + 1].ln1_b, false}
+                                          : LnNext{L.lnf_g, L.lnf_b, true};
+      block_tail(slot0, n, b, l, tap, nx);
     }
   }
 
-  // vocabulary head over the operand rows in A_d32: logits = x @ tok_emb^T, per-row argmax into g
-  void head(int slot0, int n, float* logits) {
+  // vocabulary head: logits = LN_final(x) @ tok_emb^T, per-row argmax into g
+  // Drafter pass: keep/dst receive the drafted tokens (rows 1..K).
+  void head(int slot0, int n, const float* x, size_t g, size_t gb, float* logits, int* keep = nullptr,
+            int* dst = nullptr) {
     GemvArgs a = gemv_base(slot0, n, wk(true));
-    a.a = Ad32(); a.w = W(L.tok_emb); a.bias = nullptr; a.K = c.d_model; a.N = c.n_vocab;
+    a.w = W(L.tok_emb); a.bias = nullptr; a.K = c.d_model; a.N = c.n_vocab;
     a.y = logits; a.ldy = c.n_vocab; a.hv = F32(L.hv); a.hi = I32(L.hi); a.nblk = L.head_blocks;
-    launch("gemv", gemv_bytes(n, c.d_model, c.n_vocab, EPI_ARGMAX), [&] { Ops<S>::gemv(EPI_ARGMAX, a, st); });
+    if (ln_ready) a.a = Ad32();
+    else ln_operand(a, slot0, n, x, g, gb, Ad32(), false);
+    ln_ready = false;
+    run_gemv(EPI_ARGMAX, n, a);
     launch("argmax_final", kRows * n * L.head_blocks * 8.0, [&] {
       argmax_final(F32(L.hv), I32(L.hi), L.head_blocks, slot0 * kRows, n * kRows, I32(L.g), F32(L.gmax),
-                   h->at<unsigned>(L.status), st);
+                   h->at<unsigned>(L.status), keep, dst, slot0, c.block_k, st);
     });
   }
 
@@ -383,9 +462,9 @@ struct Runner {
     gemv(EPI_STORE, slot0, n, Atap16(), L.hproj_w, L.hproj_b, c.n_tap * d, d, hp, d);
     for (int dl = 0; dl < c.n_draft_layer; ++dl) {
       const BlockW& b = L.db[dl];
-      ln(slot0, n, hp, b.ln1_g, b.ln1_b, Ad16());
       // rows d..3d of the concatenated q|k|v matrix start d*d elements in, in either order
-      gemv(EPI_STORE, slot0, n, Ad16(), b.w_qkv + (size_t)d * d, b.b_qkv + d, d, 2 * d, kvh, 2 * d);
+      gemv_ln(EPI_STORE, slot0, n, hp, b.ln1_g, b.ln1_b, Ad16(), b.w_qkv + (size_t)d * d, b.b_qkv + d, d, 2 * d, kvh,
+              2 * d);
       HistArgs ha{};
       ha.kv = kvh; ha.kcache = hkv(dl, 0); ha.vcache = hkv(dl, 1); ha.state = I32(L.state); ha.rope = F32(L.rope);
       ha.slot0 = slot0; ha.d = d; ha.n_head = c.n_head; ha.n_ctx = c.n_ctx;
@@ -400,10 +479,12 @@ struct Runner {
     ba.state = I32(L.state); ba.emb = W(L.tok_emb); ba.emb_kind = wk(true); ba.pos = W(L.mask); ba.h = h_;
     ba.slot0 = slot0; ba.d = d; ba.n_vocab = c.n_vocab; ba.n_ctx = c.n_ctx; ba.block_k = c.block_k;
     launch("begin", 0, [&] { Ops<S>::draft_begin(ba, n, st); });
+    ln_ready = false;
     for (int dl = 0; dl < c.n_draft_layer; ++dl) {
       const BlockW& b = L.db[dl];
-      ln(slot0, n, h_, b.ln1_g, b.ln1_b, Ad16());
-      gemv(EPI_STORE, slot0, n, Ad16(), b.w_qkv, b.b_qkv, d, 3 * d, qkv, 3 * d);
+      if (ln_ready) gemv(EPI_STORE, slot0, n, Ad16(), b.w_qkv, b.b_qkv, d, 3 * d, qkv, 3 * d);
+      else gemv_ln(EPI_STORE, slot0, n, h_, b.ln1_g, b.ln1_b, Ad16(), b.w_qkv, b.b_qkv, d, 3 * d, qkv, 3 * d);
+      ln_ready = false;
       AttnArgs at{};
       at.q = qkv; at.ldq = 3 * d; at.kcache = hkv(dl, 0); at.vcache = hkv(dl, 1);
       at.state = I32(L.state); at.rope = F32(L.rope); at.out = Ad16();
@@ -411,11 +492,11 @@ struct Runner {
       at.nsplit = L.nsplit_op; at.R9 = R9();
       launch("attn_draft", 0, [&] { Ops<S>::attn_draft(at, n, st); });
       gemv(EPI_RESID, slot0, n, Ad16(), b.w_o, b.b_o, d, d, h_, d);
-      block_tail(slot0, n, b, c.n_layer + dl, -1);
+      const LnNext nx = dl + 1 < c.n_draft_layer ? LnNext{L.db[dl + 1].ln1_g, L.db[dl + 1].ln1_b, false}
+                                                 : LnNext{L.dlnf_g, L.dlnf_b, true};
+      block_tail(slot0, n, b, c.n_layer + dl, -1, nx);
     }
-    ln(slot0, n, h_, L.dlnf_g, L.dlnf_b, Ad32());
-    head(slot0, n, h->debug ? F32(L.dlogits) : nullptr);
-    launch("misc", 0, [&] { draft_tokens(I32(L.g), dst, I32(L.draft), slot0, n, c.block_k, st); });
+    head(slot0, n, h_, L.dlnf_g, L.dlnf_b, h->debug ? F32(L.dlogits) : nullptr, I32(L.draft), dst);
   }
 
   void verify(int slot0, int n, const int* draft, int k_max, int* out, int* n_out, int* n_acc, int* done) {
@@ -425,8 +506,7 @@ struct Runner {
     ba.block_k = c.block_k; ba.k_max = k_max;
     launch("begin", 0, [&] { Ops<S>::verify_begin(ba, n, st); });
     target_forward(slot0, n);
-    ln(slot0, n, F32(L.h), L.lnf_g, L.lnf_b, Ad32());
-    head(slot0, n, h->debug ? F32(L.logits) : nullptr);
+    head(slot0, n, F32(L.h), L.lnf_g, L.lnf_b, h->debug ? F32(L.logits) : nullptr);
     AcceptArgs aa{};
     aa.state = I32(L.state); aa.tok = I32(L.tok); aa.g = I32(L.g); aa.out = out; aa.n_out = n_out; aa.n_acc = n_acc;
     aa.done = done; aa.slot0 = slot0; aa.n = n; aa.block_k = c.block_k; aa.eos = c.eos_id; aa.n_ctx = c.n_ctx;
@@ -434,8 +514,7 @@ struct Runner {
   }
 
   void draft(int slot0, int n, int* dst) {
-    history_apply(slot0, n);
-    launch("misc", 0, [&] { hist_done(I32(L.state), slot0, n, st); });
+    history_apply(slot0, n);  // the drafter's set-up then clears the pending rows
     drafter_forward(slot0, n, dst);
   }
 
@@ -471,8 +550,8 @@ struct Runner {
       save_last(F32(L.h), F32(L.lasth), I32(L.state), slot0, n, c.d_model, ch, st);
       history_apply(slot0, n);
     }
-    ln(slot0, n, F32(L.lasth), L.lnf_g, L.lnf_b, Ad32());
-    head(slot0, n, nullptr);
+    ln_ready = false;  // the final LayerNorm applies to the saved last rows, not to h
+    head(slot0, n, F32(L.lasth), L.lnf_g, L.lnf_b, nullptr);
     prefill_finish(I32(L.state), I32(L.g), slot0, n, c.eos_id, c.n_ctx, first, st);
   }
 };

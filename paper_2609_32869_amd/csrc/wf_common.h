@@ -61,18 +61,31 @@ template <typename S>
 __device__ __forceinline__ S from_f(float f);
 template <>
 __device__ __forceinline__ float from_f<float>(float f) { return f; }
-// round to nearest even; NaN stays NaN
+// round to nearest even; NaN stays NaN (branch-free)
+__device__ __forceinline__ uint32_t bf16_bits_rne(float f) {
+  const uint32_t u = __float_as_uint(f);
+  const uint32_t rne = (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
+  return (u & 0x7fffffffu) > 0x7f800000u ? ((u >> 16) | 0x40u) : rne;
+}
 template <>
 __device__ __forceinline__ bf16 from_f<bf16>(float f) {
-  uint32_t u = __float_as_uint(f);
   bf16 r;
-  if ((u & 0x7fffffffu) > 0x7f800000u) {
-    r.u = (uint16_t)((u >> 16) | 0x40u);
-  } else {
-    u += 0x7fffu + ((u >> 16) & 1u);
-    r.u = (uint16_t)(u >> 16);
-  }
+  r.u = (uint16_t)bf16_bits_rne(f);
   return r;
+}
+
+// Exact three-term bf16 split of an fp32 value: hi keeps the top 8 significand
+// bits (truncated), mid the next 8 bits of the exact remainder, lo the rest (at
+// most 8 bits, so exact in bf16); hi + mid + lo == f for finite f away from the
+// denormal range.  Returned as bf16 bit patterns.
+__device__ __forceinline__ void split3_bits(float f, uint32_t& hi, uint32_t& mid, uint32_t& lo) {
+  const uint32_t u = __float_as_uint(f);
+  const float r1 = f - __uint_as_float(u & 0xffff0000u);
+  const uint32_t v = __float_as_uint(r1);
+  const float r2 = r1 - __uint_as_float(v & 0xffff0000u);
+  hi = u >> 16;
+  mid = v >> 16;
+  lo = __float_as_uint(r2) >> 16;
 }
 
 // Load 8 consecutive storage elements as fp32 (p must be 16-byte aligned for bf16,
@@ -91,15 +104,44 @@ __device__ __forceinline__ void ld8(const bf16* p, float* o) {
   o[6] = __uint_as_float(v.w << 16); o[7] = __uint_as_float(v.w & 0xffff0000u);
 }
 
+// Cross-lane moves through the DPP modifier (no LDS round trip).
+template <int CTRL>
+__device__ __forceinline__ float dpp(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xf, 0xf, false));
+}
+constexpr int kDppXor1 = 0xB1;         // quad_perm [1,0,3,2]
+constexpr int kDppXor2 = 0x4E;         // quad_perm [2,3,0,1]
+constexpr int kDppHalfMirror = 0x141;  // lane i <-> 7 - i within 8 lanes
+constexpr int kDppMirror = 0x140;      // lane i <-> 15 - i within 16 lanes
+constexpr int kDppRor8 = 0x128;        // lane i <- lane (i + 8) mod 16 within 16 lanes
+
+__device__ __forceinline__ float lane_f(float v, int l) { return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), l)); }
+
+// sum / max over the 8 lanes of an aligned group (result in every lane of the group)
+__device__ __forceinline__ float sum8(float v) {
+  v += dpp<kDppXor1>(v);
+  v += dpp<kDppXor2>(v);
+  return v + dpp<kDppHalfMirror>(v);
+}
+// sum / max over the 16 lanes of a row (result in every lane of the row)
+__device__ __forceinline__ float sum16(float v) {
+  v = sum8(v);
+  return v + dpp<kDppMirror>(v);
+}
+__device__ __forceinline__ float max16(float v) {
+  v = fmaxf(v, dpp<kDppXor1>(v));
+  v = fmaxf(v, dpp<kDppXor2>(v));
+  v = fmaxf(v, dpp<kDppHalfMirror>(v));
+  return fmaxf(v, dpp<kDppMirror>(v));
+}
+// whole-wave sum / max, uniform result (fixed order: rows 0..3)
 __device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
-  return v;
+  v = sum16(v);
+  return (lane_f(v, 15) + lane_f(v, 31)) + (lane_f(v, 47) + lane_f(v, 63));
 }
 __device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
-  return v;
+  v = max16(v);
+  return fmaxf(fmaxf(lane_f(v, 15), lane_f(v, 31)), fmaxf(lane_f(v, 47), lane_f(v, 63)));
 }
 
 // (value, index) maximum with ties to the lowest index; NaN compares as larger

@@ -25,7 +25,7 @@ struct BlockW {
 struct Layout {
   // byte offsets into the workspace
   size_t state, page_table, rope, status, aux, weights, xkv, skv, hkv;
-  size_t a_d16, a_d32, a_f16, a_tap16, h, qkv, hp, kvh, hv, hi, tok, g, gmax, draft, lasth, logits, dlogits;
+  size_t a_d16, a_d32, a_f16, a_tap16, h, qkv, hp, kvh, hv, hi, tok, g, gmax, draft, lasth, logits, dlogits, part;
   size_t total;
   // element offsets inside the weight region
   size_t tok_emb, pos_emb, lnf_g, lnf_b, hproj_w, hproj_b, mask, dlnf_g, dlnf_b;
@@ -35,6 +35,7 @@ struct Layout {
   int nsplit_op;  // split terms of a matrix operand (3: bf16 at batch 1, else 1)
   int mt16, mt32; // 16-row / 32-row tiles held by an operand buffer
   size_t stage_bytes;  // raw-matrix staging at init (inside the cross K/V region)
+  int fc2_split;       // k-splits of the second MLP product (0: not split)
 };
 
 struct Handle;

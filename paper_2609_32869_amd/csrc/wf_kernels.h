@@ -6,7 +6,9 @@
 
 namespace wf {
 
-enum { EPI_STORE = 0, EPI_GELU = 1, EPI_RESID = 2, EPI_QKV = 3, EPI_ARGMAX = 4 };
+enum { EPI_STORE = 0, EPI_GELU = 1, EPI_RESID = 2, EPI_QKV = 3, EPI_ARGMAX = 4, EPI_PART = 5 };
+// EPI_PART: split-K partial sums (no bias) of k-split blockIdx.y stored to
+// y + blockIdx.y * pstride, row-major [rows][ldy].
 
 // Matrix-operand rows: the activation rows of a pass are stored once per split
 // term, row m = s * R9 + slot * 9 + i, s < nsplit (R9 = 9 * max_batch).  With
@@ -27,13 +29,23 @@ struct Operand {
 enum { W_ROW = 0, W_F16 = 1, W_F32 = 2 };
 
 struct GemvArgs {
-  Operand a;         // input operand
+  Operand a;         // input operand (unused when lnx is set)
   const void* w;     // [N, K] storage type, order wkind
   int wkind;
   const void* bias;  // [N] storage type or null
   int K, N;
   int slot0, nslots, nsplit, R9;
-  int mt0, mt1;      // 16-row tiles of the operand covering the batch (all split terms)
+  int mt0, mt1;      // operand row tiles (16 or 32 rows by wkind) covering the batch, all split terms
+  // LayerNorm folded into the product (bf16, one slot, three split terms): the
+  // operand is LN(lnx rows) with gain lng and bias lnb, built in LDS by each block.
+  const float* lnx;  // [9][K] fp32 rows, or null
+  const void* lng;
+  const void* lnb;
+  // split-K (EPI_PART): number of k-splits (grid y) and the element stride between
+  // their partial buffers
+  int ksplit;
+  size_t pstride;
+  int ct;  // 16-column tiles per block (4: wide kernel, with split-K), else 1
   float* y;          // STORE: out; RESID: residual stream; QKV: q; ARGMAX: optional logits
   int ldy;
   Operand aout;      // GELU: operand of the next product; RESID: tap operand (column offset tap * N)
@@ -76,6 +88,33 @@ struct LnArgs {
   const void* b;
   Operand out;
   int d, row0, nsplit, R9;
+};
+
+// h[row] += sum_s part[s][row] + bias; optional tap operand of the new h; then,
+// when g is set, LayerNorm(h[row]) (gain g, bias b) as the operand `out`.
+struct RlnArgs {
+  const float* part;  // [nparts][rows][d] partial sums
+  int nparts;
+  size_t pstride;     // elements between partial buffers
+  const void* bias;   // producer bias [d] or null
+  float* h;           // residual stream [rows][d]
+  Operand tap;        // tap operand (column offset tapcol) when tapcol >= 0
+  int tapcol;
+  const void* g;
+  const void* b;
+  Operand out;
+  int d, row0, nsplit, R9;
+};
+
+// Cross-attention over key chunks: partial softmax states per (slot, head, chunk,
+// row) = {m, l, 0, 0, acc[64]}.
+struct XpartArgs {
+  const float* q;
+  int ldq;
+  const void* kv;  // block base of [slot][2][head][frame][64]
+  float* part;     // [slot][head][chunk][9][68]
+  Operand out;     // combine: operand rows of the following product
+  int slot0, d, n_head, n_frames, nchunk, nsplit, R9;
 };
 
 struct BeginArgs {
@@ -124,6 +163,9 @@ struct Ops {
   static void attn_self(const AttnArgs& a, int n, hipStream_t st);
   static void attn_draft(const AttnArgs& a, int n, hipStream_t st);
   static void attn_cross(const CrossArgs& a, int n, hipStream_t st);
+  static void xattn_part(const XpartArgs& a, int n, hipStream_t st);
+  static void xattn_combine(const XpartArgs& a, int n, hipStream_t st);
+  static void reduce_ln(const RlnArgs& a, int rows, hipStream_t st);
   static void verify_begin(const BeginArgs& a, int n, hipStream_t st);
   static void draft_begin(const BeginArgs& a, int n, hipStream_t st);
   static void prefill_begin(const BeginArgs& a, int n, hipStream_t st);
@@ -134,12 +176,16 @@ struct Ops {
 template <typename S>
 void repack(const void* src, void* dst, int N, int K, int wkind, hipStream_t st);
 
+constexpr int kRlnMaxPartsHost = 16;  // most split-K partials a reduction sums
+
+// largest row length K of a product with the LayerNorm folded in (its operand is
+// staged whole in LDS)
+constexpr int kLnFoldMaxK = 1280;
+
 void argmax_final(const float* hv, const int* hi, int nblk, int row0, int rows, int* g, float* gmax, unsigned* status,
-                  hipStream_t st);
+                  int* keep, int* dst, int slot0, int K, hipStream_t st);
 void save_last(const float* h, float* lasth, const int* state, int slot0, int n, int d, int chunk, hipStream_t st);
 void prefill_finish(int* state, const int* g, int slot0, int n, int eos, int n_ctx, int* first, hipStream_t st);
-void hist_done(int* state, int slot0, int n, hipStream_t st);
 void accept_greedy(const AcceptArgs& a, hipStream_t st);
-void draft_tokens(const int* g, int* dst, int* keep, int slot0, int n, int K, hipStream_t st);
 
 }  // namespace wf

@@ -15,21 +15,21 @@ __device__ __forceinline__ size_t op_index(const Operand& o, int m, int k) {
 }
 
 // Write value v of activation row `row` (= slot * 9 + i), column `col`.  bf16 with
-// nsplit = 3: three bf16 terms hi + mid + lo, at rows row, R9 + row, 2 R9 + row,
-// whose sum is v to fp32 precision; otherwise the value in the storage type.
+// nsplit = 3: the exact three-term split hi + mid + lo == v at rows row, R9 + row,
+// 2 R9 + row; otherwise the value rounded to the storage type.
 __device__ __forceinline__ void put_operand(const Operand& o, int, int, int row, int col, float v, float) {
   reinterpret_cast<float*>(o.p)[op_index(o, row, col)] = v;
 }
 __device__ __forceinline__ void put_operand(const Operand& o, int nsplit, int R9, int row, int col, float v, bf16) {
-  bf16* A = reinterpret_cast<bf16*>(o.p);
-  const bf16 hi = from_f<bf16>(v);
-  A[op_index(o, row, col)] = hi;
+  uint16_t* A = reinterpret_cast<uint16_t*>(o.p);
   if (nsplit == 3) {
-    const float r1 = v - to_f(hi);
-    const bf16 mid = from_f<bf16>(r1);
-    const bf16 lo = from_f<bf16>(r1 - to_f(mid));
-    A[op_index(o, R9 + row, col)] = mid;
-    A[op_index(o, 2 * R9 + row, col)] = lo;
+    uint32_t hi, mid, lo;
+    split3_bits(v, hi, mid, lo);
+    A[op_index(o, row, col)] = (uint16_t)hi;
+    A[op_index(o, R9 + row, col)] = (uint16_t)mid;
+    A[op_index(o, 2 * R9 + row, col)] = (uint16_t)lo;
+  } else {
+    A[op_index(o, row, col)] = (uint16_t)bf16_bits_rne(v);
   }
 }
 template <typename S>
