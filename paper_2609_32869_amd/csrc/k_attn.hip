@@ -289,153 +289,6 @@ __global__ void __launch_bounds__(kCrossThreads) k_attn_cross(CrossArgs a) {
     put_op<S>(a.out, a.nsplit, a.R9, slot * kRows + row, head * kHeadDim + threadIdx.x, o);
 }
 
-// ---------------------------------------------------------------- cross-attention over key chunks
-// Block (head, chunk) of slot s: all nine query rows against frames
-// [chunk * cs, chunk * cs + cs), so every key/value byte is read by one block.
-// Wave w takes key octets w, w + NW, ...; each row keeps a running max, sum and
-// weighted value sums; the waves' states are merged in LDS and the chunk's state
-// {m, l, 0, 0, acc[64]} is stored for the combine.
-constexpr int kXpThreads = 512;
-constexpr int kXpStride = 68;  // floats per (chunk, row) state
-template <typename S>
-__global__ void __launch_bounds__(kXpThreads) k_xattn_part(XpartArgs a) {
-  constexpr int NW = kXpThreads / 64, B = 2;
-  __shared__ float wacc[NW][kRows][64];
-  __shared__ float wm[NW][kRows], wl[NW][kRows];
-  const int head = blockIdx.x / a.nchunk, chunk = blockIdx.x % a.nchunk;
-  const int slot = a.slot0 + blockIdx.y;
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, g = lane & 7, kl = lane >> 3;
-  const int cs = (a.n_frames + a.nchunk - 1) / a.nchunk;
-  const int f0 = min(a.n_frames, chunk * cs), nk = min(a.n_frames, f0 + cs) - f0;
-  float q8[kRows][8];
-#pragma unroll
-  for (int r = 0; r < kRows; ++r) {
-    const float* qr = a.q + (size_t)(slot * kRows + r) * a.ldq + head * kHeadDim + 8 * g;
-#pragma unroll
-    for (int e = 0; e < 8; ++e) q8[r][e] = qr[e] * 0.125f;
-  }
-  const S* Kx = reinterpret_cast<const S*>(a.kv) + (((size_t)slot * 2 * a.n_head + head) * a.n_frames + f0) * kHeadDim;
-  const S* Vx = Kx + (size_t)a.n_head * a.n_frames * kHeadDim;
-  float m[kRows], l[kRows], acc[kRows][8];
-#pragma unroll
-  for (int r = 0; r < kRows; ++r) {
-    m[r] = -INFINITY;
-    l[r] = 0.f;
-#pragma unroll
-    for (int e = 0; e < 8; ++e) acc[r][e] = 0.f;
-  }
-  const int noct = (nk + 7) >> 3;
-  for (int o0 = w; o0 < noct; o0 += NW * B) {
-    Raw8<S> kr[B], vr[B];
-#pragma unroll
-    for (int b = 0; b < B; ++b) {
-      const int key = (o0 + NW * b) * 8 + kl;
-      if (key < nk) {
-        kr[b].load(Kx + (uint32_t)key * kHeadDim + 8 * g);
-        vr[b].load(Vx + (uint32_t)key * kHeadDim + 8 * g);
-      } else {
-        kr[b].zero();
-        vr[b].zero();
-      }
-    }
-    float sc[kRows][B];
-#pragma unroll
-    for (int b = 0; b < B; ++b) {
-      float k8[8];
-      kr[b].unpack(k8);
-      const bool ok = (o0 + NW * b) * 8 + kl < nk;
-#pragma unroll
-      for (int r = 0; r < kRows; ++r) {
-        float t = 0.f;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) t = fmaf(q8[r][e], k8[e], t);
-        t = sum8(t);
-        sc[r][b] = ok ? t : -INFINITY;
-      }
-    }
-    float v8[B][8];
-#pragma unroll
-    for (int b = 0; b < B; ++b) vr[b].unpack(v8[b]);
-#pragma unroll
-    for (int r = 0; r < kRows; ++r) {
-      float bm = sc[r][0];
-#pragma unroll
-      for (int b = 1; b < B; ++b) bm = fmaxf(bm, sc[r][b]);
-      const float mn = fmaxf(m[r], wave_max(bm));  // key o0 * 8 < nk is in this batch
-      const float f = __expf(m[r] - mn);
-      l[r] *= f;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) acc[r][e] *= f;
-#pragma unroll
-      for (int b = 0; b < B; ++b) {
-        const float p = __expf(sc[r][b] - mn);
-        l[r] += g == 0 ? p : 0.f;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) acc[r][e] = fmaf(p, v8[b][e], acc[r][e]);
-      }
-      m[r] = mn;
-    }
-  }
-  // fold the 8 key lanes (bits 3..5) of each dim group, then publish per wave
-#pragma unroll
-  for (int r = 0; r < kRows; ++r) {
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      float t = acc[r][e] + dpp<kDppRor8>(acc[r][e]);
-      t += __shfl_xor(t, 16, 64);
-      t += __shfl_xor(t, 32, 64);
-      acc[r][e] = t;
-    }
-    const float lr = wave_sum(l[r]);
-    if (lane < 8) {
-#pragma unroll
-      for (int e = 0; e < 8; ++e) wacc[w][r][8 * g + e] = acc[r][e];
-    }
-    if (lane == 0) {
-      wm[w][r] = m[r];
-      wl[w][r] = lr;
-    }
-  }
-  __syncthreads();
-  float* out = a.part + (((size_t)slot * a.n_head + head) * a.nchunk + chunk) * kRows * kXpStride;
-  for (int t = threadIdx.x; t < kRows * 64; t += kXpThreads) {
-    const int r = t >> 6, dim = t & 63;
-    float M = wm[0][r];
-#pragma unroll
-    for (int i = 1; i < NW; ++i) M = fmaxf(M, wm[i][r]);
-    float L = 0.f, o = 0.f;
-#pragma unroll
-    for (int i = 0; i < NW; ++i) {
-      const float f = __expf(wm[i][r] - M);  // 0 for a wave without keys
-      L += wl[i][r] * f;
-      o += wacc[i][r][dim] * f;
-    }
-    out[r * kXpStride + 4 + dim] = o;
-    if (dim == 0) {
-      out[r * kXpStride] = M;
-      out[r * kXpStride + 1] = L;
-    }
-  }
-}
-
-// Merge the chunk states of (slot, head): thread (row, dim).
-template <typename S>
-__global__ void __launch_bounds__(kRows * 64) k_xattn_combine(XpartArgs a) {
-  const int head = blockIdx.x, slot = a.slot0 + blockIdx.y;
-  const int r = threadIdx.x >> 6, dim = threadIdx.x & 63;
-  const float* in = a.part + ((size_t)slot * a.n_head + head) * a.nchunk * kRows * kXpStride + r * kXpStride;
-  float M = -INFINITY;
-  for (int c = 0; c < a.nchunk; ++c) M = fmaxf(M, in[(size_t)c * kRows * kXpStride]);
-  float L = 0.f, o = 0.f;
-  for (int c = 0; c < a.nchunk; ++c) {
-    const float* p = in + (size_t)c * kRows * kXpStride;
-    const float f = __expf(p[0] - M);
-    L += p[1] * f;
-    o += p[4 + dim] * f;
-  }
-  put_op<S>(a.out, a.nsplit, a.R9, slot * kRows + r, head * kHeadDim + dim, o / L);
-}
-
 // ---------------------------------------------------------------- causal self-attention
 // Verify pass: row i < nv of slot s sits at position pos0 + i and attends to cached
 // positions 0..pos0 + i (Section 3.1: one causal pass).  Rows i >= nv are padding
@@ -582,19 +435,6 @@ void Ops<S>::attn_cross(const CrossArgs& a, int n, hipStream_t st) {
   k_attn_cross<S><<<dim3(row_blocks(a.n_head), n), kCrossThreads, 0, st>>>(a);
 }
 
-template <typename S>
-void Ops<S>::xattn_part(const XpartArgs& a, int n, hipStream_t st) {
-  k_xattn_part<S><<<dim3(a.n_head * a.nchunk, n), kXpThreads, 0, st>>>(a);
-}
-template <typename S>
-void Ops<S>::xattn_combine(const XpartArgs& a, int n, hipStream_t st) {
-  k_xattn_combine<S><<<dim3(a.n_head, n), kRows * 64, 0, st>>>(a);
-}
-
-template void Ops<float>::xattn_part(const XpartArgs&, int, hipStream_t);
-template void Ops<bf16>::xattn_part(const XpartArgs&, int, hipStream_t);
-template void Ops<float>::xattn_combine(const XpartArgs&, int, hipStream_t);
-template void Ops<bf16>::xattn_combine(const XpartArgs&, int, hipStream_t);
 template void Ops<float>::attn_self(const AttnArgs&, int, hipStream_t);
 template void Ops<bf16>::attn_self(const AttnArgs&, int, hipStream_t);
 template void Ops<float>::attn_draft(const AttnArgs&, int, hipStream_t);

@@ -106,17 +106,6 @@ struct RlnArgs {
   int d, row0, nsplit, R9;
 };
 
-// Cross-attention over key chunks: partial softmax states per (slot, head, chunk,
-// row) = {m, l, 0, 0, acc[64]}.
-struct XpartArgs {
-  const float* q;
-  int ldq;
-  const void* kv;  // block base of [slot][2][head][frame][64]
-  float* part;     // [slot][head][chunk][9][68]
-  Operand out;     // combine: operand rows of the following product
-  int slot0, d, n_head, n_frames, nchunk, nsplit, R9;
-};
-
 struct BeginArgs {
   int* state;
   const int* draft;  // verify: draft [n][block_k]; prefill: tokens [n][pmax]
@@ -163,8 +152,6 @@ struct Ops {
   static void attn_self(const AttnArgs& a, int n, hipStream_t st);
   static void attn_draft(const AttnArgs& a, int n, hipStream_t st);
   static void attn_cross(const CrossArgs& a, int n, hipStream_t st);
-  static void xattn_part(const XpartArgs& a, int n, hipStream_t st);
-  static void xattn_combine(const XpartArgs& a, int n, hipStream_t st);
   static void reduce_ln(const RlnArgs& a, int rows, hipStream_t st);
   static void verify_begin(const BeginArgs& a, int n, hipStream_t st);
   static void draft_begin(const BeginArgs& a, int n, hipStream_t st);
