@@ -179,10 +179,11 @@ int wf_step(wf_handle* h, int slot0, int n, int k_max, const int32_t* draft_over
 /*
  * Debug views for tests: device pointers into the workspace (valid until
  * wf_release).  which: 0 = target logits of the last verify [max_batch,
- * block_k+1, n_vocab] fp32 (written only when wf_set_debug(h, 1)), 1 = draft
- * logits of the last draft [max_batch, block_k, n_vocab] fp32 (same), 2 =
- * per-slot state int32 [max_batch, 16] (0 L, 1 anchor, 2 emitted, 3 max_new,
- * 4 done, 5 step), 3 = last drafted tokens int32 [max_batch, block_k].
+ * block_k+1, n_vocab] fp32 (written when wf_set_debug(h, 1) or when
+ * sampling), 1 = draft logits of the last draft [max_batch, block_k+1,
+ * n_vocab] fp32 (row j >= 1 is mask j; same condition), 2 = per-slot state
+ * int32 [max_batch, 16] (0 L, 1 anchor, 2 emitted, 3 max_new, 4 done,
+ * 5 step), 3 = last drafted tokens int32 [max_batch, block_k].
  */
 int wf_debug_ptr(wf_handle* h, int which, void** ptr);
 int wf_set_debug(wf_handle* h, int enable);
@@ -206,6 +207,19 @@ int wf_status(wf_handle* h, uint32_t* flags, void* stream);
 int wf_release(wf_handle* h);
 
 const char* wf_strerror(int code);
+
+/*
+ * Test entry points for the sampling generator (Philox4x64-10, Salmon et al.,
+ * SC'11, with the stream layout of wf_set_sampling): words v = 0..n-1 of
+ * stream (seed, purpose, slot, step, pos), i.e. word v & 3 of the block with
+ * counter (purpose << 32 | slot, step, pos, v >> 2) under key (seed, 0).
+ * Purposes: 1 prefill, 2 plain, 3 draft, 4 acceptance, 5 residual, 6 bonus.
+ * _host computes them on the CPU into host memory out[n]; _device enqueues a
+ * kernel writing device memory out[n] on stream.  Both use the code the
+ * sampling kernels use.
+ */
+int wf_rng_words_host(uint64_t seed, int purpose, int slot, int step, int pos, int n, uint64_t* out);
+int wf_rng_words_device(uint64_t seed, int purpose, int slot, int step, int pos, int n, uint64_t* out, void* stream);
 const char* wf_last_error(wf_handle* h);
 
 #ifdef __cplusplus

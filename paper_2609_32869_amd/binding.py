@@ -24,7 +24,7 @@ WF_STATUS_POSITION_OVERFLOW = 0x2
 EXPORTS = ["wf_workspace_bytes", "wf_weight_count", "wf_weight_numel", "wf_init_weights",
            "wf_encode_memory_set", "wf_prefill", "wf_set_sampling", "wf_draft", "wf_verify_accept",
            "wf_step", "wf_debug_ptr", "wf_set_debug", "wf_profile_enable", "wf_profile_summary", "wf_status",
-           "wf_release", "wf_strerror", "wf_last_error"]
+           "wf_release", "wf_strerror", "wf_last_error", "wf_rng_words_host", "wf_rng_words_device"]
 
 
 class WfConfig(ctypes.Structure):
@@ -71,6 +71,8 @@ def load_library(path=LIB_PATH):
         "wf_release": [P],
         "wf_strerror": [I],
         "wf_last_error": [P],
+        "wf_rng_words_host": [U64, I, I, I, I, I, ctypes.POINTER(U64)],
+        "wf_rng_words_device": [U64, I, I, I, I, I, P, P],
     }
     for name, args in sig.items():
         fn = getattr(lib, name)
@@ -78,6 +80,26 @@ def load_library(path=LIB_PATH):
         fn.restype = ctypes.c_char_p if name in ("wf_strerror", "wf_last_error") else ctypes.c_int
     _lib = lib
     return lib
+
+
+def rng_words_host(seed, purpose, slot, step, pos, n):
+    """Generator words v = 0..n-1 of a sampling stream, computed by the library on the host."""
+    lib = load_library()
+    out = np.zeros(n, np.uint64)
+    rc = lib.wf_rng_words_host(int(seed), purpose, slot, step, pos, n, out.ctypes.data_as(ctypes.POINTER(ctypes.c_uint64)))
+    if rc != 0:
+        raise WfError(lib.wf_last_error(None).decode())
+    return out
+
+
+def rng_words_device(seed, purpose, slot, step, pos, n, stream=None):
+    """The same words computed by the library's device kernel (int64 tensor holding the bits)."""
+    lib = load_library()
+    out = torch.empty(n, dtype=torch.int64, device="cuda")
+    rc = lib.wf_rng_words_device(int(seed), purpose, slot, step, pos, n, _ptr(out), _stream(stream))
+    if rc != 0:
+        raise WfError(lib.wf_last_error(None).decode())
+    return out
 
 
 def make_config(cfg, max_batch):

@@ -72,15 +72,44 @@ __device__ __forceinline__ void epi_one(const GemvArgs& a, int row, int n, float
       }
     }
   } else if constexpr (EPI == EPI_ARGMAX) {
-    if (a.y != nullptr) a.y[(size_t)row * a.ldy + n] = v;
+    if (a.y != nullptr) a.y[(size_t)row * a.ldy + n] = v;  // suppressed columns hold -inf
   } else if constexpr (EPI == EPI_PART) {
     a.y[blockIdx.y * a.pstride + (size_t)row * a.ldy + n] = v;
   }
 }
 
-// sv holds the wave-summed tile: TM operand rows (split terms) x TC columns.
+// Vocabulary head: a suppressed column's logit is -inf.
+__device__ __forceinline__ float head_logit(const GemvArgs& a, int n, float v) {
+  return (a.suppress != nullptr && n < a.N && a.suppress[n]) ? -INFINITY : v;
+}
+// Head score of (row, column n): the logit (greedy), or z = logit * inv_t plus the
+// row's Gumbel noise when sampling; oz receives z for the softmax normaliser.
+__device__ __forceinline__ void head_score(const GemvArgs& a, int row, int n, bool act, float v, float* ov, float* oz) {
+  if (!act) {
+    *ov = -INFINITY;
+    *oz = -INFINITY;
+    return;
+  }
+  if (a.inv_t > 0.f) {
+    const float z = v * a.inv_t;
+    *oz = z;
+    if (a.rng_purpose != 0) {
+      const int slot = row / kRows, pos = row - slot * kRows;
+      const int step = a.state[slot * kStateInts + ST_STEP];
+      *ov = z + rng_gumbel(rng_word(a.seed, a.rng_purpose, slot, step, pos, n));
+    } else {
+      *ov = z;
+    }
+  } else {
+    *ov = v;
+    *oz = v;
+  }
+}
+
+// sv holds the wave-summed tile: TM operand rows (split terms) x TC columns; ov and
+// oz are the head's score and z buffers (EPI_ARGMAX).
 template <typename S, int EPI, int TM, int TC, int NT>
-__device__ void finish_tile(const GemvArgs& a, float (*sv)[TC + 1], float (*ov)[TC], int m0, int nb,
+__device__ void finish_tile(const GemvArgs& a, float (*sv)[TC + 1], float (*ov)[TC], float (*oz)[TC], int m0, int nb,
                             const EpiPre<TC, NT>& pre) {
   const bool split3 = a.nsplit == 3;
   const int R = a.slot0 * kRows, Rend = (a.slot0 + a.nslots) * kRows;
@@ -93,9 +122,10 @@ __device__ void finish_tile(const GemvArgs& a, float (*sv)[TC + 1], float (*ov)[
       if (idx >= kRows * TC) break;
       const int ml = idx / TC, c = idx % TC, n = nb + c, row = R + ml;
       const bool act = n < a.N;
-      const float v = ((sv[ml][c] + sv[ml + 9][c]) + sv[ml + 18][c]) + pre.b[it];
+      float v = ((sv[ml][c] + sv[ml + 9][c]) + sv[ml + 18][c]) + pre.b[it];
+      if constexpr (EPI == EPI_ARGMAX) v = head_logit(a, n, v);
       if (act) epi_one<S, EPI>(a, row, n, v, pre.r[it]);
-      if constexpr (EPI == EPI_ARGMAX) ov[ml][c] = act ? v : -INFINITY;
+      if constexpr (EPI == EPI_ARGMAX) head_score(a, row, n, act, v, &ov[ml][c], &oz[ml][c]);
     }
   } else {
     const S* bias = reinterpret_cast<const S*>(a.bias);
@@ -104,8 +134,9 @@ __device__ void finish_tile(const GemvArgs& a, float (*sv)[TC + 1], float (*ov)[
       const bool act = row >= R && row < Rend && n < a.N;
       float v = sv[ml][c];
       if (act && bias != nullptr) v += to_f(bias[n]);
+      if constexpr (EPI == EPI_ARGMAX) v = head_logit(a, n, v);
       if (act) epi_one<S, EPI>(a, row, n, v, EPI == EPI_RESID ? a.y[(size_t)row * a.ldy + n] : 0.f);
-      if constexpr (EPI == EPI_ARGMAX) ov[ml][c] = act ? v : -INFINITY;
+      if constexpr (EPI == EPI_ARGMAX) head_score(a, row, n, act, v, &ov[ml][c], &oz[ml][c]);
     }
   }
   if constexpr (EPI == EPI_ARGMAX) {
@@ -115,13 +146,22 @@ __device__ void finish_tile(const GemvArgs& a, float (*sv)[TC + 1], float (*ov)[
       if (row < R || row >= Rend) continue;
       float bv = ov[ml][0];
       int bi = nb;
+      float zm = oz[ml][0];
       for (int j = 1; j < TC; ++j) {
         if (nb + j >= a.N) break;
         if (better(ov[ml][j], nb + j, bv, bi)) { bv = ov[ml][j]; bi = nb + j; }
+        zm = fmaxf(zm, oz[ml][j]);
       }
       const size_t o = (size_t)row * a.nblk + blockIdx.x;
       a.hv[o] = bv;
       a.hi[o] = bi;
+      if (a.hm != nullptr) {
+        float zs = 0.f;
+        if (zm > -INFINITY)
+          for (int j = 0; j < TC && nb + j < a.N; ++j) zs += expf(oz[ml][j] - zm);
+        a.hm[o] = zm;
+        a.hs[o] = zs;
+      }
     }
   }
 }
@@ -132,7 +172,8 @@ __global__ void __launch_bounds__(NW * 64) k_gemv16(GemvArgs a) {
   constexpr int U = NW >= 16 ? kU / 2 : kU;
   __shared__ float red[NW][32][17];
   __shared__ float sv[32][17];
-  __shared__ float ov[32][16];
+  __shared__ float ov[EPI == EPI_ARGMAX ? 32 : 1][16];
+  __shared__ float oz[EPI == EPI_ARGMAX ? 32 : 1][16];
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
   EpiPre<16, NW * 64> pre;
   pre.template load<bf16, EPI>(a, blockIdx.x * 16);
@@ -177,7 +218,7 @@ __global__ void __launch_bounds__(NW * 64) k_gemv16(GemvArgs a) {
       sv[ml][c] = s;
     }
     __syncthreads();
-    finish_tile<bf16, EPI, 32, 16, NW * 64>(a, sv, ov, tile0 * 16, blockIdx.x * 16, pre);
+    finish_tile<bf16, EPI, 32, 16, NW * 64>(a, sv, ov, oz, tile0 * 16, blockIdx.x * 16, pre);
     if (a.nsplit == 3) break;
   }
 }
@@ -192,7 +233,8 @@ __global__ void __launch_bounds__(NW * 64) k_gemv16w(GemvArgs a) {
   constexpr int TC = 16 * CT;
   __shared__ float red[NW][32][TC + 1];
   __shared__ float sv[32][TC + 1];
-  __shared__ float ov[32][TC];
+  __shared__ float ov[EPI == EPI_ARGMAX ? 32 : 1][TC];
+  __shared__ float oz[EPI == EPI_ARGMAX ? 32 : 1][TC];
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
   EpiPre<TC, NW * 64> pre;
   pre.template load<bf16, EPI>(a, blockIdx.x * TC);
@@ -253,7 +295,7 @@ __global__ void __launch_bounds__(NW * 64) k_gemv16w(GemvArgs a) {
       sv[ml][c] = s;
     }
     __syncthreads();
-    finish_tile<bf16, EPI, 32, TC, NW * 64>(a, sv, ov, tile0 * 16, blockIdx.x * TC, pre);
+    finish_tile<bf16, EPI, 32, TC, NW * 64>(a, sv, ov, oz, tile0 * 16, blockIdx.x * TC, pre);
     if (a.nsplit == 3) break;
   }
 }
@@ -264,7 +306,8 @@ __global__ void __launch_bounds__(NW * 64) k_gemv32(GemvArgs a) {
   constexpr int U = NW >= 16 ? kU / 2 : kU;
   __shared__ float red[NW][32][33];
   __shared__ float sv[32][33];
-  __shared__ float ov[32][32];
+  __shared__ float ov[EPI == EPI_ARGMAX ? 32 : 1][32];
+  __shared__ float oz[EPI == EPI_ARGMAX ? 32 : 1][32];
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
   EpiPre<32, NW * 64> pre;
   pre.template load<bf16, EPI>(a, blockIdx.x * 32);
@@ -303,7 +346,7 @@ __global__ void __launch_bounds__(NW * 64) k_gemv32(GemvArgs a) {
       sv[ml][c] = s;
     }
     __syncthreads();
-    finish_tile<bf16, EPI, 32, 32, NW * 64>(a, sv, ov, tile0 * 32, blockIdx.x * 32, pre);
+    finish_tile<bf16, EPI, 32, 32, NW * 64>(a, sv, ov, oz, tile0 * 32, blockIdx.x * 32, pre);
     if (a.nsplit == 3) break;
   }
 }
@@ -427,7 +470,8 @@ __global__ void __launch_bounds__(NW * 64) k_gemv16_ln(GemvArgs a) {
   __shared__ uint4 aop[kLnFoldMaxK / 32 * 2 * 64];
   __shared__ float red[NW][32][17];
   __shared__ float sv[32][17];
-  __shared__ float ov[32][16];
+  __shared__ float ov[EPI == EPI_ARGMAX ? 32 : 1][16];
+  __shared__ float oz[EPI == EPI_ARGMAX ? 32 : 1][16];
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
   EpiPre<16, NW * 64> pre;
   pre.template load<bf16, EPI>(a, blockIdx.x * 16);
@@ -467,7 +511,7 @@ __global__ void __launch_bounds__(NW * 64) k_gemv16_ln(GemvArgs a) {
     sv[ml][c] = s;
   }
   __syncthreads();
-  finish_tile<bf16, EPI, 32, 16, NW * 64>(a, sv, ov, 0, blockIdx.x * 16, pre);
+  finish_tile<bf16, EPI, 32, 16, NW * 64>(a, sv, ov, oz, 0, blockIdx.x * 16, pre);
 }
 
 // 32-column tiles; every wave's k-steps fit one batch of loads (K <= kLnFoldMaxK).
@@ -476,7 +520,8 @@ __global__ void __launch_bounds__(NW * 64) k_gemv32_ln(GemvArgs a) {
   __shared__ uint4 aop[kLnFoldMaxK / 16 * 64];
   __shared__ float red[NW][32][33];
   __shared__ float sv[32][33];
-  __shared__ float ov[32][32];
+  __shared__ float ov[EPI == EPI_ARGMAX ? 32 : 1][32];
+  __shared__ float oz[EPI == EPI_ARGMAX ? 32 : 1][32];
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
   EpiPre<32, NW * 64> pre;
   pre.template load<bf16, EPI>(a, blockIdx.x * 32);
@@ -512,7 +557,7 @@ __global__ void __launch_bounds__(NW * 64) k_gemv32_ln(GemvArgs a) {
     sv[ml][c] = s;
   }
   __syncthreads();
-  finish_tile<bf16, EPI, 32, 32, NW * 64>(a, sv, ov, 0, blockIdx.x * 32, pre);
+  finish_tile<bf16, EPI, 32, 32, NW * 64>(a, sv, ov, oz, 0, blockIdx.x * 32, pre);
 }
 
 // ---------------------------------------------------------------- fp32, row-major
@@ -523,7 +568,8 @@ __global__ void __launch_bounds__(NW * 64) k_gemv_f32(GemvArgs a) {
   constexpr int U = NW >= 16 ? kU / 2 : kU;
   __shared__ float red[NW][32][17];
   __shared__ float sv[32][17];
-  __shared__ float ov[32][16];
+  __shared__ float ov[EPI == EPI_ARGMAX ? 32 : 1][16];
+  __shared__ float oz[EPI == EPI_ARGMAX ? 32 : 1][16];
   const float* __restrict__ W = reinterpret_cast<const float*>(a.w);
   const float* __restrict__ A = reinterpret_cast<const float*>(a.a.p);
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
@@ -580,7 +626,7 @@ __global__ void __launch_bounds__(NW * 64) k_gemv_f32(GemvArgs a) {
       sv[ml][c] = s;
     }
     __syncthreads();
-    finish_tile<float, EPI, 32, 16, NW * 64>(a, sv, ov, tile0 * 16, nb, pre);
+    finish_tile<float, EPI, 32, 16, NW * 64>(a, sv, ov, oz, tile0 * 16, nb, pre);
   }
 }
 

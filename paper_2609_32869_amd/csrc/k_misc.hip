@@ -67,24 +67,51 @@ constexpr int kArgmaxLoads = 8;
 __global__ void __launch_bounds__(256) k_argmax_final(const float* __restrict__ hv, const int* __restrict__ hi,
                                                       int nblk, int row0, int* __restrict__ g,
                                                       float* __restrict__ gmax, unsigned* status, int* keep, int* dst,
-                                                      int slot0, int K) {
+                                                      int slot0, int K, const float* __restrict__ hm,
+                                                      const float* __restrict__ hs, float* rmax, float* rsum) {
   __shared__ float bvs[4];
   __shared__ int bis[4];
+  __shared__ float ms[4], ss[4];
   const int row = row0 + blockIdx.x;
   float bv = -INFINITY;
   int bi = 0x7fffffff;
+  float zm = -INFINITY, zs = 0.f;  // normaliser over this thread's blocks
   for (int j0 = threadIdx.x; j0 < nblk; j0 += 256 * kArgmaxLoads) {
-    float v[kArgmaxLoads];
+    float v[kArgmaxLoads], bm[kArgmaxLoads], bs[kArgmaxLoads];
     int ix[kArgmaxLoads];
 #pragma unroll
     for (int u = 0; u < kArgmaxLoads; ++u) {
       const int j = j0 + 256 * u;
       v[u] = j < nblk ? hv[(size_t)row * nblk + j] : -INFINITY;
       ix[u] = j < nblk ? hi[(size_t)row * nblk + j] : 0x7fffffff;
+      bm[u] = (hm != nullptr && j < nblk) ? hm[(size_t)row * nblk + j] : -INFINITY;
+      bs[u] = (hm != nullptr && j < nblk) ? hs[(size_t)row * nblk + j] : 0.f;
     }
 #pragma unroll
-    for (int u = 0; u < kArgmaxLoads; ++u)
+    for (int u = 0; u < kArgmaxLoads; ++u) {
       if (better(v[u], ix[u], bv, bi)) { bv = v[u]; bi = ix[u]; }
+      if (bm[u] > -INFINITY) {
+        const float mn = fmaxf(zm, bm[u]);
+        zs = zs * expf(zm - mn) + bs[u] * expf(bm[u] - mn);
+        zm = mn;
+      }
+    }
+  }
+  if (hm != nullptr) {
+    // fixed-order combine: within the wave, then across the four waves
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+      const float om = __shfl_xor(zm, o, 64), os = __shfl_xor(zs, o, 64);
+      const float mn = fmaxf(zm, om);
+      if (mn > -INFINITY) {
+        zs = zs * expf(zm - mn) + os * expf(om - mn);
+        zm = mn;
+      }
+    }
+    if ((threadIdx.x & 63) == 0) {
+      ms[threadIdx.x >> 6] = zm;
+      ss[threadIdx.x >> 6] = zs;
+    }
   }
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) {
@@ -101,6 +128,14 @@ __global__ void __launch_bounds__(256) k_argmax_final(const float* __restrict__ 
     g[row] = bis[0];
     gmax[row] = bvs[0];
     if (!isfinite(bvs[0])) atomicOr(status, WF_STATUS_NONFINITE_LOGITS);
+    if (hm != nullptr && rmax != nullptr) {
+      float M = ms[0];
+      for (int j = 1; j < 4; ++j) M = fmaxf(M, ms[j]);
+      float Ssum = 0.f;
+      for (int j = 0; j < 4; ++j) Ssum += ss[j] * expf(ms[j] - M);
+      rmax[row] = M;
+      rsum[row] = Ssum;
+    }
     const int slot = row / kRows, i = row - slot * kRows;
     if (keep != nullptr && i >= 1 && i <= K) {
       keep[(size_t)slot * K + i - 1] = bis[0];
@@ -351,6 +386,189 @@ __global__ void k_accept_greedy(AcceptArgs a) {
   if (a.done) a.done[s] = done;
 }
 
+// ---------------------------------------------------------------- sampling acceptance
+// Speculative rejection rule (Section 3.1, Appendix A.4) with fp32 softmaxes of the
+// scaled logits: candidate c_j (drafted from q_j = draft row j) is accepted iff
+// u_j * q_j(c_j) < p_{j-1}(c_j), u_j the acceptance uniform of position j - 1.  At
+// the first rejection a token is drawn from (p - q)_+ (from p if that set is
+// empty), after k acceptances a bonus from target row k, and with k = 0 a plain
+// draw from row 0; draws are Gumbel-max.  An accepted end-of-transcript
+// candidate ends the transcript with no draw.
+enum { SM_NONE = 0, SM_RES = 1, SM_BON = 2, SM_PLAIN = 3 };
+
+__device__ __forceinline__ float prob_of(const float* logits, int V, float zmax, float zsum, float inv_t, int c) {
+  return expf(logits[c] * inv_t - zmax) / zsum;
+}
+
+// one thread per slot: accepted count and the draw to make
+__global__ void k_sample_scan(SampleArgs a) {
+  const int s = blockIdx.x * blockDim.x + threadIdx.x;
+  if (s >= a.n) return;
+  const int slot = a.slot0 + s;
+  const int* st = a.state + slot * kStateInts;
+  int* o = a.sst + slot * 4;
+  const int nv = st[ST_NV];
+  if (nv == 0) {
+    o[0] = SM_NONE; o[1] = 0; o[2] = 0; o[3] = -1;  // nothing verified (finished slot)
+    return;
+  }
+  const int k = nv - 1, step = st[ST_STEP];
+  const int* tok = a.tok + slot * kRows;
+  const size_t V = a.V;
+  int mode = k == 0 ? SM_PLAIN : SM_BON, row = k == 0 ? 0 : k, acc = k, fin = 0;
+  for (int j = 0; j < k; ++j) {
+    const int c = tok[j + 1];
+    const int tr = slot * kRows + j, dr = slot * kRows + j + 1;
+    const float q = prob_of(a.lq + dr * V, a.V, a.dmax[dr], a.dsum[dr], a.inv_t, c);
+    const float p = prob_of(a.lp + tr * V, a.V, a.tmax[tr], a.tsum[tr], a.inv_t, c);
+    const float u = rng_uniform(rng_word(a.seed, RNG_ACC, slot, step, 0, j));
+    if (!(u * q < p)) {
+      mode = SM_RES;
+      row = j;
+      acc = j;
+      break;
+    }
+    if (c == a.eos) {
+      mode = SM_NONE;
+      acc = j + 1;
+      fin = 1;
+      break;
+    }
+  }
+  o[0] = mode; o[1] = row; o[2] = acc; o[3] = fin;
+}
+
+// grid (nsb, n): Gumbel-max partials of the slot's draw over a slice of the vocabulary
+constexpr int kSampleThreads = 256;
+__global__ void __launch_bounds__(kSampleThreads) k_sample_draw(SampleArgs a) {
+  __shared__ float sb[4][4];
+  __shared__ int si[4][4];
+  const int slot = a.slot0 + blockIdx.y;
+  const int* o = a.sst + slot * 4;
+  const int mode = o[0], row = o[1];
+  if (mode == SM_NONE) return;
+  const int step = a.state[slot * kStateInts + ST_STEP];
+  const int V = a.V;
+  const int cs = (V + a.nsb - 1) / a.nsb;
+  const int v0 = blockIdx.x * cs, v1 = min(V, v0 + cs);
+  const int tr = slot * kRows + row, dr = slot * kRows + row + 1;
+  const float* lp = a.lp + (size_t)tr * V;
+  const float* lq = a.lq + (size_t)dr * V;
+  float best = -INFINITY, fb = -INFINITY;
+  int bi = 0x7fffffff, fi = 0x7fffffff;
+  for (int v = v0 + threadIdx.x; v < v1; v += kSampleThreads) {
+    float score, fscore = -INFINITY;
+    if (mode == SM_RES) {
+      const float g = rng_gumbel(rng_word(a.seed, RNG_RES, slot, step, row + 1, v));
+      const float p = prob_of(lp, V, a.tmax[tr], a.tsum[tr], a.inv_t, v);
+      const float q = prob_of(lq, V, a.dmax[dr], a.dsum[dr], a.inv_t, v);
+      const float r = p - q;
+      score = r > 0.f ? logf(r) + g : -INFINITY;
+      fscore = p > 0.f ? logf(p) + g : -INFINITY;
+    } else {
+      const int purpose = mode == SM_BON ? RNG_BON : RNG_PLAIN;
+      score = lp[v] * a.inv_t + rng_gumbel(rng_word(a.seed, purpose, slot, step, 0, v));
+    }
+    if (better(score, v, best, bi)) { best = score; bi = v; }
+    if (better(fscore, v, fb, fi)) { fb = fscore; fi = v; }
+  }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) {
+    const float ob = __shfl_xor(best, off, 64), of = __shfl_xor(fb, off, 64);
+    const int oi = __shfl_xor(bi, off, 64), oj = __shfl_xor(fi, off, 64);
+    if (better(ob, oi, best, bi)) { best = ob; bi = oi; }
+    if (better(of, oj, fb, fi)) { fb = of; fi = oj; }
+  }
+  const int w = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 0) {
+    sb[w][0] = best; si[w][0] = bi; sb[w][1] = fb; si[w][1] = fi;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    for (int j = 1; j < 4; ++j) {
+      if (better(sb[j][0], si[j][0], best, bi)) { best = sb[j][0]; bi = si[j][0]; }
+      if (better(sb[j][1], si[j][1], fb, fi)) { fb = sb[j][1]; fi = si[j][1]; }
+    }
+    float* pp = a.part + ((size_t)slot * a.nsb + blockIdx.x) * 4;
+    pp[0] = best;
+    pp[1] = __int_as_float(bi);
+    pp[2] = fb;
+    pp[3] = __int_as_float(fi);
+  }
+}
+
+// one thread per slot: the drawn token, emitted tokens and the state update
+__global__ void k_sample_final(SampleArgs a) {
+  const int s = blockIdx.x * blockDim.x + threadIdx.x;
+  if (s >= a.n) return;
+  const int slot = a.slot0 + s;
+  int* st = a.state + slot * kStateInts;
+  const int* o = a.sst + slot * 4;
+  const int K = a.block_k;
+  int* out = a.out ? a.out + (size_t)s * (K + 1) : nullptr;
+  const int nv = st[ST_NV];
+  if (nv == 0) {
+    if (a.n_out) a.n_out[s] = 0;
+    if (a.n_acc) a.n_acc[s] = 0;
+    if (a.done) a.done[s] = st[ST_LIVE] ? 1 : 0;
+    if (st[ST_LIVE]) st[ST_DONE] = 1;
+    return;
+  }
+  const int mode = o[0], acc = o[2];
+  bool fin = o[3] != 0;
+  const int* tok = a.tok + slot * kRows;
+  int nemit = 0;
+  for (int e = 0; e < acc; ++e) {
+    if (out) out[nemit] = tok[e + 1];
+    ++nemit;
+  }
+  int last = acc > 0 ? tok[acc] : -1;
+  if (mode != SM_NONE) {
+    float best = -INFINITY, fb = -INFINITY;
+    int bi = 0x7fffffff, fi = 0x7fffffff;
+    for (int b = 0; b < a.nsb; ++b) {
+      const float* pp = a.part + ((size_t)slot * a.nsb + b) * 4;
+      if (better(pp[0], __float_as_int(pp[1]), best, bi)) { best = pp[0]; bi = __float_as_int(pp[1]); }
+      if (better(pp[2], __float_as_int(pp[3]), fb, fi)) { fb = pp[2]; fi = __float_as_int(pp[3]); }
+    }
+    last = (mode == SM_RES && best == -INFINITY) ? fi : bi;  // empty residual: draw from p
+    if (out) out[nemit] = last;
+    ++nemit;
+    fin = last == a.eos;
+  }
+  const int L = st[ST_L];
+  st[ST_HPOS] = L;
+  st[ST_HN] = nv;
+  st[ST_L] = L + 1 + acc;
+  st[ST_ANCHOR] = last;
+  st[ST_EMITTED] += nemit;
+  st[ST_STEP] += 1;
+  st[ST_K] = nv - 1;
+  st[ST_A] = acc;
+  const bool done = fin || st[ST_EMITTED] >= st[ST_MAX_NEW] || st[ST_L] >= a.n_ctx;
+  st[ST_DONE] = done;
+  if (out)
+    for (int j = nemit; j <= K; ++j) out[j] = -1;
+  if (a.n_out) a.n_out[s] = nemit;
+  if (a.n_acc) a.n_acc[s] = acc;
+  if (a.done) a.done[s] = done;
+}
+
+// raw generator words (test entry point)
+__global__ void k_rng_words(uint64_t seed, int purpose, int slot, int step, int pos, int n, uint64_t* out) {
+  const int v = blockIdx.x * blockDim.x + threadIdx.x;
+  if (v < n) out[v] = rng_word(seed, purpose, slot, step, pos, v);
+}
+void rng_words_device(uint64_t seed, int purpose, int slot, int step, int pos, int n, uint64_t* out, hipStream_t st) {
+  if (n > 0) k_rng_words<<<(n + 255) / 256, 256, 0, st>>>(seed, purpose, slot, step, pos, n, out);
+}
+
+void accept_sample(const SampleArgs& a, hipStream_t st) {
+  k_sample_scan<<<(a.n + 63) / 64, 64, 0, st>>>(a);
+  k_sample_draw<<<dim3(a.nsb, a.n), kSampleThreads, 0, st>>>(a);
+  k_sample_final<<<(a.n + 63) / 64, 64, 0, st>>>(a);
+}
+
 // ---------------------------------------------------------------- encode: cross K/V
 // C[f, n] = sum_k A[f, k] W[n, k] + b[n] for the 2d key/value columns of one
 // block, written to the per-head frame-major cross cache.  64x64 tiles, fp32
@@ -499,8 +717,9 @@ void Ops<S>::gemm_xkv(const XkvArgs& a, hipStream_t st) {
 }
 
 void argmax_final(const float* hv, const int* hi, int nblk, int row0, int rows, int* g, float* gmax,
-                  unsigned* status, int* keep, int* dst, int slot0, int K, hipStream_t st) {
-  k_argmax_final<<<rows, 256, 0, st>>>(hv, hi, nblk, row0, g, gmax, status, keep, dst, slot0, K);
+                  unsigned* status, int* keep, int* dst, int slot0, int K, const float* hm, const float* hs, float* rmax,
+                  float* rsum, hipStream_t st) {
+  k_argmax_final<<<rows, 256, 0, st>>>(hv, hi, nblk, row0, g, gmax, status, keep, dst, slot0, K, hm, hs, rmax, rsum);
 }
 void save_last(const float* h, float* lasth, const int* state, int slot0, int n, int d, int chunk, hipStream_t st) {
   k_save_last<<<n, 256, 0, st>>>(h, lasth, state, slot0, d, chunk);

@@ -184,6 +184,14 @@ int compute_layout(const wf_config& c, Layout& L) {
   L.kvh = region(R9 * 2 * d * 4);
   L.hv = region(R9 * L.head_blocks * 4);
   L.hi = region(R9 * L.head_blocks * 4);
+  L.hm = region(R9 * L.head_blocks * 4);
+  L.hs = region(R9 * L.head_blocks * 4);
+  L.tmax = region(R9 * 4);
+  L.tsum = region(R9 * 4);
+  L.dmax = region(R9 * 4);
+  L.dsum = region(R9 * 4);
+  L.sst = region(B * 4 * 4);
+  L.spart = region(B * kSampleBlocks * 4 * 4);
   L.tok = region(R9 * 4);
   L.g = region(R9 * 4);
   L.gmax = region(R9 * 4);
@@ -438,20 +446,34 @@ struct Runner {
     }
   }
 
-  // vocabulary head: logits = LN_final(x) @ tok_emb^T, per-row argmax into g
-  // Drafter pass: keep/dst receive the drafted tokens (rows 1..K).
+  bool sampling() const { return h->temperature > 0.f; }
+
+  // vocabulary head: logits = LN_final(x) @ tok_emb^T, per-row argmax into g.
+  // Drafter pass: keep/dst receive the drafted tokens (rows 1..K).  When sampling,
+  // the rows' scores are logit / T plus Gumbel noise of stream `purpose` (none for
+  // 0), the softmax normalisers go to rmax/rsum and the logits are kept.
   void head(int slot0, int n, const float* x, size_t g, size_t gb, float* logits, int* keep = nullptr,
-            int* dst = nullptr) {
+            int* dst = nullptr, int purpose = 0, float* rmax = nullptr, float* rsum = nullptr) {
     GemvArgs a = gemv_base(slot0, n, wk(true));
     a.w = W(L.tok_emb); a.bias = nullptr; a.K = c.d_model; a.N = c.n_vocab;
     a.y = logits; a.ldy = c.n_vocab; a.hv = F32(L.hv); a.hi = I32(L.hi); a.nblk = L.head_blocks;
+    a.suppress = h->suppress;
+    if (sampling()) {
+      a.inv_t = h->inv_t;
+      a.rng_purpose = purpose;
+      a.seed = h->seed;
+      if (rmax != nullptr) {  // softmax normalisers only where acceptance needs them
+        a.hm = F32(L.hm);
+        a.hs = F32(L.hs);
+      }
+    }
     if (ln_ready) a.a = Ad32();
     else ln_operand(a, slot0, n, x, g, gb, Ad32(), false);
     ln_ready = false;
     run_gemv(EPI_ARGMAX, n, a);
     launch("argmax_final", kRows * n * L.head_blocks * 8.0, [&] {
       argmax_final(F32(L.hv), I32(L.hi), L.head_blocks, slot0 * kRows, n * kRows, I32(L.g), F32(L.gmax),
-                   h->at<unsigned>(L.status), keep, dst, slot0, c.block_k, st);
+                   h->at<unsigned>(L.status), keep, dst, slot0, c.block_k, a.hm, a.hs, rmax, rsum, st);
     });
   }
 
@@ -496,7 +518,8 @@ struct Runner {
                                                  : LnNext{L.dlnf_g, L.dlnf_b, true};
       block_tail(slot0, n, b, c.n_layer + dl, -1, nx);
     }
-    head(slot0, n, h_, L.dlnf_g, L.dlnf_b, h->debug ? F32(L.dlogits) : nullptr, I32(L.draft), dst);
+    head(slot0, n, h_, L.dlnf_g, L.dlnf_b, h->debug || sampling() ? F32(L.dlogits) : nullptr, I32(L.draft), dst,
+         RNG_DRAFT, F32(L.dmax), F32(L.dsum));
   }
 
   void verify(int slot0, int n, const int* draft, int k_max, int* out, int* n_out, int* n_acc, int* done) {
@@ -506,7 +529,19 @@ struct Runner {
     ba.block_k = c.block_k; ba.k_max = k_max;
     launch("begin", 0, [&] { Ops<S>::verify_begin(ba, n, st); });
     target_forward(slot0, n);
-    head(slot0, n, F32(L.h), L.lnf_g, L.lnf_b, h->debug ? F32(L.logits) : nullptr);
+    head(slot0, n, F32(L.h), L.lnf_g, L.lnf_b, h->debug || sampling() ? F32(L.logits) : nullptr, nullptr, nullptr, 0,
+         F32(L.tmax), F32(L.tsum));
+    if (sampling()) {
+      SampleArgs sa{};
+      sa.state = I32(L.state); sa.tok = I32(L.tok); sa.lp = F32(L.logits); sa.lq = F32(L.dlogits);
+      sa.tmax = F32(L.tmax); sa.tsum = F32(L.tsum); sa.dmax = F32(L.dmax); sa.dsum = F32(L.dsum);
+      sa.sst = I32(L.sst); sa.part = F32(L.spart); sa.nsb = kSampleBlocks;
+      sa.out = out; sa.n_out = n_out; sa.n_acc = n_acc; sa.done = done;
+      sa.slot0 = slot0; sa.n = n; sa.block_k = c.block_k; sa.eos = c.eos_id; sa.n_ctx = c.n_ctx; sa.V = c.n_vocab;
+      sa.inv_t = h->inv_t; sa.seed = h->seed;
+      launch("accept", 0, [&] { accept_sample(sa, st); });
+      return;
+    }
     AcceptArgs aa{};
     aa.state = I32(L.state); aa.tok = I32(L.tok); aa.g = I32(L.g); aa.out = out; aa.n_out = n_out; aa.n_acc = n_acc;
     aa.done = done; aa.slot0 = slot0; aa.n = n; aa.block_k = c.block_k; aa.eos = c.eos_id; aa.n_ctx = c.n_ctx;
@@ -551,7 +586,7 @@ struct Runner {
       history_apply(slot0, n);
     }
     ln_ready = false;  // the final LayerNorm applies to the saved last rows, not to h
-    head(slot0, n, F32(L.lasth), L.lnf_g, L.lnf_b, nullptr);
+    head(slot0, n, F32(L.lasth), L.lnf_g, L.lnf_b, nullptr, nullptr, nullptr, RNG_PREFILL);
     prefill_finish(I32(L.state), I32(L.g), slot0, n, c.eos_id, c.n_ctx, first, st);
   }
 };
@@ -702,7 +737,6 @@ int wf_prefill(wf_handle* hh, int slot0, int n, const int32_t* tokens, int pmax,
   Handle* h = reinterpret_cast<Handle*>(hh);
   if (int r = check_batch(h, slot0, n, false)) return r;
   if (!tokens || !lens || !max_new || pmax < 1) return fail(h, WF_EINVAL, "null argument");
-  if (h->temperature > 0.f) return fail(h, WF_EINVAL, "sampling is not available in this build");
   int max_len = 0;
   for (int s = 0; s < n; ++s) {
     if (lens[s] < 1 || lens[s] > pmax || lens[s] > h->cfg.n_ctx) return fail(h, WF_EINVAL, "prompt length out of range");
@@ -731,10 +765,13 @@ int wf_set_sampling(wf_handle* hh, float temperature, uint64_t seed, const uint8
   Handle* h = reinterpret_cast<Handle*>(hh);
   if (!h) return fail(nullptr, WF_EINVAL, "null handle");
   if (!(temperature >= 0.f) || std::isinf(temperature)) return fail(h, WF_EINVAL, "temperature must be finite and >= 0");
-  if (temperature > 0.f) return fail(h, WF_EINVAL, "sampling is not available in this build");
   h->temperature = temperature;
+  h->inv_t = temperature > 0.f ? (float)(1.0 / (double)temperature) : 0.f;
   h->seed = seed;
   h->suppress = suppress;
+  // captured steps bake the sampling parameters in
+  for (auto& kv : h->graphs) (void)hipGraphExecDestroy(kv.second);
+  h->graphs.clear();
   return WF_OK;
 }
 
@@ -886,6 +923,20 @@ int wf_release(wf_handle* hh) {
   for (auto& r : h->prof_recs) { (void)hipEventDestroy(r.a); (void)hipEventDestroy(r.b); }
   for (auto e : h->ev_pool) (void)hipEventDestroy(e);
   delete h;
+  return WF_OK;
+}
+
+int wf_rng_words_host(uint64_t seed, int purpose, int slot, int step, int pos, int n, uint64_t* out) {
+  if (!out || n < 0) return fail(nullptr, WF_EINVAL, "null output or negative count");
+  for (int v = 0; v < n; ++v) out[v] = rng_word(seed, purpose, slot, step, pos, v);
+  return WF_OK;
+}
+
+int wf_rng_words_device(uint64_t seed, int purpose, int slot, int step, int pos, int n, uint64_t* out, void* stream) {
+  if (!out || n < 0) return fail(nullptr, WF_EINVAL, "null output or negative count");
+  rng_words_device(seed, purpose, slot, step, pos, n, out, static_cast<hipStream_t>(stream));
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return fail(nullptr, WF_EHIP, std::string("kernel launch: ") + hipGetErrorString(e));
   return WF_OK;
 }
 

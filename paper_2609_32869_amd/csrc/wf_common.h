@@ -153,6 +153,61 @@ __device__ __forceinline__ bool better(float v, int i, float bv, int bi) {
   return i < bi;
 }
 
+// ---------------------------------------------------------------- counter-based randomness
+// Philox4x64-10 (Salmon, Moraes, Dror, Shaw, SC'11): ten rounds mapping a 256-bit
+// counter and a 128-bit key to 256 bits.  A round multiplies words 0 and 2 by two
+// fixed 64-bit constants, swaps the halves of the 128-bit products into the
+// other words and mixes in the key; the key advances by two Weyl increments
+// between rounds.
+constexpr uint64_t kPhiloxM0 = 0xD2E7470EE14C6C93ull;
+constexpr uint64_t kPhiloxM1 = 0xCA5A826395121157ull;
+constexpr uint64_t kPhiloxW0 = 0x9E3779B97F4A7C15ull;
+constexpr uint64_t kPhiloxW1 = 0xBB67AE8584CAA73Bull;
+
+struct Philox4 {
+  uint64_t w[4];
+};
+
+__host__ __device__ __forceinline__ uint64_t mul_hi64(uint64_t a, uint64_t b) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  return __umul64hi(a, b);
+#else
+  return (uint64_t)(((unsigned __int128)a * b) >> 64);
+#endif
+}
+
+__host__ __device__ __forceinline__ Philox4 philox4x64_10(uint64_t c0, uint64_t c1, uint64_t c2, uint64_t c3,
+                                                         uint64_t k0, uint64_t k1) {
+#pragma unroll
+  for (int r = 0; r < 10; ++r) {
+    if (r > 0) {
+      k0 += kPhiloxW0;
+      k1 += kPhiloxW1;
+    }
+    const uint64_t lo0 = kPhiloxM0 * c0, hi0 = mul_hi64(kPhiloxM0, c0);
+    const uint64_t lo1 = kPhiloxM1 * c2, hi1 = mul_hi64(kPhiloxM1, c2);
+    const uint64_t n0 = hi1 ^ c1 ^ k0, n2 = hi0 ^ c3 ^ k1;
+    c0 = n0;
+    c1 = lo1;
+    c2 = n2;
+    c3 = lo0;
+  }
+  return Philox4{{c0, c1, c2, c3}};
+}
+
+// Decoding randomness: key (seed, 0), counter (purpose << 32 | slot, step, pos, v >> 2),
+// word v & 3.  purpose: 1 prefill, 2 plain, 3 draft, 4 acceptance, 5 residual, 6 bonus.
+enum { RNG_PREFILL = 1, RNG_PLAIN = 2, RNG_DRAFT = 3, RNG_ACC = 4, RNG_RES = 5, RNG_BON = 6 };
+__host__ __device__ __forceinline__ uint64_t rng_word(uint64_t seed, int purpose, int slot, int step, int pos, int v) {
+  const Philox4 r = philox4x64_10(((uint64_t)purpose << 32) | (uint32_t)slot, (uint64_t)(uint32_t)step,
+                                  (uint64_t)(uint32_t)pos, (uint64_t)((uint32_t)v >> 2), seed, 0);
+  return r.w[v & 3];
+}
+// fp32 uniform in (0, 1): the top 23 bits plus one half, scaled by 2^-23
+__device__ __forceinline__ float rng_uniform(uint64_t x) { return ((float)(x >> 41) + 0.5f) * 0x1p-23f; }
+// Gumbel noise -log(-log(u)) in fp32
+__device__ __forceinline__ float rng_gumbel(uint64_t x) { return -logf(-logf(rng_uniform(x))); }
+
 __device__ __forceinline__ float gelu_erf(float x) { return 0.5f * x * (1.0f + erff(x * 0.70710678118654752440f)); }
 
 }  // namespace wf

@@ -26,6 +26,7 @@ struct Layout {
   // byte offsets into the workspace
   size_t state, page_table, rope, status, aux, weights, xkv, skv, hkv;
   size_t a_d16, a_d32, a_f16, a_tap16, h, qkv, hp, kvh, hv, hi, tok, g, gmax, draft, lasth, logits, dlogits, part;
+  size_t hm, hs, tmax, tsum, dmax, dsum, sst, spart;  // sampling: normalisers and draw partials
   size_t total;
   // element offsets inside the weight region
   size_t tok_emb, pos_emb, lnf_g, lnf_b, hproj_w, hproj_b, mask, dlnf_g, dlnf_b;
@@ -61,6 +62,7 @@ struct Handle {
   char* ws;
   size_t ws_bytes;
   float temperature = 0.f;
+  float inv_t = 0.f;  // fp32(1 / temperature) when sampling
   uint64_t seed = 0;
   const uint8_t* suppress = nullptr;
   bool debug = false;

@@ -56,10 +56,19 @@ struct GemvArgs {
   void* cache;
   size_t kv_stride;
   int d, n_head, n_ctx, pages_per_slot;
-  // ARGMAX partials
+  // ARGMAX partials: best score and its column per (row, block); with inv_t > 0
+  // the scores are z = logit * inv_t, plus Gumbel noise of stream rng_purpose (if
+  // nonzero; position = row within the slot), and hm/hs receive the block's max of z
+  // and sum of exp(z - max) for the softmax normaliser
   float* hv;
   int* hi;
   int nblk;
+  const uint8_t* suppress;  // [N] nonzero: column excluded (logit -inf), or null
+  float inv_t;
+  int rng_purpose;
+  uint64_t seed;
+  float* hm;
+  float* hs;
 };
 
 struct AttnArgs {
@@ -163,14 +172,44 @@ struct Ops {
 template <typename S>
 void repack(const void* src, void* dst, int N, int K, int wkind, hipStream_t st);
 
-constexpr int kRlnMaxPartsHost = 16;  // most split-K partials a reduction sums
+constexpr int kRlnMaxPartsHost = 16;
+constexpr int kSampleBlocks = 64;     // vocabulary slices of a sampling draw per slot  // most split-K partials a reduction sums
 
 // largest row length K of a product with the LayerNorm folded in (its operand is
 // staged whole in LDS)
 constexpr int kLnFoldMaxK = 1280;
 
+// Per-row final argmax over the head's block partials; with hm set also the
+// softmax normaliser (rmax = max z, rsum = sum exp(z - rmax)).
 void argmax_final(const float* hv, const int* hi, int nblk, int row0, int rows, int* g, float* gmax, unsigned* status,
-                  int* keep, int* dst, int slot0, int K, hipStream_t st);
+                  int* keep, int* dst, int slot0, int K, const float* hm, const float* hs, float* rmax, float* rsum,
+                  hipStream_t st);
+
+// Sampling acceptance (rejection rule), three launches: per-slot scan of the
+// candidates, a Gumbel-max pass over the vocabulary for the residual / bonus /
+// plain draw, and the final token plus state update.
+struct SampleArgs {
+  int* state;
+  const int* tok;       // [rows] verify tokens (anchor, c_1..c_k)
+  const float* lp;      // target logits [rows][V]
+  const float* lq;      // draft logits [rows][V] (row j holds mask j)
+  const float* tmax;    // target row normalisers
+  const float* tsum;
+  const float* dmax;    // draft row normalisers
+  const float* dsum;
+  int* sst;             // per slot: mode, row, accepted count, finished
+  float* part;          // [slot][nsb][4]: best, index, fallback best, fallback index
+  int nsb;
+  int* out;
+  int* n_out;
+  int* n_acc;
+  int* done;
+  int slot0, n, block_k, eos, n_ctx, V;
+  float inv_t;
+  uint64_t seed;
+};
+void accept_sample(const SampleArgs& a, hipStream_t st);
+void rng_words_device(uint64_t seed, int purpose, int slot, int step, int pos, int n, uint64_t* out, hipStream_t st);
 void save_last(const float* h, float* lasth, const int* state, int slot0, int n, int d, int chunk, hipStream_t st);
 void prefill_finish(int* state, const int* g, int slot0, int n, int eos, int n_ctx, int* first, hipStream_t st);
 void accept_greedy(const AcceptArgs& a, hipStream_t st);
