@@ -331,13 +331,14 @@ struct Runner {
     a.tap = tap;
     return a;
   }
-  void run_gemv(int epi, int n, const GemvArgs& a) {
-    launch("gemv", gemv_bytes(n, a.K, a.N, epi), [&] { Ops<S>::gemv(epi, a, st); });
+  // tag: the product's role in the step, for the eager profile
+  void run_gemv(const char* tag, int epi, int n, const GemvArgs& a) {
+    launch(tag, gemv_bytes(n, a.K, a.N, epi), [&] { Ops<S>::gemv(epi, a, st); });
   }
 
-  void gemv(int epi, int slot0, int n, Operand x, size_t w, size_t b, int K, int N, float* y, int ldy,
+  void gemv(const char* tag, int epi, int slot0, int n, Operand x, size_t w, size_t b, int K, int N, float* y, int ldy,
             Operand aout = Operand{nullptr, 0, OP_ROW, 0}, int tap = -1) {
-    run_gemv(epi, n, gemv_args(slot0, n, x, w, b, K, N, y, ldy, aout, tap));
+    run_gemv(tag, epi, n, gemv_args(slot0, n, x, w, b, K, N, y, ldy, aout, tap));
   }
 
   // LayerNorm folded into the product that consumes it: bf16 storage at batch 1
@@ -360,11 +361,11 @@ struct Runner {
   }
 
   // y = LN(x) W^T + bias with the LayerNorm operand in `op` when not folded
-  void gemv_ln(int epi, int slot0, int n, const float* x, size_t g, size_t gb, Operand op, size_t w, size_t b, int K,
-               int N, float* y, int ldy, Operand aout = Operand{nullptr, 0, OP_ROW, 0}) {
+  void gemv_ln(const char* tag, int epi, int slot0, int n, const float* x, size_t g, size_t gb, Operand op, size_t w,
+               size_t b, int K, int N, float* y, int ldy, Operand aout = Operand{nullptr, 0, OP_ROW, 0}) {
     GemvArgs a = gemv_args(slot0, n, op, w, b, K, N, y, ldy, aout, -1);
     ln_operand(a, slot0, n, x, g, gb, op);
-    run_gemv(epi, n, a);
+    run_gemv(tag, epi, n, a);
   }
 
   void ln(int slot0, int n, const float* x, size_t g, size_t b, Operand out) {
@@ -394,10 +395,11 @@ struct Runner {
   void block_tail(int slot0, int n, const BlockW& b, int xlayer, int tap, const LnNext& nx) {
     const int d = c.d_model;
     float *h_ = F32(L.h), *qkv = F32(L.qkv);
-    gemv_ln(EPI_STORE, slot0, n, h_, b.ln2_g, b.ln2_b, Ad16(), b.w_q2, b.b_q2, d, d, qkv, 3 * d);
+    gemv_ln("gemv_q2", EPI_STORE, slot0, n, h_, b.ln2_g, b.ln2_b, Ad16(), b.w_q2, b.b_q2, d, d, qkv, 3 * d);
     cross(slot0, n, xlayer);
-    gemv(EPI_RESID, slot0, n, Ad16(), b.w_o2, b.b_o2, d, d, h_, d);
-    gemv_ln(EPI_GELU, slot0, n, h_, b.ln3_g, b.ln3_b, Ad32(), b.w_fc1, b.b_fc1, d, c.d_ff, nullptr, 0, Af16());
+    gemv("gemv_o", EPI_RESID, slot0, n, Ad16(), b.w_o2, b.b_o2, d, d, h_, d);
+    gemv_ln("gemv_fc1", EPI_GELU, slot0, n, h_, b.ln3_g, b.ln3_b, Ad32(), b.w_fc1, b.b_fc1, d, c.d_ff, nullptr, 0,
+            Af16());
     if (L.fc2_split > 0) {
       // k-split partial sums, then h += sum + bias, the tap, and the next LayerNorm
       GemvArgs a = gemv_args(slot0, n, Af16(), b.w_fc2, b.b_fc2, c.d_ff, d, F32(L.part), d, Operand{nullptr, 0, OP_ROW, 0}, -1);
@@ -405,7 +407,7 @@ struct Runner {
       a.ct = 4;
       a.ksplit = L.fc2_split;
       a.pstride = (size_t)R9() * d;
-      run_gemv(EPI_PART, n, a);
+      run_gemv("gemv_fc2", EPI_PART, n, a);
       RlnArgs ra{};
       ra.part = F32(L.part); ra.nparts = L.fc2_split; ra.pstride = (size_t)R9() * d; ra.bias = W(b.b_fc2); ra.h = h_;
       ra.tap = Atap16(); ra.tapcol = tap >= 0 ? tap * d : -1; ra.g = W(nx.g); ra.b = W(nx.b); ra.out = nx.wide ? Ad32() : Ad16();
@@ -413,7 +415,7 @@ struct Runner {
       launch("reduce_ln", 4.0 * kRows * n * d * (L.fc2_split + 3), [&] { Ops<S>::reduce_ln(ra, n * kRows, st); });
       ln_ready = true;
     } else {
-      gemv(EPI_RESID, slot0, n, Af16(), b.w_fc2, b.b_fc2, c.d_ff, d, h_, d, Atap16(), tap);
+      gemv("gemv_fc2", EPI_RESID, slot0, n, Af16(), b.w_fc2, b.b_fc2, c.d_ff, d, h_, d, Atap16(), tap);
     }
   }
 
@@ -432,14 +434,14 @@ struct Runner {
       if (ln_ready) a.a = Ad16();
       else ln_operand(a, slot0, n, h_, b.ln1_g, b.ln1_b, Ad16());
       ln_ready = false;
-      run_gemv(EPI_QKV, n, a);
+      run_gemv("gemv_qkv", EPI_QKV, n, a);
       AttnArgs at{};
       at.q = qkv; at.ldq = 3 * d; at.kcache = skv_layer(l); at.vcache = skv_layer(l) + kv_stride();
       at.state = I32(L.state); at.page_table = I32(L.page_table); at.rope = F32(L.rope); at.out = Ad16();
       at.slot0 = slot0; at.d = d; at.n_head = c.n_head; at.n_ctx = c.n_ctx; at.pages_per_slot = L.pages_per_slot;
       at.nsplit = L.nsplit_op; at.R9 = R9();
       launch("attn_self", 0, [&] { Ops<S>::attn_self(at, n, st); });
-      gemv(EPI_RESID, slot0, n, Ad16(), b.w_o, b.b_o, d, d, h_, d);
+      gemv("gemv_o", EPI_RESID, slot0, n, Ad16(), b.w_o, b.b_o, d, d, h_, d);
       const LnNext nx = l + 1 < c.n_layer ? LnNext{L.tb[l + 1].ln1_g, L.tb[l + 1].ln1_b, false}
                                           : LnNext{L.lnf_g, L.lnf_b, true};
       block_tail(slot0, n, b, l, tap, nx);
@@ -470,7 +472,7 @@ struct Runner {
     if (ln_ready) a.a = Ad32();
     else ln_operand(a, slot0, n, x, g, gb, Ad32(), false);
     ln_ready = false;
-    run_gemv(EPI_ARGMAX, n, a);
+    run_gemv("head", EPI_ARGMAX, n, a);
     launch("argmax_final", kRows * n * L.head_blocks * 8.0, [&] {
       argmax_final(F32(L.hv), I32(L.hi), L.head_blocks, slot0 * kRows, n * kRows, I32(L.g), F32(L.gmax),
                    h->at<unsigned>(L.status), keep, dst, slot0, c.block_k, a.hm, a.hs, rmax, rsum, st);
@@ -481,12 +483,12 @@ struct Runner {
   void history_apply(int slot0, int n) {
     const int d = c.d_model;
     float *hp = F32(L.hp), *kvh = F32(L.kvh);
-    gemv(EPI_STORE, slot0, n, Atap16(), L.hproj_w, L.hproj_b, c.n_tap * d, d, hp, d);
+    gemv("gemv_hproj", EPI_STORE, slot0, n, Atap16(), L.hproj_w, L.hproj_b, c.n_tap * d, d, hp, d);
     for (int dl = 0; dl < c.n_draft_layer; ++dl) {
       const BlockW& b = L.db[dl];
       // rows d..3d of the concatenated q|k|v matrix start d*d elements in, in either order
-      gemv_ln(EPI_STORE, slot0, n, hp, b.ln1_g, b.ln1_b, Ad16(), b.w_qkv + (size_t)d * d, b.b_qkv + d, d, 2 * d, kvh,
-              2 * d);
+      gemv_ln("gemv_hist_kv", EPI_STORE, slot0, n, hp, b.ln1_g, b.ln1_b, Ad16(), b.w_qkv + (size_t)d * d, b.b_qkv + d, d,
+              2 * d, kvh, 2 * d);
       HistArgs ha{};
       ha.kv = kvh; ha.kcache = hkv(dl, 0); ha.vcache = hkv(dl, 1); ha.state = I32(L.state); ha.rope = F32(L.rope);
       ha.slot0 = slot0; ha.d = d; ha.n_head = c.n_head; ha.n_ctx = c.n_ctx;
@@ -504,8 +506,9 @@ struct Runner {
     ln_ready = false;
     for (int dl = 0; dl < c.n_draft_layer; ++dl) {
       const BlockW& b = L.db[dl];
-      if (ln_ready) gemv(EPI_STORE, slot0, n, Ad16(), b.w_qkv, b.b_qkv, d, 3 * d, qkv, 3 * d);
-      else gemv_ln(EPI_STORE, slot0, n, h_, b.ln1_g, b.ln1_b, Ad16(), b.w_qkv, b.b_qkv, d, 3 * d, qkv, 3 * d);
+      if (ln_ready) gemv("gemv_draft_qkv", EPI_STORE, slot0, n, Ad16(), b.w_qkv, b.b_qkv, d, 3 * d, qkv, 3 * d);
+      else gemv_ln("gemv_draft_qkv", EPI_STORE, slot0, n, h_, b.ln1_g, b.ln1_b, Ad16(), b.w_qkv, b.b_qkv, d, 3 * d, qkv,
+                   3 * d);
       ln_ready = false;
       AttnArgs at{};
       at.q = qkv; at.ldq = 3 * d; at.kcache = hkv(dl, 0); at.vcache = hkv(dl, 1);
@@ -513,7 +516,7 @@ struct Runner {
       at.slot0 = slot0; at.d = d; at.n_head = c.n_head; at.n_ctx = c.n_ctx;
       at.nsplit = L.nsplit_op; at.R9 = R9();
       launch("attn_draft", 0, [&] { Ops<S>::attn_draft(at, n, st); });
-      gemv(EPI_RESID, slot0, n, Ad16(), b.w_o, b.b_o, d, d, h_, d);
+      gemv("gemv_o", EPI_RESID, slot0, n, Ad16(), b.w_o, b.b_o, d, d, h_, d);
       const LnNext nx = dl + 1 < c.n_draft_layer ? LnNext{L.db[dl + 1].ln1_g, L.db[dl + 1].ln1_b, false}
                                                  : LnNext{L.dlnf_g, L.dlnf_b, true};
       block_tail(slot0, n, b, c.n_layer + dl, -1, nx);

@@ -30,7 +30,10 @@ def build_engine(cfg, W, max_batch):
 
 
 class Lockstep:
-    def __init__(self, cfg, W, prompts, max_new, tol, opts=None, mems=None, slots=None):
+    """GPU engine over all prompts; the oracle follows the slots in ``check`` (all by
+    default).  Slots are independent, so a sample of them checks the whole batch."""
+
+    def __init__(self, cfg, W, prompts, max_new, tol, opts=None, mems=None, slots=None, check=None):
         self.cfg, self.W, self.tol = cfg, W, tol
         n = len(prompts)
         self.n = n
@@ -49,14 +52,17 @@ class Lockstep:
             toks[i, :len(p)] = p
         first = self.eng.prefill(0, torch.from_numpy(toks).cuda(), [len(p) for p in prompts], max_new)
         self.gpu_first = first.cpu().numpy()
-        self.sess = [Session(self.T, self.D, mems[i], prompts[i], max_new[i]) for i in range(n)]
-        self.live = [True] * n          # slot still compared
+        check = set(range(n) if check is None else check)
+        self.sess = [Session(self.T, self.D, mems[i], prompts[i], max_new[i]) if i in check else None for i in range(n)]
+        self.live = [i in check for i in range(n)]  # slot compared (until a near tie)
         self.near_ties = []             # (slot, what, margin)
         self.max_dlogit = 0.0
         self.max_tlogit = 0.0
         self.steps = 0
         self.accepted = []
         for i, s in enumerate(self.sess):
+            if s is None:
+                continue
             if self.gpu_first[i] != s.out[0]:
                 m = margin(s.last_logits[-1])
                 assert m <= tol, f"slot {i}: first token {self.gpu_first[i]} vs oracle {s.out[0]} (margin {m})"

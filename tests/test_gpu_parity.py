@@ -153,3 +153,70 @@ def test_large_v3_bf16_lockstep_b1():
     # through the oracle inside the step comparison
     print(f"large-v3: max |dlogit| draft {ls.max_dlogit:.3e} target {ls.max_tlogit:.3e}, near ties {ls.near_ties}")
     ls.close()
+
+
+# ---------------------------------------------------------------- large batches (sampled slots)
+# At batch >= 2 product inputs are bf16 (the oracle's gemm_bf16 option rounds at
+# the same points); the oracle follows a sample of the slots, which are
+# independent by construction (no per-row dependence on the batch).
+LARGE_BATCH_OPTS = dict(dtype=np.float32, kv_bf16=True, gemm_bf16=True, exact=False)
+
+
+def _planted_subset(ls, refs, rng):
+    """Planted drafts for the checked slots (oracle greedy continuation with index r
+    replaced); the other slots keep random tokens."""
+    K = ls.cfg.block_k
+    ov = rng.integers(0, ls.cfg.n_vocab, size=(ls.n, K)).astype(np.int32)
+    for i, s in enumerate(ls.sess):
+        if s is None or i not in refs:
+            continue
+        cont = (list(refs[i]) + [0] * (K + 1))[s.emitted:s.emitted + K]
+        ov[i] = plant_drafts(cont, int(rng.integers(0, K + 1)), ls.cfg.n_vocab, rng)
+    return ov
+
+
+@pytest.mark.timeout(1200)
+def test_large_v3_b16_ragged_planted():
+    """16 slots, prefixes uniform in [4, 440] over 16-token pages, first-rejection
+    index uniform in 0..8; the oracle follows the shortest, the longest and two
+    other slots (the longest exercises the context-limited budget)."""
+    from lockstep import Lockstep
+    cfg = LARGE_V3
+    W = make_weights(cfg)
+    n = 16
+    lens = [int(x) for x in make_prefix_lengths(n, 4, 440, seed=300)]
+    prompts = [make_prefix(cfg, s, lens[s]) for s in range(n)]
+    check = sorted({int(np.argmin(lens)), int(np.argmax(lens)), 3, 9})
+    opts = OracleOpts(**LARGE_BATCH_OPTS)
+    ls = Lockstep(cfg, W, prompts, [cfg.n_ctx] * n, TOL_BF16, opts=opts, check=check)
+    print(f"b16: lens {lens}, checked {check}", flush=True)
+    refs = {i: plain_greedy(ls.T, make_memory(cfg, i), prompts[i], 24) for i in check}
+    rng = np.random.default_rng(4)
+    for step in range(4):
+        ls.step(override=_planted_subset(ls, refs, rng))
+        print(f"b16 step {step}: accepted so far {ls.accepted}, max dlogit draft {ls.max_dlogit:.2e} "
+              f"target {ls.max_tlogit:.2e}, near ties {ls.near_ties}", flush=True)
+    assert max(ls.accepted) > 0
+    ls.close()
+
+
+@pytest.mark.timeout(1500)
+def test_large_v3_b96_sampled_slots():
+    """96 slots (864 verify rows per step), prefixes uniform in [4, 440], one
+    acoustic memory per slot; the oracle follows three slots."""
+    from lockstep import Lockstep
+    cfg = LARGE_V3
+    W = make_weights(cfg)
+    n = 96
+    lens = [int(x) for x in make_prefix_lengths(n, 4, 440, seed=300)]
+    prompts = [make_prefix(cfg, s, lens[s]) for s in range(n)]
+    check = [0, 47, 95]
+    opts = OracleOpts(**LARGE_BATCH_OPTS)
+    ls = Lockstep(cfg, W, prompts, [cfg.n_ctx] * n, TOL_BF16, opts=opts, check=check)
+    print(f"b96: checked slots {check} with prefixes {[lens[i] for i in check]}", flush=True)
+    for step in range(2):
+        ls.step()
+        print(f"b96 step {step}: max dlogit draft {ls.max_dlogit:.2e} target {ls.max_tlogit:.2e}, "
+              f"near ties {ls.near_ties}", flush=True)
+    assert ls.steps == 2
+    ls.close()

@@ -44,17 +44,24 @@ def _gap(scores):
     return float(top[1] - top[0])
 
 
-def _sampling_lockstep(cfg, temperature, suppress=None, steps=10, plant_every=3):
+def _sampling_lockstep(cfg, temperature, suppress=None, steps=10, plant_every=3, prompts=None, check=None,
+                       opts=None, gap_tol=1e-4, margin_tol=1e-5):
+    """Sampling decisions of the GPU vs the oracle for the slots in ``check``.  A
+    disagreement is accepted only where the oracle's own decision is within
+    gap_tol (Gumbel top-2 gap) or margin_tol (|u q - p| / p) of a tie."""
     W = make_weights(cfg)
-    prompts = [make_prefix(cfg, 0, 5), make_prefix(cfg, 1, 12)]
-    max_new = [40, 40]
+    if prompts is None:
+        prompts = [make_prefix(cfg, 0, 5), make_prefix(cfg, 1, 12)]
     n = len(prompts)
+    max_new = [min(40, cfg.n_ctx)] * n
+    check = set(range(n) if check is None else check)
     eng = build_engine(cfg, W, n)
     sup_dev = None
     if suppress is not None:
         sup_dev = torch.from_numpy(suppress.astype(np.uint8)).cuda()
     eng.set_sampling(temperature, seed=500, suppress=sup_dev)
-    opts = OracleOpts(dtype=np.float32, exact=True)
+    if opts is None:
+        opts = OracleOpts(dtype=np.float32, exact=True)
     T, D = Target(cfg, W.values, opts), Drafter(cfg, W.values, opts)
     mems = [make_memory(cfg, s) for s in range(n)]
     eng.encode_memory_set(0, torch.stack([to_device_storage(m, cfg.dtype) for m in mems]))
@@ -64,14 +71,16 @@ def _sampling_lockstep(cfg, temperature, suppress=None, steps=10, plant_every=3)
     sup_idx = np.nonzero(suppress)[0] if suppress is not None else None
     first = eng.prefill(0, torch.from_numpy(toks).cuda(), [len(p) for p in prompts], max_new).cpu().numpy()
     sess = [Session(T, D, mems[i], prompts[i], max_new[i], slot=i, temperature=temperature, seed=500,
-                    suppress=sup_idx) for i in range(n)]
-    live = [True] * n
+                    suppress=sup_idx) if i in check else None for i in range(n)]
+    live = [i in check for i in range(n)]
     ties = []
     for i, s in enumerate(sess):
+        if s is None:
+            continue
         if first[i] != s.out[0]:
             g = gumbel(uniforms(500, PURPOSE["PREFILL"], i, 0, 0, cfg.n_vocab))
             gap = _gap(s.last_logits[-1].astype(np.float32) * s.inv_t + g)
-            assert gap < 1e-4, f"slot {i}: first token {first[i]} vs {s.out[0]} (gap {gap})"
+            assert gap < gap_tol, f"slot {i}: first token {first[i]} vs {s.out[0]} (gap {gap})"
             ties.append((i, "prefill", gap))
             live[i] = False
     rng = np.random.default_rng(3)
@@ -92,7 +101,7 @@ def _sampling_lockstep(cfg, temperature, suppress=None, steps=10, plant_every=3)
                 j = int(np.nonzero(otoks != drafts[i])[0][0])
                 g = gumbel(uniforms(500, PURPOSE["DRAFT"], i, s.step_no, j + 1, cfg.n_vocab))
                 gap = _gap(lq[j].astype(np.float32) * s.inv_t + g)
-                assert gap < 1e-4, f"slot {i} step {step}: draft {drafts[i]} vs {otoks} (gap {gap})"
+                assert gap < gap_tol, f"slot {i} step {step}: draft {drafts[i]} vs {otoks} (gap {gap})"
                 ties.append((i, f"draft {step}", gap))
                 live[i] = False
                 continue
@@ -109,7 +118,7 @@ def _sampling_lockstep(cfg, temperature, suppress=None, steps=10, plant_every=3)
                 for j in range(k):
                     c = int(used[i, j])
                     margins.append(abs(float(u[j]) * float(q[j, c]) - float(p[j, c])) / max(float(p[j, c]), 1e-30))
-                assert margins and min(margins) < 1e-5, \
+                assert margins and min(margins) < margin_tol, \
                     f"slot {i} step {step}: GPU {gpu} a={n_acc[i]} vs oracle {rec['tokens']} a={rec['a']}"
                 ties.append((i, f"accept {step}", min(margins)))
                 live[i] = False
@@ -183,3 +192,20 @@ def test_v64_emitted_law_equals_target(temperature, k_max):
     print(f"T={temperature} k_max={k_max}: n={n} p(first)={pv1:.3g} p(second)={pv2:.3g} power control p={pv_power:.3g}")
     assert pv1 > ALPHA and pv2 > ALPHA
     assert pv_power < ALPHA
+
+
+@pytest.mark.timeout(1200)
+@pytest.mark.parametrize("temperature", [0.7, 1.0])
+def test_large_v3_b8_sampling(temperature):
+    """Large-v3 shapes, 8 slots, prefixes uniform in [4, 440]; the oracle follows two
+    slots.  Product inputs are bf16 at this batch, so logits differ from the fp32
+    oracle by up to ~3e-3 and decisions are compared outside that band."""
+    from wf_fixtures import LARGE_V3, make_prefix_lengths
+    cfg = LARGE_V3
+    lens = [int(x) for x in make_prefix_lengths(8, 4, 440, seed=300)]
+    prompts = [make_prefix(cfg, s, lens[s]) for s in range(8)]
+    opts = OracleOpts(dtype=np.float32, kv_bf16=True, gemm_bf16=True, exact=False)
+    decisions, ties = _sampling_lockstep(cfg, temperature, steps=3, prompts=prompts, check=[0, 5], opts=opts,
+                                         gap_tol=3e-2, margin_tol=3e-2)
+    print(f"large b8 T={temperature}: {decisions} verified rows compared, near ties {ties}", flush=True)
+    assert decisions > 0
