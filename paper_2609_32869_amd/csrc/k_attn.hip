@@ -289,6 +289,126 @@ __global__ void __launch_bounds__(kCrossThreads) k_attn_cross(CrossArgs a) {
     put_op<S>(a.out, a.nsplit, a.R9, slot * kRows + row, head * kHeadDim + threadIdx.x, o);
 }
 
+// ---------------------------------------------------------------- cross-attention, all rows per block
+// Several slots: block (head, slot) computes all nine query rows, so each key /
+// value byte of the slot is read by one block.  Wave w takes key octets w, w + NW,
+// ... two at a time; per row a running max, sum and weighted value sums (the lane
+// holds 8 dims of its key's contribution); the waves merge in LDS at the end.
+constexpr int kXrThreads = 512;
+template <typename S>
+__global__ void __launch_bounds__(kXrThreads) k_attn_cross_rows(CrossArgs a) {
+  constexpr int NW = kXrThreads / 64, B = 2;
+  __shared__ float wacc[NW][kRows][64];
+  __shared__ float wm[NW][kRows], wl[NW][kRows];
+  const int head = blockIdx.x, slot = a.slot0 + blockIdx.y;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, g = lane & 7, kl = lane >> 3;
+  const int nk = a.n_frames;
+  float q8[kRows][8];
+#pragma unroll
+  for (int r = 0; r < kRows; ++r) {
+    const float* qr = a.q + (size_t)(slot * kRows + r) * a.ldq + head * kHeadDim + 8 * g;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) q8[r][e] = qr[e] * 0.125f;
+  }
+  const S* Kx = reinterpret_cast<const S*>(a.kv) + ((size_t)slot * 2 * a.n_head + head) * a.n_frames * kHeadDim;
+  const S* Vx = Kx + (size_t)a.n_head * a.n_frames * kHeadDim;
+  float m[kRows], l[kRows], acc[kRows][8];
+#pragma unroll
+  for (int r = 0; r < kRows; ++r) {
+    m[r] = -INFINITY;
+    l[r] = 0.f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc[r][e] = 0.f;
+  }
+  const int noct = (nk + 7) >> 3;
+  for (int o0 = w; o0 < noct; o0 += NW * B) {
+    Raw8<S> kr[B], vr[B];
+#pragma unroll
+    for (int b = 0; b < B; ++b) {
+      const int key = (o0 + NW * b) * 8 + kl;
+      if (key < nk) {
+        kr[b].load(Kx + (uint32_t)key * kHeadDim + 8 * g);
+        vr[b].load(Vx + (uint32_t)key * kHeadDim + 8 * g);
+      } else {
+        kr[b].zero();
+        vr[b].zero();
+      }
+    }
+    float sc[kRows][B];
+#pragma unroll
+    for (int b = 0; b < B; ++b) {
+      float k8[8];
+      kr[b].unpack(k8);
+      const bool ok = (o0 + NW * b) * 8 + kl < nk;
+#pragma unroll
+      for (int r = 0; r < kRows; ++r) {
+        float t = 0.f;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) t = fmaf(q8[r][e], k8[e], t);
+        t = sum8(t);
+        sc[r][b] = ok ? t : -INFINITY;
+      }
+    }
+    float v8[B][8];
+#pragma unroll
+    for (int b = 0; b < B; ++b) vr[b].unpack(v8[b]);
+#pragma unroll
+    for (int r = 0; r < kRows; ++r) {
+      float bm = sc[r][0];
+#pragma unroll
+      for (int b = 1; b < B; ++b) bm = fmaxf(bm, sc[r][b]);
+      const float mn = fmaxf(m[r], wave_max(bm));  // key o0 * 8 < nk is in this batch
+      const float f = __expf(m[r] - mn);
+      l[r] *= f;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) acc[r][e] *= f;
+#pragma unroll
+      for (int b = 0; b < B; ++b) {
+        const float p = __expf(sc[r][b] - mn);
+        l[r] += g == 0 ? p : 0.f;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc[r][e] = fmaf(p, v8[b][e], acc[r][e]);
+      }
+      m[r] = mn;
+    }
+  }
+  // fold the 8 key lanes (bits 3..5) of each dim group, then publish per wave
+#pragma unroll
+  for (int r = 0; r < kRows; ++r) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      float t = acc[r][e] + dpp<kDppRor8>(acc[r][e]);
+      t += __shfl_xor(t, 16, 64);
+      t += __shfl_xor(t, 32, 64);
+      acc[r][e] = t;
+    }
+    const float lr = wave_sum(l[r]);
+    if (lane < 8) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) wacc[w][r][8 * g + e] = acc[r][e];
+    }
+    if (lane == 0) {
+      wm[w][r] = m[r];
+      wl[w][r] = lr;
+    }
+  }
+  __syncthreads();
+  for (int t = threadIdx.x; t < kRows * 64; t += kXrThreads) {
+    const int r = t >> 6, dim = t & 63;
+    float M = wm[0][r];
+#pragma unroll
+    for (int i = 1; i < NW; ++i) M = fmaxf(M, wm[i][r]);
+    float L = 0.f, o = 0.f;
+#pragma unroll
+    for (int i = 0; i < NW; ++i) {
+      const float f = __expf(wm[i][r] - M);  // 0 for a wave without keys
+      L += wl[i][r] * f;
+      o += wacc[i][r][dim] * f;
+    }
+    put_op<S>(a.out, a.nsplit, a.R9, slot * kRows + r, head * kHeadDim + dim, o / L);
+  }
+}
+
 // ---------------------------------------------------------------- causal self-attention
 // Verify pass: row i < nv of slot s sits at position pos0 + i and attends to cached
 // positions 0..pos0 + i (Section 3.1: one causal pass).  Rows i >= nv are padding
@@ -430,9 +550,12 @@ template <typename S>
 void Ops<S>::attn_draft(const AttnArgs& a, int n, hipStream_t st) {
   k_attn_draft<S><<<dim3(row_blocks(a.n_head), n), kSelfThreads, 0, st>>>(a);
 }
+// enough slots to fill the chip with (head, slot) blocks: all rows per block;
+// otherwise one block per (head, row)
 template <typename S>
 void Ops<S>::attn_cross(const CrossArgs& a, int n, hipStream_t st) {
-  k_attn_cross<S><<<dim3(row_blocks(a.n_head), n), kCrossThreads, 0, st>>>(a);
+  if (n * a.n_head >= 128) k_attn_cross_rows<S><<<dim3(a.n_head, n), kXrThreads, 0, st>>>(a);
+  else k_attn_cross<S><<<dim3(row_blocks(a.n_head), n), kCrossThreads, 0, st>>>(a);
 }
 
 template void Ops<float>::attn_self(const AttnArgs&, int, hipStream_t);

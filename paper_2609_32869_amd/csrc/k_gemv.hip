@@ -152,7 +152,7 @@ __device__ void finish_tile(const GemvArgs& a, float (*sv)[TC + 1], float (*ov)[
         if (better(ov[ml][j], nb + j, bv, bi)) { bv = ov[ml][j]; bi = nb + j; }
         zm = fmaxf(zm, oz[ml][j]);
       }
-      const size_t o = (size_t)row * a.nblk + blockIdx.x;
+      const size_t o = (size_t)row * a.nblk + nb / TC;  // column block of this tile
       a.hv[o] = bv;
       a.hi[o] = bi;
       if (a.hm != nullptr) {
@@ -298,6 +298,68 @@ __global__ void __launch_bounds__(NW * 64) k_gemv16w(GemvArgs a) {
     finish_tile<bf16, EPI, 32, TC, NW * 64>(a, sv, ov, oz, tile0 * 16, blockIdx.x * TC, pre);
     if (a.nsplit == 3) break;
   }
+}
+
+// ---------------------------------------------------------------- bf16 GEMM (batch >= 2)
+// The rows of several slots (nine each) times W^T over 64 x 64 block tiles: each of
+// the four waves computes a 32 x 32 sub-tile (2 x 2 fragments of
+// v_mfma_f32_16x16x32_bf16), loading operand and weight fragments straight from
+// their fragment orders (1 KB per wave load), kGemmU k-steps of loads in flight.
+// Block b runs on XCD b % 8; the row blocks of one column block are numbered so
+// they share an XCD and its L2 serves them the weight tile.
+constexpr int kGemmU = 4;
+template <int EPI>
+__global__ void __launch_bounds__(256) k_gemm16(GemvArgs a, int mb0, int nmb, int nnb) {
+  __shared__ float sv[64][65];
+  __shared__ float ov[EPI == EPI_ARGMAX ? 64 : 1][64];
+  __shared__ float oz[EPI == EPI_ARGMAX ? 64 : 1][64];
+  const int x = blockIdx.x & 7, i = blockIdx.x >> 3;
+  const int nbk = x + 8 * (i / nmb), mbk = i % nmb;
+  if (nbk >= nnb) return;
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const int wm = wv >> 1, wn = wv & 1;
+  const int KS = a.K / 32, MT = a.a.mt, ntile = (a.N + 15) / 16;
+  const int mt0 = (mb0 + mbk) * 4 + wm * 2, nt0 = nbk * 4 + wn * 2;  // 16-row / 16-column tiles
+  const bf16x8* Ab = reinterpret_cast<const bf16x8*>(a.a.p) + lane;
+  const bf16x8* Wb = reinterpret_cast<const bf16x8*>(a.w) + lane;
+  const bool mv0 = mt0 < MT, mv1 = mt0 + 1 < MT, nv0 = nt0 < ntile, nv1 = nt0 + 1 < ntile;
+  const bf16x8 zero = __builtin_bit_cast(bf16x8, make_uint4(0u, 0u, 0u, 0u));
+  floatx4 acc[2][2];
+#pragma unroll
+  for (int p = 0; p < 2; ++p)
+#pragma unroll
+    for (int q = 0; q < 2; ++q) acc[p][q] = floatx4{0.f, 0.f, 0.f, 0.f};
+  for (int st = 0; st < KS; st += kGemmU) {
+    bf16x8 af[kGemmU][2], wf[kGemmU][2];
+#pragma unroll
+    for (int u = 0; u < kGemmU; ++u) {
+      const int ss = min(st + u, KS - 1);
+      af[u][0] = mv0 ? Ab[((size_t)ss * MT + mt0) * 64] : zero;
+      af[u][1] = mv1 ? Ab[((size_t)ss * MT + mt0 + 1) * 64] : zero;
+      wf[u][0] = nv0 ? Wb[((size_t)nt0 * KS + ss) * 64] : zero;
+      wf[u][1] = nv1 ? Wb[((size_t)(nt0 + 1) * KS + ss) * 64] : zero;
+    }
+#pragma unroll
+    for (int u = 0; u < kGemmU; ++u)
+      if (st + u < KS) {
+#pragma unroll
+        for (int p = 0; p < 2; ++p)
+#pragma unroll
+          for (int q = 0; q < 2; ++q)
+            acc[p][q] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[u][p], wf[u][q], acc[p][q], 0, 0, 0);
+      }
+  }
+  // result fragment: lane l holds column l % 16, rows 4 (l / 16) + v
+#pragma unroll
+  for (int p = 0; p < 2; ++p)
+#pragma unroll
+    for (int q = 0; q < 2; ++q)
+#pragma unroll
+      for (int v = 0; v < 4; ++v)
+        sv[wm * 32 + p * 16 + 4 * (lane >> 4) + v][wn * 32 + q * 16 + (lane & 15)] = acc[p][q][v];
+  __syncthreads();
+  EpiPre<64, 256> pre;  // batch-1 prefetch, unused here
+  finish_tile<bf16, EPI, 64, 64, 256>(a, sv, ov, oz, (mb0 + mbk) * 64, nbk * 64, pre);
 }
 
 // ---------------------------------------------------------------- bf16, 32-column tiles
@@ -693,6 +755,13 @@ static void launch_epi(const GemvArgs& a, hipStream_t st) {
       const int ntile = (a.N + 15) / 16;
       k_gemv16w<EPI, 8, 4><<<dim3((ntile + 3) / 4, a.ksplit > 1 ? a.ksplit : 1), 512, 0, st>>>(a);
       return;
+    } else {
+      if (a.nsplit == 1 && a.wkind == W_F16) {  // several slots: 64 x 64 GEMM tiles
+        const int mb0 = a.slot0 * kRows / 64, mb1 = ((a.slot0 + a.nslots) * kRows + 63) / 64;
+        const int nmb = mb1 - mb0, nnb = (a.N + 63) / 64;
+        k_gemm16<EPI><<<(unsigned)(8 * ((nnb + 7) / 8) * nmb), 256, 0, st>>>(a, mb0, nmb, nnb);
+        return;
+      }
     }
   }
   // waves per block: enough that each wave's share of the k-steps fits one batch

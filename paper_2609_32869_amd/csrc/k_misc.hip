@@ -146,14 +146,6 @@ __global__ void __launch_bounds__(256) k_argmax_final(const float* __restrict__ 
 
 // ---------------------------------------------------------------- attention helpers
 
-// Row `tok`, column c of the token embedding, stored in the order the vocabulary
-// head streams it (32-column fragment order for bf16, row-major for fp32).
-template <typename S>
-__device__ __forceinline__ float emb_at(const BeginArgs& a, int tok, int c) {
-  const S* E = reinterpret_cast<const S*>(a.emb);
-  if (a.emb_kind == W_F32) return to_f(E[wfrag32_index(tok, c, a.d / 16)]);
-  return to_f(E[(size_t)tok * a.d + c]);
-}
 
 // ---------------------------------------------------------------- pass set-up
 // Rows of a pass: h[slot * 9 + i] = E[toks[i]] + P[pos[i]] (target) or E[anchor] /
@@ -173,7 +165,9 @@ __device__ __forceinline__ void fill_rows(const BeginArgs& a, int slot, const in
       const int tok = toks[i];
       const bool from_mask = mask_rows && i > 0;
       if (!from_mask) {
-        const size_t ei = a.emb_kind == W_F32 ? wfrag32_index(tok, c, a.d / 16) : (size_t)tok * a.d + c;
+        const size_t ei = a.emb_kind == W_F32   ? wfrag32_index(tok, c, a.d / 16)
+                          : a.emb_kind == W_F16 ? wfrag16_index(tok, c, a.d / 32)
+                                                : (size_t)tok * a.d + c;
         ld8(E + ei, e8[j]);
       } else {
 #pragma unroll

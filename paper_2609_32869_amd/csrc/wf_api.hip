@@ -83,7 +83,10 @@ std::vector<ManEntry> manifest(const wf_config& c, const Layout& L, std::vector<
     mm.push_back({dst, (int)N, (int)K, kind});
     return (int)mm.size() - 1;
   };
-  const int emb = mat(L.tok_emb, c.n_vocab, d, W_F32);
+  // 32-column tiles (W_1, head) only at batch 1; with several slots every matrix
+  // uses 16-column tiles for the GEMM kernel
+  const int wide = L.nsplit_op == 3 ? W_F32 : W_F16;
+  const int emb = mat(L.tok_emb, c.n_vocab, d, wide);
   m.push_back({(size_t)c.n_vocab * d, L.tok_emb, emb});
   m.push_back({(size_t)c.n_ctx * d, L.pos_emb, -1});
   auto block = [&](const BlockW& b) {
@@ -99,7 +102,7 @@ std::vector<ManEntry> manifest(const wf_config& c, const Layout& L, std::vector<
     m.push_back({d * d, b.w_kv2 + d * d, -1}); m.push_back({d, b.b_kv2 + d, -1});
     m.push_back({d * d, b.w_o2, mat(b.w_o2, d, d, W_F16)}); m.push_back({d, b.b_o2, -1});
     m.push_back({d, b.ln3_g, -1}); m.push_back({d, b.ln3_b, -1});
-    m.push_back({F * d, b.w_fc1, mat(b.w_fc1, F, d, W_F32)}); m.push_back({F, b.b_fc1, -1});
+    m.push_back({F * d, b.w_fc1, mat(b.w_fc1, F, d, wide)}); m.push_back({F, b.b_fc1, -1});
     m.push_back({d * F, b.w_fc2, mat(b.w_fc2, d, F, W_F16)}); m.push_back({d, b.b_fc2, -1});
   };
   for (auto& b : L.tb) block(b);
@@ -148,8 +151,10 @@ int compute_layout(const wf_config& c, Layout& L) {
   L.dlnf_g = take(d); L.dlnf_b = take(d);
   L.weight_elems = w;
   L.pages_per_slot = c.n_ctx / kPage;
-  // the vocabulary head streams 32-column tiles (bf16) or 16-column tiles (fp32)
-  L.head_blocks = c.dtype == WF_BF16 ? (int)((V + 31) / 32) : (int)((V + 15) / 16);
+  // column blocks of the vocabulary head: 32-column tiles (bf16, batch 1), 64-column
+  // GEMM blocks (bf16, several slots) or 16-column tiles (fp32)
+  L.nsplit_op = (c.dtype == WF_BF16 && c.max_batch == 1) ? 3 : 1;
+  L.head_blocks = c.dtype != WF_BF16 ? (int)((V + 15) / 16) : L.nsplit_op == 3 ? (int)((V + 31) / 32) : (int)((V + 63) / 64);
   // raw bf16 matrices are staged at init in the cross K/V region before reordering
   L.stage_bytes = 0;
   if (c.dtype == WF_BF16) {
@@ -168,8 +173,7 @@ int compute_layout(const wf_config& c, Layout& L) {
   L.xkv = region(std::max((size_t)(c.n_layer + c.n_draft_layer) * B * 2 * c.n_frames * d * eb, L.stage_bytes));
   L.skv = region((size_t)c.n_layer * 2 * B * L.pages_per_slot * H * kPage * kHeadDim * eb);
   L.hkv = region((size_t)c.n_draft_layer * 2 * B * H * c.n_ctx * kHeadDim * eb);
-  // matrix operands: 3 bf16 terms per fp32 value at batch 1 with bf16 storage
-  L.nsplit_op = (c.dtype == WF_BF16 && c.max_batch == 1) ? 3 : 1;
+  // matrix operands: 3 bf16 terms per fp32 value at batch 1 with bf16 storage (set above)
   const size_t rows = L.nsplit_op * R9;
   L.mt16 = (int)((rows + 15) / 16);
   L.mt32 = (int)((rows + 31) / 32);
@@ -276,13 +280,14 @@ struct Runner {
   // weights have 32-column (wide) or 16-column tiles.
   Operand op(size_t off, int K, bool wide) const {
     if (!frag()) return Operand{h->at<void>(off), K, OP_ROW, L.mt16};
-    return wide ? Operand{h->at<void>(off), K, OP_F32, L.mt32} : Operand{h->at<void>(off), K, OP_F16, L.mt16};
+    return wide && L.nsplit_op == 3 ? Operand{h->at<void>(off), K, OP_F32, L.mt32}
+                                    : Operand{h->at<void>(off), K, OP_F16, L.mt16};
   }
   Operand Ad16() const { return op(L.a_d16, c.d_model, false); }
   Operand Ad32() const { return op(L.a_d32, c.d_model, true); }
   Operand Af16() const { return op(L.a_f16, c.d_ff, false); }
   Operand Atap16() const { return op(L.a_tap16, c.n_tap * c.d_model, false); }
-  int wk(bool wide) const { return frag() ? (wide ? W_F32 : W_F16) : W_ROW; }
+  int wk(bool wide) const { return frag() ? (wide && L.nsplit_op == 3 ? W_F32 : W_F16) : W_ROW; }
   int R9() const { return c.max_batch * kRows; }
 
   GemvArgs gemv_base(int slot0, int n, int wkind) const {

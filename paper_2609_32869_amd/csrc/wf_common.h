@@ -201,7 +201,8 @@ enum { RNG_PREFILL = 1, RNG_PLAIN = 2, RNG_DRAFT = 3, RNG_ACC = 4, RNG_RES = 5, 
 __host__ __device__ __forceinline__ uint64_t rng_word(uint64_t seed, int purpose, int slot, int step, int pos, int v) {
   const Philox4 r = philox4x64_10(((uint64_t)purpose << 32) | (uint32_t)slot, (uint64_t)(uint32_t)step,
                                   (uint64_t)(uint32_t)pos, (uint64_t)((uint32_t)v >> 2), seed, 0);
-  return r.w[v & 3];
+  const int j = v & 3;  // select without indexing, so the words stay in registers
+  return j == 0 ? r.w[0] : j == 1 ? r.w[1] : j == 2 ? r.w[2] : r.w[3];
 }
 // fp32 uniform in (0, 1): the top 23 bits plus one half, scaled by 2^-23
 __device__ __forceinline__ float rng_uniform(uint64_t x) { return ((float)(x >> 41) + 0.5f) * 0x1p-23f; }

@@ -119,7 +119,7 @@ struct BeginArgs {
   int* state;
   const int* draft;  // verify: draft [n][block_k]; prefill: tokens [n][pmax]
   int* tok;
-  const void* emb;  // token embedding, order emb_kind (W_ROW or W_F32)
+  const void* emb;  // token embedding, order emb_kind (W_ROW, W_F16 or W_F32)
   int emb_kind;
   const void* pos;  // positional table (target) or mask vector (drafter)
   float* h;
