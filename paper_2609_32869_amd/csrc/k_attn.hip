@@ -290,89 +290,141 @@ __global__ void __launch_bounds__(kCrossThreads) k_attn_cross(CrossArgs a) {
 }
 
 // ---------------------------------------------------------------- cross-attention, all rows per block
-// Several slots: block (head, slot) computes all nine query rows, so each key /
-// value byte of the slot is read by one block.  Wave w takes key octets w, w + NW,
-// ... two at a time; per row a running max, sum and weighted value sums (the lane
-// holds 8 dims of its key's contribution); the waves merge in LDS at the end.
+// Block (head, slot, chunk) computes all nine query rows of one slot over one
+// chunk of the frames, so each key / value byte is read once.  The chunk's scores
+// live in LDS ([frame][12] fp32):
+//   pass 1  scores (a key's 64-dim product summed over its 8 lanes);
+//   sweeps  one thread per (frame, row): the row maxima m, then p = exp(s - m)
+//           in place and the row sums l, each reduced in a fixed order;
+//   pass 2  acc += p * v over the values (no rescaling), then the 8 key lanes and
+//           the waves merge.
+// With one chunk the block divides by l and stores.  With several, each block
+// stores (max, l, acc) and a second kernel merges the chunks in chunk order:
+// out = sum_c e^(m_c - m) acc_c / sum_c e^(m_c - m) l_c.
+// The per-wave sums reuse the score buffer once every wave is done with it.
 constexpr int kXrThreads = 512;
+constexpr int kXrWaves = kXrThreads / 64;
+constexpr int kXrStride = 12;                     // floats per frame in the score buffer (9 rows, padded)
+constexpr int kXrSweepKeys = kXrThreads / kRows;  // frames per sweep step (56)
+inline size_t xr_lds_bytes(int chunk) {
+  const size_t sc = (size_t)chunk * kXrStride, wacc = (size_t)kXrWaves * kRows * 64;
+  return 4 * (sc > wacc ? sc : wacc);
+}
 template <typename S>
-__global__ void __launch_bounds__(kXrThreads) k_attn_cross_rows(CrossArgs a) {
-  constexpr int NW = kXrThreads / 64, B = 2;
-  __shared__ float wacc[NW][kRows][64];
-  __shared__ float wm[NW][kRows], wl[NW][kRows];
-  const int head = blockIdx.x, slot = a.slot0 + blockIdx.y;
+__global__ void __launch_bounds__(kXrThreads, 4) k_attn_cross_rows(CrossArgs a) {
+  constexpr int NW = kXrWaves, B = sizeof(S) == 2 ? 4 : 2;  // key octets in flight per wave
+  extern __shared__ float sc[];
+  float(*wacc)[kRows][64] = reinterpret_cast<float(*)[kRows][64]>(sc);
+  __shared__ float rmax[kRows], lsum[kRows];
+  __shared__ float lpart[kXrSweepKeys * kRows];
+  const int head = blockIdx.x, slot = a.slot0 + blockIdx.y, c = blockIdx.z;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, g = lane & 7, kl = lane >> 3;
-  const int nk = a.n_frames;
-  float q8[kRows][8];
-#pragma unroll
-  for (int r = 0; r < kRows; ++r) {
-    const float* qr = a.q + (size_t)(slot * kRows + r) * a.ldq + head * kHeadDim + 8 * g;
-#pragma unroll
-    for (int e = 0; e < 8; ++e) q8[r][e] = qr[e] * 0.125f;
-  }
-  const S* Kx = reinterpret_cast<const S*>(a.kv) + ((size_t)slot * 2 * a.n_head + head) * a.n_frames * kHeadDim;
+  const int k0 = c * a.chunk, nk = min(a.n_frames - k0, a.chunk), noct = (nk + 7) >> 3;
+  const S* Kx = reinterpret_cast<const S*>(a.kv) +
+                (((size_t)slot * 2 * a.n_head + head) * a.n_frames + k0) * kHeadDim;
   const S* Vx = Kx + (size_t)a.n_head * a.n_frames * kHeadDim;
-  float m[kRows], l[kRows], acc[kRows][8];
+  {  // pass 1: scores
+    float q8[kRows][8];
 #pragma unroll
-  for (int r = 0; r < kRows; ++r) {
-    m[r] = -INFINITY;
-    l[r] = 0.f;
+    for (int r = 0; r < kRows; ++r) {
+      const float* qr = a.q + (size_t)(slot * kRows + r) * a.ldq + head * kHeadDim + 8 * g;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) q8[r][e] = qr[e] * 0.125f;
+    }
+    for (int o0 = w; o0 < noct; o0 += NW * B) {
+      Raw8<S> kr[B];
+#pragma unroll
+      for (int b = 0; b < B; ++b) {  // keys past the end re-read the last one (not stored)
+        const int key = min((o0 + NW * b) * 8 + kl, nk - 1);
+        kr[b].load(Kx + (uint32_t)key * kHeadDim + 8 * g);
+      }
+#pragma unroll
+      for (int b = 0; b < B; ++b) {
+        const int key = (o0 + NW * b) * 8 + kl;
+        float k8[8];
+        kr[b].unpack(k8);
+        float t[kRows];
+#pragma unroll
+        for (int r = 0; r < kRows; ++r) {
+          float u = 0.f;
+#pragma unroll
+          for (int e = 0; e < 8; ++e) u = fmaf(q8[r][e], k8[e], u);
+          t[r] = sum8(u);
+        }
+        if (g == 0 && key < nk) {
+          float4* d = reinterpret_cast<float4*>(sc + key * kXrStride);
+          d[0] = make_float4(t[0], t[1], t[2], t[3]);
+          d[1] = make_float4(t[4], t[5], t[6], t[7]);
+          d[2] = make_float4(t[8], 0.f, 0.f, 0.f);
+        }
+      }
+    }
+  }
+  __syncthreads();
+  // sweeps over the scores, one thread per (frame, row): row maxima, then
+  // probabilities in place and the row sums
+  const bool sweeper = threadIdx.x < kXrSweepKeys * kRows;
+  const int sr = threadIdx.x % kRows;
+  if (sweeper) {
+    float m = -INFINITY;
+    for (int key = threadIdx.x / kRows; key < nk; key += kXrSweepKeys) m = fmaxf(m, sc[key * kXrStride + sr]);
+    lpart[threadIdx.x] = m;
+  }
+  __syncthreads();
+  if (threadIdx.x < kRows) {
+    float m = lpart[threadIdx.x];
+    for (int i = 1; i < kXrSweepKeys; ++i) m = fmaxf(m, lpart[i * kRows + threadIdx.x]);
+    rmax[threadIdx.x] = m;
+  }
+  __syncthreads();
+  if (sweeper) {
+    const float M = rmax[sr];
+    float lp = 0.f;
+    for (int key = threadIdx.x / kRows; key < nk; key += kXrSweepKeys) {
+      const float p = __expf(sc[key * kXrStride + sr] - M);
+      sc[key * kXrStride + sr] = p;
+      lp += p;
+    }
+    lpart[threadIdx.x] = lp;
+  }
+  __syncthreads();
+  if (threadIdx.x < kRows) {
+    float L = 0.f;
+    for (int i = 0; i < kXrSweepKeys; ++i) L += lpart[i * kRows + threadIdx.x];
+    lsum[threadIdx.x] = L;
+  }
+  // pass 2: values
+  float acc[kRows][8];
+#pragma unroll
+  for (int r = 0; r < kRows; ++r)
 #pragma unroll
     for (int e = 0; e < 8; ++e) acc[r][e] = 0.f;
-  }
-  const int noct = (nk + 7) >> 3;
   for (int o0 = w; o0 < noct; o0 += NW * B) {
-    Raw8<S> kr[B], vr[B];
+    Raw8<S> vr[B];
+#pragma unroll
+    for (int b = 0; b < B; ++b) {
+      const int key = min((o0 + NW * b) * 8 + kl, nk - 1);
+      vr[b].load(Vx + (uint32_t)key * kHeadDim + 8 * g);
+    }
 #pragma unroll
     for (int b = 0; b < B; ++b) {
       const int key = (o0 + NW * b) * 8 + kl;
-      if (key < nk) {
-        kr[b].load(Kx + (uint32_t)key * kHeadDim + 8 * g);
-        vr[b].load(Vx + (uint32_t)key * kHeadDim + 8 * g);
-      } else {
-        kr[b].zero();
-        vr[b].zero();
-      }
-    }
-    float sc[kRows][B];
+      const bool in = key < nk;
+      const float4* d = reinterpret_cast<const float4*>(sc + min(key, nk - 1) * kXrStride);
+      const float4 s0 = d[0], s1 = d[1], s2 = d[2];
+      const float p[kRows] = {in ? s0.x : 0.f, in ? s0.y : 0.f, in ? s0.z : 0.f, in ? s0.w : 0.f, in ? s1.x : 0.f,
+                              in ? s1.y : 0.f, in ? s1.z : 0.f, in ? s1.w : 0.f, in ? s2.x : 0.f};
+      float v8[8];
+      vr[b].unpack(v8);
 #pragma unroll
-    for (int b = 0; b < B; ++b) {
-      float k8[8];
-      kr[b].unpack(k8);
-      const bool ok = (o0 + NW * b) * 8 + kl < nk;
+      for (int r = 0; r < kRows; ++r)
 #pragma unroll
-      for (int r = 0; r < kRows; ++r) {
-        float t = 0.f;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) t = fmaf(q8[r][e], k8[e], t);
-        t = sum8(t);
-        sc[r][b] = ok ? t : -INFINITY;
-      }
-    }
-    float v8[B][8];
-#pragma unroll
-    for (int b = 0; b < B; ++b) vr[b].unpack(v8[b]);
-#pragma unroll
-    for (int r = 0; r < kRows; ++r) {
-      float bm = sc[r][0];
-#pragma unroll
-      for (int b = 1; b < B; ++b) bm = fmaxf(bm, sc[r][b]);
-      const float mn = fmaxf(m[r], wave_max(bm));  // key o0 * 8 < nk is in this batch
-      const float f = __expf(m[r] - mn);
-      l[r] *= f;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) acc[r][e] *= f;
-#pragma unroll
-      for (int b = 0; b < B; ++b) {
-        const float p = __expf(sc[r][b] - mn);
-        l[r] += g == 0 ? p : 0.f;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) acc[r][e] = fmaf(p, v8[b][e], acc[r][e]);
-      }
-      m[r] = mn;
+        for (int e = 0; e < 8; ++e) acc[r][e] = fmaf(p[r], v8[e], acc[r][e]);
     }
   }
-  // fold the 8 key lanes (bits 3..5) of each dim group, then publish per wave
+  // fold the 8 key lanes (lane bits 3..5) of each dim group and publish per wave,
+  // row by row so each row's sums die at its store
+  __syncthreads();  // every wave is done with the probabilities
 #pragma unroll
   for (int r = 0; r < kRows; ++r) {
 #pragma unroll
@@ -380,30 +432,41 @@ __global__ void __launch_bounds__(kXrThreads) k_attn_cross_rows(CrossArgs a) {
       float t = acc[r][e] + dpp<kDppRor8>(acc[r][e]);
       t += __shfl_xor(t, 16, 64);
       t += __shfl_xor(t, 32, 64);
-      acc[r][e] = t;
-    }
-    const float lr = wave_sum(l[r]);
-    if (lane < 8) {
-#pragma unroll
-      for (int e = 0; e < 8; ++e) wacc[w][r][8 * g + e] = acc[r][e];
-    }
-    if (lane == 0) {
-      wm[w][r] = m[r];
-      wl[w][r] = lr;
+      if (lane < 8) wacc[w][r][8 * g + e] = t;
     }
   }
   __syncthreads();
+  const int pair = blockIdx.y * a.n_head + head;
+  float* part = a.part + (size_t)pair * a.nchunk * kXrPart;
   for (int t = threadIdx.x; t < kRows * 64; t += kXrThreads) {
     const int r = t >> 6, dim = t & 63;
-    float M = wm[0][r];
+    float o = 0.f;
 #pragma unroll
-    for (int i = 1; i < NW; ++i) M = fmaxf(M, wm[i][r]);
+    for (int i = 0; i < NW; ++i) o += wacc[i][r][dim];
+    if (a.nchunk == 1) put_op<S>(a.out, a.nsplit, a.R9, slot * kRows + r, head * kHeadDim + dim, o / lsum[r]);
+    else part[c * kXrPart + 32 + t] = o;
+  }
+  if (a.nchunk > 1 && threadIdx.x < kRows) {
+    part[c * kXrPart + threadIdx.x] = rmax[threadIdx.x];
+    part[c * kXrPart + 16 + threadIdx.x] = lsum[threadIdx.x];
+  }
+}
+
+// Merge of the chunk records of one (head, slot) in chunk order.
+constexpr int kXmThreads = 192;
+template <typename S>
+__global__ void __launch_bounds__(kXmThreads) k_attn_cross_merge(CrossArgs a) {
+  const int head = blockIdx.x, slot = a.slot0 + blockIdx.y;
+  const float* part = a.part + (size_t)(blockIdx.y * a.n_head + head) * a.nchunk * kXrPart;
+  for (int t = threadIdx.x; t < kRows * 64; t += kXmThreads) {
+    const int r = t >> 6, dim = t & 63;
+    float M = -INFINITY;
+    for (int i = 0; i < a.nchunk; ++i) M = fmaxf(M, part[i * kXrPart + r]);
     float L = 0.f, o = 0.f;
-#pragma unroll
-    for (int i = 0; i < NW; ++i) {
-      const float f = __expf(wm[i][r] - M);  // 0 for a wave without keys
-      L += wl[i][r] * f;
-      o += wacc[i][r][dim] * f;
+    for (int i = 0; i < a.nchunk; ++i) {
+      const float f = __expf(part[i * kXrPart + r] - M);
+      L = fmaf(f, part[i * kXrPart + 16 + r], L);
+      o = fmaf(f, part[i * kXrPart + 32 + t], o);
     }
     put_op<S>(a.out, a.nsplit, a.R9, slot * kRows + r, head * kHeadDim + dim, o / L);
   }
@@ -554,8 +617,12 @@ void Ops<S>::attn_draft(const AttnArgs& a, int n, hipStream_t st) {
 // otherwise one block per (head, row)
 template <typename S>
 void Ops<S>::attn_cross(const CrossArgs& a, int n, hipStream_t st) {
-  if (n * a.n_head >= 128) k_attn_cross_rows<S><<<dim3(a.n_head, n), kXrThreads, 0, st>>>(a);
-  else k_attn_cross<S><<<dim3(row_blocks(a.n_head), n), kCrossThreads, 0, st>>>(a);
+  if (n == 1) {  // one slot: a block per (head, row) streams all frames (9 blocks per head share an L2)
+    k_attn_cross<S><<<dim3(row_blocks(a.n_head), n), kCrossThreads, 0, st>>>(a);
+    return;
+  }
+  k_attn_cross_rows<S><<<dim3(a.n_head, n, a.nchunk), kXrThreads, xr_lds_bytes(a.chunk), st>>>(a);
+  if (a.nchunk > 1) k_attn_cross_merge<S><<<dim3(a.n_head, n), kXmThreads, 0, st>>>(a);
 }
 
 template void Ops<float>::attn_self(const AttnArgs&, int, hipStream_t);

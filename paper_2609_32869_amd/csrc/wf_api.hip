@@ -211,6 +211,7 @@ int compute_layout(const wf_config& c, Layout& L) {
     L.fc2_split = std::max(1, std::min({kRlnMaxPartsHost, 240 / tiles64, ksteps}));
   }
   L.part = region((size_t)std::max(L.fc2_split, 1) * R9 * d * 4);
+  L.xpart = region((size_t)kXrMaxPartials * kXrPart * 4);
   L.total = o;
   return WF_OK;
 }
@@ -393,6 +394,8 @@ struct Runner {
     a.n_frames = c.n_frames;
     a.nsplit = L.nsplit_op;
     a.R9 = R9();
+    cross_chunks(n * c.n_head, c.n_frames, a.nchunk, a.chunk);
+    a.part = F32(L.xpart);
     launch("attn_cross", 2.0 * c.n_head * c.n_frames * kHeadDim * eb() * n, [&] { Ops<S>::attn_cross(a, n, st); });
   }
 

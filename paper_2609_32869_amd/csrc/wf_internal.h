@@ -27,6 +27,7 @@ struct Layout {
   size_t state, page_table, rope, status, aux, weights, xkv, skv, hkv;
   size_t a_d16, a_d32, a_f16, a_tap16, h, qkv, hp, kvh, hv, hi, tok, g, gmax, draft, lasth, logits, dlogits, part;
   size_t hm, hs, tmax, tsum, dmax, dsum, sst, spart;  // sampling: normalisers and draw partials
+  size_t xpart;  // chunked cross-attention: partial records
   size_t total;
   // element offsets inside the weight region
   size_t tok_emb, pos_emb, lnf_g, lnf_b, hproj_w, hproj_b, mask, dlnf_g, dlnf_b;

@@ -89,7 +89,28 @@ struct CrossArgs {
   const void* kv;  // block base of [slot][2][head][frame][64]
   Operand out;
   int slot0, d, n_head, n_frames, nsplit, R9;
+  int nchunk, chunk;  // frame chunks per (head, slot) and frames per chunk (multiple of 8)
+  float* part;        // [pair][nchunk][kXrPart] chunk partials (nchunk > 1)
 };
+// Chunk partial record: max [9] at 0, sum [9] at 16, acc [9][64] at 32.
+constexpr int kXrPart = 32 + kRows * 64;
+constexpr int kXrMaxPairs = 128;      // chunking only below this many (head, slot) pairs
+constexpr int kXrMaxPartials = 512;   // pair * chunk records of a chunked launch
+// Chunking of cross-attention over the frames for a few slots (2 to 6 at 20
+// heads): about 240 blocks, chunks of >= 64 frames.  nchunk <= want, so
+// pairs * nchunk <= kXrMaxPartials.
+inline void cross_chunks(int pairs, int n_frames, int& nchunk, int& chunk) {
+  nchunk = 1;
+  chunk = n_frames;
+  if (pairs >= kXrMaxPairs) return;
+  int want = (240 + pairs - 1) / pairs;
+  if (want > kXrMaxPartials / pairs) want = kXrMaxPartials / pairs;
+  int ch = (n_frames + want - 1) / want;
+  ch = ch < 64 ? 64 : (ch + 7) / 8 * 8;
+  if (ch >= n_frames) return;
+  chunk = ch;
+  nchunk = (n_frames + ch - 1) / ch;
+}
 
 struct LnArgs {
   const float* x;  // [rows][d]

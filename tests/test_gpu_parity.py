@@ -139,6 +139,42 @@ def test_micro_bf16_b3_bf16_operands():
 
 
 @pytest.mark.timeout(900)
+# Several slots over many frames: cross-attention splits the frames into chunks
+# of 64 (the last one ragged, with a partial key octet) whose partial softmax
+# sums a second kernel merges.
+def test_micro_bf16_b3_chunked_cross_attention():
+    from lockstep import Lockstep
+    cfg = MICRO_BF16.with_(name="micro-bf16-997f", n_frames=997)
+    W = make_weights(cfg)
+    prompts = [make_prefix(cfg, 0, 6), make_prefix(cfg, 1, 17), make_prefix(cfg, 2, 30)]
+    max_new = [24, 24, 24]
+    opts = OracleOpts(dtype=np.float32, kv_bf16=True, gemm_bf16=True)
+    ls = Lockstep(cfg, W, prompts, max_new, TOL_BF16, opts=opts)
+    T = Target(cfg, W.values, opts)
+    refs = [plain_greedy(T, make_memory(cfg, i), prompts[i], max_new[i]) for i in range(3)]
+    _run_planted(ls, refs, np.random.default_rng(7), 6)
+    print(f"micro-bf16 997 frames b3: max |dlogit| draft {ls.max_dlogit:.3e} target {ls.max_tlogit:.3e}, near ties {ls.near_ties}")
+    assert ls.steps == 6
+    ls.close()
+
+
+def test_tiny_b2_chunked_cross_attention():
+    """fp32, two slots over 1500 frames: 19 chunks of 80 frames and a ragged 60."""
+    from lockstep import Lockstep
+    cfg = TINY
+    W = make_weights(cfg)
+    prompts = [make_prefix(cfg, 0, 9), make_prefix(cfg, 1, 25)]
+    ls = Lockstep(cfg, W, prompts, [20, 20], TOL_F32)
+    T = Target(cfg, W.values, OracleOpts())
+    refs = [plain_greedy(T, make_memory(cfg, i), prompts[i], 20) for i in range(2)]
+    _run_planted(ls, refs, np.random.default_rng(8), 5)
+    print(f"tiny b2: max |dlogit| draft {ls.max_dlogit:.3e} target {ls.max_tlogit:.3e}, near ties {ls.near_ties}")
+    for i, s in enumerate(ls.sess):
+        if ls.live[i]:
+            assert s.out == refs[i][:len(s.out)]
+    ls.close()
+
+
 def test_large_v3_bf16_lockstep_b1():
     """Whisper-large-v3 shapes, bf16 weights/caches, one slot, prefix in [20, 200]."""
     from lockstep import Lockstep
