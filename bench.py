@@ -32,6 +32,51 @@ METRIC = "verified tokens/s per draft+verify step (bs 1 / 96); HBM GB/s vs peak"
 HBM_PEAK_GBS = 8000.0
 
 
+# profile role -> kernel symbol as a kernel trace names it (batch-1 bf16 path)
+SYMBOL_OF_ROLE = {
+    "attn_cross": "void wf::k_attn_cross<wf::bf16>(wf::CrossArgs)",
+    "attn_self": "void wf::k_attn_self<wf::bf16>(wf::AttnArgs)",
+    "gemv_o": "void wf::k_gemv16<2, 4>(wf::GemvArgs)",
+    "gemv_qkv": "void wf::k_gemv16<3, 4>(wf::GemvArgs)",
+    "gemv_q2": "void wf::k_gemv16_ln<0, 16, 5>(wf::GemvArgs)",
+    "gemv_fc1": "void wf::k_gemv32_ln<1, 16, 5>(wf::GemvArgs)",
+    "gemv_fc2": "void wf::k_gemv16w<5, 8, 4>(wf::GemvArgs)",
+    "reduce_ln": "void wf::k_reduce_ln<wf::bf16>(wf::RlnArgs)",
+    "head": "void wf::k_gemv32<4, 8>(wf::GemvArgs)",
+}
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic_large-v3_b1_pmc.md")
+
+
+def source_digest():
+    """sha256 over the kernel sources (csrc/*.hip, csrc/*.h), in name order."""
+    import hashlib
+    d = hashlib.sha256()
+    src = os.path.join(ROOT, "paper_2609_32869_amd", "csrc")
+    for name in sorted(os.listdir(src)):
+        if name.endswith((".hip", ".h")):
+            with open(os.path.join(src, name), "rb") as f:
+                d.update(name.encode() + b"\0" + f.read())
+    return d.hexdigest()
+
+
+def measured_traffic(role):
+    """HBM bytes per launch of the role's kernel from the committed counter summary
+    (FETCH_SIZE and WRITE_SIZE passes, copy-calibrated), or None when there is
+    none or the kernel sources changed since the counters were taken."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            line = next(l for l in f if l.startswith("traffic-json: "))
+        rec = json.loads(line[len("traffic-json: "):])
+    except (OSError, StopIteration, ValueError):
+        return None, "no counter summary"
+    if rec.get("source_sha256") != source_digest():
+        return None, "kernel sources changed since the counter passes"
+    k = rec.get("kernels", {}).get(SYMBOL_OF_ROLE.get(role, ""))
+    if not k:
+        return None, "kernel not in the counter summary"
+    return k["hbm_bytes_per_dispatch"], "FETCH_SIZE and WRITE_SIZE passes scaled by a 256 MiB copy (" + TRAFFIC_FILE[len(ROOT) + 1:] + ")"
+
+
 # profile role -> kernel symbol of the batch-1 bf16 path (the roofline names the kernel)
 KERNEL_OF_ROLE = {
     "attn_cross": "wf::k_attn_cross<wf::bf16>",
@@ -199,6 +244,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--profile-steps", type=int, default=4)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--pmc-run", action="store_true",
+                    help="short run for hardware-counter passes: 1 warm-up, 2 timed and 1 profiled step, no oracle, "
+                         "then a plain 256 MiB device-to-device copy (x3) whose counters calibrate byte counts")
     ap.add_argument("--batch", type=int, default=1,
                     help="sequences per step; > 1 runs the ragged large-batch workload (prefixes U[4,440], "
                          "one acoustic memory per slot) instead of the batch-1 line")
@@ -208,6 +256,8 @@ def main():
               "(sequences shard across GPUs with no communication; see the design notes)", file=sys.stderr)
         sys.exit(2)
 
+    if args.pmc_run:
+        args.steps, args.warmup, args.profile_steps, args.no_cpu_baseline = 2, 1, 1, True
     if args.batch > 1:
         return run_batch(args)
     import torch
@@ -233,7 +283,7 @@ def main():
 
     # untimed plain-greedy pass on the GPU: the target's own continuation
     first = eng.prefill(0, toks, [L0], [cfg.n_ctx])
-    n_traj = min(cfg.n_ctx - L0, (K + 1) * (total + args.profile_steps + 2) + K)
+    n_traj = min(cfg.n_ctx - L0, (K + 1) * (total + args.profile_steps + 3) + K)
     outs = eng._outs(1)
     zero = torch.zeros((1, K), dtype=torch.int32, device="cuda")
     traj_t = torch.empty(n_traj, dtype=torch.int32, device="cuda")
@@ -253,7 +303,7 @@ def main():
         nat.append(int(o[1][0].item()))
 
     rng = np.random.default_rng(400)
-    plans, accs = plan_planted(traj, L0, 1, total + args.profile_steps, cfg, rng)
+    plans, accs = plan_planted(traj, L0, 1, total + args.profile_steps + 1, cfg, rng)
     plan_t = torch.from_numpy(plans[:, None, :].copy()).cuda()
 
     # timed: graph replay of wf_step
@@ -282,11 +332,15 @@ def main():
     planted_ok = bool(np.array_equal(emitted, expect))
     value = timed_tokens / (total_ms / 1e3)
 
-    # profiling pass (eager, same plan continued): per-kernel HIP event timings
+    # profiling pass (same plan continued): replays of a second capture of the step
+    # in which every hot kernel stamps its first-wave start and last-wave end with
+    # the device wall clock; the first replay is a warm-up and is discarded
     eng.profile(True)
-    for i in range(args.profile_steps):
+    for i in range(args.profile_steps + 1):
         ovr.copy_(plan_t[total + i])
-        eng.step(0, 1, K, draft_override=ovr, outs=outs, use_graph=False)
+        eng.step(0, 1, K, draft_override=ovr, outs=outs, use_graph=True)
+        if i == 0:
+            eng.profile_summary()
     torch.cuda.synchronize()
     prof = eng.profile_summary()
     eng.profile(False)
@@ -295,6 +349,8 @@ def main():
     role, dom = max(((k, v) for k, v in prof.items() if v["bytes"] > 0), key=lambda kv: kv[1]["ms"])
     dom_gbs = dom["bytes"] / (dom["ms"] / 1e3) / 1e9
     avg_launch_us = 1e3 * dom["ms"] / dom["launches"]
+    avg_exec_us = 1e3 * dom["exec_ms"] / dom["launches"]
+    traffic, traffic_src = measured_traffic(role)
     bytes_per_launch = dom["bytes"] / dom["launches"]
     gemv_ms = sum(v["ms"] for k, v in prof.items() if k.startswith("gemv") or k == "head")
     kernel_ms = sum(v["ms"] for v in prof.values()) / args.profile_steps
@@ -321,11 +377,16 @@ def main():
                    "batch": 1, "prefix_len": L0, "storage": "bf16", "drafts": "planted r~U{0..8}",
                    "graph": True},
         "roofline": {"bound": "hbm", "achieved": round(dom_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": round(dom_gbs / HBM_PEAK_GBS, 4), "traffic": None,
+                     "frac": round(dom_gbs / HBM_PEAK_GBS, 4),
+                     "traffic": round(traffic, 1) if traffic else None, "traffic_source": traffic_src,
                      "kernel": KERNEL_OF_ROLE.get(role, role), "role": role,
                      "launches_per_step": dom["launches"] / args.profile_steps,
                      "bytes_per_launch": round(bytes_per_launch, 1), "avg_launch_us": round(avg_launch_us, 3),
-                     "timing": "HIP events around each eager launch on the library's stream"},
+                     "avg_exec_us": round(avg_exec_us, 3),
+                     "timing": "device wall clock stamped by the kernel itself inside replays of the captured "
+                               "step graph on the library's stream; avg_launch_us = previous launch's last-wave end "
+                               "to this launch's (dispatch included, as a kernel trace counts it), avg_exec_us = "
+                               "first-wave start to last-wave end"},
         "step": {"median_ms": round(med, 4), "p10_ms": round(float(np.percentile(step_ms, 10)), 4),
                  "p90_ms": round(float(np.percentile(step_ms, 90)), 4),
                  "algorithmic_bytes": sb, "achieved_GBs": round(sb / (med / 1e3) / 1e9, 1),
@@ -333,10 +394,12 @@ def main():
                  "roofline_us_at_peak": round(sb / HBM_PEAK_GBS / 1e3, 1),
                  "tau": round(timed_tokens / args.steps, 3), "planted_acceptance_exact": planted_ok,
                  "tau_natural": round(float(np.mean(nat)), 3),
-                 "sum_kernel_ms_eager": round(kernel_ms, 4),
+                 "sum_kernel_ms_profiled": round(kernel_ms, 4),
                  "gemv_tflops": round(gemv_flops_per_step(cfg) / (gemv_ms / args.profile_steps / 1e3) / 1e12, 2)},
-        "profile_eager": {k: {"launches_per_step": v["launches"] / args.profile_steps,
+        "profile_graph": {k: {"launches_per_step": v["launches"] / args.profile_steps,
                               "us_per_step": round(1e3 * v["ms"] / args.profile_steps, 2),
+                              "exec_us_per_step": round(1e3 * v["exec_ms"] / args.profile_steps, 2),
+                              "bytes_per_launch": round(v["bytes"] / v["launches"], 1) if v["launches"] else 0,
                               "GBs": round(v["bytes"] / (v["ms"] / 1e3) / 1e9, 1) if v["bytes"] else None}
                           for k, v in prof.items()},
     }
@@ -347,6 +410,20 @@ def main():
         result["cpu_baseline"] = cpu_baseline(cfg, W, mem, prompt, plans[:total])
         result["gpu_over_cpu"] = round(value / result["cpu_baseline"]["value"], 1)
     print(json.dumps(result), flush=True)
+    if args.pmc_run:
+        calibration_copy(log)
+
+
+def calibration_copy(log, mib=256, reps=3):
+    """A plain device-to-device copy of known size: its FETCH_SIZE / WRITE_SIZE
+    counters give the factor that turns counter readings into bytes."""
+    import torch
+    x = torch.ones(mib << 18, dtype=torch.float32, device="cuda")
+    y = torch.empty_like(x)
+    for _ in range(reps):
+        y.copy_(x)
+    torch.cuda.synchronize()
+    log(f"[bench] calibration copy: {reps} x {mib} MiB device-to-device")
 
 
 if __name__ == "__main__":

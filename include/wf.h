@@ -189,13 +189,21 @@ int wf_debug_ptr(wf_handle* h, int which, void** ptr);
 int wf_set_debug(wf_handle* h, int enable);
 
 /*
- * Profiling of eager calls: when enabled, every kernel launch of later
- * non-graph calls is bracketed by HIP events on the call's stream.
- * wf_profile_summary synchronises those events and writes a JSON object
- * {"<kernel class>": {"launches": n, "ms": total, "bytes": algorithmic bytes}}
- * into buf (len bytes, including the terminating NUL), then forgets them.
- * Algorithmic bytes count parameters, caches and activations each launch must
- * move once.  Graph replays are never instrumented.
+ * Profiling: while enabled, every launch of the weight products, attention,
+ * LayerNorm and residual-reduction kernels records the wall-clock time at
+ * which its first wave starts and its last wave ends (a device timing slot per
+ * launch).  "exec_ms" sums those spans; "ms" sums each launch's share of the
+ * timeline, from the previous timed launch's last wave end to its own (the
+ * dispatch and completion between kernels included).  Eager calls synchronise
+ * their stream and collect the durations before returning; wf_step with
+ * use_graph captures a separate profiled graph and each replay of it
+ * synchronises and collects.  wf_profile_summary writes a JSON object
+ * {"<kernel class>": {"launches": n, "ms": total, "exec_ms": total, "bytes":
+ * algorithmic bytes}} of everything collected since the previous summary into
+ * buf (len bytes, including the terminating NUL), then forgets it (also when
+ * buf is too small: WF_ESIZE).  Algorithmic bytes count parameters, caches and
+ * activations each launch must move once.  Calls made while profiling is off
+ * carry no timing.
  */
 int wf_profile_enable(wf_handle* h, int enable);
 int wf_profile_summary(wf_handle* h, char* buf, size_t len);

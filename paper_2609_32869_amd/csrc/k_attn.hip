@@ -269,6 +269,7 @@ template <typename S>
 constexpr int kCrossB = sizeof(S) == 2 ? 24 : 12;  // key octets in flight per wave
 template <typename S>
 __global__ void __launch_bounds__(kCrossThreads) k_attn_cross(CrossArgs a) {
+  StampScope stamp_scope(a.stamp);
   constexpr int NW = kCrossThreads / 64;
   __shared__ float part[NW][4][64];
   __shared__ float pm[NW], pl[NW];
@@ -312,6 +313,7 @@ inline size_t xr_lds_bytes(int chunk) {
 }
 template <typename S>
 __global__ void __launch_bounds__(kXrThreads, 4) k_attn_cross_rows(CrossArgs a) {
+  StampScope stamp_scope(a.stamp);
   constexpr int NW = kXrWaves, B = sizeof(S) == 2 ? 4 : 2;  // key octets in flight per wave
   extern __shared__ float sc[];
   float(*wacc)[kRows][64] = reinterpret_cast<float(*)[kRows][64]>(sc);
@@ -456,6 +458,7 @@ __global__ void __launch_bounds__(kXrThreads, 4) k_attn_cross_rows(CrossArgs a) 
 constexpr int kXmThreads = 192;
 template <typename S>
 __global__ void __launch_bounds__(kXmThreads) k_attn_cross_merge(CrossArgs a) {
+  StampScope stamp_scope(a.stamp);
   const int head = blockIdx.x, slot = a.slot0 + blockIdx.y;
   const float* part = a.part + (size_t)(blockIdx.y * a.n_head + head) * a.nchunk * kXrPart;
   for (int t = threadIdx.x; t < kRows * 64; t += kXmThreads) {
@@ -479,6 +482,7 @@ __global__ void __launch_bounds__(kXmThreads) k_attn_cross_merge(CrossArgs a) {
 constexpr int kSelfThreads = 256;
 template <typename S>
 __global__ void __launch_bounds__(kSelfThreads) k_attn_self(AttnArgs a) {
+  StampScope stamp_scope(a.stamp);
   constexpr int NW = kSelfThreads / 64;
   static_assert(NW * 14 * 8 >= kMaxCtx, "one batch of key octets covers the context");
   __shared__ float part[NW][4][64];
@@ -522,6 +526,7 @@ __global__ void __launch_bounds__(kSelfThreads) k_attn_self(AttnArgs a) {
 // positions.
 template <typename S>
 __global__ void __launch_bounds__(kSelfThreads) k_attn_draft(AttnArgs a) {
+  StampScope stamp_scope(a.stamp);
   constexpr int NT = kSelfThreads, NW = NT / 64;
   __shared__ float sc[kMaxCtx + 16];
   __shared__ float part[NW][64];

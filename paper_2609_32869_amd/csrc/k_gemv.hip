@@ -169,6 +169,7 @@ __device__ void finish_tile(const GemvArgs& a, float (*sv)[TC + 1], float (*ov)[
 // ---------------------------------------------------------------- bf16, 16-column tiles
 template <int EPI, int NW>
 __global__ void __launch_bounds__(NW * 64) k_gemv16(GemvArgs a) {
+  StampScope stamp_scope(a.stamp);
   constexpr int U = NW >= 16 ? kU / 2 : kU;
   __shared__ float red[NW][32][17];
   __shared__ float sv[32][17];
@@ -229,6 +230,7 @@ __global__ void __launch_bounds__(NW * 64) k_gemv16(GemvArgs a) {
 // with more than one k-range the epilogue must be EPI_PART.
 template <int EPI, int NW, int CT>
 __global__ void __launch_bounds__(NW * 64) k_gemv16w(GemvArgs a) {
+  StampScope stamp_scope(a.stamp);
   constexpr int U = CT >= 4 ? 4 : 8;
   constexpr int TC = 16 * CT;
   __shared__ float red[NW][32][TC + 1];
@@ -310,6 +312,7 @@ __global__ void __launch_bounds__(NW * 64) k_gemv16w(GemvArgs a) {
 constexpr int kGemmU = 4;
 template <int EPI>
 __global__ void __launch_bounds__(256) k_gemm16(GemvArgs a, int mb0, int nmb, int nnb) {
+  StampScope stamp_scope(a.stamp);
   __shared__ float sv[64][65];
   __shared__ float ov[EPI == EPI_ARGMAX ? 64 : 1][64];
   __shared__ float oz[EPI == EPI_ARGMAX ? 64 : 1][64];
@@ -365,6 +368,7 @@ __global__ void __launch_bounds__(256) k_gemm16(GemvArgs a, int mb0, int nmb, in
 // ---------------------------------------------------------------- bf16, 32-column tiles
 template <int EPI, int NW>
 __global__ void __launch_bounds__(NW * 64) k_gemv32(GemvArgs a) {
+  StampScope stamp_scope(a.stamp);
   constexpr int U = NW >= 16 ? kU / 2 : kU;
   __shared__ float red[NW][32][33];
   __shared__ float sv[32][33];
@@ -529,6 +533,7 @@ struct LnRows {
 // 16-column tiles; every wave's k-steps fit one batch of loads (K <= kLnFoldMaxK).
 template <int EPI, int NW, int U>
 __global__ void __launch_bounds__(NW * 64) k_gemv16_ln(GemvArgs a) {
+  StampScope stamp_scope(a.stamp);
   __shared__ uint4 aop[kLnFoldMaxK / 32 * 2 * 64];
   __shared__ float red[NW][32][17];
   __shared__ float sv[32][17];
@@ -579,6 +584,7 @@ __global__ void __launch_bounds__(NW * 64) k_gemv16_ln(GemvArgs a) {
 // 32-column tiles; every wave's k-steps fit one batch of loads (K <= kLnFoldMaxK).
 template <int EPI, int NW, int U>
 __global__ void __launch_bounds__(NW * 64) k_gemv32_ln(GemvArgs a) {
+  StampScope stamp_scope(a.stamp);
   __shared__ uint4 aop[kLnFoldMaxK / 16 * 64];
   __shared__ float red[NW][32][33];
   __shared__ float sv[32][33];
@@ -627,6 +633,7 @@ __global__ void __launch_bounds__(NW * 64) k_gemv32_ln(GemvArgs a) {
 // k does not depend on the order in which k is visited).
 template <int EPI, int NW>
 __global__ void __launch_bounds__(NW * 64) k_gemv_f32(GemvArgs a) {
+  StampScope stamp_scope(a.stamp);
   constexpr int U = NW >= 16 ? kU / 2 : kU;
   __shared__ float red[NW][32][17];
   __shared__ float sv[32][17];

@@ -17,6 +17,7 @@ namespace wf {
 // block of 256 threads per row; the row stays in registers (d <= 2048).
 template <typename S>
 __global__ void __launch_bounds__(256) k_ln_operand(LnArgs a) {
+  StampScope stamp_scope(a.stamp);
   __shared__ float red[8];
   const int row = a.row0 + blockIdx.x;
   const float* xr = a.x + (size_t)row * a.d;
@@ -624,6 +625,7 @@ constexpr int kRlnThreads = 1024;
 constexpr int kRlnMaxParts = 16;
 template <typename S>
 __global__ void __launch_bounds__(kRlnThreads) k_reduce_ln(RlnArgs a) {
+  StampScope stamp_scope(a.stamp);
   constexpr int NW = kRlnThreads / 64;
   constexpr int J = 2;  // d <= 2048
   __shared__ float red[2][NW];
@@ -733,5 +735,18 @@ void accept_greedy(const AcceptArgs& a, hipStream_t st) { k_accept_greedy<<<(a.n
   template void Ops<S>::gemm_xkv(const XkvArgs&, hipStream_t);
 WF_MISC_INST(float)
 WF_MISC_INST(bf16)
+
+// ---------------------------------------------------------------- launch timing slots
+__global__ void __launch_bounds__(256) k_stamp_init(unsigned long long* s, int n) {
+  const int i = blockIdx.x * 256 + threadIdx.x;  // one (start, end) pair
+  if (i < n) {
+    s[2 * i] = ~0ull;
+    s[2 * i + 1] = 0ull;
+  }
+}
+void stamp_init(unsigned long long* s, int n, hipStream_t st) {
+  const int pairs = n * kStampWords / 2;
+  k_stamp_init<<<(unsigned)((pairs + 255) / 256), 256, 0, st>>>(s, pairs);
+}
 
 }  // namespace wf

@@ -212,6 +212,7 @@ int compute_layout(const wf_config& c, Layout& L) {
   }
   L.part = region((size_t)std::max(L.fc2_split, 1) * R9 * d * 4);
   L.xpart = region((size_t)kXrMaxPartials * kXrPart * 4);
+  L.stamps = region((size_t)kStampSlots * kStampWords * 8);
   L.total = o;
   return WF_OK;
 }
@@ -239,28 +240,17 @@ struct Runner {
     bool wide;
   };
 
-  // Run one launch; when profiling (eager calls only) bracket it with events.
+  // Run one launch.  When profiling, the launch gets a timing slot (kernels that
+  // take one record their first-wave start and last-wave end in it).
   template <typename F>
   void launch(const char* tag, double bytes, F&& f) {
-    if (!h->prof || h->capturing) {
-      f();
-      return;
+    unsigned long long* stamp = nullptr;
+    if (h->prof && h->nstamp < kStampSlots) {
+      const int slot = h->nstamp++;
+      stamp = h->at<unsigned long long>(L.stamps) + (size_t)kStampWords * slot;
+      (h->capturing ? h->cap_recs : h->prof_recs).push_back(ProfRec{tag, bytes, slot});
     }
-    ProfRec r{tag, bytes, nullptr, nullptr};
-    for (hipEvent_t* e : {&r.a, &r.b}) {
-      if (!h->ev_pool.empty()) {
-        *e = h->ev_pool.back();
-        h->ev_pool.pop_back();
-      } else if (hipEventCreate(e) != hipSuccess) {
-        *e = nullptr;
-      }
-    }
-    if (r.a && r.b) (void)hipEventRecord(r.a, st);
-    f();
-    if (r.a && r.b) {
-      (void)hipEventRecord(r.b, st);
-      h->prof_recs.push_back(r);
-    }
+    f(stamp);
   }
   double eb() const { return c.dtype == WF_BF16 ? 2.0 : 4.0; }
 
@@ -339,7 +329,11 @@ struct Runner {
   }
   // tag: the product's role in the step, for the eager profile
   void run_gemv(const char* tag, int epi, int n, const GemvArgs& a) {
-    launch(tag, gemv_bytes(n, a.K, a.N, epi), [&] { Ops<S>::gemv(epi, a, st); });
+    launch(tag, gemv_bytes(n, a.K, a.N, epi), [&](unsigned long long* sp) {
+      GemvArgs b = a;
+      b.stamp = sp;
+      Ops<S>::gemv(epi, b, st);
+    });
   }
 
   void gemv(const char* tag, int epi, int slot0, int n, Operand x, size_t w, size_t b, int K, int N, float* y, int ldy,
@@ -379,7 +373,10 @@ struct Runner {
     la.x = x; la.g = W(g); la.b = W(b); la.out = out; la.d = c.d_model; la.row0 = slot0 * kRows;
     la.nsplit = L.nsplit_op; la.R9 = R9();
     launch("layernorm", 4.0 * kRows * n * c.d_model * (1 + L.nsplit_op * eb() / 4.0),
-           [&] { Ops<S>::ln_operand(la, n * kRows, st); });
+           [&](unsigned long long* sp) {
+             la.stamp = sp;
+             Ops<S>::ln_operand(la, n * kRows, st);
+           });
   }
 
   void cross(int slot0, int n, int layer) {
@@ -396,7 +393,10 @@ struct Runner {
     a.R9 = R9();
     cross_chunks(n * c.n_head, c.n_frames, a.nchunk, a.chunk);
     a.part = F32(L.xpart);
-    launch("attn_cross", 2.0 * c.n_head * c.n_frames * kHeadDim * eb() * n, [&] { Ops<S>::attn_cross(a, n, st); });
+    launch("attn_cross", 2.0 * c.n_head * c.n_frames * kHeadDim * eb() * n, [&](unsigned long long* sp) {
+      a.stamp = sp;
+      Ops<S>::attn_cross(a, n, st);
+    });
   }
 
   // second half of a decoder block shared by target and drafter: cross-attention and MLP
@@ -420,7 +420,10 @@ struct Runner {
       ra.part = F32(L.part); ra.nparts = L.fc2_split; ra.pstride = (size_t)R9() * d; ra.bias = W(b.b_fc2); ra.h = h_;
       ra.tap = Atap16(); ra.tapcol = tap >= 0 ? tap * d : -1; ra.g = W(nx.g); ra.b = W(nx.b); ra.out = nx.wide ? Ad32() : Ad16();
       ra.d = d; ra.row0 = slot0 * kRows; ra.nsplit = L.nsplit_op; ra.R9 = R9();
-      launch("reduce_ln", 4.0 * kRows * n * d * (L.fc2_split + 3), [&] { Ops<S>::reduce_ln(ra, n * kRows, st); });
+      launch("reduce_ln", 4.0 * kRows * n * d * (L.fc2_split + 3), [&](unsigned long long* sp) {
+        ra.stamp = sp;
+        Ops<S>::reduce_ln(ra, n * kRows, st);
+      });
       ln_ready = true;
     } else {
       gemv("gemv_fc2", EPI_RESID, slot0, n, Af16(), b.w_fc2, b.b_fc2, c.d_ff, d, h_, d, Atap16(), tap);
@@ -448,7 +451,10 @@ struct Runner {
       at.state = I32(L.state); at.page_table = I32(L.page_table); at.rope = F32(L.rope); at.out = Ad16();
       at.slot0 = slot0; at.d = d; at.n_head = c.n_head; at.n_ctx = c.n_ctx; at.pages_per_slot = L.pages_per_slot;
       at.nsplit = L.nsplit_op; at.R9 = R9();
-      launch("attn_self", 0, [&] { Ops<S>::attn_self(at, n, st); });
+      launch("attn_self", 0, [&](unsigned long long* sp) {
+        at.stamp = sp;
+        Ops<S>::attn_self(at, n, st);
+      });
       gemv("gemv_o", EPI_RESID, slot0, n, Ad16(), b.w_o, b.b_o, d, d, h_, d);
       const LnNext nx = l + 1 < c.n_layer ? LnNext{L.tb[l + 1].ln1_g, L.tb[l + 1].ln1_b, false}
                                           : LnNext{L.lnf_g, L.lnf_b, true};
@@ -481,7 +487,7 @@ struct Runner {
     else ln_operand(a, slot0, n, x, g, gb, Ad32(), false);
     ln_ready = false;
     run_gemv("head", EPI_ARGMAX, n, a);
-    launch("argmax_final", kRows * n * L.head_blocks * 8.0, [&] {
+    launch("argmax_final", kRows * n * L.head_blocks * 8.0, [&](unsigned long long*) {
       argmax_final(F32(L.hv), I32(L.hi), L.head_blocks, slot0 * kRows, n * kRows, I32(L.g), F32(L.gmax),
                    h->at<unsigned>(L.status), keep, dst, slot0, c.block_k, a.hm, a.hs, rmax, rsum, st);
     });
@@ -500,7 +506,7 @@ struct Runner {
       HistArgs ha{};
       ha.kv = kvh; ha.kcache = hkv(dl, 0); ha.vcache = hkv(dl, 1); ha.state = I32(L.state); ha.rope = F32(L.rope);
       ha.slot0 = slot0; ha.d = d; ha.n_head = c.n_head; ha.n_ctx = c.n_ctx;
-      launch("hist_write", 0, [&] { Ops<S>::hist_write(ha, n, st); });
+      launch("hist_write", 0, [&](unsigned long long*) { Ops<S>::hist_write(ha, n, st); });
     }
   }
 
@@ -510,7 +516,7 @@ struct Runner {
     BeginArgs ba{};
     ba.state = I32(L.state); ba.emb = W(L.tok_emb); ba.emb_kind = wk(true); ba.pos = W(L.mask); ba.h = h_;
     ba.slot0 = slot0; ba.d = d; ba.n_vocab = c.n_vocab; ba.n_ctx = c.n_ctx; ba.block_k = c.block_k;
-    launch("begin", 0, [&] { Ops<S>::draft_begin(ba, n, st); });
+    launch("begin", 0, [&](unsigned long long*) { Ops<S>::draft_begin(ba, n, st); });
     ln_ready = false;
     for (int dl = 0; dl < c.n_draft_layer; ++dl) {
       const BlockW& b = L.db[dl];
@@ -523,7 +529,10 @@ struct Runner {
       at.state = I32(L.state); at.rope = F32(L.rope); at.out = Ad16();
       at.slot0 = slot0; at.d = d; at.n_head = c.n_head; at.n_ctx = c.n_ctx;
       at.nsplit = L.nsplit_op; at.R9 = R9();
-      launch("attn_draft", 0, [&] { Ops<S>::attn_draft(at, n, st); });
+      launch("attn_draft", 0, [&](unsigned long long* sp) {
+        at.stamp = sp;
+        Ops<S>::attn_draft(at, n, st);
+      });
       gemv("gemv_o", EPI_RESID, slot0, n, Ad16(), b.w_o, b.b_o, d, d, h_, d);
       const LnNext nx = dl + 1 < c.n_draft_layer ? LnNext{L.db[dl + 1].ln1_g, L.db[dl + 1].ln1_b, false}
                                                  : LnNext{L.dlnf_g, L.dlnf_b, true};
@@ -538,7 +547,7 @@ struct Runner {
     ba.state = I32(L.state); ba.draft = draft; ba.tok = I32(L.tok); ba.emb = W(L.tok_emb); ba.emb_kind = wk(true); ba.pos = W(L.pos_emb);
     ba.h = F32(L.h); ba.slot0 = slot0; ba.d = c.d_model; ba.n_vocab = c.n_vocab; ba.n_ctx = c.n_ctx;
     ba.block_k = c.block_k; ba.k_max = k_max;
-    launch("begin", 0, [&] { Ops<S>::verify_begin(ba, n, st); });
+    launch("begin", 0, [&](unsigned long long*) { Ops<S>::verify_begin(ba, n, st); });
     target_forward(slot0, n);
     head(slot0, n, F32(L.h), L.lnf_g, L.lnf_b, h->debug || sampling() ? F32(L.logits) : nullptr, nullptr, nullptr, 0,
          F32(L.tmax), F32(L.tsum));
@@ -550,13 +559,13 @@ struct Runner {
       sa.out = out; sa.n_out = n_out; sa.n_acc = n_acc; sa.done = done;
       sa.slot0 = slot0; sa.n = n; sa.block_k = c.block_k; sa.eos = c.eos_id; sa.n_ctx = c.n_ctx; sa.V = c.n_vocab;
       sa.inv_t = h->inv_t; sa.seed = h->seed;
-      launch("accept", 0, [&] { accept_sample(sa, st); });
+      launch("accept", 0, [&](unsigned long long*) { accept_sample(sa, st); });
       return;
     }
     AcceptArgs aa{};
     aa.state = I32(L.state); aa.tok = I32(L.tok); aa.g = I32(L.g); aa.out = out; aa.n_out = n_out; aa.n_acc = n_acc;
     aa.done = done; aa.slot0 = slot0; aa.n = n; aa.block_k = c.block_k; aa.eos = c.eos_id; aa.n_ctx = c.n_ctx;
-    launch("accept", 0, [&] { accept_greedy(aa, st); });
+    launch("accept", 0, [&](unsigned long long*) { accept_greedy(aa, st); });
   }
 
   void draft(int slot0, int n, int* dst) {
@@ -602,8 +611,56 @@ struct Runner {
   }
 };
 
+// Accumulate the durations of recorded launches (in launch order) from the stamp
+// buffer; the stream must be synchronised.  Launches whose kernels take no slot
+// are skipped.  Two durations per launch: the execution span (longest per-XCD
+// first-wave-start to last-wave-end) and the share of the timeline, from the
+// previous timed launch's last wave end to this launch's (dispatch and
+// completion included, comparable to a profiler's per-dispatch duration).
+int collect_stamps(Handle* h, const std::vector<ProfRec>& recs) {
+  if (recs.empty()) return WF_OK;
+  int top = 0;
+  for (auto& r : recs) top = std::max(top, r.slot + 1);
+  std::vector<unsigned long long> t((size_t)top * kStampWords);
+  HIPCK(h, hipMemcpy(t.data(), h->at<unsigned long long>(h->lay.stamps), t.size() * 8, hipMemcpyDeviceToHost));
+  unsigned long long prev_end = 0;
+  for (auto& r : recs) {
+    unsigned long long span = 0, end = 0;
+    bool any = false;
+    for (int x = 0; x < kStampXcds; ++x) {  // per XCD: earliest start and latest end over the residues
+      unsigned long long a = ~0ull, b = 0;
+      for (int j = 0; j < kStampSub; ++j) {
+        const size_t w = (size_t)r.slot * kStampWords + 2 * (x * kStampSub + j);
+        a = std::min(a, t[w]);
+        b = std::max(b, t[w + 1]);
+      }
+      if (a == ~0ull || b < a) continue;
+      any = true;
+      span = std::max(span, b - a);
+      end = std::max(end, b);
+    }
+    if (!any) continue;
+    const unsigned long long share = prev_end && end > prev_end ? end - prev_end : span;
+    prev_end = end;
+    ProfAgg& g = h->prof_acc[r.tag];
+    g.ms += (double)share / h->wall_khz;
+    g.exec_ms += (double)span / h->wall_khz;
+    g.bytes += r.bytes;
+    g.n += 1;
+  }
+  return WF_OK;
+}
+
+// Run fn with the storage type of the handle.  When profiling, the timing slots
+// are reset first (a fill kernel, so a capture records it) and an eager call
+// synchronises and collects its launch durations.
 template <typename Fn>
-int dispatch(Handle* h, Fn&& fn) {
+int dispatch(Handle* h, hipStream_t st, Fn&& fn) {
+  const bool prof = h->prof;
+  if (prof) {
+    h->nstamp = 0;
+    stamp_init(h->at<unsigned long long>(h->lay.stamps), kStampSlots, st);
+  }
   if (h->cfg.dtype == WF_BF16) {
     fn(static_cast<bf16*>(nullptr));
   } else {
@@ -611,6 +668,12 @@ int dispatch(Handle* h, Fn&& fn) {
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return fail(h, WF_EHIP, std::string("kernel launch: ") + hipGetErrorString(e));
+  if (prof && !h->capturing) {
+    HIPCK(h, hipStreamSynchronize(st));
+    int r = collect_stamps(h, h->prof_recs);
+    h->prof_recs.clear();
+    if (r) return r;
+  }
   return WF_OK;
 }
 
@@ -692,6 +755,13 @@ int wf_init_weights(wf_handle** out, const wf_config* cfg, const void* const* we
   h->live.assign(cfg->max_batch, 0);
   hipStream_t st = static_cast<hipStream_t>(stream);
   auto cleanup = [&](int code, const std::string& msg) { delete h; return fail(nullptr, code, msg); };
+  {
+    int dev = 0, khz = 0;
+    hipError_t e0 = hipGetDevice(&dev);
+    if (e0 == hipSuccess) e0 = hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, dev);
+    if (e0 != hipSuccess || khz <= 0) return cleanup(WF_EHIP, "wall clock rate unavailable");
+    h->wall_khz = khz;
+  }
   hipError_t e = hipMemsetAsync(workspace, 0, L.total, st);
   if (e != hipSuccess) return cleanup(WF_EHIP, std::string("hipMemsetAsync: ") + hipGetErrorString(e));
   const size_t eb = elt_bytes(*cfg);
@@ -737,7 +807,7 @@ int wf_encode_memory_set(wf_handle* hh, int slot0, int n, const void* mem, void*
   if (int r = check_batch(h, slot0, n, false)) return r;
   if (!mem) return fail(h, WF_EINVAL, "null memory");
   hipStream_t st = static_cast<hipStream_t>(stream);
-  return dispatch(h, [&](auto* tag) {
+  return dispatch(h, st, [&](auto* tag) {
     using S = std::remove_pointer_t<decltype(tag)>;
     Runner<S>(h, st).encode(slot0, n, mem);
   });
@@ -762,7 +832,7 @@ int wf_prefill(wf_handle* hh, int slot0, int n, const int32_t* tokens, int pmax,
   }
   HIPCK(h, hipMemcpyAsync(h->at<int>(h->lay.state) + (size_t)slot0 * kStateInts, init.data(), init.size() * 4,
                           hipMemcpyHostToDevice, st));
-  int r = dispatch(h, [&](auto* tag) {
+  int r = dispatch(h, st, [&](auto* tag) {
     using S = std::remove_pointer_t<decltype(tag)>;
     Runner<S>(h, st).prefill(slot0, n, tokens, pmax, max_len, first);
   });
@@ -770,6 +840,13 @@ int wf_prefill(wf_handle* hh, int slot0, int n, const int32_t* tokens, int pmax,
   HIPCK(h, hipStreamSynchronize(st));
   for (int s = slot0; s < slot0 + n; ++s) h->live[s] = 1;
   return WF_OK;
+}
+
+// Destroy every captured graph.
+static void clear_graphs(Handle* h) {
+  for (auto& kv : h->graphs) (void)hipGraphExecDestroy(kv.second);
+  h->graphs.clear();
+  h->graph_recs.clear();
 }
 
 int wf_set_sampling(wf_handle* hh, float temperature, uint64_t seed, const uint8_t* suppress) {
@@ -781,8 +858,7 @@ int wf_set_sampling(wf_handle* hh, float temperature, uint64_t seed, const uint8
   h->seed = seed;
   h->suppress = suppress;
   // captured steps bake the sampling parameters in
-  for (auto& kv : h->graphs) (void)hipGraphExecDestroy(kv.second);
-  h->graphs.clear();
+  clear_graphs(h);
   return WF_OK;
 }
 
@@ -790,7 +866,7 @@ int wf_draft(wf_handle* hh, int slot0, int n, int32_t* draft, void* stream) {
   Handle* h = reinterpret_cast<Handle*>(hh);
   if (int r = check_batch(h, slot0, n, true)) return r;
   hipStream_t st = static_cast<hipStream_t>(stream);
-  return dispatch(h, [&](auto* tag) {
+  return dispatch(h, st, [&](auto* tag) {
     using S = std::remove_pointer_t<decltype(tag)>;
     Runner<S>(h, st).draft(slot0, n, draft);
   });
@@ -803,7 +879,7 @@ int wf_verify_accept(wf_handle* hh, int slot0, int n, const int32_t* draft, int 
   if (!draft) return fail(h, WF_EINVAL, "null draft");
   if (k_max < 0 || k_max > h->cfg.block_k) return fail(h, WF_EINVAL, "k_max out of range");
   hipStream_t st = static_cast<hipStream_t>(stream);
-  return dispatch(h, [&](auto* tag) {
+  return dispatch(h, st, [&](auto* tag) {
     using S = std::remove_pointer_t<decltype(tag)>;
     Runner<S>(h, st).verify(slot0, n, draft, k_max, out, n_out, n_acc, done);
   });
@@ -811,7 +887,7 @@ int wf_verify_accept(wf_handle* hh, int slot0, int n, const int32_t* draft, int 
 
 static int step_enqueue(Handle* h, int slot0, int n, int k_max, const int32_t* ovr, int32_t* out, int32_t* n_out,
                         int32_t* n_acc, int32_t* done, hipStream_t st) {
-  return dispatch(h, [&](auto* tag) {
+  return dispatch(h, st, [&](auto* tag) {
     using S = std::remove_pointer_t<decltype(tag)>;
     Runner<S> R(h, st);
     R.draft(slot0, n, nullptr);
@@ -828,24 +904,32 @@ int wf_step(wf_handle* hh, int slot0, int n, int k_max, const int32_t* ovr, int3
   hipStream_t st = static_cast<hipStream_t>(stream);
   if (!use_graph) return step_enqueue(h, slot0, n, k_max, ovr, out, n_out, n_acc, done, st);
   if (!st) return fail(h, WF_EINVAL, "graph replay needs a non-null stream");
-  GraphKey key{slot0, n, k_max, ovr, out, n_out, n_acc, done};
+  GraphKey key{slot0, n, k_max, ovr, out, n_out, n_acc, done, h->prof};
   auto it = h->graphs.find(key);
   if (it == h->graphs.end()) {
+    h->cap_recs.clear();
     HIPCK(h, hipStreamBeginCapture(st, hipStreamCaptureModeThreadLocal));
     h->capturing = true;
     int r = step_enqueue(h, slot0, n, k_max, ovr, out, n_out, n_acc, done, st);
     h->capturing = false;
     hipGraph_t g = nullptr;
     hipError_t e = hipStreamEndCapture(st, &g);
-    if (r) { if (g) (void)hipGraphDestroy(g); return r; }
-    if (e != hipSuccess) return fail(h, WF_EHIP, std::string("hipStreamEndCapture: ") + hipGetErrorString(e));
+    auto drop_recs = [&] { h->cap_recs.clear(); };
+    if (r) { if (g) (void)hipGraphDestroy(g); drop_recs(); return r; }
+    if (e != hipSuccess) { drop_recs(); return fail(h, WF_EHIP, std::string("hipStreamEndCapture: ") + hipGetErrorString(e)); }
     hipGraphExec_t ex = nullptr;
     e = hipGraphInstantiate(&ex, g, nullptr, nullptr, 0);
     (void)hipGraphDestroy(g);
-    if (e != hipSuccess) return fail(h, WF_EHIP, std::string("hipGraphInstantiate: ") + hipGetErrorString(e));
+    if (e != hipSuccess) { drop_recs(); return fail(h, WF_EHIP, std::string("hipGraphInstantiate: ") + hipGetErrorString(e)); }
     it = h->graphs.emplace(key, ex).first;
+    if (key.prof) h->graph_recs[key] = h->cap_recs;
+    h->cap_recs.clear();
   }
   HIPCK(h, hipGraphLaunch(it->second, st));
+  if (key.prof) {  // profiled replay: read this replay's launch durations now
+    HIPCK(h, hipStreamSynchronize(st));
+    return collect_stamps(h, h->graph_recs[key]);
+  }
   return WF_OK;
 }
 
@@ -865,10 +949,7 @@ int wf_debug_ptr(wf_handle* hh, int which, void** ptr) {
 int wf_set_debug(wf_handle* hh, int enable) {
   Handle* h = reinterpret_cast<Handle*>(hh);
   if (!h) return fail(nullptr, WF_EINVAL, "null handle");
-  if (h->debug != (enable != 0)) {
-    for (auto& kv : h->graphs) (void)hipGraphExecDestroy(kv.second);
-    h->graphs.clear();
-  }
+  if (h->debug != (enable != 0)) clear_graphs(h);
   h->debug = enable != 0;
   return WF_OK;
 }
@@ -883,29 +964,14 @@ int wf_profile_enable(wf_handle* hh, int enable) {
 int wf_profile_summary(wf_handle* hh, char* buf, size_t len) {
   Handle* h = reinterpret_cast<Handle*>(hh);
   if (!h || !buf || len == 0) return fail(h, WF_EINVAL, "null argument");
-  struct Agg {
-    double ms = 0, bytes = 0;
-    long n = 0;
-  };
-  std::map<std::string, Agg> agg;
-  for (auto& r : h->prof_recs) {
-    HIPCK(h, hipEventSynchronize(r.b));
-    float ms = 0.f;
-    HIPCK(h, hipEventElapsedTime(&ms, r.a, r.b));
-    Agg& a = agg[r.tag];
-    a.ms += ms;
-    a.bytes += r.bytes;
-    a.n += 1;
-    h->ev_pool.push_back(r.a);
-    h->ev_pool.push_back(r.b);
-  }
-  h->prof_recs.clear();
+  std::map<std::string, ProfAgg> agg;
+  agg.swap(h->prof_acc);
   std::string js = "{";
   bool first = true;
   for (auto& kv : agg) {
     char item[256];
-    snprintf(item, sizeof(item), "%s\"%s\": {\"launches\": %ld, \"ms\": %.6f, \"bytes\": %.1f}", first ? "" : ", ",
-             kv.first.c_str(), kv.second.n, kv.second.ms, kv.second.bytes);
+    snprintf(item, sizeof(item), "%s\"%s\": {\"launches\": %ld, \"ms\": %.6f, \"exec_ms\": %.6f, \"bytes\": %.1f}",
+             first ? "" : ", ", kv.first.c_str(), kv.second.n, kv.second.ms, kv.second.exec_ms, kv.second.bytes);
     js += item;
     first = false;
   }
@@ -930,9 +996,7 @@ int wf_status(wf_handle* hh, uint32_t* flags, void* stream) {
 int wf_release(wf_handle* hh) {
   Handle* h = reinterpret_cast<Handle*>(hh);
   if (!h) return fail(nullptr, WF_EINVAL, "null handle");
-  for (auto& kv : h->graphs) (void)hipGraphExecDestroy(kv.second);
-  for (auto& r : h->prof_recs) { (void)hipEventDestroy(r.a); (void)hipEventDestroy(r.b); }
-  for (auto e : h->ev_pool) (void)hipEventDestroy(e);
+  clear_graphs(h);
   delete h;
   return WF_OK;
 }

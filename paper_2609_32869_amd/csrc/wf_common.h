@@ -153,6 +153,44 @@ __device__ __forceinline__ bool better(float v, int i, float bv, int bi) {
   return i < bi;
 }
 
+// Launch timing for profiled calls.  A timing slot holds, per XCD (the chip's
+// eight dies) and per block-number residue mod 8, the earliest block start and
+// the latest block end (the block's last wave to leave, found with an LDS
+// count), read from the chip's constant-rate wall clock.  The launch lasts the
+// longest per-XCD span.  Spreading the global atomics over 64 words keeps them
+// from queueing on one address (which slowed large launches measurably).  A
+// null slot (the normal case) costs one uniform branch.
+constexpr int kStampXcds = 8, kStampSub = 8;
+constexpr int kStampWords = 2 * kStampXcds * kStampSub;  // per launch: (start, end) pairs
+__device__ __forceinline__ int xcc_id() {
+  return (int)__builtin_amdgcn_s_getreg((20) | (0 << 6) | (3 << 11)) & (kStampXcds - 1);  // HW_REG_XCC_ID[3:0]
+}
+__device__ __forceinline__ unsigned long long* stamp_pair(unsigned long long* s) {
+  const unsigned blk = blockIdx.x + gridDim.x * (blockIdx.y + gridDim.y * blockIdx.z);
+  return s + 2 * (xcc_id() * kStampSub + (int)(blk & (kStampSub - 1)));
+}
+struct StampScope {
+  unsigned long long* s;
+  unsigned* left;
+  // Must be the kernel's first statement: every thread of the block runs it.
+  __device__ __forceinline__ explicit StampScope(unsigned long long* p) : s(p) {
+    __shared__ unsigned waves_left;
+    left = &waves_left;
+    if (s) {
+      if (threadIdx.x == 0) {
+        waves_left = (blockDim.x * blockDim.y * blockDim.z + 63) / 64;
+        atomicMin(stamp_pair(s), (unsigned long long)wall_clock64());
+      }
+      __syncthreads();
+    }
+  }
+  __device__ __forceinline__ ~StampScope() {
+    if (s && (threadIdx.x & 63) == 0 && atomicSub(left, 1u) == 1u)
+      atomicMax(stamp_pair(s) + 1, (unsigned long long)wall_clock64());
+  }
+};
+constexpr int kStampSlots = 4096;  // instrumented launches per profiled call (kStampWords each)
+
 // ---------------------------------------------------------------- counter-based randomness
 // Philox4x64-10 (Salmon, Moraes, Dror, Shaw, SC'11): ten rounds mapping a 256-bit
 // counter and a 128-bit key to 256 bits.  A round multiplies words 0 and 2 by two

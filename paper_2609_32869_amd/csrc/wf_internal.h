@@ -27,7 +27,8 @@ struct Layout {
   size_t state, page_table, rope, status, aux, weights, xkv, skv, hkv;
   size_t a_d16, a_d32, a_f16, a_tap16, h, qkv, hp, kvh, hv, hi, tok, g, gmax, draft, lasth, logits, dlogits, part;
   size_t hm, hs, tmax, tsum, dmax, dsum, sst, spart;  // sampling: normalisers and draw partials
-  size_t xpart;  // chunked cross-attention: partial records
+  size_t xpart;   // chunked cross-attention: partial records
+  size_t stamps;  // launch timing slots (profiling)
   size_t total;
   // element offsets inside the weight region
   size_t tok_emb, pos_emb, lnf_g, lnf_b, hproj_w, hproj_b, mask, dlnf_g, dlnf_b;
@@ -45,16 +46,23 @@ struct Handle;
 struct GraphKey {
   int slot0, n, k_max;
   const void *ovr, *out, *nout, *nacc, *done;
+  bool prof;  // captured with event records around every launch
   bool operator<(const GraphKey& o) const {
-    return std::tie(slot0, n, k_max, ovr, out, nout, nacc, done) <
-           std::tie(o.slot0, o.n, o.k_max, o.ovr, o.out, o.nout, o.nacc, o.done);
+    return std::tie(slot0, n, k_max, ovr, out, nout, nacc, done, prof) <
+           std::tie(o.slot0, o.n, o.k_max, o.ovr, o.out, o.nout, o.nacc, o.done, o.prof);
   }
 };
 
 struct ProfRec {
   const char* tag;
   double bytes;
-  hipEvent_t a, b;
+  int slot;  // timing slot in the stamp buffer
+};
+struct ProfAgg {
+  double ms = 0;       // end of the previous launch's last wave to the end of this one's
+  double exec_ms = 0;  // first-wave start to last-wave end
+  double bytes = 0;
+  long n = 0;
 };
 
 struct Handle {
@@ -70,10 +78,14 @@ struct Handle {
   std::string err;
   std::vector<int> live;  // host mirror: slot prefilled
   std::map<GraphKey, hipGraphExec_t> graphs;
-  bool prof = false;       // record events around eager launches
-  bool capturing = false;  // inside graph capture: never record events
-  std::vector<ProfRec> prof_recs;
-  std::vector<hipEvent_t> ev_pool;
+  bool prof = false;       // time launches (eager calls and profiled graph replays)
+  bool capturing = false;  // inside graph capture
+  int nstamp = 0;          // timing slots handed out in the current call or capture
+  std::vector<ProfRec> prof_recs;                        // launches of the current eager call
+  std::vector<ProfRec> cap_recs;                         // launches of the graph being captured
+  std::map<GraphKey, std::vector<ProfRec>> graph_recs;  // launches of each profiled graph
+  std::map<std::string, ProfAgg> prof_acc;              // durations per launch class
+  double wall_khz = 0;                                   // device wall-clock rate
 
   template <typename T>
   T* at(size_t off) const { return reinterpret_cast<T*>(ws + off); }

@@ -25,6 +25,9 @@ struct Operand {
   int mt;    // row tiles held by the buffer (fragment orders)
 };
 
+// Reset n launch timing slots (start = max, end = 0).
+void stamp_init(unsigned long long* s, int n, hipStream_t st);
+
 // Weight orders: row-major [N][K] or bf16 fragment order (16- or 32-column tiles).
 enum { W_ROW = 0, W_F16 = 1, W_F32 = 2 };
 
@@ -69,6 +72,7 @@ struct GemvArgs {
   uint64_t seed;
   float* hm;
   float* hs;
+  unsigned long long* stamp;  // launch timing slot (profiled calls), or null
 };
 
 struct AttnArgs {
@@ -81,6 +85,7 @@ struct AttnArgs {
   const float* rope;  // [pos][32][cos, sin]
   Operand out;        // operand rows of the following product
   int slot0, d, n_head, n_ctx, pages_per_slot, nsplit, R9;
+  unsigned long long* stamp;  // launch timing slot (profiled calls), or null
 };
 
 struct CrossArgs {
@@ -91,6 +96,7 @@ struct CrossArgs {
   int slot0, d, n_head, n_frames, nsplit, R9;
   int nchunk, chunk;  // frame chunks per (head, slot) and frames per chunk (multiple of 8)
   float* part;        // [pair][nchunk][kXrPart] chunk partials (nchunk > 1)
+  unsigned long long* stamp;  // launch timing slot (profiled calls), or null
 };
 // Chunk partial record: max [9] at 0, sum [9] at 16, acc [9][64] at 32.
 constexpr int kXrPart = 32 + kRows * 64;
@@ -118,6 +124,7 @@ struct LnArgs {
   const void* b;
   Operand out;
   int d, row0, nsplit, R9;
+  unsigned long long* stamp;  // launch timing slot (profiled calls), or null
 };
 
 // h[row] += sum_s part[s][row] + bias; optional tap operand of the new h; then,
@@ -134,6 +141,7 @@ struct RlnArgs {
   const void* b;
   Operand out;
   int d, row0, nsplit, R9;
+  unsigned long long* stamp;  // launch timing slot (profiled calls), or null
 };
 
 struct BeginArgs {
