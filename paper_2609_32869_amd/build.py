@@ -1,5 +1,6 @@
 """Build libwf.so (HIP kernels + C ABI) for gfx950 in-tree with hipcc."""
 import os
+import re
 import subprocess
 import sys
 
@@ -11,11 +12,40 @@ SOURCES = ["k_gemv.hip", "k_attn.hip", "k_misc.hip", "wf_api.hip"]
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",
          # packed fp32 arithmetic is kept out of every kernel
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-         "-Wno-unused-result"]
+         "-Wno-unused-result",
+         # per-kernel register / scratch report, checked below
+         "-Rpass-analysis=kernel-resource-usage"]
 
 
 def _filter(text):
-    return "\n".join(l for l in text.splitlines() if "packed-fp32-ops" not in l)
+    """Drop the packed-fp32 feature notes and the resource-usage remarks (each
+    followed by its source excerpt)."""
+    keep, in_remark = [], False
+    for line in text.splitlines():
+        if "packed-fp32-ops" in line:
+            continue
+        if "kernel-resource-usage" in line:
+            in_remark = True
+            continue
+        if in_remark and re.match(r"^\s*(\d+\s*)?\|", line):
+            continue
+        in_remark = False
+        keep.append(line)
+    return "\n".join(keep)
+
+
+def _scratch_kernels(text):
+    """Kernels whose registers spill to scratch memory: a launch of such a kernel
+    pays for per-dispatch scratch set-up, so none is allowed."""
+    bad, name = [], None
+    for line in text.splitlines():
+        m = re.search(r"Function Name: (\S+)", line)
+        if m:
+            name = m.group(1)
+        m = re.search(r"ScratchSize \[bytes/lane\]: (\d+)", line)
+        if m and int(m.group(1)) > 0:
+            bad.append(f"{name} ({m.group(1)} bytes/lane)")
+    return bad
 
 
 def build(verbose=False):
@@ -30,10 +60,15 @@ def build(verbose=False):
         procs.append((s, subprocess.Popen(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True)))
     errors, notes = [], []
     for s, p in procs:
-        out = _filter(p.communicate()[0])
+        raw = p.communicate()[0]
+        out = _filter(raw)
         if p.returncode != 0:
             errors.append(f"{s}: hipcc failed ({p.returncode}):\n{out}")
-        elif out.strip():
+            continue
+        spills = _scratch_kernels(raw)
+        if spills:
+            errors.append(f"{s}: kernels spill registers to scratch: " + ", ".join(spills))
+        if out.strip():
             notes.append(f"{s}:\n{out}")
     if errors:
         raise RuntimeError("\n".join(errors))

@@ -22,32 +22,106 @@ namespace wf {
 constexpr int kU = 10;  // k-steps whose loads a wave issues together (16-wave blocks: 5)
 
 // ---------------------------------------------------------------- epilogue
-// Bias and residual values of the batch-1 tile (9 rows x TC columns), loaded at
-// kernel start so the epilogue does not wait on a global read.  Element it of a
-// thread is tile entry threadIdx.x + it * NT, as in the epilogue loop.
+// Everything the batch-1 epilogue reads from memory for its tile (9 rows x TC
+// columns), loaded at kernel start so the epilogue does not wait on a global
+// read.  Element it of a thread is tile entry threadIdx.x + it * NT, as in the
+// epilogue loop.  The loads are unconditional (indexes clamped into the buffers,
+// unused values discarded) so no load waits for another.
 template <int TC, int NT>
 struct EpiPre {
   static constexpr int P = (kRows * TC + NT - 1) / NT;
-  float b[P], r[P];
+  uint32_t bb[P];    // bf16 bias bits (converted when used, so nothing waits here)
+  float r[P];
+  uint8_t sup[P];    // ARGMAX: suppressed
+  int s0, s1, s2, s3;  // QKV: valid rows, first position, its page, the next page; ARGMAX: step
 
   template <typename S, int EPI>
   __device__ __forceinline__ void load(const GemvArgs& a, int nb) {
     if (a.nsplit != 3) return;
-    const S* bias = reinterpret_cast<const S*>(a.bias);
+    const bool has_bias = a.bias != nullptr;  // without one, read the weights and discard
+    const uint16_t* bias = reinterpret_cast<const uint16_t*>(has_bias ? a.bias : a.w);
+    const int* st = a.state != nullptr ? a.state + a.slot0 * kStateInts : reinterpret_cast<const int*>(a.w);
 #pragma unroll
     for (int it = 0; it < P; ++it) {
-      const int idx = threadIdx.x + it * NT, ml = idx / TC, n = nb + idx % TC;
-      const bool in = idx < kRows * TC && n < a.N;
-      b[it] = (in && bias != nullptr) ? to_f(bias[n]) : 0.f;
-      if constexpr (EPI == EPI_RESID) r[it] = in ? a.y[(size_t)(a.slot0 * kRows + ml) * a.ldy + n] : 0.f;
+      const int idx = threadIdx.x + it * NT, ml = min(idx / TC, kRows - 1), n = min(nb + idx % TC, a.N - 1);
+      bb[it] = bias[n];
+      r[it] = EPI == EPI_RESID ? a.y[(size_t)(a.slot0 * kRows + ml) * a.ldy + n] : 0.f;
+      if constexpr (EPI == EPI_ARGMAX) {
+        const uint8_t* sp = a.suppress != nullptr ? a.suppress : reinterpret_cast<const uint8_t*>(a.w);
+        sup[it] = sp[n];
+      }
+    }
+    if constexpr (EPI == EPI_QKV) {
+      s0 = st[ST_NV];
+      s1 = st[ST_POS0];
+      s2 = st[ST_PG0];
+      s3 = st[ST_PG1];
+    } else if constexpr (EPI == EPI_ARGMAX) {
+      s0 = st[a.state != nullptr ? ST_STEP : 0];
+    }
+  }
+  __device__ __forceinline__ float bias(const GemvArgs& a, int it) const {
+    return a.bias != nullptr ? __uint_as_float(bb[it] << 16) : 0.f;
+  }
+  // Called where the epilogue starts: an empty asm redefines every prefetched
+  // value here, so no arithmetic on them (and no wait for their loads) can be
+  // scheduled before the main loop.
+  __device__ __forceinline__ void arrive() {
+#pragma unroll
+    for (int it = 0; it < P; ++it) {
+      __asm__ volatile("" : "+v"(bb[it]));
+      __asm__ volatile("" : "+v"(r[it]));
+      uint32_t sp = sup[it];
+      __asm__ volatile("" : "+v"(sp));
+      sup[it] = (uint8_t)sp;
+    }
+    __asm__ volatile("" : "+v"(s0), "+v"(s1), "+v"(s2), "+v"(s3));
+  }
+};
+
+// Appends the k or v value v of column n (>= d) at cache page `page`, position pos.
+template <typename S>
+__device__ __forceinline__ void qkv_append(const GemvArgs& a, int n, float v, int page, int pos) {
+  const int d = a.d, kv = n >= 2 * d;
+  const int cc = n - d - kv * d, head = cc >> 6, dim = cc & 63;
+  S* cache = reinterpret_cast<S*>(a.cache) + (size_t)kv * a.kv_stride;
+  cache[(((size_t)page * a.n_head + head) * kPage + (pos & 15)) * kHeadDim + dim] = from_f<S>(v);
+}
+
+// Bias and residual values of a multi-slot tile (TM rows x TC columns), loaded at
+// kernel start like EpiPre so the epilogue starts without a global read.
+template <int TM, int TC, int NT>
+struct RowsPre {
+  static constexpr int P = (TM * TC + NT - 1) / NT;
+  uint32_t bb[P];  // bf16 bias bits
+  float r[P];
+
+  template <typename S, int EPI>
+  __device__ __forceinline__ void load(const GemvArgs& a, int m0, int nb) {
+    const bool has_bias = a.bias != nullptr;  // without one, read the weights and discard
+    const uint16_t* bias = reinterpret_cast<const uint16_t*>(has_bias ? a.bias : a.w);
+#pragma unroll
+    for (int it = 0; it < P; ++it) {
+      const int idx = threadIdx.x + it * NT;
+      const int row = min(m0 + idx / TC, a.R9 - 1), n = min(nb + idx % TC, a.N - 1);
+      bb[it] = bias[n];
+      r[it] = EPI == EPI_RESID ? a.y[(size_t)row * a.ldy + n] : 0.f;
+    }
+  }
+  __device__ __forceinline__ void arrive() {
+#pragma unroll
+    for (int it = 0; it < P; ++it) {
+      __asm__ volatile("" : "+v"(bb[it]));
+      __asm__ volatile("" : "+v"(r[it]));
     }
   }
 };
 
-// Output value v of (row, column n); res = current residual value (EPI_RESID).
+// Output value v of (row, column n) for the store, GELU, residual and partial-sum
+// epilogues; res = current residual value (EPI_RESID).  The k/v append and the
+// head scores are written by the epilogue loops from prefetched values.
 template <typename S, int EPI>
 __device__ __forceinline__ void epi_one(const GemvArgs& a, int row, int n, float v, float res) {
-  const int slot = row / kRows, r = row - slot * kRows;
   if constexpr (EPI == EPI_STORE) {
     a.y[(size_t)row * a.ldy + n] = v;
   } else if constexpr (EPI == EPI_GELU) {
@@ -56,35 +130,16 @@ __device__ __forceinline__ void epi_one(const GemvArgs& a, int row, int n, float
     const float hn = res + v;
     a.y[(size_t)row * a.ldy + n] = hn;
     if (a.tap >= 0) put_op<S>(a.aout, a.nsplit, a.R9, row, a.tap * a.N + n, hn);
-  } else if constexpr (EPI == EPI_QKV) {
-    const int d = a.d;
-    if (n < d) {
-      a.y[(size_t)row * a.ldy + n] = v;
-    } else {
-      const int* st = a.state + slot * kStateInts;
-      const int nv = st[ST_NV], pos = st[ST_POS0] + r;
-      if (r < nv && pos < a.n_ctx) {
-        const int kv = n >= 2 * d;
-        const int cc = n - d - kv * d, head = cc >> 6, dim = cc & 63;
-        const int page = a.page_table[slot * a.pages_per_slot + (pos >> 4)];
-        S* cache = reinterpret_cast<S*>(a.cache) + (size_t)kv * a.kv_stride;
-        cache[(((size_t)page * a.n_head + head) * kPage + (pos & 15)) * kHeadDim + dim] = from_f<S>(v);
-      }
-    }
-  } else if constexpr (EPI == EPI_ARGMAX) {
-    if (a.y != nullptr) a.y[(size_t)row * a.ldy + n] = v;  // suppressed columns hold -inf
   } else if constexpr (EPI == EPI_PART) {
     a.y[blockIdx.y * a.pstride + (size_t)row * a.ldy + n] = v;
   }
 }
 
-// Vocabulary head: a suppressed column's logit is -inf.
-__device__ __forceinline__ float head_logit(const GemvArgs& a, int n, float v) {
-  return (a.suppress != nullptr && n < a.N && a.suppress[n]) ? -INFINITY : v;
-}
 // Head score of (row, column n): the logit (greedy), or z = logit * inv_t plus the
 // row's Gumbel noise when sampling; oz receives z for the softmax normaliser.
-__device__ __forceinline__ void head_score(const GemvArgs& a, int row, int n, bool act, float v, float* ov, float* oz) {
+// step: the slot's step counter (read only when drawing noise; -1: read it here).
+__device__ __forceinline__ void head_score(const GemvArgs& a, int row, int n, bool act, float v, float* ov, float* oz,
+                                           int step = -1) {
   if (!act) {
     *ov = -INFINITY;
     *oz = -INFINITY;
@@ -95,7 +150,7 @@ __device__ __forceinline__ void head_score(const GemvArgs& a, int row, int n, bo
     *oz = z;
     if (a.rng_purpose != 0) {
       const int slot = row / kRows, pos = row - slot * kRows;
-      const int step = a.state[slot * kStateInts + ST_STEP];
+      if (step < 0) step = a.state[slot * kStateInts + ST_STEP];
       *ov = z + rng_gumbel(rng_word(a.seed, a.rng_purpose, slot, step, pos, n));
     } else {
       *ov = z;
@@ -108,13 +163,16 @@ __device__ __forceinline__ void head_score(const GemvArgs& a, int row, int n, bo
 
 // sv holds the wave-summed tile: TM operand rows (split terms) x TC columns; ov and
 // oz are the head's score and z buffers (EPI_ARGMAX).
-template <typename S, int EPI, int TM, int TC, int NT>
-__device__ void finish_tile(const GemvArgs& a, float (*sv)[TC + 1], float (*ov)[TC], float (*oz)[TC], int m0, int nb,
-                            const EpiPre<TC, NT>& pre) {
+// RP: rp holds the bias / residual of a multi-slot tile prefetched at kernel start
+// (bf16); otherwise the epilogue loads them.
+template <typename S, int EPI, int TM, int TC, int NT, bool RP = false>
+__device__ __forceinline__ void finish_tile(const GemvArgs& a, float (*sv)[TC + 1], float (*ov)[TC], float (*oz)[TC], int m0, int nb,
+                            EpiPre<TC, NT>& pre, RowsPre<TM, TC, NT>& rp) {
   const bool split3 = a.nsplit == 3;
   const int R = a.slot0 * kRows, Rend = (a.slot0 + a.nslots) * kRows;
   const int nrows = split3 ? kRows : TM;
   if (split3) {
+    pre.arrive();
     // rows r, r + 9, r + 18 hold the three split terms of row r
 #pragma unroll
     for (int it = 0; it < EpiPre<TC, NT>::P; ++it) {
@@ -122,21 +180,83 @@ __device__ void finish_tile(const GemvArgs& a, float (*sv)[TC + 1], float (*ov)[
       if (idx >= kRows * TC) break;
       const int ml = idx / TC, c = idx % TC, n = nb + c, row = R + ml;
       const bool act = n < a.N;
-      float v = ((sv[ml][c] + sv[ml + 9][c]) + sv[ml + 18][c]) + pre.b[it];
-      if constexpr (EPI == EPI_ARGMAX) v = head_logit(a, n, v);
-      if (act) epi_one<S, EPI>(a, row, n, v, pre.r[it]);
-      if constexpr (EPI == EPI_ARGMAX) head_score(a, row, n, act, v, &ov[ml][c], &oz[ml][c]);
+      float v = ((sv[ml][c] + sv[ml + 9][c]) + sv[ml + 18][c]) + pre.bias(a, it);
+      if constexpr (EPI == EPI_ARGMAX) {
+        if (a.suppress != nullptr && pre.sup[it]) v = -INFINITY;
+        head_score(a, row, n, act, v, &ov[ml][c], &oz[ml][c], pre.s0);
+        if (act && a.y != nullptr) a.y[(size_t)row * a.ldy + n] = v;
+      } else if constexpr (EPI == EPI_QKV) {
+        if (act) {
+          const int pos = pre.s1 + ml;
+          if (n < a.d) a.y[(size_t)row * a.ldy + n] = v;
+          else if (ml < pre.s0 && pos < a.n_ctx)
+            qkv_append<S>(a, n, v, ((pre.s1 & 15) + ml >= 16) ? pre.s3 : pre.s2, pos);
+        }
+      } else {
+        if (act) epi_one<S, EPI>(a, row, n, v, pre.r[it]);
+      }
     }
   } else {
-    const S* bias = reinterpret_cast<const S*>(a.bias);
-    for (int idx = threadIdx.x; idx < TM * TC; idx += NT) {
+    // Every global load of the epilogue is issued before any result is formed, and
+    // unconditionally (indexes clamped into the buffers, unused values discarded),
+    // so their latencies overlap instead of adding up element by element.
+    constexpr int P = (TM * TC + NT - 1) / NT;
+    if constexpr (RP) rp.arrive();
+    const bool has_bias = a.bias != nullptr;  // without one, read the weights and discard
+    const S* bias = reinterpret_cast<const S*>(has_bias ? a.bias : a.w);
+    const int rmax = a.R9 - 1, nmax = a.N - 1;
+    float bv[P], rv[P];
+    int iv[P], pv[P];  // QKV: cache page (-1: no append) and position; ARGMAX: step, suppressed
+#pragma unroll
+    for (int it = 0; it < P; ++it) {
+      const int idx = threadIdx.x + it * NT;
+      const int ml = idx / TC, c = idx % TC, row = min(m0 + ml, rmax), n = min(nb + c, nmax);
+      if constexpr (RP) {
+        bv[it] = has_bias ? __uint_as_float(rp.bb[it] << 16) : 0.f;
+        rv[it] = rp.r[it];
+      } else {
+        const float bb = to_f(bias[n]);
+        bv[it] = has_bias ? bb : 0.f;
+        rv[it] = EPI == EPI_RESID ? a.y[(size_t)row * a.ldy + n] : 0.f;
+      }
+      iv[it] = -1;
+      pv[it] = 0;
+      if constexpr (EPI == EPI_QKV) {
+        const int* st = a.state + (row / kRows) * kStateInts;
+        const int r = row - (row / kRows) * kRows, nv = st[ST_NV], pos0 = st[ST_POS0];
+        const int pg0 = st[ST_PG0], pg1 = st[ST_PG1];
+        iv[it] = r < nv ? ((pos0 & 15) + r >= 16 ? pg1 : pg0) : -1;
+        pv[it] = pos0 + r;
+      } else if constexpr (EPI == EPI_ARGMAX) {
+        // absent state / suppression: read the weights instead and discard
+        const int* stp = a.state != nullptr ? a.state : reinterpret_cast<const int*>(a.w);
+        const uint8_t* sup = a.suppress != nullptr ? a.suppress : reinterpret_cast<const uint8_t*>(a.w);
+        const int step = stp[a.state != nullptr ? (row / kRows) * kStateInts + ST_STEP : 0];
+        const int supv = sup[n];
+        iv[it] = a.inv_t > 0.f && a.rng_purpose != 0 ? step : -1;
+        pv[it] = a.suppress != nullptr ? supv : 0;
+      }
+    }
+#pragma unroll
+    for (int it = 0; it < P; ++it) {
+      const int idx = threadIdx.x + it * NT;
       const int ml = idx / TC, c = idx % TC, row = m0 + ml, n = nb + c;
-      const bool act = row >= R && row < Rend && n < a.N;
-      float v = sv[ml][c];
-      if (act && bias != nullptr) v += to_f(bias[n]);
-      if constexpr (EPI == EPI_ARGMAX) v = head_logit(a, n, v);
-      if (act) epi_one<S, EPI>(a, row, n, v, EPI == EPI_RESID ? a.y[(size_t)row * a.ldy + n] : 0.f);
-      if constexpr (EPI == EPI_ARGMAX) head_score(a, row, n, act, v, &ov[ml][c], &oz[ml][c]);
+      const bool act = idx < TM * TC && row >= R && row < Rend && n < a.N;
+      if (idx >= TM * TC) break;
+      float v = sv[ml][c] + bv[it];
+      if constexpr (EPI == EPI_ARGMAX) {
+        if (pv[it]) v = -INFINITY;
+        head_score(a, row, n, act, v, &ov[ml][c], &oz[ml][c], iv[it]);
+        if (act && a.y != nullptr) a.y[(size_t)row * a.ldy + n] = v;
+      } else if constexpr (EPI == EPI_QKV) {
+        if (act) {
+          const int d = a.d;
+          if (n < d) a.y[(size_t)row * a.ldy + n] = v;
+          else if (iv[it] >= 0 && pv[it] < a.n_ctx) qkv_append<S>(a, n, v, iv[it], pv[it]);
+        }
+      } else {
+        if (act) epi_one<S, EPI>(a, row, n, v, rv[it]);
+      }
     }
   }
   if constexpr (EPI == EPI_ARGMAX) {
@@ -219,7 +339,10 @@ __global__ void __launch_bounds__(NW * 64) k_gemv16(GemvArgs a) {
       sv[ml][c] = s;
     }
     __syncthreads();
-    finish_tile<bf16, EPI, 32, 16, NW * 64>(a, sv, ov, oz, tile0 * 16, blockIdx.x * 16, pre);
+    {
+      RowsPre<32, 16, NW * 64> none;
+      finish_tile<bf16, EPI, 32, 16, NW * 64>(a, sv, ov, oz, tile0 * 16, blockIdx.x * 16, pre, none);
+    }
     if (a.nsplit == 3) break;
   }
 }
@@ -297,7 +420,10 @@ __global__ void __launch_bounds__(NW * 64) k_gemv16w(GemvArgs a) {
       sv[ml][c] = s;
     }
     __syncthreads();
-    finish_tile<bf16, EPI, 32, TC, NW * 64>(a, sv, ov, oz, tile0 * 16, blockIdx.x * TC, pre);
+    {
+      RowsPre<32, TC, NW * 64> none;
+      finish_tile<bf16, EPI, 32, TC, NW * 64>(a, sv, ov, oz, tile0 * 16, blockIdx.x * TC, pre, none);
+    }
     if (a.nsplit == 3) break;
   }
 }
@@ -306,10 +432,12 @@ __global__ void __launch_bounds__(NW * 64) k_gemv16w(GemvArgs a) {
 // The rows of several slots (nine each) times W^T over 64 x 64 block tiles: each of
 // the four waves computes a 32 x 32 sub-tile (2 x 2 fragments of
 // v_mfma_f32_16x16x32_bf16), loading operand and weight fragments straight from
-// their fragment orders (1 KB per wave load), kGemmU k-steps of loads in flight.
-// Block b runs on XCD b % 8; the row blocks of one column block are numbered so
-// they share an XCD and its L2 serves them the weight tile.
-constexpr int kGemmU = 4;
+// their fragment orders (1 KB per wave load).  Loads are double-buffered: the
+// fragments of the next kGemmU k-steps are in flight while the current ones
+// multiply.  Grid y splits the k-steps (EPI_PART stores each split's partial
+// sums).  Block b runs on XCD b % 8; the row blocks of one column block are
+// numbered so they share an XCD and its L2 serves them the weight tile.
+constexpr int kGemmU = 2;
 template <int EPI>
 __global__ void __launch_bounds__(256) k_gemm16(GemvArgs a, int mb0, int nmb, int nnb) {
   StampScope stamp_scope(a.stamp);
@@ -322,35 +450,50 @@ __global__ void __launch_bounds__(256) k_gemm16(GemvArgs a, int mb0, int nmb, in
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
   const int wm = wv >> 1, wn = wv & 1;
   const int KS = a.K / 32, MT = a.a.mt, ntile = (a.N + 15) / 16;
+  const int kper = KS / gridDim.y, ks0 = blockIdx.y * kper, ks1 = ks0 + kper;
   const int mt0 = (mb0 + mbk) * 4 + wm * 2, nt0 = nbk * 4 + wn * 2;  // 16-row / 16-column tiles
+  RowsPre<64, 64, 256> rp;
+  rp.template load<bf16, EPI>(a, (mb0 + mbk) * 64, nbk * 64);
   const bf16x8* Ab = reinterpret_cast<const bf16x8*>(a.a.p) + lane;
   const bf16x8* Wb = reinterpret_cast<const bf16x8*>(a.w) + lane;
-  const bool mv0 = mt0 < MT, mv1 = mt0 + 1 < MT, nv0 = nt0 < ntile, nv1 = nt0 + 1 < ntile;
-  const bf16x8 zero = __builtin_bit_cast(bf16x8, make_uint4(0u, 0u, 0u, 0u));
+  // Tiles past the operand's rows or the matrix's columns re-read the last one:
+  // their products only reach output rows / columns the epilogue skips, and the
+  // loads stay unconditional, so the compiler can wait for one buffer at a time.
+  const int ma0 = min(mt0, MT - 1), ma1 = min(mt0 + 1, MT - 1);
+  const int na0 = min(nt0, ntile - 1), na1 = min(nt0 + 1, ntile - 1);
   floatx4 acc[2][2];
 #pragma unroll
   for (int p = 0; p < 2; ++p)
 #pragma unroll
     for (int q = 0; q < 2; ++q) acc[p][q] = floatx4{0.f, 0.f, 0.f, 0.f};
-  for (int st = 0; st < KS; st += kGemmU) {
-    bf16x8 af[kGemmU][2], wf[kGemmU][2];
+  bf16x8 af[2][kGemmU][2], wf[2][kGemmU][2];
+  auto load = [&](int b, int st) {  // k-steps st.. (past the range: re-read the last one)
 #pragma unroll
     for (int u = 0; u < kGemmU; ++u) {
-      const int ss = min(st + u, KS - 1);
-      af[u][0] = mv0 ? Ab[((size_t)ss * MT + mt0) * 64] : zero;
-      af[u][1] = mv1 ? Ab[((size_t)ss * MT + mt0 + 1) * 64] : zero;
-      wf[u][0] = nv0 ? Wb[((size_t)nt0 * KS + ss) * 64] : zero;
-      wf[u][1] = nv1 ? Wb[((size_t)(nt0 + 1) * KS + ss) * 64] : zero;
+      const int ss = min(st + u, ks1 - 1);
+      af[b][u][0] = Ab[((size_t)ss * MT + ma0) * 64];
+      af[b][u][1] = Ab[((size_t)ss * MT + ma1) * 64];
+      wf[b][u][0] = Wb[((size_t)na0 * KS + ss) * 64];
+      wf[b][u][1] = Wb[((size_t)na1 * KS + ss) * 64];
     }
+  };
+  auto mul = [&](int b, int st) {
 #pragma unroll
     for (int u = 0; u < kGemmU; ++u)
-      if (st + u < KS) {
+      if (st + u < ks1) {
 #pragma unroll
         for (int p = 0; p < 2; ++p)
 #pragma unroll
           for (int q = 0; q < 2; ++q)
-            acc[p][q] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[u][p], wf[u][q], acc[p][q], 0, 0, 0);
+            acc[p][q] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[b][u][p], wf[b][u][q], acc[p][q], 0, 0, 0);
       }
+  };
+  load(0, ks0);
+  for (int st = ks0; st < ks1; st += 2 * kGemmU) {
+    load(1, st + kGemmU);
+    mul(0, st);
+    load(0, st + 2 * kGemmU);
+    mul(1, st + kGemmU);
   }
   // result fragment: lane l holds column l % 16, rows 4 (l / 16) + v
 #pragma unroll
@@ -362,7 +505,7 @@ __global__ void __launch_bounds__(256) k_gemm16(GemvArgs a, int mb0, int nmb, in
         sv[wm * 32 + p * 16 + 4 * (lane >> 4) + v][wn * 32 + q * 16 + (lane & 15)] = acc[p][q][v];
   __syncthreads();
   EpiPre<64, 256> pre;  // batch-1 prefetch, unused here
-  finish_tile<bf16, EPI, 64, 64, 256>(a, sv, ov, oz, (mb0 + mbk) * 64, nbk * 64, pre);
+  finish_tile<bf16, EPI, 64, 64, 256, true>(a, sv, ov, oz, (mb0 + mbk) * 64, nbk * 64, pre, rp);
 }
 
 // ---------------------------------------------------------------- bf16, 32-column tiles
@@ -412,7 +555,10 @@ __global__ void __launch_bounds__(NW * 64) k_gemv32(GemvArgs a) {
       sv[ml][c] = s;
     }
     __syncthreads();
-    finish_tile<bf16, EPI, 32, 32, NW * 64>(a, sv, ov, oz, tile0 * 32, blockIdx.x * 32, pre);
+    {
+      RowsPre<32, 32, NW * 64> none;
+      finish_tile<bf16, EPI, 32, 32, NW * 64>(a, sv, ov, oz, tile0 * 32, blockIdx.x * 32, pre, none);
+    }
     if (a.nsplit == 3) break;
   }
 }
@@ -578,7 +724,10 @@ __global__ void __launch_bounds__(NW * 64) k_gemv16_ln(GemvArgs a) {
     sv[ml][c] = s;
   }
   __syncthreads();
-  finish_tile<bf16, EPI, 32, 16, NW * 64>(a, sv, ov, oz, 0, blockIdx.x * 16, pre);
+  {
+      RowsPre<32, 16, NW * 64> none;
+      finish_tile<bf16, EPI, 32, 16, NW * 64>(a, sv, ov, oz, 0, blockIdx.x * 16, pre, none);
+    }
 }
 
 // 32-column tiles; every wave's k-steps fit one batch of loads (K <= kLnFoldMaxK).
@@ -625,7 +774,10 @@ __global__ void __launch_bounds__(NW * 64) k_gemv32_ln(GemvArgs a) {
     sv[ml][c] = s;
   }
   __syncthreads();
-  finish_tile<bf16, EPI, 32, 32, NW * 64>(a, sv, ov, oz, 0, blockIdx.x * 32, pre);
+  {
+      RowsPre<32, 32, NW * 64> none;
+      finish_tile<bf16, EPI, 32, 32, NW * 64>(a, sv, ov, oz, 0, blockIdx.x * 32, pre, none);
+    }
 }
 
 // ---------------------------------------------------------------- fp32, row-major
@@ -695,7 +847,10 @@ __global__ void __launch_bounds__(NW * 64) k_gemv_f32(GemvArgs a) {
       sv[ml][c] = s;
     }
     __syncthreads();
-    finish_tile<float, EPI, 32, 16, NW * 64>(a, sv, ov, oz, tile0 * 16, nb, pre);
+    {
+      RowsPre<32, 16, NW * 64> none;
+      finish_tile<float, EPI, 32, 16, NW * 64>(a, sv, ov, oz, tile0 * 16, nb, pre, none);
+    }
   }
 }
 
@@ -758,17 +913,17 @@ static void launch_epi(const GemvArgs& a, hipStream_t st) {
       launch_ln<EPI>(a, st);
       return;
     }
-    if constexpr (EPI == EPI_PART) {  // 64-column blocks, k split over grid y
-      const int ntile = (a.N + 15) / 16;
-      k_gemv16w<EPI, 8, 4><<<dim3((ntile + 3) / 4, a.ksplit > 1 ? a.ksplit : 1), 512, 0, st>>>(a);
+    const int ks = a.ksplit > 1 ? a.ksplit : 1;
+    if (a.nsplit == 1 && a.wkind == W_F16) {  // several slots: 64 x 64 GEMM tiles (k split over grid y)
+      const int mb0 = a.slot0 * kRows / 64, mb1 = ((a.slot0 + a.nslots) * kRows + 63) / 64;
+      const int nmb = mb1 - mb0, nnb = (a.N + 63) / 64;
+      k_gemm16<EPI><<<dim3((unsigned)(8 * ((nnb + 7) / 8) * nmb), ks), 256, 0, st>>>(a, mb0, nmb, nnb);
       return;
-    } else {
-      if (a.nsplit == 1 && a.wkind == W_F16) {  // several slots: 64 x 64 GEMM tiles
-        const int mb0 = a.slot0 * kRows / 64, mb1 = ((a.slot0 + a.nslots) * kRows + 63) / 64;
-        const int nmb = mb1 - mb0, nnb = (a.N + 63) / 64;
-        k_gemm16<EPI><<<(unsigned)(8 * ((nnb + 7) / 8) * nmb), 256, 0, st>>>(a, mb0, nmb, nnb);
-        return;
-      }
+    }
+    if constexpr (EPI == EPI_PART) {  // batch 1: 64-column blocks, k split over grid y
+      const int ntile = (a.N + 15) / 16;
+      k_gemv16w<EPI, 8, 4><<<dim3((ntile + 3) / 4, ks), 512, 0, st>>>(a);
+      return;
     }
   }
   // waves per block: enough that each wave's share of the k-steps fits one batch
@@ -776,8 +931,8 @@ static void launch_epi(const GemvArgs& a, hipStream_t st) {
   const int steps = a.K / kstep;
   if constexpr (sizeof(S) == 4) {
     if (steps <= 4 * kU) launch_f32<EPI, 4>(a, st);
-    else if (steps <= 8 * kU) launch_f32<EPI, 8>(a, st);
-    else launch_f32<EPI, 16>(a, st);
+    else if (steps <= 8 * kU || EPI == EPI_ARGMAX) launch_f32<EPI, 8>(a, st);  // the head's epilogue needs > 128 VGPRs
+    else launch_f32<EPI, EPI == EPI_ARGMAX ? 8 : 16>(a, st);
   } else {
     if (steps <= 4 * kU) launch_bf16<EPI, 4>(a, st);
     else if (steps <= 8 * kU) launch_bf16<EPI, 8>(a, st);

@@ -197,6 +197,14 @@ __device__ __forceinline__ void fill_rows(const BeginArgs& a, int slot, const in
   }
 }
 
+// Pages of the nine rows of a pass starting at pos0 (they span at most two).
+__device__ __forceinline__ void set_pass_pages(const BeginArgs& a, int slot, int* st, int pos0) {
+  const int* pt = a.page_table + slot * a.pages_per_slot;
+  const int p = min(max(pos0, 0) >> 4, a.pages_per_slot - 1);
+  st[ST_PG0] = pt[p];
+  st[ST_PG1] = pt[min(p + 1, a.pages_per_slot - 1)];
+}
+
 // Verify rows: [anchor, c_1..c_k] at positions L..L+k with the budget rule
 // k = min(K, k_max, max_new - emitted - 1, n_ctx - L - 1) (Appendix A.1).
 template <typename S>
@@ -218,6 +226,7 @@ __global__ void __launch_bounds__(256) k_verify_begin(BeginArgs a) {
   if (threadIdx.x == 0) {
     st[ST_POS0] = L;
     st[ST_NV] = nv;
+    set_pass_pages(a, slot, st, L);
   }
   __syncthreads();
   fill_rows<S>(a, slot, toks, poss, false);
@@ -258,6 +267,7 @@ __global__ void __launch_bounds__(256) k_prefill_begin(BeginArgs a) {
     st[ST_NV] = nv;
     st[ST_HPOS] = pos0;
     st[ST_HN] = nv;
+    set_pass_pages(a, slot, st, pos0);
   }
   __syncthreads();
   fill_rows<S>(a, slot, toks, poss, false);

@@ -210,7 +210,8 @@ int compute_layout(const wf_config& c, Layout& L) {
     const int tiles64 = (int)((d + 63) / 64), ksteps = (int)(F / 32);
     L.fc2_split = std::max(1, std::min({kRlnMaxPartsHost, 240 / tiles64, ksteps}));
   }
-  L.part = region((size_t)std::max(L.fc2_split, 1) * R9 * d * 4);
+  const int nparts = std::max({L.fc2_split, c.dtype == WF_BF16 && L.nsplit_op == 1 ? kFc2SplitBatch : 0, 1});
+  L.part = region((size_t)nparts * R9 * d * 4);
   L.xpart = region((size_t)kXrMaxPartials * kXrPart * 4);
   L.stamps = region((size_t)kStampSlots * kStampWords * 8);
   L.total = o;
@@ -399,6 +400,17 @@ struct Runner {
     });
   }
 
+  // Several slots with bf16 operands: when the 64 x 64 tiles of the second MLP
+  // product cover too few blocks to fill the chip, split its k-steps in
+  // kFc2SplitBatch (partial sums reduced with the residual update and the next
+  // LayerNorm), else 0.
+  int fc2_split_batch(int slot0, int n) const {
+    if (!frag() || L.nsplit_op != 1) return 0;
+    const int mb0 = slot0 * kRows / 64, mb1 = ((slot0 + n) * kRows + 63) / 64;
+    const int tiles = (mb1 - mb0) * ((c.d_model + 63) / 64);
+    return tiles < 160 && (c.d_ff / 32) % kFc2SplitBatch == 0 ? kFc2SplitBatch : 0;
+  }
+
   // second half of a decoder block shared by target and drafter: cross-attention and MLP
   void block_tail(int slot0, int n, const BlockW& b, int xlayer, int tap, const LnNext& nx) {
     const int d = c.d_model;
@@ -408,19 +420,20 @@ struct Runner {
     gemv("gemv_o", EPI_RESID, slot0, n, Ad16(), b.w_o2, b.b_o2, d, d, h_, d);
     gemv_ln("gemv_fc1", EPI_GELU, slot0, n, h_, b.ln3_g, b.ln3_b, Ad32(), b.w_fc1, b.b_fc1, d, c.d_ff, nullptr, 0,
             Af16());
-    if (L.fc2_split > 0) {
+    const int ksplit = L.fc2_split > 0 ? L.fc2_split : fc2_split_batch(slot0, n);
+    if (ksplit > 0) {
       // k-split partial sums, then h += sum + bias, the tap, and the next LayerNorm
       GemvArgs a = gemv_args(slot0, n, Af16(), b.w_fc2, b.b_fc2, c.d_ff, d, F32(L.part), d, Operand{nullptr, 0, OP_ROW, 0}, -1);
       a.bias = nullptr;
       a.ct = 4;
-      a.ksplit = L.fc2_split;
+      a.ksplit = ksplit;
       a.pstride = (size_t)R9() * d;
       run_gemv("gemv_fc2", EPI_PART, n, a);
       RlnArgs ra{};
-      ra.part = F32(L.part); ra.nparts = L.fc2_split; ra.pstride = (size_t)R9() * d; ra.bias = W(b.b_fc2); ra.h = h_;
+      ra.part = F32(L.part); ra.nparts = ksplit; ra.pstride = (size_t)R9() * d; ra.bias = W(b.b_fc2); ra.h = h_;
       ra.tap = Atap16(); ra.tapcol = tap >= 0 ? tap * d : -1; ra.g = W(nx.g); ra.b = W(nx.b); ra.out = nx.wide ? Ad32() : Ad16();
       ra.d = d; ra.row0 = slot0 * kRows; ra.nsplit = L.nsplit_op; ra.R9 = R9();
-      launch("reduce_ln", 4.0 * kRows * n * d * (L.fc2_split + 3), [&](unsigned long long* sp) {
+      launch("reduce_ln", 4.0 * kRows * n * d * (ksplit + 3), [&](unsigned long long* sp) {
         ra.stamp = sp;
         Ops<S>::reduce_ln(ra, n * kRows, st);
       });
@@ -547,6 +560,7 @@ struct Runner {
     ba.state = I32(L.state); ba.draft = draft; ba.tok = I32(L.tok); ba.emb = W(L.tok_emb); ba.emb_kind = wk(true); ba.pos = W(L.pos_emb);
     ba.h = F32(L.h); ba.slot0 = slot0; ba.d = c.d_model; ba.n_vocab = c.n_vocab; ba.n_ctx = c.n_ctx;
     ba.block_k = c.block_k; ba.k_max = k_max;
+    ba.page_table = I32(L.page_table); ba.pages_per_slot = L.pages_per_slot;
     launch("begin", 0, [&](unsigned long long*) { Ops<S>::verify_begin(ba, n, st); });
     target_forward(slot0, n);
     head(slot0, n, F32(L.h), L.lnf_g, L.lnf_b, h->debug || sampling() ? F32(L.logits) : nullptr, nullptr, nullptr, 0,
@@ -598,6 +612,7 @@ struct Runner {
     ba.state = I32(L.state); ba.draft = tokens; ba.tok = I32(L.tok); ba.emb = W(L.tok_emb); ba.emb_kind = wk(true); ba.pos = W(L.pos_emb);
     ba.h = F32(L.h); ba.slot0 = slot0; ba.d = c.d_model; ba.n_vocab = c.n_vocab; ba.n_ctx = c.n_ctx;
     ba.block_k = c.block_k; ba.pmax = pmax;
+    ba.page_table = I32(L.page_table); ba.pages_per_slot = L.pages_per_slot;
     for (int ch = 0; ch < nchunks; ++ch) {
       ba.chunk = ch;
       Ops<S>::prefill_begin(ba, n, st);

@@ -28,6 +28,8 @@ enum {
   ST_A = 11,       // candidates accepted in the last verify
   ST_LEN = 12,     // prompt length
   ST_LIVE = 13,    // slot has been prefilled
+  ST_PG0 = 14,     // cache page of position ST_POS0
+  ST_PG1 = 15,     // the page after it (rows of the pass that cross a page boundary)
 };
 
 // Matrix-core fragment orders.  v_mfma_f32_16x16x32_bf16 reads, per lane l, 8

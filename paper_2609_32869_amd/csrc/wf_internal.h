@@ -43,6 +43,8 @@ struct Layout {
 
 struct Handle;
 
+constexpr int kFc2SplitBatch = 4;  // k-splits of the second MLP product for small multi-slot batches
+
 struct GraphKey {
   int slot0, n, k_max;
   const void *ovr, *out, *nout, *nacc, *done;

@@ -152,6 +152,8 @@ struct BeginArgs {
   int emb_kind;
   const void* pos;  // positional table (target) or mask vector (drafter)
   float* h;
+  const int* page_table;  // [slot][pages_per_slot] (target passes: sets ST_PG0 / ST_PG1)
+  int pages_per_slot;
   int slot0, d, n_vocab, n_ctx, block_k, k_max, chunk, pmax;
 };
 
