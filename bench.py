@@ -117,14 +117,15 @@ def gemv_flops_per_step(cfg):
     return 2 * 9 * ((cfg.n_layer + cfg.n_draft_layer) * blk + 2 * V * d + cfg.n_tap * d * d)
 
 
-def plan_planted(traj, L0, e0, n_steps, cfg, rng):
+def plan_planted(traj, L0, e0, n_steps, cfg, rng, k_max=None):
     """Planted draft blocks and the acceptance each must produce."""
     from wf_fixtures import plant_drafts
     K, V = cfg.block_k, cfg.n_vocab
+    k_max = K if k_max is None else k_max
     plans, accs = [], []
     e, L = e0, L0
     for _ in range(n_steps):
-        k = max(0, min(K, cfg.n_ctx - e - 1, cfg.n_ctx - L - 1))
+        k = max(0, min(K, k_max, cfg.n_ctx - e - 1, cfg.n_ctx - L - 1))
         cont = [int(t) for t in traj[e:e + K]]
         cont += [0] * (K - len(cont))
         r = int(rng.integers(0, K + 1))
@@ -237,6 +238,102 @@ def run_batch(args):
     print(json.dumps(result), flush=True)
 
 
+def _b1_engine(log):
+    import torch
+    from wf_fixtures import LARGE_V3, make_weights, make_memory, make_prefix, make_prefix_lengths
+    from paper_2609_32869_amd import WhisperFlash, to_device_storage
+    cfg = LARGE_V3
+    stream = torch.cuda.Stream()
+    torch.cuda.set_stream(stream)
+    W = make_weights(cfg)
+    eng = WhisperFlash.from_host(cfg, 1, [W.values[n] for n, _ in W.order])
+    mem = to_device_storage(make_memory(cfg, 0), cfg.dtype)[None]
+    eng.encode_memory_set(0, mem)
+    L0 = int(make_prefix_lengths(1, 20, 200)[0])
+    toks = torch.from_numpy(make_prefix(cfg, 0, L0)[None].copy()).cuda()
+    return cfg, eng, mem, L0, toks
+
+
+def run_kmax_sweep(args):
+    """Verification-budget sweep (the paper's k_max knob, Appendix A.1, Table A5):
+    step latency against the rows verified, on the batch-1 workload with planted
+    drafts from the target's own greedy continuation."""
+    import torch
+    log = lambda *a: print(*a, file=sys.stderr, flush=True)
+    cfg, eng, mem, L0, toks = _b1_engine(log)
+    K, steps, warm = cfg.block_k, args.steps, args.warmup
+    first = eng.prefill(0, toks, [L0], [cfg.n_ctx])
+    outs = eng._outs(1)
+    zero = torch.zeros((1, K), dtype=torch.int32, device="cuda")
+    n_traj = min(cfg.n_ctx - L0, (K + 1) * (steps + warm) + K)
+    traj_t = torch.empty(n_traj, dtype=torch.int32, device="cuda")
+    traj_t[0] = first[0]
+    for i in range(1, n_traj):
+        eng.verify_accept(0, zero, 0, outs=outs)
+        traj_t[i].copy_(outs[0][0, 0])
+    traj = traj_t.cpu().numpy()
+    rows = []
+    for k_max in (0, 1, 2, 4, 8):
+        rng = np.random.default_rng(400)
+        plans, accs = plan_planted(traj, L0, 1, steps + warm, cfg, rng, k_max=k_max)
+        plan_t = torch.from_numpy(plans[:, None, :].copy()).cuda()
+        eng.prefill(0, toks, [L0], [cfg.n_ctx])
+        ovr = torch.empty((1, K), dtype=torch.int32, device="cuda")
+        res = torch.zeros(steps + warm, dtype=torch.int32, device="cuda")
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        for i in range(steps + warm):
+            if i == warm:
+                ev[0].record()
+            ovr.copy_(plan_t[i])
+            eng.step(0, 1, k_max, draft_override=ovr, outs=outs, use_graph=True)
+            res[i].copy_(outs[1][0])
+        ev[1].record()
+        torch.cuda.synchronize()
+        ms = ev[0].elapsed_time(ev[1])
+        toks_out = int(res[warm:].sum().item())
+        rows.append({"k_max": k_max, "ms_per_step": round(ms / steps, 4), "tokens_per_step": round(toks_out / steps, 3),
+                     "verified_tokens_per_s": round(toks_out / (ms / 1e3), 1),
+                     "planted_acceptance_exact": bool(np.array_equal(res.cpu().numpy(), accs[:steps + warm] + 1))})
+        log(f"[bench] k_max={k_max}: {rows[-1]}")
+    print(json.dumps({"sweep": "k_max", "unit": "ms/step", "steps": steps, "warmup": warm,
+                      "config": {"workload": "whisper-large-v3-shaped draft+verify step, batch 1, greedy, planted drafts",
+                                 "prefix_len": L0}, "rows": rows}), flush=True)
+
+
+def run_request(args):
+    """Request set-up around the step loop: the acoustic K/V projection of every
+    target and drafter block for one 30 s memory, and the prompt prefill."""
+    import torch
+    from wf_fixtures import make_prefix
+    log = lambda *a: print(*a, file=sys.stderr, flush=True)
+    cfg, eng, mem, L0, toks = _b1_engine(log)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    reps = 5
+
+    def timed(fn):
+        fn()
+        torch.cuda.synchronize()
+        ev[0].record()
+        for _ in range(reps):
+            fn()
+        ev[1].record()
+        torch.cuda.synchronize()
+        return ev[0].elapsed_time(ev[1]) / reps
+
+    enc_ms = timed(lambda: eng.encode_memory_set(0, mem))
+    nblk = cfg.n_layer + cfg.n_draft_layer
+    enc_flops = nblk * 2.0 * cfg.n_frames * cfg.d_model * 2 * cfg.d_model
+    out = {"measure": "request set-up", "encode_memory_set_ms": round(enc_ms, 3),
+           "encode_tflops": round(enc_flops / (enc_ms / 1e3) / 1e12, 1), "prefill_ms": {}}
+    for P in (32, 128, 400):
+        t = torch.from_numpy(make_prefix(cfg, 0, P)[None].copy()).cuda()
+        out["prefill_ms"][str(P)] = round(timed(lambda: eng.prefill(0, t, [P], [cfg.n_ctx])), 3)
+    out["config"] = {"workload": "whisper-large-v3-shaped encode of one 1500-frame memory (32 target + 2 drafter "
+                                 "blocks) and prefill of one prompt", "storage": "bf16"}
+    log(f"[bench] {out}")
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -244,6 +341,12 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--profile-steps", type=int, default=4)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--kmax-sweep", action="store_true",
+                    help="batch-1 step latency and verified tokens/s for verification budgets k_max in {0,1,2,4,8} "
+                         "(k_max = 0 is plain decoding through the same kernels); prints one JSON line")
+    ap.add_argument("--request", action="store_true",
+                    help="batch-1 request set-up: time wf_encode_memory_set (acoustic K/V of all blocks) and "
+                         "wf_prefill for prompts of 32 / 128 / 400 tokens; prints one JSON line")
     ap.add_argument("--pmc-run", action="store_true",
                     help="short run for hardware-counter passes: 1 warm-up, 2 timed and 1 profiled step, no oracle, "
                          "then a plain 256 MiB device-to-device copy (x3) whose counters calibrate byte counts")
@@ -260,6 +363,10 @@ def main():
         args.steps, args.warmup, args.profile_steps, args.no_cpu_baseline = 2, 1, 1, True
     if args.batch > 1:
         return run_batch(args)
+    if args.kmax_sweep:
+        return run_kmax_sweep(args)
+    if args.request:
+        return run_request(args)
     import torch
     from wf_fixtures import LARGE_V3, make_weights, make_memory, make_prefix, make_prefix_lengths
     from paper_2609_32869_amd import WhisperFlash, to_device_storage
