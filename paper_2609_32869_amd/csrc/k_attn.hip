@@ -296,7 +296,8 @@ __global__ void __launch_bounds__(kCrossThreads) k_attn_cross(CrossArgs a) {
 // live in LDS ([frame][12] fp32):
 //   pass 1  scores (a key's 64-dim product summed over its 8 lanes);
 //   sweeps  one thread per (frame, row): the row maxima m, then p = exp(s - m)
-//           in place and the row sums l, each reduced in a fixed order;
+//           in place and the row sums l, each reduced in a fixed order (one wave
+//           per row);
 //   pass 2  acc += p * v over the values (no rescaling), then the 8 key lanes and
 //           the waves merge.
 // With one chunk the block divides by l and stores.  With several, each block
@@ -311,10 +312,21 @@ inline size_t xr_lds_bytes(int chunk) {
   const size_t sc = (size_t)chunk * kXrStride, wacc = (size_t)kXrWaves * kRows * 64;
   return 4 * (sc > wacc ? sc : wacc);
 }
+// Sum over the key lanes (lane bits 3..5) for each dim group (lane bits 0..2): a
+// DPP rotation within 16-lane rows, then the gfx950 row-pair and half-wave swaps.
+__device__ __forceinline__ float fold_key_lanes(float v) {
+  v += dpp<kDppRor8>(v);
+  const auto p = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  v = __uint_as_float(p[0]) + __uint_as_float(p[1]);
+  const auto q = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(q[0]) + __uint_as_float(q[1]);
+}
+
 template <typename S>
 __global__ void __launch_bounds__(kXrThreads, 4) k_attn_cross_rows(CrossArgs a) {
   StampScope stamp_scope(a.stamp);
-  constexpr int NW = kXrWaves, B = sizeof(S) == 2 ? 4 : 2;  // key octets in flight per wave
+  // key octets per load stage; two stages in flight per wave
+  constexpr int NW = kXrWaves, B = sizeof(S) == 2 ? 2 : 1;
   extern __shared__ float sc[];
   float(*wacc)[kRows][64] = reinterpret_cast<float(*)[kRows][64]>(sc);
   __shared__ float rmax[kRows], lsum[kRows];
@@ -322,9 +334,12 @@ __global__ void __launch_bounds__(kXrThreads, 4) k_attn_cross_rows(CrossArgs a) 
   const int head = blockIdx.x, slot = a.slot0 + blockIdx.y, c = blockIdx.z;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, g = lane & 7, kl = lane >> 3;
   const int k0 = c * a.chunk, nk = min(a.n_frames - k0, a.chunk), noct = (nk + 7) >> 3;
+  const int nst = ((noct - w + NW - 1) / NW + B - 1) / B;  // load stages of this wave
   const S* Kx = reinterpret_cast<const S*>(a.kv) +
                 (((size_t)slot * 2 * a.n_head + head) * a.n_frames + k0) * kHeadDim;
   const S* Vx = Kx + (size_t)a.n_head * a.n_frames * kHeadDim;
+  // key of lane group kl in octet b of stage st of this wave (may lie past the end)
+  auto key_of = [&](int st, int b) { return (w + NW * (st * B + b)) * 8 + kl; };
   {  // pass 1: scores
     float q8[kRows][8];
 #pragma unroll
@@ -333,18 +348,17 @@ __global__ void __launch_bounds__(kXrThreads, 4) k_attn_cross_rows(CrossArgs a) 
 #pragma unroll
       for (int e = 0; e < 8; ++e) q8[r][e] = qr[e] * 0.125f;
     }
-    for (int o0 = w; o0 < noct; o0 += NW * B) {
-      Raw8<S> kr[B];
+    Raw8<S> kr[2][B];
+    auto load = [&](int buf, int st) {  // keys past the end re-read the last one (not stored)
 #pragma unroll
-      for (int b = 0; b < B; ++b) {  // keys past the end re-read the last one (not stored)
-        const int key = min((o0 + NW * b) * 8 + kl, nk - 1);
-        kr[b].load(Kx + (uint32_t)key * kHeadDim + 8 * g);
-      }
+      for (int b = 0; b < B; ++b) kr[buf][b].load(Kx + (uint32_t)min(key_of(st, b), nk - 1) * kHeadDim + 8 * g);
+    };
+    auto scores = [&](int buf, int st) {
 #pragma unroll
       for (int b = 0; b < B; ++b) {
-        const int key = (o0 + NW * b) * 8 + kl;
+        const int key = key_of(st, b);
         float k8[8];
-        kr[b].unpack(k8);
+        kr[buf][b].unpack(k8);
         float t[kRows];
 #pragma unroll
         for (int r = 0; r < kRows; ++r) {
@@ -360,11 +374,19 @@ __global__ void __launch_bounds__(kXrThreads, 4) k_attn_cross_rows(CrossArgs a) 
           d[2] = make_float4(t[8], 0.f, 0.f, 0.f);
         }
       }
+    };
+    load(0, 0);
+    for (int st = 0; st < nst; st += 2) {
+      load(1, st + 1);
+      scores(0, st);
+      load(0, st + 2);
+      scores(1, st + 1);
     }
   }
   __syncthreads();
   // sweeps over the scores, one thread per (frame, row): row maxima, then
-  // probabilities in place and the row sums
+  // probabilities in place and the row sums; each row's 56 partials are then
+  // reduced by one wave (rows 0..7 by waves 0..7, row 8 by wave 0)
   const bool sweeper = threadIdx.x < kXrSweepKeys * kRows;
   const int sr = threadIdx.x % kRows;
   if (sweeper) {
@@ -373,10 +395,13 @@ __global__ void __launch_bounds__(kXrThreads, 4) k_attn_cross_rows(CrossArgs a) 
     lpart[threadIdx.x] = m;
   }
   __syncthreads();
-  if (threadIdx.x < kRows) {
-    float m = lpart[threadIdx.x];
-    for (int i = 1; i < kXrSweepKeys; ++i) m = fmaxf(m, lpart[i * kRows + threadIdx.x]);
-    rmax[threadIdx.x] = m;
+  {
+    const float m = wave_max(lane < kXrSweepKeys ? lpart[lane * kRows + w] : -INFINITY);
+    const float m8 = wave_max(lane < kXrSweepKeys && w == 0 ? lpart[lane * kRows + 8] : -INFINITY);
+    if (lane == 0) {
+      rmax[w] = m;
+      if (w == 0) rmax[8] = m8;
+    }
   }
   __syncthreads();
   if (sweeper) {
@@ -390,10 +415,13 @@ __global__ void __launch_bounds__(kXrThreads, 4) k_attn_cross_rows(CrossArgs a) 
     lpart[threadIdx.x] = lp;
   }
   __syncthreads();
-  if (threadIdx.x < kRows) {
-    float L = 0.f;
-    for (int i = 0; i < kXrSweepKeys; ++i) L += lpart[i * kRows + threadIdx.x];
-    lsum[threadIdx.x] = L;
+  {
+    const float l = wave_sum(lane < kXrSweepKeys ? lpart[lane * kRows + w] : 0.f);
+    const float l8 = wave_sum(lane < kXrSweepKeys && w == 0 ? lpart[lane * kRows + 8] : 0.f);
+    if (lane == 0) {
+      lsum[w] = l;
+      if (w == 0) lsum[8] = l8;
+    }
   }
   // pass 2: values
   float acc[kRows][8];
@@ -401,39 +429,45 @@ __global__ void __launch_bounds__(kXrThreads, 4) k_attn_cross_rows(CrossArgs a) 
   for (int r = 0; r < kRows; ++r)
 #pragma unroll
     for (int e = 0; e < 8; ++e) acc[r][e] = 0.f;
-  for (int o0 = w; o0 < noct; o0 += NW * B) {
-    Raw8<S> vr[B];
+  {
+    Raw8<S> vr[2][B];
+    auto load = [&](int buf, int st) {
 #pragma unroll
-    for (int b = 0; b < B; ++b) {
-      const int key = min((o0 + NW * b) * 8 + kl, nk - 1);
-      vr[b].load(Vx + (uint32_t)key * kHeadDim + 8 * g);
-    }
+      for (int b = 0; b < B; ++b) vr[buf][b].load(Vx + (uint32_t)min(key_of(st, b), nk - 1) * kHeadDim + 8 * g);
+    };
+    auto accumulate = [&](int buf, int st) {
 #pragma unroll
-    for (int b = 0; b < B; ++b) {
-      const int key = (o0 + NW * b) * 8 + kl;
-      const bool in = key < nk;
-      const float4* d = reinterpret_cast<const float4*>(sc + min(key, nk - 1) * kXrStride);
-      const float4 s0 = d[0], s1 = d[1], s2 = d[2];
-      const float p[kRows] = {in ? s0.x : 0.f, in ? s0.y : 0.f, in ? s0.z : 0.f, in ? s0.w : 0.f, in ? s1.x : 0.f,
-                              in ? s1.y : 0.f, in ? s1.z : 0.f, in ? s1.w : 0.f, in ? s2.x : 0.f};
-      float v8[8];
-      vr[b].unpack(v8);
+      for (int b = 0; b < B; ++b) {
+        const int key = key_of(st, b);
+        const bool in = key < nk;
+        const float4* d = reinterpret_cast<const float4*>(sc + min(key, nk - 1) * kXrStride);
+        const float4 s0 = d[0], s1 = d[1], s2 = d[2];
+        const float p[kRows] = {in ? s0.x : 0.f, in ? s0.y : 0.f, in ? s0.z : 0.f, in ? s0.w : 0.f, in ? s1.x : 0.f,
+                                in ? s1.y : 0.f, in ? s1.z : 0.f, in ? s1.w : 0.f, in ? s2.x : 0.f};
+        float v8[8];
+        vr[buf][b].unpack(v8);
 #pragma unroll
-      for (int r = 0; r < kRows; ++r)
+        for (int r = 0; r < kRows; ++r)
 #pragma unroll
-        for (int e = 0; e < 8; ++e) acc[r][e] = fmaf(p[r], v8[e], acc[r][e]);
+          for (int e = 0; e < 8; ++e) acc[r][e] = fmaf(p[r], v8[e], acc[r][e]);
+      }
+    };
+    load(0, 0);
+    for (int st = 0; st < nst; st += 2) {
+      load(1, st + 1);
+      accumulate(0, st);
+      load(0, st + 2);
+      accumulate(1, st + 1);
     }
   }
-  // fold the 8 key lanes (lane bits 3..5) of each dim group and publish per wave,
-  // row by row so each row's sums die at its store
+  // fold the key lanes of each dim group and publish per wave, row by row so each
+  // row's sums die at its store
   __syncthreads();  // every wave is done with the probabilities
 #pragma unroll
   for (int r = 0; r < kRows; ++r) {
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
-      float t = acc[r][e] + dpp<kDppRor8>(acc[r][e]);
-      t += __shfl_xor(t, 16, 64);
-      t += __shfl_xor(t, 32, 64);
+      const float t = fold_key_lanes(acc[r][e]);
       if (lane < 8) wacc[w][r][8 * g + e] = t;
     }
   }

@@ -432,7 +432,9 @@ __global__ void __launch_bounds__(NW * 64) k_gemv16w(GemvArgs a) {
 // The rows of several slots (nine each) times W^T over 64 x 64 block tiles: each of
 // the four waves computes a 32 x 32 sub-tile (2 x 2 fragments of
 // v_mfma_f32_16x16x32_bf16), loading operand and weight fragments straight from
-// their fragment orders (1 KB per wave load).  Loads are double-buffered: the
+// their fragment orders (1 KB per wave load).  The operand holds each value as
+// two bf16 planes (hi + lo, 2^-17 relative), both multiplied into one
+// accumulator, so the product is accurate to fp32 rounding.  Loads are double-buffered: the
 // fragments of the next kGemmU k-steps are in flight while the current ones
 // multiply.  Grid y splits the k-steps (EPI_PART stores each split's partial
 // sums).  Block b runs on XCD b % 8; the row blocks of one column block are
@@ -466,13 +468,18 @@ __global__ void __launch_bounds__(256) k_gemm16(GemvArgs a, int mb0, int nmb, in
   for (int p = 0; p < 2; ++p)
 #pragma unroll
     for (int q = 0; q < 2; ++q) acc[p][q] = floatx4{0.f, 0.f, 0.f, 0.f};
-  bf16x8 af[2][kGemmU][2], wf[2][kGemmU][2];
+  // the operand's two bf16 planes (hi, lo): both multiply the same weight fragment
+  const size_t plane = (size_t)MT * KS * 64;
+  bf16x8 af[2][kGemmU][2][2], wf[2][kGemmU][2];
   auto load = [&](int b, int st) {  // k-steps st.. (past the range: re-read the last one)
 #pragma unroll
     for (int u = 0; u < kGemmU; ++u) {
       const int ss = min(st + u, ks1 - 1);
-      af[b][u][0] = Ab[((size_t)ss * MT + ma0) * 64];
-      af[b][u][1] = Ab[((size_t)ss * MT + ma1) * 64];
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        af[b][u][0][h] = Ab[h * plane + ((size_t)ss * MT + ma0) * 64];
+        af[b][u][1][h] = Ab[h * plane + ((size_t)ss * MT + ma1) * 64];
+      }
       wf[b][u][0] = Wb[((size_t)na0 * KS + ss) * 64];
       wf[b][u][1] = Wb[((size_t)na1 * KS + ss) * 64];
     }
@@ -482,10 +489,12 @@ __global__ void __launch_bounds__(256) k_gemm16(GemvArgs a, int mb0, int nmb, in
     for (int u = 0; u < kGemmU; ++u)
       if (st + u < ks1) {
 #pragma unroll
-        for (int p = 0; p < 2; ++p)
+        for (int h = 0; h < 2; ++h)
 #pragma unroll
-          for (int q = 0; q < 2; ++q)
-            acc[p][q] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[b][u][p], wf[b][u][q], acc[p][q], 0, 0, 0);
+          for (int p = 0; p < 2; ++p)
+#pragma unroll
+            for (int q = 0; q < 2; ++q)
+              acc[p][q] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[b][u][p][h], wf[b][u][q], acc[p][q], 0, 0, 0);
       }
   };
   load(0, ks0);
@@ -914,7 +923,7 @@ static void launch_epi(const GemvArgs& a, hipStream_t st) {
       return;
     }
     const int ks = a.ksplit > 1 ? a.ksplit : 1;
-    if (a.nsplit == 1 && a.wkind == W_F16) {  // several slots: 64 x 64 GEMM tiles (k split over grid y)
+    if (a.nsplit == 2 && a.wkind == W_F16) {  // several slots: 64 x 64 GEMM tiles (k split over grid y)
       const int mb0 = a.slot0 * kRows / 64, mb1 = ((a.slot0 + a.nslots) * kRows + 63) / 64;
       const int nmb = mb1 - mb0, nnb = (a.N + 63) / 64;
       k_gemm16<EPI><<<dim3((unsigned)(8 * ((nnb + 7) / 8) * nmb), ks), 256, 0, st>>>(a, mb0, nmb, nnb);

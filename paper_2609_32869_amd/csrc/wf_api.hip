@@ -153,7 +153,7 @@ int compute_layout(const wf_config& c, Layout& L) {
   L.pages_per_slot = c.n_ctx / kPage;
   // column blocks of the vocabulary head: 32-column tiles (bf16, batch 1), 64-column
   // GEMM blocks (bf16, several slots) or 16-column tiles (fp32)
-  L.nsplit_op = (c.dtype == WF_BF16 && c.max_batch == 1) ? 3 : 1;
+  L.nsplit_op = c.dtype != WF_BF16 ? 1 : c.max_batch == 1 ? 3 : 2;
   L.head_blocks = c.dtype != WF_BF16 ? (int)((V + 15) / 16) : L.nsplit_op == 3 ? (int)((V + 31) / 32) : (int)((V + 63) / 64);
   // raw bf16 matrices are staged at init in the cross K/V region before reordering
   L.stage_bytes = 0;
@@ -173,15 +173,16 @@ int compute_layout(const wf_config& c, Layout& L) {
   L.xkv = region(std::max((size_t)(c.n_layer + c.n_draft_layer) * B * 2 * c.n_frames * d * eb, L.stage_bytes));
   L.skv = region((size_t)c.n_layer * 2 * B * L.pages_per_slot * H * kPage * kHeadDim * eb);
   L.hkv = region((size_t)c.n_draft_layer * 2 * B * H * c.n_ctx * kHeadDim * eb);
-  // matrix operands: 3 bf16 terms per fp32 value at batch 1 with bf16 storage (set above)
-  const size_t rows = L.nsplit_op * R9;
+  // matrix operands: 3 bf16 terms per fp32 value as extra rows at batch 1, 2 terms as
+  // two planes with several slots (bf16 storage, set above)
+  const size_t rows = (L.nsplit_op == 3 ? 3 : 1) * R9, planes = L.nsplit_op == 2 ? 2 : 1;
   L.mt16 = (int)((rows + 15) / 16);
   L.mt32 = (int)((rows + 31) / 32);
   const size_t M16 = (size_t)L.mt16 * 16, M32 = std::max((size_t)L.mt32 * 32, M16);
-  L.a_d16 = region(M16 * d * eb);
-  L.a_d32 = region(M32 * d * eb);
-  L.a_f16 = region(M16 * F * eb);
-  L.a_tap16 = region(M16 * c.n_tap * d * eb);
+  L.a_d16 = region(planes * M16 * d * eb);
+  L.a_d32 = region(planes * M32 * d * eb);
+  L.a_f16 = region(planes * M16 * F * eb);
+  L.a_tap16 = region(planes * M16 * c.n_tap * d * eb);
   L.h = region(R9 * d * 4);
   L.qkv = region(R9 * 3 * d * 4);
   L.hp = region(R9 * d * 4);
@@ -210,7 +211,7 @@ int compute_layout(const wf_config& c, Layout& L) {
     const int tiles64 = (int)((d + 63) / 64), ksteps = (int)(F / 32);
     L.fc2_split = std::max(1, std::min({kRlnMaxPartsHost, 240 / tiles64, ksteps}));
   }
-  const int nparts = std::max({L.fc2_split, c.dtype == WF_BF16 && L.nsplit_op == 1 ? kFc2SplitBatch : 0, 1});
+  const int nparts = std::max({L.fc2_split, L.nsplit_op == 2 ? kFc2SplitBatch : 0, 1});
   L.part = region((size_t)nparts * R9 * d * 4);
   L.xpart = region((size_t)kXrMaxPartials * kXrPart * 4);
   L.stamps = region((size_t)kStampSlots * kStampWords * 8);
@@ -405,7 +406,7 @@ struct Runner {
   // kFc2SplitBatch (partial sums reduced with the residual update and the next
   // LayerNorm), else 0.
   int fc2_split_batch(int slot0, int n) const {
-    if (!frag() || L.nsplit_op != 1) return 0;
+    if (L.nsplit_op != 2) return 0;
     const int mb0 = slot0 * kRows / 64, mb1 = ((slot0 + n) * kRows + 63) / 64;
     const int tiles = (mb1 - mb0) * ((c.d_model + 63) / 64);
     return tiles < 160 && (c.d_ff / 32) % kFc2SplitBatch == 0 ? kFc2SplitBatch : 0;

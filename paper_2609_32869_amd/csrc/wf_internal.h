@@ -35,7 +35,7 @@ struct Layout {
   std::vector<BlockW> tb, db;
   size_t weight_elems;
   int pages_per_slot, head_blocks;
-  int nsplit_op;  // split terms of a matrix operand (3: bf16 at batch 1, else 1)
+  int nsplit_op;  // bf16 terms of a matrix operand value (3: rows, batch 1; 2: planes, several slots; fp32: 1)
   int mt16, mt32; // 16-row / 32-row tiles held by an operand buffer
   size_t stage_bytes;  // raw-matrix staging at init (inside the cross K/V region)
   int fc2_split;       // k-splits of the second MLP product (0: not split)

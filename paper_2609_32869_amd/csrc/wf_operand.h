@@ -14,9 +14,13 @@ __device__ __forceinline__ size_t op_index(const Operand& o, int m, int k) {
   return (size_t)m * o.ld + k;
 }
 
-// Write value v of activation row `row` (= slot * 9 + i), column `col`.  bf16 with
-// nsplit = 3: the exact three-term split hi + mid + lo == v at rows row, R9 + row,
-// 2 R9 + row; otherwise the value rounded to the storage type.
+// Write value v of activation row `row` (= slot * 9 + i), column `col`.  bf16
+// with nsplit = 3 (batch 1): the exact three-term split hi + mid + lo == v at rows
+// row, R9 + row, 2 R9 + row.  nsplit = 2 (several slots, 16-row fragment order):
+// hi (v truncated to bf16) in the operand and lo = RNE(v - hi) at the same place
+// of a second plane right after it (mt * 16 * ld elements on), so hi + lo
+// equals v to 2^-17 relative and the two products share one accumulator.
+// Otherwise the value rounded to the storage type.
 __device__ __forceinline__ void put_operand(const Operand& o, int, int, int row, int col, float v, float) {
   reinterpret_cast<float*>(o.p)[op_index(o, row, col)] = v;
 }
@@ -28,6 +32,11 @@ __device__ __forceinline__ void put_operand(const Operand& o, int nsplit, int R9
     A[op_index(o, row, col)] = (uint16_t)hi;
     A[op_index(o, R9 + row, col)] = (uint16_t)mid;
     A[op_index(o, 2 * R9 + row, col)] = (uint16_t)lo;
+  } else if (nsplit == 2) {
+    const uint32_t hb = __float_as_uint(v) & 0xffff0000u;
+    const size_t i = op_index(o, row, col);
+    A[i] = (uint16_t)(hb >> 16);
+    A[i + (size_t)o.mt * 16 * o.ld] = (uint16_t)bf16_bits_rne(v - __uint_as_float(hb));
   } else {
     A[op_index(o, row, col)] = (uint16_t)bf16_bits_rne(v);
   }

@@ -119,18 +119,16 @@ def test_micro_bf16_b1_split_operands():
     ls.close()
 
 
-def test_micro_bf16_b3_bf16_operands():
-    """Batch 3, bf16: operands rounded to bf16 (the oracle rounds them the same way)."""
+def test_micro_bf16_b3_two_plane_operands():
+    """Batch 3, bf16: each operand value as two bf16 planes (hi + lo), products
+    accurate to fp32 rounding; compared with the plain fp32 oracle."""
     from lockstep import Lockstep
     cfg = MICRO_BF16
     W = make_weights(cfg)
     prompts = [make_prefix(cfg, 0, 4), make_prefix(cfg, 1, 20), make_prefix(cfg, 2, 9)]
     max_new = [40, 9, 30]
-    opts = OracleOpts(dtype=np.float32, kv_bf16=True, gemm_bf16=True)
-    # Rounding every product input to bf16 makes the result sensitive to the fp32
-    # summation order: the oracle in fp32 and in fp64 (same rounding points)
-    # already differ by 3e-3 in the draft logits here, so the bf16 bar applies.
-    ls = Lockstep(cfg, W, prompts, max_new, TOL_BF16, opts=opts)
+    opts = OracleOpts(dtype=np.float32, kv_bf16=True)
+    ls = Lockstep(cfg, W, prompts, max_new, TOL_MICRO_BF16, opts=opts)
     T = Target(cfg, W.values, opts)
     refs = [plain_greedy(T, make_memory(cfg, i), prompts[i], max_new[i]) for i in range(3)]
     _run_planted(ls, refs, np.random.default_rng(6), 10)
@@ -148,8 +146,8 @@ def test_micro_bf16_b3_chunked_cross_attention():
     W = make_weights(cfg)
     prompts = [make_prefix(cfg, 0, 6), make_prefix(cfg, 1, 17), make_prefix(cfg, 2, 30)]
     max_new = [24, 24, 24]
-    opts = OracleOpts(dtype=np.float32, kv_bf16=True, gemm_bf16=True)
-    ls = Lockstep(cfg, W, prompts, max_new, TOL_BF16, opts=opts)
+    opts = OracleOpts(dtype=np.float32, kv_bf16=True)
+    ls = Lockstep(cfg, W, prompts, max_new, TOL_MICRO_BF16, opts=opts)
     T = Target(cfg, W.values, opts)
     refs = [plain_greedy(T, make_memory(cfg, i), prompts[i], max_new[i]) for i in range(3)]
     _run_planted(ls, refs, np.random.default_rng(7), 6)
@@ -192,10 +190,11 @@ def test_large_v3_bf16_lockstep_b1():
 
 
 # ---------------------------------------------------------------- large batches (sampled slots)
-# At batch >= 2 product inputs are bf16 (the oracle's gemm_bf16 option rounds at
-# the same points); the oracle follows a sample of the slots, which are
-# independent by construction (no per-row dependence on the batch).
-LARGE_BATCH_OPTS = dict(dtype=np.float32, kv_bf16=True, gemm_bf16=True, exact=False)
+# At batch >= 2 operands are two bf16 planes (products accurate to fp32
+# rounding), compared with the plain fp32 oracle; the oracle follows a sample of
+# the slots, which are independent by construction (no per-row dependence on
+# the batch).
+LARGE_BATCH_OPTS = dict(dtype=np.float32, kv_bf16=True, exact=False)
 
 
 def _planted_subset(ls, refs, rng):

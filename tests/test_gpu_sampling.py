@@ -198,14 +198,13 @@ def test_v64_emitted_law_equals_target(temperature, k_max):
 @pytest.mark.parametrize("temperature", [0.7, 1.0])
 def test_large_v3_b8_sampling(temperature):
     """Large-v3 shapes, 8 slots, prefixes uniform in [4, 440]; the oracle follows two
-    slots.  Product inputs are bf16 at this batch, so logits differ from the fp32
-    oracle by up to ~3e-3 and decisions are compared outside that band."""
+    slots; decisions are compared where the oracle's margins exceed the bf16 bar."""
     from wf_fixtures import LARGE_V3, make_prefix_lengths
     cfg = LARGE_V3
     lens = [int(x) for x in make_prefix_lengths(8, 4, 440, seed=300)]
     prompts = [make_prefix(cfg, s, lens[s]) for s in range(8)]
-    opts = OracleOpts(dtype=np.float32, kv_bf16=True, gemm_bf16=True, exact=False)
+    opts = OracleOpts(dtype=np.float32, kv_bf16=True, exact=False)
     decisions, ties = _sampling_lockstep(cfg, temperature, steps=3, prompts=prompts, check=[0, 5], opts=opts,
-                                         gap_tol=3e-2, margin_tol=3e-2)
+                                         gap_tol=2e-2, margin_tol=2e-2)
     print(f"large b8 T={temperature}: {decisions} verified rows compared, near ties {ties}", flush=True)
     assert decisions > 0
