@@ -21,16 +21,19 @@ __global__ void __launch_bounds__(256) k_ln_operand(LnArgs a) {
   __shared__ float red[8];
   const int row = a.row0 + blockIdx.x;
   const float* xr = a.x + (size_t)row * a.d;
-  const S* g = reinterpret_cast<const S*>(a.g);
-  const S* b = reinterpret_cast<const S*>(a.b);
+  // every load first and unconditionally (columns past d re-read the last one)
   float v[8];
-  float s = 0.f;
+  uint32_t gv[8], bv[8];
 #pragma unroll
   for (int j = 0; j < 8; ++j) {
-    const int i = threadIdx.x + j * 256;
-    v[j] = i < a.d ? xr[i] : 0.f;
-    s += v[j];
+    const int i = min(threadIdx.x + j * 256, a.d - 1);
+    v[j] = xr[i];
+    gv[j] = ld_bits<S>(a.g, i);
+    bv[j] = ld_bits<S>(a.b, i);
   }
+  float s = 0.f;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) s += threadIdx.x + j * 256 < a.d ? v[j] : 0.f;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   s = wave_sum(s);
   if (lane == 0) red[w] = s;
@@ -51,7 +54,7 @@ __global__ void __launch_bounds__(256) k_ln_operand(LnArgs a) {
 #pragma unroll
   for (int j = 0; j < 8; ++j) {
     const int i = threadIdx.x + j * 256;
-    if (i < a.d) put_op<S>(a.out, a.nsplit, a.R9, row, i, (v[j] - mean) * inv * to_f(g[i]) + to_f(b[i]));
+    if (i < a.d) put_op<S>(a.out, a.nsplit, a.R9, row, i, (v[j] - mean) * inv * from_bits<S>(gv[j]) + from_bits<S>(bv[j]));
   }
 }
 
@@ -644,25 +647,33 @@ __global__ void __launch_bounds__(kRlnThreads) k_reduce_ln(RlnArgs a) {
   const S* bias = reinterpret_cast<const S*>(a.bias);
   float* hr = a.h + (size_t)row * d;
   float v[J];
-  // every load of the row is issued before the first add
-  float x[J], pv[J][kRlnMaxParts], bv[J];
+  // every load of the row is issued before the first add, unconditionally
+  // (columns past d and partials past nparts re-read valid ones, then discarded)
+  const bool has_bias = bias != nullptr, has_ln = a.g != nullptr;
+  const void* bp = has_bias ? a.bias : a.part;
+  const void* gp = has_ln ? a.g : a.part;
+  const void* lp = has_ln ? a.b : a.part;
+  float x[J], pv[J][kRlnMaxParts];
+  uint32_t bv[J], gv[J], lv[J];
 #pragma unroll
   for (int j = 0; j < J; ++j) {
-    const int c = threadIdx.x + j * kRlnThreads;
-    const bool ok = c < d;
-    x[j] = ok ? hr[c] : 0.f;
-    bv[j] = (ok && bias != nullptr) ? to_f(bias[c]) : 0.f;
+    const int c = min((int)threadIdx.x + j * kRlnThreads, d - 1);
+    x[j] = hr[c];
+    bv[j] = ld_bits<S>(bp, c);
+    gv[j] = ld_bits<S>(gp, c);
+    lv[j] = ld_bits<S>(lp, c);
 #pragma unroll
     for (int p = 0; p < kRlnMaxParts; ++p)
-      pv[j][p] = (ok && p < a.nparts) ? a.part[p * a.pstride + (size_t)row * d + c] : 0.f;
+      pv[j][p] = a.part[min(p, a.nparts - 1) * a.pstride + (size_t)row * d + c];
   }
 #pragma unroll
   for (int j = 0; j < J; ++j) {
     const int c = threadIdx.x + j * kRlnThreads;
     float sum = 0.f;
 #pragma unroll
-    for (int p = 0; p < kRlnMaxParts; ++p) sum += pv[j][p];
-    v[j] = x[j] + (sum + bv[j]);
+    for (int p = 0; p < kRlnMaxParts; ++p) sum += p < a.nparts ? pv[j][p] : 0.f;
+    const float bb = has_bias ? from_bits<S>(bv[j]) : 0.f;
+    v[j] = c < d ? x[j] + (sum + bb) : 0.f;  // columns past d stay out of the statistics
     if (c < d) {
       hr[c] = v[j];
       if (a.tapcol >= 0) put_op<S>(a.tap, a.nsplit, a.R9, row, a.tapcol + c, v[j]);
@@ -691,12 +702,10 @@ __global__ void __launch_bounds__(kRlnThreads) k_reduce_ln(RlnArgs a) {
 #pragma unroll
   for (int i = 0; i < NW; ++i) qt += red[1][i];
   const float inv = 1.0f / sqrtf(qt / (float)d + 1e-5f);
-  const S* g = reinterpret_cast<const S*>(a.g);
-  const S* b = reinterpret_cast<const S*>(a.b);
 #pragma unroll
   for (int j = 0; j < J; ++j) {
     const int c = threadIdx.x + j * kRlnThreads;
-    if (c < d) put_op<S>(a.out, a.nsplit, a.R9, row, c, (v[j] - mean) * inv * to_f(g[c]) + to_f(b[c]));
+    if (c < d) put_op<S>(a.out, a.nsplit, a.R9, row, c, (v[j] - mean) * inv * from_bits<S>(gv[j]) + from_bits<S>(lv[j]));
   }
 }
 

@@ -155,6 +155,19 @@ __device__ __forceinline__ bool better(float v, int i, float bv, int bi) {
   return i < bi;
 }
 
+// A stored parameter element as raw bits, converted only where it is used (so no
+// instruction right after the load waits for it).
+template <typename S>
+__device__ __forceinline__ uint32_t ld_bits(const void* p, int i) {
+  if constexpr (sizeof(S) == 2) return reinterpret_cast<const uint16_t*>(p)[i];
+  else return reinterpret_cast<const uint32_t*>(p)[i];
+}
+template <typename S>
+__device__ __forceinline__ float from_bits(uint32_t b) {
+  if constexpr (sizeof(S) == 2) return __uint_as_float(b << 16);
+  else return __uint_as_float(b);
+}
+
 // Launch timing for profiled calls.  A timing slot holds, per XCD (the chip's
 // eight dies) and per block-number residue mod 8, the earliest block start and
 // the latest block end (the block's last wave to leave, found with an LDS
