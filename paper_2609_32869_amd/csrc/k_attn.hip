@@ -294,12 +294,15 @@ __global__ void __launch_bounds__(kCrossThreads) k_attn_cross(CrossArgs a) {
 // Block (head, slot, chunk) computes all nine query rows of one slot over one
 // chunk of the frames, so each key / value byte is read once.  The chunk's scores
 // live in LDS ([frame][12] fp32):
-//   pass 1  scores (a key's 64-dim product summed over its 8 lanes);
+//   pass 1  scores (bf16 keys: matrix-core tiles of 16 frames against the query
+//           rows as hi + lo bf16 planes; fp32 keys: a key's 64-dim product
+//           summed over its 8 lanes);
 //   sweeps  one thread per (frame, row): the row maxima m, then p = exp(s - m)
 //           in place and the row sums l, each reduced in a fixed order (one wave
 //           per row);
-//   pass 2  acc += p * v over the values (no rescaling), then the 8 key lanes and
-//           the waves merge.
+//   pass 2  acc += p * v over the values (no rescaling; the first value loads
+//           are issued before the sweeps), then the 8 key lanes and the waves
+//           merge.
 // With one chunk the block divides by l and stores.  With several, each block
 // stores (max, l, acc) and a second kernel merges the chunks in chunk order:
 // out = sum_c e^(m_c - m) acc_c / sum_c e^(m_c - m) l_c.
@@ -322,10 +325,82 @@ __device__ __forceinline__ float fold_key_lanes(float v) {
   return __uint_as_float(q[0]) + __uint_as_float(q[1]);
 }
 
+// Pass 1 on the matrix cores (bf16 keys): S^T[frame][row] = K[frame] . q[row] over
+// 16-frame tiles with v_mfma_f32_16x16x32_bf16.  The key tile is the A operand read
+// straight from the row-major key rows (lane l: frame l % 16, dims 8 (l / 16)..+7
+// and the same 32 further on); the scaled query rows are the B operand as two bf16
+// planes, hi (truncated) and lo = RNE(q - hi), both multiplied into the same
+// accumulator so the scores keep fp32 accuracy.  Lane l receives rows l % 16
+// (>= 9: zero padding, not stored) of frames 4 (l / 16)..+3 of the tile.  Each
+// wave keeps the next stage of kXrTiles tiles (8 KB) in flight while it multiplies.
+constexpr int kXrTiles = 4;
+__device__ __forceinline__ void xr_scores_mfma(const CrossArgs& a, int slot, int head, const bf16* Kx, int nk,
+                                               float* sc) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, n = lane & 15, kg = lane >> 4;
+  bf16x8 qh[2], ql[2];
+  {
+    const float* qr = a.q + (size_t)(slot * kRows + min(n, kRows - 1)) * a.ldq + head * kHeadDim + 8 * kg;
+    const float scale = n < kRows ? 0.125f : 0.f;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const float4 x0 = *reinterpret_cast<const float4*>(qr + 32 * h);
+      const float4 x1 = *reinterpret_cast<const float4*>(qr + 32 * h + 4);
+      const float f[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
+      uint32_t hb[8], lb[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const float v = f[j] * scale;
+        hb[j] = __float_as_uint(v) >> 16;
+        lb[j] = bf16_bits_rne(v - __uint_as_float(hb[j] << 16));
+      }
+      qh[h] = __builtin_bit_cast(bf16x8, make_uint4(hb[0] | hb[1] << 16, hb[2] | hb[3] << 16, hb[4] | hb[5] << 16,
+                                                    hb[6] | hb[7] << 16));
+      ql[h] = __builtin_bit_cast(bf16x8, make_uint4(lb[0] | lb[1] << 16, lb[2] | lb[3] << 16, lb[4] | lb[5] << 16,
+                                                    lb[6] | lb[7] << 16));
+    }
+  }
+  const int ntile = (nk + 15) >> 4;
+  const int nst = ((ntile - w + kXrWaves - 1) / kXrWaves + kXrTiles - 1) / kXrTiles;  // load stages of this wave
+  auto tile_of = [&](int st, int t) { return w + kXrWaves * (st * kXrTiles + t); };
+  bf16x8 kt[2][kXrTiles][2];
+  auto load = [&](int buf, int st) {  // frames past the end re-read the last one (not stored)
+#pragma unroll
+    for (int t = 0; t < kXrTiles; ++t) {
+      const int f = min(tile_of(st, t) * 16 + n, nk - 1);
+      const bf16x8* kp = reinterpret_cast<const bf16x8*>(Kx + (size_t)f * kHeadDim) + kg;
+      kt[buf][t][0] = kp[0];
+      kt[buf][t][1] = kp[4];
+    }
+  };
+  auto scores = [&](int buf, int st) {
+#pragma unroll
+    for (int t = 0; t < kXrTiles; ++t) {
+      floatx4 acc = {0.f, 0.f, 0.f, 0.f};
+      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kt[buf][t][0], qh[0], acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kt[buf][t][0], ql[0], acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kt[buf][t][1], qh[1], acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kt[buf][t][1], ql[1], acc, 0, 0, 0);
+      const int f0 = tile_of(st, t) * 16 + 4 * kg;
+      if (n < kRows) {
+#pragma unroll
+        for (int v = 0; v < 4; ++v)
+          if (f0 + v < nk) sc[(f0 + v) * kXrStride + n] = acc[v];
+      }
+    }
+  };
+  load(0, 0);
+  for (int st = 0; st < nst; st += 2) {
+    load(1, st + 1);
+    scores(0, st);
+    load(0, st + 2);
+    scores(1, st + 1);
+  }
+}
+
 template <typename S>
 __global__ void __launch_bounds__(kXrThreads, 4) k_attn_cross_rows(CrossArgs a) {
   StampScope stamp_scope(a.stamp);
-  // key octets per load stage; two stages in flight per wave
+  // key octets per vector load stage (the fp32 score pass and the value pass)
   constexpr int NW = kXrWaves, B = sizeof(S) == 2 ? 2 : 1;
   extern __shared__ float sc[];
   float(*wacc)[kRows][64] = reinterpret_cast<float(*)[kRows][64]>(sc);
@@ -340,7 +415,9 @@ __global__ void __launch_bounds__(kXrThreads, 4) k_attn_cross_rows(CrossArgs a) 
   const S* Vx = Kx + (size_t)a.n_head * a.n_frames * kHeadDim;
   // key of lane group kl in octet b of stage st of this wave (may lie past the end)
   auto key_of = [&](int st, int b) { return (w + NW * (st * B + b)) * 8 + kl; };
-  {  // pass 1: scores
+  if constexpr (sizeof(S) == 2) {
+    xr_scores_mfma(a, slot, head, reinterpret_cast<const bf16*>(Kx), nk, sc);
+  } else {  // pass 1: scores
     float q8[kRows][8];
 #pragma unroll
     for (int r = 0; r < kRows; ++r) {
@@ -383,6 +460,15 @@ __global__ void __launch_bounds__(kXrThreads, 4) k_attn_cross_rows(CrossArgs a) 
       scores(1, st + 1);
     }
   }
+  // pass 2's first value stages go out now, so their latency overlaps the sweeps
+  constexpr int NB2 = sizeof(S) == 2 ? 3 : 2;  // value load stages in flight
+  Raw8<S> vr[NB2][B];
+  auto loadv = [&](int buf, int st) {  // keys past the end re-read the last one (weight 0)
+#pragma unroll
+    for (int b = 0; b < B; ++b) vr[buf][b].load(Vx + (uint32_t)min(key_of(st, b), nk - 1) * kHeadDim + 8 * g);
+  };
+#pragma unroll
+  for (int i = 0; i < NB2 - 1; ++i) loadv(i, i);
   __syncthreads();
   // sweeps over the scores, one thread per (frame, row): row maxima, then
   // probabilities in place and the row sums; each row's 56 partials are then
@@ -430,11 +516,6 @@ __global__ void __launch_bounds__(kXrThreads, 4) k_attn_cross_rows(CrossArgs a) 
 #pragma unroll
     for (int e = 0; e < 8; ++e) acc[r][e] = 0.f;
   {
-    Raw8<S> vr[2][B];
-    auto load = [&](int buf, int st) {
-#pragma unroll
-      for (int b = 0; b < B; ++b) vr[buf][b].load(Vx + (uint32_t)min(key_of(st, b), nk - 1) * kHeadDim + 8 * g);
-    };
     auto accumulate = [&](int buf, int st) {
 #pragma unroll
       for (int b = 0; b < B; ++b) {
@@ -452,12 +533,12 @@ __global__ void __launch_bounds__(kXrThreads, 4) k_attn_cross_rows(CrossArgs a) 
           for (int e = 0; e < 8; ++e) acc[r][e] = fmaf(p[r], v8[e], acc[r][e]);
       }
     };
-    load(0, 0);
-    for (int st = 0; st < nst; st += 2) {
-      load(1, st + 1);
-      accumulate(0, st);
-      load(0, st + 2);
-      accumulate(1, st + 1);
+    for (int st0 = 0; st0 < nst; st0 += NB2) {
+#pragma unroll
+      for (int i = 0; i < NB2; ++i) {
+        loadv((i + NB2 - 1) % NB2, st0 + i + NB2 - 1);
+        accumulate(i, st0 + i);
+      }
     }
   }
   // fold the key lanes of each dim group and publish per wave, row by row so each
@@ -488,25 +569,43 @@ __global__ void __launch_bounds__(kXrThreads, 4) k_attn_cross_rows(CrossArgs a) 
   }
 }
 
-// Merge of the chunk records of one (head, slot) in chunk order.
-constexpr int kXmThreads = 192;
+// Merge of the chunk records of one (head, slot): one thread per (row, dim).  The
+// records are read kXmGroup chunks at a time with every load of a group issued
+// together (indices clamped, chunks past the end weighted 0); groups combine with
+// the same max-shifted rule.
+constexpr int kXmThreads = kRows * 64;
+constexpr int kXmGroup = 16;
 template <typename S>
 __global__ void __launch_bounds__(kXmThreads) k_attn_cross_merge(CrossArgs a) {
   StampScope stamp_scope(a.stamp);
   const int head = blockIdx.x, slot = a.slot0 + blockIdx.y;
+  const int t = threadIdx.x, r = t >> 6, dim = t & 63;
   const float* part = a.part + (size_t)(blockIdx.y * a.n_head + head) * a.nchunk * kXrPart;
-  for (int t = threadIdx.x; t < kRows * 64; t += kXmThreads) {
-    const int r = t >> 6, dim = t & 63;
-    float M = -INFINITY;
-    for (int i = 0; i < a.nchunk; ++i) M = fmaxf(M, part[i * kXrPart + r]);
-    float L = 0.f, o = 0.f;
-    for (int i = 0; i < a.nchunk; ++i) {
-      const float f = __expf(part[i * kXrPart + r] - M);
-      L = fmaf(f, part[i * kXrPart + 16 + r], L);
-      o = fmaf(f, part[i * kXrPart + 32 + t], o);
+  float M = -INFINITY, L = 0.f, o = 0.f;
+  for (int c0 = 0; c0 < a.nchunk; c0 += kXmGroup) {
+    float m[kXmGroup], l[kXmGroup], v[kXmGroup];
+#pragma unroll
+    for (int j = 0; j < kXmGroup; ++j) {
+      const float* pc = part + (size_t)min(c0 + j, a.nchunk - 1) * kXrPart;
+      m[j] = pc[r];
+      l[j] = pc[16 + r];
+      v[j] = pc[32 + t];
     }
-    put_op<S>(a.out, a.nsplit, a.R9, slot * kRows + r, head * kHeadDim + dim, o / L);
+    float Mg = M;
+#pragma unroll
+    for (int j = 0; j < kXmGroup; ++j) Mg = fmaxf(Mg, m[j]);
+    const float f0 = __expf(M - Mg);  // 0 before the first group
+    L *= f0;
+    o *= f0;
+#pragma unroll
+    for (int j = 0; j < kXmGroup; ++j) {
+      const float f = c0 + j < a.nchunk ? __expf(m[j] - Mg) : 0.f;
+      L = fmaf(f, l[j], L);
+      o = fmaf(f, v[j], o);
+    }
+    M = Mg;
   }
+  put_op<S>(a.out, a.nsplit, a.R9, slot * kRows + r, head * kHeadDim + dim, o / L);
 }
 
 // ---------------------------------------------------------------- causal self-attention

@@ -162,29 +162,27 @@ __device__ __forceinline__ void fill_rows(const BeginArgs& a, int slot, const in
   const S* P = reinterpret_cast<const S*>(a.pos);
   const int nch = a.d >> 3;
   float e8[kBeginTasks][8], p8[kBeginTasks][8];
+  // every load unconditionally (tasks past the nine rows re-read row 8), so all
+  // chunks are in flight together; rows that take no embedding / no position
+  // read one anyway and zero it below
 #pragma unroll
   for (int j = 0; j < kBeginTasks; ++j) {
-    const int t = threadIdx.x + 256 * j, i = t / nch, c = 8 * (t % nch);
-    if (i < kRows) {
-      const int tok = toks[i];
-      const bool from_mask = mask_rows && i > 0;
-      if (!from_mask) {
-        const size_t ei = a.emb_kind == W_F32   ? wfrag32_index(tok, c, a.d / 16)
-                          : a.emb_kind == W_F16 ? wfrag16_index(tok, c, a.d / 32)
-                                                : (size_t)tok * a.d + c;
-        ld8(E + ei, e8[j]);
-      } else {
+    const int t = threadIdx.x + 256 * j, i = min(t / nch, kRows - 1), c = 8 * (t % nch);
+    const int tok = toks[i];
+    const size_t ei = a.emb_kind == W_F32   ? wfrag32_index(tok, c, a.d / 16)
+                      : a.emb_kind == W_F16 ? wfrag16_index(tok, c, a.d / 32)
+                                            : (size_t)tok * a.d + c;
+    ld8(E + ei, e8[j]);
+    ld8(mask_rows ? P + c : P + (size_t)poss[i] * a.d + c, p8[j]);
+  }
 #pragma unroll
-        for (int e = 0; e < 8; ++e) e8[j][e] = 0.f;
-      }
-      if (mask_rows) {
-        if (from_mask) ld8(P + c, p8[j]);
-        else {
+  for (int j = 0; j < kBeginTasks; ++j) {
+    const int t = threadIdx.x + 256 * j, i = t / nch;
+    if (mask_rows) {  // draft block: row 0 is the anchor's embedding, rows 1.. the mask vector
 #pragma unroll
-          for (int e = 0; e < 8; ++e) p8[j][e] = 0.f;
-        }
-      } else {
-        ld8(P + (size_t)poss[i] * a.d + c, p8[j]);
+      for (int e = 0; e < 8; ++e) {
+        if (i > 0) e8[j][e] = 0.f;
+        else p8[j][e] = 0.f;
       }
     }
   }
@@ -339,56 +337,63 @@ __global__ void k_accept_greedy(AcceptArgs a) {
   if (s >= a.n) return;
   const int slot = a.slot0 + s;
   int* st = a.state + slot * kStateInts;
-  const int nv = st[ST_NV];
-  const int K = a.block_k;
-  int* out = a.out ? a.out + (size_t)s * (K + 1) : nullptr;
-  if (nv == 0) {
-    if (a.n_out) a.n_out[s] = 0;
-    if (a.n_acc) a.n_acc[s] = 0;
-    if (a.done) a.done[s] = st[ST_LIVE] ? 1 : 0;
-    if (st[ST_LIVE]) st[ST_DONE] = 1;
-    return;
-  }
-  const int k = nv - 1;
+  // every read before the first branch or store (the stores below may alias)
+  const int nv = st[ST_NV], live = st[ST_LIVE], L = st[ST_L], emitted = st[ST_EMITTED];
+  const int max_new = st[ST_MAX_NEW], step = st[ST_STEP];
   int tok[kRows], g[kRows];
 #pragma unroll
   for (int i = 0; i < kRows; ++i) {
     tok[i] = a.tok[slot * kRows + i];
     g[i] = a.g[slot * kRows + i];
   }
+  const int K = a.block_k;
+  int* out = a.out ? a.out + (size_t)s * (K + 1) : nullptr;
+  if (nv == 0) {
+    if (a.n_out) a.n_out[s] = 0;
+    if (a.n_acc) a.n_acc[s] = 0;
+    if (a.done) a.done[s] = live ? 1 : 0;
+    if (live) st[ST_DONE] = 1;
+    return;
+  }
+  const int k = nv - 1;
   int acc = 0;
   while (acc < k && tok[acc + 1] == g[acc]) ++acc;
-  int nemit = 0;
-  bool fin = false;
-  for (int e = 0; e < acc; ++e) {
-    const int c = tok[e + 1];
-    if (out) out[nemit] = c;
-    ++nemit;
-    if (c == a.eos) { fin = true; break; }
-  }
-  int last;
-  if (!fin) {
-    last = g[acc];
-    if (out) out[nemit] = last;
-    ++nemit;
-    fin = (last == a.eos);
+  // accepted candidates up to and including the first end-of-transcript one
+  int nacc = acc;
+  bool eos_acc = false;
+  for (int e = 0; e < acc; ++e)
+    if (tok[e + 1] == a.eos) {
+      nacc = e + 1;
+      eos_acc = true;
+      break;
+    }
+  int nemit, last;
+  bool fin;
+  if (eos_acc) {  // the transcript ends inside the accepted prefix: no correction token
+    nemit = nacc;
+    acc = nacc;
+    last = tok[nacc];
+    fin = true;
   } else {
-    last = tok[nemit];
-    acc = nemit;
+    nemit = acc + 1;
+    last = g[acc];
+    fin = last == a.eos;
   }
-  const int L = st[ST_L];
   st[ST_HPOS] = L;
   st[ST_HN] = nv;
   st[ST_L] = L + 1 + acc;
   st[ST_ANCHOR] = last;
-  st[ST_EMITTED] += nemit;
-  st[ST_STEP] += 1;
+  st[ST_EMITTED] = emitted + nemit;
+  st[ST_STEP] = step + 1;
   st[ST_K] = k;
   st[ST_A] = acc;
-  const bool done = fin || st[ST_EMITTED] >= st[ST_MAX_NEW] || st[ST_L] >= a.n_ctx;
+  const bool done = fin || emitted + nemit >= max_new || L + 1 + acc >= a.n_ctx;
   st[ST_DONE] = done;
-  if (out)
-    for (int j = nemit; j <= K; ++j) out[j] = -1;
+  if (out) {
+#pragma unroll
+    for (int j = 0; j < kRows; ++j)
+      if (j <= K) out[j] = j < acc ? tok[j + 1] : j == acc && !eos_acc ? last : -1;
+  }
   if (a.n_out) a.n_out[s] = nemit;
   if (a.n_acc) a.n_acc[s] = acc;
   if (a.done) a.done[s] = done;
