@@ -269,7 +269,7 @@ template <typename S>
 constexpr int kCrossB = sizeof(S) == 2 ? 24 : 12;  // key octets in flight per wave
 template <typename S>
 __global__ void __launch_bounds__(kCrossThreads) k_attn_cross(CrossArgs a) {
-  StampScope stamp_scope(a.stamp);
+  StampScope stamp_scope(a.stamp, kCrossThreads);
   constexpr int NW = kCrossThreads / 64;
   __shared__ float part[NW][4][64];
   __shared__ float pm[NW], pl[NW];
@@ -315,14 +315,29 @@ inline size_t xr_lds_bytes(int chunk) {
   const size_t sc = (size_t)chunk * kXrStride, wacc = (size_t)kXrWaves * kRows * 64;
   return 4 * (sc > wacc ? sc : wacc);
 }
-// Sum over the key lanes (lane bits 3..5) for each dim group (lane bits 0..2): a
-// DPP rotation within 16-lane rows, then the gfx950 row-pair and half-wave swaps.
-__device__ __forceinline__ float fold_key_lanes(float v) {
-  v += dpp<kDppRor8>(v);
-  const auto p = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
-  v = __uint_as_float(p[0]) + __uint_as_float(p[1]);
-  const auto q = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
-  return __uint_as_float(q[0]) + __uint_as_float(q[1]);
+// Sum of acc[r][e] over the eight key lanes of each dim group (lane bits 3..5),
+// scattered so that lane l ends with out[r] = the sums of dim 8 (l % 8) + l / 8
+// for the nine rows.  Each level halves the values a lane holds: the half-wave
+// swap pairs dims e and e + 4 (lanes < 32 keep e), the row-pair swap pairs e and
+// e + 2 (even 16-lane rows keep e), a DPP rotation by 8 within 16 lanes pairs e and
+// e + 1 (lanes with bit 3 clear keep e).  63 exchanges instead of 72 full folds.
+__device__ __forceinline__ void scatter_key_lanes(float (*acc)[8], float* out) {
+  const bool hi8 = (threadIdx.x & 8) != 0;
+#pragma unroll
+  for (int r = 0; r < kRows; ++r) {
+    float u[4], v[2];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const auto x = __builtin_amdgcn_permlane32_swap(__float_as_uint(acc[r][e]), __float_as_uint(acc[r][e + 4]), false, false);
+      u[e] = __uint_as_float(x[0]) + __uint_as_float(x[1]);
+    }
+#pragma unroll
+    for (int e = 0; e < 2; ++e) {
+      const auto x = __builtin_amdgcn_permlane16_swap(__float_as_uint(u[e]), __float_as_uint(u[e + 2]), false, false);
+      v[e] = __uint_as_float(x[0]) + __uint_as_float(x[1]);
+    }
+    out[r] = (hi8 ? v[1] : v[0]) + dpp<kDppRor8>(hi8 ? v[0] : v[1]);
+  }
 }
 
 // Pass 1 on the matrix cores (bf16 keys): S^T[frame][row] = K[frame] . q[row] over
@@ -399,7 +414,7 @@ __device__ __forceinline__ void xr_scores_mfma(const CrossArgs& a, int slot, int
 
 template <typename S>
 __global__ void __launch_bounds__(kXrThreads, 4) k_attn_cross_rows(CrossArgs a) {
-  StampScope stamp_scope(a.stamp);
+  StampScope stamp_scope(a.stamp, kXrThreads);
   // key octets per vector load stage (the fp32 score pass and the value pass)
   constexpr int NW = kXrWaves, B = sizeof(S) == 2 ? 2 : 1;
   extern __shared__ float sc[];
@@ -475,9 +490,16 @@ __global__ void __launch_bounds__(kXrThreads, 4) k_attn_cross_rows(CrossArgs a) 
   // reduced by one wave (rows 0..7 by waves 0..7, row 8 by wave 0)
   const bool sweeper = threadIdx.x < kXrSweepKeys * kRows;
   const int sr = threadIdx.x % kRows;
+  constexpr int U = 4;  // sweep steps whose LDS reads are issued together
   if (sweeper) {
     float m = -INFINITY;
-    for (int key = threadIdx.x / kRows; key < nk; key += kXrSweepKeys) m = fmaxf(m, sc[key * kXrStride + sr]);
+    for (int key0 = threadIdx.x / kRows; key0 < nk; key0 += U * kXrSweepKeys) {
+      float x[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) x[u] = sc[min(key0 + u * kXrSweepKeys, nk - 1) * kXrStride + sr];
+#pragma unroll
+      for (int u = 0; u < U; ++u) m = fmaxf(m, x[u]);  // a clamped re-read repeats a present score
+    }
     lpart[threadIdx.x] = m;
   }
   __syncthreads();
@@ -493,10 +515,19 @@ __global__ void __launch_bounds__(kXrThreads, 4) k_attn_cross_rows(CrossArgs a) 
   if (sweeper) {
     const float M = rmax[sr];
     float lp = 0.f;
-    for (int key = threadIdx.x / kRows; key < nk; key += kXrSweepKeys) {
-      const float p = __expf(sc[key * kXrStride + sr] - M);
-      sc[key * kXrStride + sr] = p;
-      lp += p;
+    for (int key0 = threadIdx.x / kRows; key0 < nk; key0 += U * kXrSweepKeys) {
+      float x[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) x[u] = sc[min(key0 + u * kXrSweepKeys, nk - 1) * kXrStride + sr];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int key = key0 + u * kXrSweepKeys;
+        const float p = __expf(x[u] - M);
+        if (key < nk) {
+          sc[key * kXrStride + sr] = p;
+          lp += p;
+        }
+      }
     }
     lpart[threadIdx.x] = lp;
   }
@@ -541,16 +572,15 @@ __global__ void __launch_bounds__(kXrThreads, 4) k_attn_cross_rows(CrossArgs a) 
       }
     }
   }
-  // fold the key lanes of each dim group and publish per wave, row by row so each
-  // row's sums die at its store
+  // sum the key lanes of each dim group and publish per wave: lane l holds the
+  // nine rows of dim 8 (l % 8) + l / 8
   __syncthreads();  // every wave is done with the probabilities
+  {
+    float o9[kRows];
+    scatter_key_lanes(acc, o9);
+    const int dim = 8 * g + kl;
 #pragma unroll
-  for (int r = 0; r < kRows; ++r) {
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const float t = fold_key_lanes(acc[r][e]);
-      if (lane < 8) wacc[w][r][8 * g + e] = t;
-    }
+    for (int r = 0; r < kRows; ++r) wacc[w][r][dim] = o9[r];
   }
   __syncthreads();
   const int pair = blockIdx.y * a.n_head + head;
@@ -569,6 +599,193 @@ __global__ void __launch_bounds__(kXrThreads, 4) k_attn_cross_rows(CrossArgs a) 
   }
 }
 
+// ---------------------------------------------------------------- cross-attention, bf16, matrix cores
+// Block (head, slot, chunk of 128 KS frames), four waves of 32 KS frames each, all
+// nine query rows, both products on the matrix cores.  Keys are row-major
+// [frame][64]; values are stored transposed [dim][vt_frames] (zeros past the last
+// frame), so both operands are 16-byte reads of consecutive elements.  Every load
+// of the block is issued at its start (query rows, key tiles, value fragments),
+// so the block waits for memory once.
+//   scores       S^T = K q^T per 16-frame tile (v_mfma_f32_16x16x32_bf16, the query
+//                rows as hi + lo bf16 planes): lane l gets row l % 16 of frames
+//                4 (l / 16)..+3 of the tile.
+//   softmax      the chunk's row maxima (lane swaps, then across waves in LDS);
+//                p = exp(s - max) in place, row sums.
+//   values       O^T = V^T P^T per 32-frame step: two lane swaps (half-wave, then
+//                row pair) turn the two score tiles of the step into the B operand
+//                (lane l: row l % 16, frames 8 (l / 16)..+7); P as hi + lo planes.
+//   output       waves summed in LDS; one chunk: O / l, else the chunk's
+//                (max, l, O) record for the merge kernel.
+constexpr int kMxThreads = 256;
+constexpr int kMxWaves = kMxThreads / 64;
+
+__device__ __forceinline__ bf16x8 pack_bf16x8(const uint32_t* b) {
+  return __builtin_bit_cast(bf16x8, make_uint4(b[0] | b[1] << 16, b[2] | b[3] << 16, b[4] | b[5] << 16, b[6] | b[7] << 16));
+}
+// v = hi + lo: hi truncated to bf16, lo = RNE(v - hi) (2^-17 relative)
+__device__ __forceinline__ void split_planes(const float* v, bf16x8& hi, bf16x8& lo) {
+  uint32_t hb[8], lb[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    hb[j] = __float_as_uint(v[j]) >> 16;
+    lb[j] = bf16_bits_rne(v[j] - __uint_as_float(hb[j] << 16));
+  }
+  hi = pack_bf16x8(hb);
+  lo = pack_bf16x8(lb);
+}
+
+template <int KS>
+__global__ void __launch_bounds__(kMxThreads, 3) k_attn_cross_mx(CrossArgs a) {
+  StampScope stamp_scope(a.stamp, kMxThreads);
+  constexpr int NT = 2 * KS;  // 16-frame score tiles per wave
+  __shared__ float wmax[kMxWaves][16];
+  __shared__ float wsum[kMxWaves][16];
+  __shared__ float wo[kMxWaves][kRows][64];
+  const int head = blockIdx.x, slot = a.slot0 + blockIdx.y, c = blockIdx.z;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, n = lane & 15, kg = lane >> 4;
+  const int F = a.n_frames, Fp = a.vt_frames;
+  const int f0w = c * a.chunk + w * 32 * KS;  // first frame of this wave
+  const bf16* base = reinterpret_cast<const bf16*>(a.kv) + (size_t)slot * a.d * (F + Fp);
+  const bf16* Kh = base + (size_t)head * F * kHeadDim;
+  const bf16* Vt = base + (size_t)a.n_head * F * kHeadDim + (size_t)head * kHeadDim * Fp;
+  // loads: query row n (rows >= 9 re-read row 8, zeroed below), key tiles (frames
+  // past the end re-read the last one, masked below), value fragments (inside the
+  // padded rows)
+  float4 qx[2][2];
+  {
+    const float* qr = a.q + (size_t)(slot * kRows + min(n, kRows - 1)) * a.ldq + head * kHeadDim + 8 * kg;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      qx[h][0] = *reinterpret_cast<const float4*>(qr + 32 * h);
+      qx[h][1] = *reinterpret_cast<const float4*>(qr + 32 * h + 4);
+    }
+  }
+  bf16x8 kt[NT][2];
+#pragma unroll
+  for (int t = 0; t < NT; ++t) {
+    const int f = min(f0w + 16 * t + n, F - 1);
+    const bf16x8* kp = reinterpret_cast<const bf16x8*>(Kh + (size_t)f * kHeadDim) + kg;
+    kt[t][0] = kp[0];
+    kt[t][1] = kp[4];
+  }
+  bf16x8 vt[KS][4];
+#pragma unroll
+  for (int st = 0; st < KS; ++st)
+#pragma unroll
+    for (int dt = 0; dt < 4; ++dt)
+      vt[st][dt] = *reinterpret_cast<const bf16x8*>(Vt + (size_t)(16 * dt + n) * Fp + f0w + 32 * st + 8 * kg);
+  __builtin_amdgcn_sched_barrier(0);  // every load above is issued before any use below
+  // query planes of the scaled rows
+  bf16x8 qh[2], ql[2];
+  {
+    const float scale = n < kRows ? 0.125f : 0.f;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const float v[8] = {qx[h][0].x * scale, qx[h][0].y * scale, qx[h][0].z * scale, qx[h][0].w * scale,
+                          qx[h][1].x * scale, qx[h][1].y * scale, qx[h][1].z * scale, qx[h][1].w * scale};
+      split_planes(v, qh[h], ql[h]);
+    }
+  }
+  // scores and this wave's row maxima
+  floatx4 sct[NT];
+  float mx = -INFINITY;
+#pragma unroll
+  for (int t = 0; t < NT; ++t) {
+    floatx4 acc = {0.f, 0.f, 0.f, 0.f};
+    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kt[t][0], qh[0], acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kt[t][0], ql[0], acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kt[t][1], qh[1], acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kt[t][1], ql[1], acc, 0, 0, 0);
+    sct[t] = acc;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      if (f0w + 16 * t + 4 * kg + i < F) mx = fmaxf(mx, acc[i]);
+  }
+  {
+    const auto x = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx), false, false);
+    mx = fmaxf(__uint_as_float(x[0]), __uint_as_float(x[1]));
+    const auto y = __builtin_amdgcn_permlane16_swap(__float_as_uint(mx), __float_as_uint(mx), false, false);
+    mx = fmaxf(__uint_as_float(y[0]), __uint_as_float(y[1]));
+    if (lane < 16) wmax[w][lane] = mx;
+  }
+  __syncthreads();
+  float M = wmax[0][n];
+#pragma unroll
+  for (int i = 1; i < kMxWaves; ++i) M = fmaxf(M, wmax[i][n]);  // finite: frame c * chunk is present
+  // probabilities and row sums
+  float lsum = 0.f;
+#pragma unroll
+  for (int t = 0; t < NT; ++t)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const float p = f0w + 16 * t + 4 * kg + i < F ? __expf(sct[t][i] - M) : 0.f;
+      sct[t][i] = p;
+      lsum += p;
+    }
+  // values: O^T[dim][row] over the wave's 32-frame steps
+  floatx4 oacc[4];
+#pragma unroll
+  for (int dt = 0; dt < 4; ++dt) oacc[dt] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int st = 0; st < KS; ++st) {
+    float pb[8];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      // tiles 2st (frames 4kg + i) and 2st + 1 (16 + 4kg + i) -> frames 8kg..8kg+7
+      const auto x = __builtin_amdgcn_permlane32_swap(__float_as_uint(sct[2 * st][i]), __float_as_uint(sct[2 * st + 1][i]),
+                                                      false, false);
+      const auto y = __builtin_amdgcn_permlane16_swap(x[0], x[1], false, false);
+      pb[i] = __uint_as_float(y[0]);
+      pb[4 + i] = __uint_as_float(y[1]);
+    }
+    bf16x8 ph, pl;
+    split_planes(pb, ph, pl);
+#pragma unroll
+    for (int dt = 0; dt < 4; ++dt) {
+      oacc[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vt[st][dt], ph, oacc[dt], 0, 0, 0);
+      oacc[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vt[st][dt], pl, oacc[dt], 0, 0, 0);
+    }
+  }
+  // this wave's row sums (over the four frame groups) and outputs to LDS
+  {
+    const auto x = __builtin_amdgcn_permlane32_swap(__float_as_uint(lsum), __float_as_uint(lsum), false, false);
+    lsum = __uint_as_float(x[0]) + __uint_as_float(x[1]);
+    const auto y = __builtin_amdgcn_permlane16_swap(__float_as_uint(lsum), __float_as_uint(lsum), false, false);
+    lsum = __uint_as_float(y[0]) + __uint_as_float(y[1]);
+  }
+  if (n < kRows) {
+    if (lane < 16) wsum[w][n] = lsum;
+#pragma unroll
+    for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) wo[w][n][16 * dt + 4 * kg + i] = oacc[dt][i];
+  }
+  __syncthreads();
+  const int pair = blockIdx.y * a.n_head + head;
+  float* part = a.part + ((size_t)pair * a.nchunk + c) * kXrPart;
+  for (int t = threadIdx.x; t < kRows * 64; t += kMxThreads) {
+    const int r = t >> 6, dim = t & 63;
+    float o = 0.f, L = 0.f;
+#pragma unroll
+    for (int i = 0; i < kMxWaves; ++i) {
+      o += wo[i][r][dim];
+      L += wsum[i][r];
+    }
+    if (a.nchunk == 1) {
+      put_op<bf16>(a.out, a.nsplit, a.R9, slot * kRows + r, head * kHeadDim + dim, o / L);
+    } else {
+      part[32 + t] = o;
+      if (dim == 0) {
+        float m = wmax[0][r];
+#pragma unroll
+        for (int i = 1; i < kMxWaves; ++i) m = fmaxf(m, wmax[i][r]);
+        part[r] = m;
+        part[16 + r] = L;
+      }
+    }
+  }
+}
+
 // Merge of the chunk records of one (head, slot): one thread per (row, dim).  The
 // records are read kXmGroup chunks at a time with every load of a group issued
 // together (indices clamped, chunks past the end weighted 0); groups combine with
@@ -577,7 +794,7 @@ constexpr int kXmThreads = kRows * 64;
 constexpr int kXmGroup = 16;
 template <typename S>
 __global__ void __launch_bounds__(kXmThreads) k_attn_cross_merge(CrossArgs a) {
-  StampScope stamp_scope(a.stamp);
+  StampScope stamp_scope(a.stamp, kXmThreads);
   const int head = blockIdx.x, slot = a.slot0 + blockIdx.y;
   const int t = threadIdx.x, r = t >> 6, dim = t & 63;
   const float* part = a.part + (size_t)(blockIdx.y * a.n_head + head) * a.nchunk * kXrPart;
@@ -615,7 +832,7 @@ __global__ void __launch_bounds__(kXmThreads) k_attn_cross_merge(CrossArgs a) {
 constexpr int kSelfThreads = 256;
 template <typename S>
 __global__ void __launch_bounds__(kSelfThreads) k_attn_self(AttnArgs a) {
-  StampScope stamp_scope(a.stamp);
+  StampScope stamp_scope(a.stamp, kSelfThreads);
   constexpr int NW = kSelfThreads / 64;
   static_assert(NW * 14 * 8 >= kMaxCtx, "one batch of key octets covers the context");
   __shared__ float part[NW][4][64];
@@ -659,7 +876,7 @@ __global__ void __launch_bounds__(kSelfThreads) k_attn_self(AttnArgs a) {
 // positions.
 template <typename S>
 __global__ void __launch_bounds__(kSelfThreads) k_attn_draft(AttnArgs a) {
-  StampScope stamp_scope(a.stamp);
+  StampScope stamp_scope(a.stamp, kSelfThreads);
   constexpr int NT = kSelfThreads, NW = NT / 64;
   __shared__ float sc[kMaxCtx + 16];
   __shared__ float part[NW][64];
@@ -755,11 +972,16 @@ void Ops<S>::attn_draft(const AttnArgs& a, int n, hipStream_t st) {
 // otherwise one block per (head, row)
 template <typename S>
 void Ops<S>::attn_cross(const CrossArgs& a, int n, hipStream_t st) {
-  if (n == 1) {  // one slot: a block per (head, row) streams all frames (9 blocks per head share an L2)
-    k_attn_cross<S><<<dim3(row_blocks(a.n_head), n), kCrossThreads, 0, st>>>(a);
-    return;
+  if constexpr (sizeof(S) == 2) {  // transposed values, matrix cores, frame chunks + merge
+    if (a.chunk == 128) k_attn_cross_mx<1><<<dim3(a.n_head, n, a.nchunk), kMxThreads, 0, st>>>(a);
+    else k_attn_cross_mx<2><<<dim3(a.n_head, n, a.nchunk), kMxThreads, 0, st>>>(a);
+  } else {
+    if (n == 1) {  // one slot: a block per (head, row) streams all frames (9 blocks per head share an L2)
+      k_attn_cross<S><<<dim3(row_blocks(a.n_head), n), kCrossThreads, 0, st>>>(a);
+      return;
+    }
+    k_attn_cross_rows<S><<<dim3(a.n_head, n, a.nchunk), kXrThreads, xr_lds_bytes(a.chunk), st>>>(a);
   }
-  k_attn_cross_rows<S><<<dim3(a.n_head, n, a.nchunk), kXrThreads, xr_lds_bytes(a.chunk), st>>>(a);
   if (a.nchunk > 1) k_attn_cross_merge<S><<<dim3(a.n_head, n), kXmThreads, 0, st>>>(a);
 }
 

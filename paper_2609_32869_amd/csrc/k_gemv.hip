@@ -289,7 +289,7 @@ __device__ __forceinline__ void finish_tile(const GemvArgs& a, float (*sv)[TC + 
 // ---------------------------------------------------------------- bf16, 16-column tiles
 template <int EPI, int NW>
 __global__ void __launch_bounds__(NW * 64) k_gemv16(GemvArgs a) {
-  StampScope stamp_scope(a.stamp);
+  StampScope stamp_scope(a.stamp, NW * 64);
   constexpr int U = NW >= 16 ? kU / 2 : kU;
   __shared__ float red[NW][32][17];
   __shared__ float sv[32][17];
@@ -353,7 +353,7 @@ __global__ void __launch_bounds__(NW * 64) k_gemv16(GemvArgs a) {
 // with more than one k-range the epilogue must be EPI_PART.
 template <int EPI, int NW, int CT>
 __global__ void __launch_bounds__(NW * 64) k_gemv16w(GemvArgs a) {
-  StampScope stamp_scope(a.stamp);
+  StampScope stamp_scope(a.stamp, NW * 64);
   constexpr int U = CT >= 4 ? 4 : 8;
   constexpr int TC = 16 * CT;
   __shared__ float red[NW][32][TC + 1];
@@ -442,7 +442,7 @@ __global__ void __launch_bounds__(NW * 64) k_gemv16w(GemvArgs a) {
 constexpr int kGemmU = 2;
 template <int EPI>
 __global__ void __launch_bounds__(256) k_gemm16(GemvArgs a, int mb0, int nmb, int nnb) {
-  StampScope stamp_scope(a.stamp);
+  StampScope stamp_scope(a.stamp, 256);
   __shared__ float sv[64][65];
   __shared__ float ov[EPI == EPI_ARGMAX ? 64 : 1][64];
   __shared__ float oz[EPI == EPI_ARGMAX ? 64 : 1][64];
@@ -520,7 +520,7 @@ __global__ void __launch_bounds__(256) k_gemm16(GemvArgs a, int mb0, int nmb, in
 // ---------------------------------------------------------------- bf16, 32-column tiles
 template <int EPI, int NW>
 __global__ void __launch_bounds__(NW * 64) k_gemv32(GemvArgs a) {
-  StampScope stamp_scope(a.stamp);
+  StampScope stamp_scope(a.stamp, NW * 64);
   constexpr int U = NW >= 16 ? kU / 2 : kU;
   __shared__ float red[NW][32][33];
   __shared__ float sv[32][33];
@@ -688,7 +688,7 @@ struct LnRows {
 // 16-column tiles; every wave's k-steps fit one batch of loads (K <= kLnFoldMaxK).
 template <int EPI, int NW, int U>
 __global__ void __launch_bounds__(NW * 64) k_gemv16_ln(GemvArgs a) {
-  StampScope stamp_scope(a.stamp);
+  StampScope stamp_scope(a.stamp, NW * 64);
   __shared__ uint4 aop[kLnFoldMaxK / 32 * 2 * 64];
   __shared__ float red[NW][32][17];
   __shared__ float sv[32][17];
@@ -742,7 +742,7 @@ __global__ void __launch_bounds__(NW * 64) k_gemv16_ln(GemvArgs a) {
 // 32-column tiles; every wave's k-steps fit one batch of loads (K <= kLnFoldMaxK).
 template <int EPI, int NW, int U>
 __global__ void __launch_bounds__(NW * 64) k_gemv32_ln(GemvArgs a) {
-  StampScope stamp_scope(a.stamp);
+  StampScope stamp_scope(a.stamp, NW * 64);
   __shared__ uint4 aop[kLnFoldMaxK / 16 * 64];
   __shared__ float red[NW][32][33];
   __shared__ float sv[32][33];
@@ -794,7 +794,7 @@ __global__ void __launch_bounds__(NW * 64) k_gemv32_ln(GemvArgs a) {
 // k does not depend on the order in which k is visited).
 template <int EPI, int NW>
 __global__ void __launch_bounds__(NW * 64) k_gemv_f32(GemvArgs a) {
-  StampScope stamp_scope(a.stamp);
+  StampScope stamp_scope(a.stamp, NW * 64);
   constexpr int U = NW >= 16 ? kU / 2 : kU;
   __shared__ float red[NW][32][17];
   __shared__ float sv[32][17];

@@ -17,7 +17,7 @@ namespace wf {
 // block of 256 threads per row; the row stays in registers (d <= 2048).
 template <typename S>
 __global__ void __launch_bounds__(256) k_ln_operand(LnArgs a) {
-  StampScope stamp_scope(a.stamp);
+  StampScope stamp_scope(a.stamp, 256);
   __shared__ float red[8];
   const int row = a.row0 + blockIdx.x;
   const float* xr = a.x + (size_t)row * a.d;
@@ -584,7 +584,9 @@ void accept_sample(const SampleArgs& a, hipStream_t st) {
 
 // ---------------------------------------------------------------- encode: cross K/V
 // C[f, n] = sum_k A[f, k] W[n, k] + b[n] for the 2d key/value columns of one
-// block, written to the per-head frame-major cross cache.  64x64 tiles, fp32
+// block, written to the per-head cross cache: keys frame-major [head][frame][64];
+// values frame-major too, or transposed [head][dim][vt_frames] when vt_frames > 0
+// (bf16 storage, read by the matrix-core cross-attention).  64x64 tiles, fp32
 // accumulation.
 template <typename S>
 __global__ void __launch_bounds__(256) k_gemm_xkv(XkvArgs a) {
@@ -619,6 +621,24 @@ __global__ void __launch_bounds__(256) k_gemm_xkv(XkvArgs a) {
     __syncthreads();
   }
   S* out = reinterpret_cast<S*>(a.out);
+  if (a.vt_frames > 0 && n0 >= a.d) {
+    // value columns of one head, stored transposed [dim][frame]: the tile goes
+    // through LDS so that consecutive threads write consecutive frames; frames
+    // from n_frames to vt_frames are written as zeros
+    __shared__ float Ct[64][65];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) Ct[tx * 4 + j][ty * 4 + i] = acc[i][j] + to_f(bias[n0 + tx * 4 + j]);
+    __syncthreads();
+    const int head = (n0 - a.d) >> 6;
+    S* vt = out + (size_t)a.n_head * M * kHeadDim + (size_t)head * kHeadDim * a.vt_frames;
+    for (int t = threadIdx.x; t < 64 * 64; t += 256) {
+      const int dim = t >> 6, fl = t & 63, f = m0 + fl;
+      if (f < a.vt_frames) vt[(size_t)dim * a.vt_frames + f] = from_f<S>(f < M ? Ct[dim][fl] : 0.f);
+    }
+    return;
+  }
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const int f = m0 + ty * 4 + i;
@@ -643,7 +663,7 @@ constexpr int kRlnThreads = 1024;
 constexpr int kRlnMaxParts = 16;
 template <typename S>
 __global__ void __launch_bounds__(kRlnThreads) k_reduce_ln(RlnArgs a) {
-  StampScope stamp_scope(a.stamp);
+  StampScope stamp_scope(a.stamp, kRlnThreads);
   constexpr int NW = kRlnThreads / 64;
   constexpr int J = 2;  // d <= 2048
   __shared__ float red[2][NW];
@@ -733,7 +753,8 @@ template <typename S>
 void Ops<S>::hist_write(const HistArgs& a, int n, hipStream_t st) { k_hist_write<S><<<dim3(kRows, n), 256, 0, st>>>(a); }
 template <typename S>
 void Ops<S>::gemm_xkv(const XkvArgs& a, hipStream_t st) {
-  k_gemm_xkv<S><<<dim3((a.n_frames + 63) / 64, 2 * a.d / 64), 256, 0, st>>>(a);
+  const int frames = a.vt_frames > a.n_frames ? a.vt_frames : a.n_frames;  // blocks past n_frames write value padding
+  k_gemm_xkv<S><<<dim3((frames + 63) / 64, 2 * a.d / 64), 256, 0, st>>>(a);
 }
 
 void argmax_final(const float* hv, const int* hi, int nblk, int row0, int rows, int* g, float* gmax,

@@ -170,7 +170,8 @@ int compute_layout(const wf_config& c, Layout& L) {
   L.status = region(256);
   L.aux = region(4 * B * 4);
   L.weights = region(w * eb);
-  L.xkv = region(std::max((size_t)(c.n_layer + c.n_draft_layer) * B * 2 * c.n_frames * d * eb, L.stage_bytes));
+  L.xkv = region(std::max((size_t)(c.n_layer + c.n_draft_layer) * B * xkv_slot_elems(c.dtype == WF_BF16, c.n_frames, (int)d) * eb,
+                          L.stage_bytes));
   L.skv = region((size_t)c.n_layer * 2 * B * L.pages_per_slot * H * kPage * kHeadDim * eb);
   L.hkv = region((size_t)c.n_draft_layer * 2 * B * H * c.n_ctx * kHeadDim * eb);
   // matrix operands: 3 bf16 terms per fp32 value as extra rows at batch 1, 2 terms as
@@ -213,7 +214,8 @@ int compute_layout(const wf_config& c, Layout& L) {
   }
   const int nparts = std::max({L.fc2_split, L.nsplit_op == 2 ? kFc2SplitBatch : 0, 1});
   L.part = region((size_t)nparts * R9 * d * 4);
-  L.xpart = region((size_t)kXrMaxPartials * kXrPart * 4);
+  const size_t xrec = c.dtype == WF_BF16 ? B * H * (size_t)cross_mx_chunks(1, c.n_frames) : 0;  // 1 slot: the smallest chunks
+  L.xpart = region(std::max((size_t)kXrMaxPartials, xrec) * kXrPart * 4);
   L.stamps = region((size_t)kStampSlots * kStampWords * 8);
   L.total = o;
   return WF_OK;
@@ -259,7 +261,9 @@ struct Runner {
   const S* W(size_t off) const { return h->at<const S>(L.weights) + off; }
   float* F32(size_t off) const { return h->at<float>(off); }
   int* I32(size_t off) const { return h->at<int>(off); }
-  S* xkv_layer(int l) const { return h->at<S>(L.xkv) + (size_t)l * c.max_batch * 2 * c.n_frames * c.d_model; }
+  size_t xkv_slot() const { return xkv_slot_elems(c.dtype == WF_BF16, c.n_frames, c.d_model); }
+  int vt_frames() const { return c.dtype == WF_BF16 ? xkv_vt_frames(c.n_frames) : 0; }
+  S* xkv_layer(int l) const { return h->at<S>(L.xkv) + (size_t)l * c.max_batch * xkv_slot(); }
   S* skv_layer(int l) const {
     return h->at<S>(L.skv) + (size_t)l * 2 * kv_stride();
   }
@@ -393,7 +397,13 @@ struct Runner {
     a.n_frames = c.n_frames;
     a.nsplit = L.nsplit_op;
     a.R9 = R9();
-    cross_chunks(n * c.n_head, c.n_frames, a.nchunk, a.chunk);
+    a.vt_frames = vt_frames();
+    if (c.dtype == WF_BF16) {
+      a.chunk = cross_mx_chunk(n);
+      a.nchunk = cross_mx_chunks(n, c.n_frames);
+    } else {
+      cross_chunks(n * c.n_head, c.n_frames, a.nchunk, a.chunk);
+    }
     a.part = F32(L.xpart);
     launch("attn_cross", 2.0 * c.n_head * c.n_frames * kHeadDim * eb() * n, [&](unsigned long long* sp) {
       a.stamp = sp;
@@ -598,10 +608,11 @@ struct Runner {
         a.mem = reinterpret_cast<const S*>(mem) + s * per;
         a.w = W(b.w_kv2);
         a.bias = W(b.b_kv2);
-        a.out = xkv_layer(l) + (size_t)slot * 2 * c.n_frames * c.d_model;
+        a.out = xkv_layer(l) + (size_t)slot * xkv_slot();
         a.d = c.d_model;
         a.n_head = c.n_head;
         a.n_frames = c.n_frames;
+        a.vt_frames = vt_frames();
         Ops<S>::gemm_xkv(a, st);
       }
     }

@@ -188,12 +188,14 @@ struct StampScope {
   unsigned long long* s;
   unsigned* left;
   // Must be the kernel's first statement: every thread of the block runs it.
-  __device__ __forceinline__ explicit StampScope(unsigned long long* p) : s(p) {
+  // nthreads is the block size every launch of the kernel uses (a compile-time
+  // constant, so no load of the launch's dimensions delays the start).
+  __device__ __forceinline__ StampScope(unsigned long long* p, int nthreads) : s(p) {
     __shared__ unsigned waves_left;
     left = &waves_left;
     if (s) {
       if (threadIdx.x == 0) {
-        waves_left = (blockDim.x * blockDim.y * blockDim.z + 63) / 64;
+        waves_left = (unsigned)(nthreads + 63) / 64;
         atomicMin(stamp_pair(s), (unsigned long long)wall_clock64());
       }
       __syncthreads();

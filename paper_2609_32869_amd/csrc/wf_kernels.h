@@ -91,9 +91,11 @@ struct AttnArgs {
 struct CrossArgs {
   const float* q;
   int ldq;
-  const void* kv;  // block base of [slot][2][head][frame][64]
+  const void* kv;  // block base: per slot the keys [head][frame][64], then the values
+                   // [head][frame][64] (fp32) or transposed [head][dim][vt_frames] (bf16)
   Operand out;
   int slot0, d, n_head, n_frames, nsplit, R9;
+  int vt_frames;  // padded frame count of the transposed values (bf16), else 0
   int nchunk, chunk;  // frame chunks per (head, slot) and frames per chunk (multiple of 8)
   float* part;        // [pair][nchunk][kXrPart] chunk partials (nchunk > 1)
   unsigned long long* stamp;  // launch timing slot (profiled calls), or null
@@ -102,8 +104,19 @@ struct CrossArgs {
 constexpr int kXrPart = 32 + kRows * 64;
 constexpr int kXrMaxPairs = 128;      // chunking only below this many (head, slot) pairs
 constexpr int kXrMaxPartials = 512;   // pair * chunk records of a chunked launch
-// Chunking of cross-attention over the frames for a few slots (2 to 6 at 20
-// heads): about 240 blocks, chunks of >= 64 frames.  nchunk <= want, so
+// bf16 acoustic memory: values stored transposed with the frame count padded to a
+// multiple of kMxChunkMax (zeros past n_frames), so every matrix-core chunk reads
+// whole 16-byte groups inside its slot.  Cross-attention blocks take chunks of
+// 128 frames for one slot (more blocks) and 256 for several.
+constexpr int kMxChunkMax = 256;
+inline int xkv_vt_frames(int n_frames) { return (n_frames + kMxChunkMax - 1) / kMxChunkMax * kMxChunkMax; }
+inline size_t xkv_slot_elems(bool bf16, int n_frames, int d) {
+  return bf16 ? (size_t)d * (n_frames + xkv_vt_frames(n_frames)) : (size_t)2 * n_frames * d;
+}
+inline int cross_mx_chunk(int n) { return n == 1 ? 128 : 256; }
+inline int cross_mx_chunks(int n, int n_frames) { return (n_frames + cross_mx_chunk(n) - 1) / cross_mx_chunk(n); }
+// Chunking of cross-attention over the frames for a few slots with fp32
+// storage (2 to 6 at 20 heads): about 240 blocks, chunks of >= 64 frames.  nchunk <= want, so
 // pairs * nchunk <= kXrMaxPartials.
 inline void cross_chunks(int pairs, int n_frames, int& nchunk, int& chunk) {
   nchunk = 1;
@@ -183,6 +196,7 @@ struct XkvArgs {
   const void* bias; // [2d]
   void* out;        // block base + slot offset
   int d, n_head, n_frames;
+  int vt_frames;    // > 0: values stored transposed [head][dim][vt_frames], padding zero
 };
 
 template <typename S>
