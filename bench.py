@@ -33,16 +33,16 @@ HBM_PEAK_GBS = 8000.0
 
 
 # profile role -> kernel symbol as a kernel trace names it (batch-1 bf16 path)
-SYMBOL_OF_ROLE = {
-    "attn_cross": "void wf::k_attn_cross<wf::bf16>(wf::CrossArgs)",
-    "attn_self": "void wf::k_attn_self<wf::bf16>(wf::AttnArgs)",
-    "gemv_o": "void wf::k_gemv16<2, 4>(wf::GemvArgs)",
-    "gemv_qkv": "void wf::k_gemv16<3, 4>(wf::GemvArgs)",
-    "gemv_q2": "void wf::k_gemv16_ln<0, 16, 5>(wf::GemvArgs)",
-    "gemv_fc1": "void wf::k_gemv32_ln<1, 16, 5>(wf::GemvArgs)",
-    "gemv_fc2": "void wf::k_gemv16w<5, 8, 4>(wf::GemvArgs)",
-    "reduce_ln": "void wf::k_reduce_ln<wf::bf16>(wf::RlnArgs)",
-    "head": "void wf::k_gemv32<4, 8>(wf::GemvArgs)",
+SYMBOL_OF_ROLE = {  # kernels (rocprofv3 names) that one launch of the role dispatches
+    "attn_cross": ("void wf::k_attn_cross_mx<1>(wf::CrossArgs)", "void wf::k_attn_cross_merge<wf::bf16>(wf::CrossArgs)"),
+    "attn_self": ("void wf::k_attn_self<wf::bf16>(wf::AttnArgs)",),
+    "gemv_o": ("void wf::k_gemv16<2, 4>(wf::GemvArgs)",),
+    "gemv_qkv": ("void wf::k_gemv16<3, 4>(wf::GemvArgs)",),
+    "gemv_q2": ("void wf::k_gemv16_ln<0, 16, 5>(wf::GemvArgs)",),
+    "gemv_fc1": ("void wf::k_gemv32_ln<1, 16, 5>(wf::GemvArgs)",),
+    "gemv_fc2": ("void wf::k_gemv16w<5, 8, 4>(wf::GemvArgs)",),
+    "reduce_ln": ("void wf::k_reduce_ln<wf::bf16>(wf::RlnArgs)",),
+    "head": ("void wf::k_gemv32<4, 8>(wf::GemvArgs)",),
 }
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic_large-v3_b1_pmc.md")
 
@@ -71,15 +71,16 @@ def measured_traffic(role):
         return None, "no counter summary"
     if rec.get("source_sha256") != source_digest():
         return None, "kernel sources changed since the counter passes"
-    k = rec.get("kernels", {}).get(SYMBOL_OF_ROLE.get(role, ""))
-    if not k:
+    ks = [rec.get("kernels", {}).get(sym) for sym in SYMBOL_OF_ROLE.get(role, ())]
+    if not ks or not all(ks):
         return None, "kernel not in the counter summary"
-    return k["hbm_bytes_per_dispatch"], "FETCH_SIZE and WRITE_SIZE passes scaled by a 256 MiB copy (" + TRAFFIC_FILE[len(ROOT) + 1:] + ")"
+    return (sum(k["hbm_bytes_per_dispatch"] for k in ks),
+            "FETCH_SIZE and WRITE_SIZE passes scaled by a 256 MiB copy (" + TRAFFIC_FILE[len(ROOT) + 1:] + ")")
 
 
 # profile role -> kernel symbol of the batch-1 bf16 path (the roofline names the kernel)
 KERNEL_OF_ROLE = {
-    "attn_cross": "wf::k_attn_cross<wf::bf16>",
+    "attn_cross": "wf::k_attn_cross_mx<1> + wf::k_attn_cross_merge<wf::bf16>",
     "attn_self": "wf::k_attn_self<wf::bf16>",
     "gemv_o": "wf::k_gemv16<2, 4> (EPI_RESID)",
     "gemv_qkv": "wf::k_gemv16<3, 4> (EPI_QKV)",

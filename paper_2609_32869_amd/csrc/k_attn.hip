@@ -868,6 +868,159 @@ __global__ void __launch_bounds__(kSelfThreads) k_attn_self(AttnArgs a) {
     put_op<S>(a.out, a.nsplit, a.R9, slot * kRows + row, head * kHeadDim + threadIdx.x, o);
 }
 
+// ---------------------------------------------------------------- causal self-attention, bf16, matrix cores
+// Block (head, slot): all nine rows of the pass over the slot's cached positions
+// 0..pos0 + nv - 1 (the pass's own rows included); wave w takes positions
+// 32w..32w+31 (logical pages 2w and 2w + 1), so kMaxCtx / 32 waves cover the
+// context and waves past the last key only take part in the combine.  Values
+// are stored transposed within a page ([page][head][64][16]).  A wave computes
+// S^T = K q^T for its two 16-position tiles (query rows as hi + lo bf16 planes),
+// applies the causal mask (row i sees positions <= pos0 + i), takes its own row
+// maxima m_w, p = exp(s - m_w), the row sums l_w and O_w^T = V^T P^T as in the
+// cross-attention; the waves' (m_w, l_w, O_w) are then combined max-shifted in
+// LDS.  Rows i >= nv are padding and get zeros.
+constexpr int kSxWaves = kMaxCtx / 32;
+constexpr int kSxThreads = kSxWaves * 64;
+__global__ void __launch_bounds__(kSxThreads) k_attn_self_mx(AttnArgs a) {
+  StampScope stamp_scope(a.stamp, kSxThreads);
+  __shared__ float wmax[kSxWaves][16];
+  __shared__ float wsum[kSxWaves][16];
+  __shared__ float wo[kSxWaves][kRows][64];
+  __shared__ int pts[kMaxCtx / kPage];
+  const int head = blockIdx.x, slot = a.slot0 + blockIdx.y;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, n = lane & 15, kg = lane >> 4;
+  const int* st = a.state + slot * kStateInts;
+  // state, page table and query rows are independent loads
+  if (threadIdx.x < a.pages_per_slot) pts[threadIdx.x] = a.page_table[slot * a.pages_per_slot + threadIdx.x];
+  const int pos0 = st[ST_POS0], nv = st[ST_NV];
+  float4 qx[2][2];
+  {
+    const float* qr = a.q + (size_t)(slot * kRows + min(n, kRows - 1)) * a.ldq + head * kHeadDim + 8 * kg;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      qx[h][0] = *reinterpret_cast<const float4*>(qr + 32 * h);
+      qx[h][1] = *reinterpret_cast<const float4*>(qr + 32 * h + 4);
+    }
+  }
+  __syncthreads();
+  float mrow = -INFINITY, lrow = 0.f;
+  floatx4 oacc[4];
+#pragma unroll
+  for (int dt = 0; dt < 4; ++dt) oacc[dt] = floatx4{0.f, 0.f, 0.f, 0.f};
+  if (32 * w < pos0 + nv) {  // this wave holds keys (uniform)
+    const int pg0 = pts[min(2 * w, a.pages_per_slot - 1)], pg1 = pts[min(2 * w + 1, a.pages_per_slot - 1)];
+    const bf16* Kc = reinterpret_cast<const bf16*>(a.kcache);
+    const bf16* Vc = reinterpret_cast<const bf16*>(a.vcache);
+    const int H = a.n_head;
+    bf16x8 kt[2][2], vt[4];
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+      const bf16x8* kp = reinterpret_cast<const bf16x8*>(Kc + (((size_t)(t ? pg1 : pg0) * H + head) * kPage + n) * kHeadDim) + kg;
+      kt[t][0] = kp[0];
+      kt[t][1] = kp[4];
+    }
+    const size_t vpage = (size_t)(kg < 2 ? pg0 : pg1) * H + head;
+#pragma unroll
+    for (int dt = 0; dt < 4; ++dt)
+      vt[dt] = *reinterpret_cast<const bf16x8*>(Vc + (vpage * kHeadDim + 16 * dt + n) * kPage + 8 * (kg & 1));
+    __builtin_amdgcn_sched_barrier(0);  // every load above is issued before any use below
+    bf16x8 qh[2], ql[2];
+    {
+      const float scale = n < kRows ? 0.125f : 0.f;
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const float v[8] = {qx[h][0].x * scale, qx[h][0].y * scale, qx[h][0].z * scale, qx[h][0].w * scale,
+                            qx[h][1].x * scale, qx[h][1].y * scale, qx[h][1].z * scale, qx[h][1].w * scale};
+        split_planes(v, qh[h], ql[h]);
+      }
+    }
+    floatx4 sct[2];
+    float mx = -INFINITY;
+    const int last = pos0 + n;  // row n sees positions <= last
+    const bool row_ok = n < nv;
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+      floatx4 acc = {0.f, 0.f, 0.f, 0.f};
+      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kt[t][0], qh[0], acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kt[t][0], ql[0], acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kt[t][1], qh[1], acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kt[t][1], ql[1], acc, 0, 0, 0);
+      sct[t] = acc;
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        if (row_ok && 32 * w + 16 * t + 4 * kg + i <= last) mx = fmaxf(mx, acc[i]);
+    }
+    {
+      const auto x = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx), false, false);
+      mx = fmaxf(__uint_as_float(x[0]), __uint_as_float(x[1]));
+      const auto y = __builtin_amdgcn_permlane16_swap(__float_as_uint(mx), __float_as_uint(mx), false, false);
+      mx = fmaxf(__uint_as_float(y[0]), __uint_as_float(y[1]));
+    }
+    float ls = 0.f;
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const bool ok = row_ok && 32 * w + 16 * t + 4 * kg + i <= last;  // then mx is finite
+        const float p = ok ? __expf(sct[t][i] - mx) : 0.f;
+        sct[t][i] = p;
+        ls += p;
+      }
+    float pb[8];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const auto x = __builtin_amdgcn_permlane32_swap(__float_as_uint(sct[0][i]), __float_as_uint(sct[1][i]), false, false);
+      const auto y = __builtin_amdgcn_permlane16_swap(x[0], x[1], false, false);
+      pb[i] = __uint_as_float(y[0]);
+      pb[4 + i] = __uint_as_float(y[1]);
+    }
+    bf16x8 ph, pl;
+    split_planes(pb, ph, pl);
+#pragma unroll
+    for (int dt = 0; dt < 4; ++dt) {
+      oacc[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vt[dt], ph, oacc[dt], 0, 0, 0);
+      oacc[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vt[dt], pl, oacc[dt], 0, 0, 0);
+    }
+    {
+      const auto x = __builtin_amdgcn_permlane32_swap(__float_as_uint(ls), __float_as_uint(ls), false, false);
+      ls = __uint_as_float(x[0]) + __uint_as_float(x[1]);
+      const auto y = __builtin_amdgcn_permlane16_swap(__float_as_uint(ls), __float_as_uint(ls), false, false);
+      ls = __uint_as_float(y[0]) + __uint_as_float(y[1]);
+    }
+    mrow = mx;
+    lrow = ls;
+  }
+  if (lane < 16) {
+    wmax[w][lane] = mrow;
+    wsum[w][lane] = lrow;
+  }
+  if (n < kRows) {
+#pragma unroll
+    for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) wo[w][n][16 * dt + 4 * kg + i] = oacc[dt][i];
+  }
+  __syncthreads();
+  for (int t = threadIdx.x; t < kRows * 64; t += kSxThreads) {
+    const int r = t >> 6, dim = t & 63;
+    float o = 0.f;
+    if (r < nv) {
+      float M = wmax[0][r];  // finite: wave 0 holds position 0
+#pragma unroll
+      for (int i = 1; i < kSxWaves; ++i) M = fmaxf(M, wmax[i][r]);
+      float L = 0.f;
+#pragma unroll
+      for (int i = 0; i < kSxWaves; ++i) {
+        const float f = __expf(wmax[i][r] - M);  // 0 for a wave without keys of this row
+        L = fmaf(f, wsum[i][r], L);
+        o = fmaf(f, wo[i][r][dim], o);
+      }
+      o /= L;
+    }
+    put_op<bf16>(a.out, a.nsplit, a.R9, slot * kRows + r, head * kHeadDim + dim, o);
+  }
+}
+
 // ---------------------------------------------------------------- drafter attention
 // Block row i (position t+i, t = anchor position) attends in one softmax to the
 // history keys at positions 0..t-1 and to all nine block keys (Section 3.2:
@@ -962,7 +1115,8 @@ static inline unsigned row_blocks(int H) { return (unsigned)(8 * ((H + 7) / 8) *
 
 template <typename S>
 void Ops<S>::attn_self(const AttnArgs& a, int n, hipStream_t st) {
-  k_attn_self<S><<<dim3(row_blocks(a.n_head), n), kSelfThreads, 0, st>>>(a);
+  if constexpr (sizeof(S) == 2) k_attn_self_mx<<<dim3(a.n_head, n), kSxThreads, 0, st>>>(a);
+  else k_attn_self<S><<<dim3(row_blocks(a.n_head), n), kSelfThreads, 0, st>>>(a);
 }
 template <typename S>
 void Ops<S>::attn_draft(const AttnArgs& a, int n, hipStream_t st) {

@@ -80,12 +80,17 @@ struct EpiPre {
 };
 
 // Appends the k or v value v of column n (>= d) at cache page `page`, position pos.
+// Keys are [page][head][16][64]; values too with fp32 storage, and transposed
+// within the page, [page][head][64][16], with bf16 storage (the matrix-core
+// self-attention reads 8 consecutive positions of one dim).
 template <typename S>
 __device__ __forceinline__ void qkv_append(const GemvArgs& a, int n, float v, int page, int pos) {
   const int d = a.d, kv = n >= 2 * d;
   const int cc = n - d - kv * d, head = cc >> 6, dim = cc & 63;
   S* cache = reinterpret_cast<S*>(a.cache) + (size_t)kv * a.kv_stride;
-  cache[(((size_t)page * a.n_head + head) * kPage + (pos & 15)) * kHeadDim + dim] = from_f<S>(v);
+  const size_t ph = (size_t)page * a.n_head + head;
+  const size_t i = sizeof(S) == 2 && kv ? (ph * kHeadDim + dim) * kPage + (pos & 15) : (ph * kPage + (pos & 15)) * kHeadDim + dim;
+  cache[i] = from_f<S>(v);
 }
 
 // Bias and residual values of a multi-slot tile (TM rows x TC columns), loaded at

@@ -137,9 +137,10 @@ def test_micro_bf16_b3_two_plane_operands():
 
 
 @pytest.mark.timeout(900)
-# Several slots over many frames: cross-attention splits the frames into chunks
-# of 64 (the last one ragged, with a partial key octet) whose partial softmax
-# sums a second kernel merges.
+# Several slots over many frames: bf16 cross-attention splits the frames into
+# chunks of 256 (997 = 3 x 256 + 229: the last chunk ends inside a 16-frame
+# score tile and inside an 8-frame value group, read from the zero padding of
+# the transposed values) whose partial softmax sums a second kernel merges.
 def test_micro_bf16_b3_chunked_cross_attention():
     from lockstep import Lockstep
     cfg = MICRO_BF16.with_(name="micro-bf16-997f", n_frames=997)
@@ -153,6 +154,24 @@ def test_micro_bf16_b3_chunked_cross_attention():
     _run_planted(ls, refs, np.random.default_rng(7), 6)
     print(f"micro-bf16 997 frames b3: max |dlogit| draft {ls.max_dlogit:.3e} target {ls.max_tlogit:.3e}, near ties {ls.near_ties}")
     assert ls.steps == 6
+    ls.close()
+
+
+@pytest.mark.timeout(900)
+def test_micro_bf16_b1_chunked_cross_attention():
+    """One slot, bf16, 300 frames: chunks of 128, 128 and a ragged 44 merged,
+    the three-term operand split written by the merge kernel."""
+    from lockstep import Lockstep
+    cfg = MICRO_BF16.with_(name="micro-bf16-300f", n_frames=300)
+    W = make_weights(cfg)
+    prompts = [make_prefix(cfg, 0, 13)]
+    ls = Lockstep(cfg, W, prompts, [40], TOL_MICRO_BF16)
+    opts = OracleOpts(dtype=np.float32, kv_bf16=True)
+    T = Target(cfg, W.values, opts)
+    refs = [plain_greedy(T, make_memory(cfg, 0), prompts[0], 40)]
+    _run_planted(ls, refs, np.random.default_rng(9), 8)
+    print(f"micro-bf16 300 frames b1: max |dlogit| draft {ls.max_dlogit:.3e} target {ls.max_tlogit:.3e}, near ties {ls.near_ties}")
+    assert ls.steps == 8
     ls.close()
 
 
