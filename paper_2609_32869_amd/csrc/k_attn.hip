@@ -600,10 +600,11 @@ __global__ void __launch_bounds__(kXrThreads, 4) k_attn_cross_rows(CrossArgs a) 
 }
 
 // ---------------------------------------------------------------- cross-attention, bf16, matrix cores
-// Block (head, slot, chunk of 128 KS frames), four waves of 32 KS frames each, all
+// Block (head, slot, chunk of 32 KS NW frames), NW waves of 32 KS frames each, all
 // nine query rows, both products on the matrix cores.  Keys are row-major
-// [frame][64]; values are stored transposed [dim][vt_frames] (zeros past the last
-// frame), so both operands are 16-byte reads of consecutive elements.  Every load
+// [frame][64]; values are stored transposed in 256-frame pieces [frame / 256]
+// [dim][256] (zeros past the last frame), so both operands are 16-byte reads of
+// consecutive elements.  Every load
 // of the block is issued at its start (query rows, key tiles, value fragments),
 // so the block waits for memory once.
 //   scores       S^T = K q^T per 16-frame tile (v_mfma_f32_16x16x32_bf16, the query
@@ -616,8 +617,6 @@ __global__ void __launch_bounds__(kXrThreads, 4) k_attn_cross_rows(CrossArgs a) 
 //                (lane l: row l % 16, frames 8 (l / 16)..+7); P as hi + lo planes.
 //   output       waves summed in LDS; one chunk: O / l, else the chunk's
 //                (max, l, O) record for the merge kernel.
-constexpr int kMxThreads = 256;
-constexpr int kMxWaves = kMxThreads / 64;
 
 __device__ __forceinline__ bf16x8 pack_bf16x8(const uint32_t* b) {
   return __builtin_bit_cast(bf16x8, make_uint4(b[0] | b[1] << 16, b[2] | b[3] << 16, b[4] | b[5] << 16, b[6] | b[7] << 16));
@@ -634,13 +633,13 @@ __device__ __forceinline__ void split_planes(const float* v, bf16x8& hi, bf16x8&
   lo = pack_bf16x8(lb);
 }
 
-template <int KS>
-__global__ void __launch_bounds__(kMxThreads, 3) k_attn_cross_mx(CrossArgs a) {
-  StampScope stamp_scope(a.stamp, kMxThreads);
+template <int KS, int NW>
+__global__ void __launch_bounds__(NW * 64) k_attn_cross_mx(CrossArgs a) {
+  StampScope stamp_scope(a.stamp, NW * 64);
   constexpr int NT = 2 * KS;  // 16-frame score tiles per wave
-  __shared__ float wmax[kMxWaves][16];
-  __shared__ float wsum[kMxWaves][16];
-  __shared__ float wo[kMxWaves][kRows][64];
+  __shared__ float wmax[NW][16];
+  __shared__ float wsum[NW][16];
+  __shared__ float wo[NW][kRows][64];
   const int head = blockIdx.x, slot = a.slot0 + blockIdx.y, c = blockIdx.z;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, n = lane & 15, kg = lane >> 4;
   const int F = a.n_frames, Fp = a.vt_frames;
@@ -673,7 +672,7 @@ __global__ void __launch_bounds__(kMxThreads, 3) k_attn_cross_mx(CrossArgs a) {
   for (int st = 0; st < KS; ++st)
 #pragma unroll
     for (int dt = 0; dt < 4; ++dt)
-      vt[st][dt] = *reinterpret_cast<const bf16x8*>(Vt + (size_t)(16 * dt + n) * Fp + f0w + 32 * st + 8 * kg);
+      vt[st][dt] = *reinterpret_cast<const bf16x8*>(Vt + vt_index(16 * dt + n, f0w + 32 * st + 8 * kg));
   __builtin_amdgcn_sched_barrier(0);  // every load above is issued before any use below
   // query planes of the scaled rows
   bf16x8 qh[2], ql[2];
@@ -711,7 +710,7 @@ __global__ void __launch_bounds__(kMxThreads, 3) k_attn_cross_mx(CrossArgs a) {
   __syncthreads();
   float M = wmax[0][n];
 #pragma unroll
-  for (int i = 1; i < kMxWaves; ++i) M = fmaxf(M, wmax[i][n]);  // finite: frame c * chunk is present
+  for (int i = 1; i < NW; ++i) M = fmaxf(M, wmax[i][n]);  // finite: frame c * chunk is present
   // probabilities and row sums
   float lsum = 0.f;
 #pragma unroll
@@ -763,11 +762,11 @@ __global__ void __launch_bounds__(kMxThreads, 3) k_attn_cross_mx(CrossArgs a) {
   __syncthreads();
   const int pair = blockIdx.y * a.n_head + head;
   float* part = a.part + ((size_t)pair * a.nchunk + c) * kXrPart;
-  for (int t = threadIdx.x; t < kRows * 64; t += kMxThreads) {
+  for (int t = threadIdx.x; t < kRows * 64; t += NW * 64) {
     const int r = t >> 6, dim = t & 63;
     float o = 0.f, L = 0.f;
 #pragma unroll
-    for (int i = 0; i < kMxWaves; ++i) {
+    for (int i = 0; i < NW; ++i) {
       o += wo[i][r][dim];
       L += wsum[i][r];
     }
@@ -778,7 +777,7 @@ __global__ void __launch_bounds__(kMxThreads, 3) k_attn_cross_mx(CrossArgs a) {
       if (dim == 0) {
         float m = wmax[0][r];
 #pragma unroll
-        for (int i = 1; i < kMxWaves; ++i) m = fmaxf(m, wmax[i][r]);
+        for (int i = 1; i < NW; ++i) m = fmaxf(m, wmax[i][r]);
         part[r] = m;
         part[16 + r] = L;
       }
@@ -1127,8 +1126,8 @@ void Ops<S>::attn_draft(const AttnArgs& a, int n, hipStream_t st) {
 template <typename S>
 void Ops<S>::attn_cross(const CrossArgs& a, int n, hipStream_t st) {
   if constexpr (sizeof(S) == 2) {  // transposed values, matrix cores, frame chunks + merge
-    if (a.chunk == 128) k_attn_cross_mx<1><<<dim3(a.n_head, n, a.nchunk), kMxThreads, 0, st>>>(a);
-    else k_attn_cross_mx<2><<<dim3(a.n_head, n, a.nchunk), kMxThreads, 0, st>>>(a);
+    if (a.chunk == 128) k_attn_cross_mx<1, 4><<<dim3(a.n_head, n, a.nchunk), 256, 0, st>>>(a);
+    else k_attn_cross_mx<2, 8><<<dim3(a.n_head, n, a.nchunk), 512, 0, st>>>(a);
   } else {
     if (n == 1) {  // one slot: a block per (head, row) streams all frames (9 blocks per head share an L2)
       k_attn_cross<S><<<dim3(row_blocks(a.n_head), n), kCrossThreads, 0, st>>>(a);

@@ -585,7 +585,8 @@ void accept_sample(const SampleArgs& a, hipStream_t st) {
 // ---------------------------------------------------------------- encode: cross K/V
 // C[f, n] = sum_k A[f, k] W[n, k] + b[n] for the 2d key/value columns of one
 // block, written to the per-head cross cache: keys frame-major [head][frame][64];
-// values frame-major too, or transposed [head][dim][vt_frames] when vt_frames > 0
+// values frame-major too, or transposed in 256-frame pieces
+// [head][frame / 256][dim][256] (vt_frames frames per head) when vt_frames > 0
 // (bf16 storage, read by the matrix-core cross-attention).  64x64 tiles, fp32
 // accumulation.
 template <typename S>
@@ -622,9 +623,10 @@ __global__ void __launch_bounds__(256) k_gemm_xkv(XkvArgs a) {
   }
   S* out = reinterpret_cast<S*>(a.out);
   if (a.vt_frames > 0 && n0 >= a.d) {
-    // value columns of one head, stored transposed [dim][frame]: the tile goes
-    // through LDS so that consecutive threads write consecutive frames; frames
-    // from n_frames to vt_frames are written as zeros
+    // value columns of one head, stored transposed in 256-frame pieces
+    // [frame / 256][dim][256]: the tile goes through LDS so that consecutive
+    // threads write consecutive frames; frames from n_frames to vt_frames are
+    // written as zeros
     __shared__ float Ct[64][65];
 #pragma unroll
     for (int i = 0; i < 4; ++i)
@@ -635,7 +637,7 @@ __global__ void __launch_bounds__(256) k_gemm_xkv(XkvArgs a) {
     S* vt = out + (size_t)a.n_head * M * kHeadDim + (size_t)head * kHeadDim * a.vt_frames;
     for (int t = threadIdx.x; t < 64 * 64; t += 256) {
       const int dim = t >> 6, fl = t & 63, f = m0 + fl;
-      if (f < a.vt_frames) vt[(size_t)dim * a.vt_frames + f] = from_f<S>(f < M ? Ct[dim][fl] : 0.f);
+      if (f < a.vt_frames) vt[vt_index(dim, f)] = from_f<S>(f < M ? Ct[dim][fl] : 0.f);
     }
     return;
   }

@@ -104,16 +104,21 @@ struct CrossArgs {
 constexpr int kXrPart = 32 + kRows * 64;
 constexpr int kXrMaxPairs = 128;      // chunking only below this many (head, slot) pairs
 constexpr int kXrMaxPartials = 512;   // pair * chunk records of a chunked launch
-// bf16 acoustic memory: values stored transposed with the frame count padded to a
-// multiple of kMxChunkMax (zeros past n_frames), so every matrix-core chunk reads
-// whole 16-byte groups inside its slot.  Cross-attention blocks take chunks of
-// 128 frames for one slot (more blocks) and 256 for several.
-constexpr int kMxChunkMax = 256;
+// bf16 acoustic memory: values stored transposed in 256-frame pieces,
+// [head][frame / 256][dim][256], with the frame count padded to a multiple of
+// kMxChunkMax (zeros past n_frames), so every matrix-core chunk reads whole
+// 16-byte groups of one contiguous region.  Cross-attention blocks take chunks of
+// 128 frames (four waves) for one slot and 512 (eight waves) for several.
+constexpr int kMxChunkMax = 512;
+constexpr int kVtPiece = 256;
+__host__ __device__ __forceinline__ size_t vt_index(int dim, int f) {
+  return ((size_t)(f / kVtPiece) * 64 + dim) * kVtPiece + (f % kVtPiece);
+}
 inline int xkv_vt_frames(int n_frames) { return (n_frames + kMxChunkMax - 1) / kMxChunkMax * kMxChunkMax; }
 inline size_t xkv_slot_elems(bool bf16, int n_frames, int d) {
   return bf16 ? (size_t)d * (n_frames + xkv_vt_frames(n_frames)) : (size_t)2 * n_frames * d;
 }
-inline int cross_mx_chunk(int n) { return n == 1 ? 128 : 256; }
+inline int cross_mx_chunk(int n) { return n == 1 ? 128 : 512; }
 inline int cross_mx_chunks(int n, int n_frames) { return (n_frames + cross_mx_chunk(n) - 1) / cross_mx_chunk(n); }
 // Chunking of cross-attention over the frames for a few slots with fp32
 // storage (2 to 6 at 20 heads): about 240 blocks, chunks of >= 64 frames.  nchunk <= want, so
