@@ -599,6 +599,51 @@ __global__ void __launch_bounds__(kXrThreads, 4) k_attn_cross_rows(CrossArgs a) 
   }
 }
 
+
+// ---------------------------------------------------------------- fused attention output product (one slot)
+// Items t < 2C (C = N / kOpGroups columns in group g): column c = gC + t % C and
+// half hs = t / C of the head's two 32-dim k-steps.  op_load fetches the item's
+// weights (four 8-element fragment pieces) and bias at block start; op_apply forms
+// the nine partial sums from the head's output rows in LDS and adds them to h
+// (the bias once, by head 0's first half).  Threads past the items re-read the
+// last one and add nothing.
+struct OpPre {
+  uint4 w[4];
+  uint32_t b;
+};
+__device__ __forceinline__ void op_load(const OprojArgs& op, int head, int g, int t, OpPre& pre) {
+  const int C = op.N / kOpGroups, KS = op.K / 32;
+  const int tt = min(t, 2 * C - 1);
+  const int c = g * C + tt % C, hs = tt / C;
+  const uint4* wp = reinterpret_cast<const uint4*>(op.w) + ((size_t)(c >> 4) * KS + 2 * head + hs) * 64 + (c & 15);
+#pragma unroll
+  for (int kq = 0; kq < 4; ++kq) pre.w[kq] = wp[16 * kq];
+  pre.b = reinterpret_cast<const uint16_t*>(op.bias)[c];
+}
+__device__ __forceinline__ void op_apply(const OprojArgs& op, int head, int g, int t, const OpPre& pre,
+                                         const float (*Ob)[64], int row0) {
+  const int C = op.N / kOpGroups;
+  if (t >= 2 * C) return;
+  const int c = g * C + t % C, hs = t / C;
+  float acc[kRows];
+#pragma unroll
+  for (int r = 0; r < kRows; ++r) acc[r] = 0.f;
+#pragma unroll
+  for (int kq = 0; kq < 4; ++kq) {
+    const uint4 v = pre.w[kq];
+    const float w8[8] = {__uint_as_float(v.x << 16), __uint_as_float(v.x & 0xffff0000u), __uint_as_float(v.y << 16),
+                         __uint_as_float(v.y & 0xffff0000u), __uint_as_float(v.z << 16), __uint_as_float(v.z & 0xffff0000u),
+                         __uint_as_float(v.w << 16), __uint_as_float(v.w & 0xffff0000u)};
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+#pragma unroll
+      for (int r = 0; r < kRows; ++r) acc[r] = fmaf(Ob[r][32 * hs + 8 * kq + j], w8[j], acc[r]);
+  }
+  const float b = head == 0 && hs == 0 ? __uint_as_float(pre.b << 16) : 0.f;
+#pragma unroll
+  for (int r = 0; r < kRows; ++r) atomicAdd(op.h + (size_t)(row0 + r) * op.ldh + c, acc[r] + b);
+}
+
 // ---------------------------------------------------------------- cross-attention, bf16, matrix cores
 // Block (head, slot, chunk of 32 KS NW frames), NW waves of 32 KS frames each, all
 // nine query rows, both products on the matrix cores.  Keys are row-major
@@ -770,7 +815,7 @@ __global__ void __launch_bounds__(NW * 64) k_attn_cross_mx(CrossArgs a) {
       o += wo[i][r][dim];
       L += wsum[i][r];
     }
-    if (a.nchunk == 1) {
+    if (a.nchunk == 1 && a.op.w == nullptr) {
       put_op<bf16>(a.out, a.nsplit, a.R9, slot * kRows + r, head * kHeadDim + dim, o / L);
     } else {
       part[32 + t] = o;
@@ -788,40 +833,52 @@ __global__ void __launch_bounds__(NW * 64) k_attn_cross_mx(CrossArgs a) {
 // Merge of the chunk records of one (head, slot): one thread per (row, dim).  The
 // records are read kXmGroup chunks at a time with every load of a group issued
 // together (indices clamped, chunks past the end weighted 0); groups combine with
-// the same max-shifted rule.
-constexpr int kXmThreads = kRows * 64;
+// the same max-shifted rule.  With a fused output product (grid z = column group)
+// the merged rows go to LDS and the block adds their product to h.
+constexpr int kXmThreads = 640;  // >= kRows * 64 and >= the fused product's 2C items
 constexpr int kXmGroup = 16;
 template <typename S>
 __global__ void __launch_bounds__(kXmThreads) k_attn_cross_merge(CrossArgs a) {
   StampScope stamp_scope(a.stamp, kXmThreads);
-  const int head = blockIdx.x, slot = a.slot0 + blockIdx.y;
+  __shared__ float Ob[kRows][64];
+  const int head = blockIdx.x, slot = a.slot0 + blockIdx.y, g = blockIdx.z;
+  const bool fused = a.op.w != nullptr;
+  OpPre opre;
+  if (fused) op_load(a.op, head, g, threadIdx.x, opre);
   const int t = threadIdx.x, r = t >> 6, dim = t & 63;
-  const float* part = a.part + (size_t)(blockIdx.y * a.n_head + head) * a.nchunk * kXrPart;
-  float M = -INFINITY, L = 0.f, o = 0.f;
-  for (int c0 = 0; c0 < a.nchunk; c0 += kXmGroup) {
-    float m[kXmGroup], l[kXmGroup], v[kXmGroup];
+  if (t < kRows * 64) {
+    const float* part = a.part + (size_t)(blockIdx.y * a.n_head + head) * a.nchunk * kXrPart;
+    float M = -INFINITY, L = 0.f, o = 0.f;
+    for (int c0 = 0; c0 < a.nchunk; c0 += kXmGroup) {
+      float m[kXmGroup], l[kXmGroup], v[kXmGroup];
 #pragma unroll
-    for (int j = 0; j < kXmGroup; ++j) {
-      const float* pc = part + (size_t)min(c0 + j, a.nchunk - 1) * kXrPart;
-      m[j] = pc[r];
-      l[j] = pc[16 + r];
-      v[j] = pc[32 + t];
+      for (int j = 0; j < kXmGroup; ++j) {
+        const float* pc = part + (size_t)min(c0 + j, a.nchunk - 1) * kXrPart;
+        m[j] = pc[r];
+        l[j] = pc[16 + r];
+        v[j] = pc[32 + t];
+      }
+      float Mg = M;
+#pragma unroll
+      for (int j = 0; j < kXmGroup; ++j) Mg = fmaxf(Mg, m[j]);
+      const float f0 = __expf(M - Mg);  // 0 before the first group
+      L *= f0;
+      o *= f0;
+#pragma unroll
+      for (int j = 0; j < kXmGroup; ++j) {
+        const float f = c0 + j < a.nchunk ? __expf(m[j] - Mg) : 0.f;
+        L = fmaf(f, l[j], L);
+        o = fmaf(f, v[j], o);
+      }
+      M = Mg;
     }
-    float Mg = M;
-#pragma unroll
-    for (int j = 0; j < kXmGroup; ++j) Mg = fmaxf(Mg, m[j]);
-    const float f0 = __expf(M - Mg);  // 0 before the first group
-    L *= f0;
-    o *= f0;
-#pragma unroll
-    for (int j = 0; j < kXmGroup; ++j) {
-      const float f = c0 + j < a.nchunk ? __expf(m[j] - Mg) : 0.f;
-      L = fmaf(f, l[j], L);
-      o = fmaf(f, v[j], o);
-    }
-    M = Mg;
+    if (fused) Ob[r][dim] = o / L;
+    else put_op<S>(a.out, a.nsplit, a.R9, slot * kRows + r, head * kHeadDim + dim, o / L);
   }
-  put_op<S>(a.out, a.nsplit, a.R9, slot * kRows + r, head * kHeadDim + dim, o / L);
+  if (fused) {
+    __syncthreads();
+    op_apply(a.op, head, g, t, opre, Ob, slot * kRows);
+  }
 }
 
 // ---------------------------------------------------------------- causal self-attention
@@ -886,9 +943,13 @@ __global__ void __launch_bounds__(kSxThreads) k_attn_self_mx(AttnArgs a) {
   __shared__ float wsum[kSxWaves][16];
   __shared__ float wo[kSxWaves][kRows][64];
   __shared__ int pts[kMaxCtx / kPage];
-  const int head = blockIdx.x, slot = a.slot0 + blockIdx.y;
+  __shared__ float Ob[kRows][64];
+  const int head = blockIdx.x, slot = a.slot0 + blockIdx.y, g = blockIdx.z;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, n = lane & 15, kg = lane >> 4;
   const int* st = a.state + slot * kStateInts;
+  const bool fused = a.op.w != nullptr;
+  OpPre opre;
+  if (fused) op_load(a.op, head, g, threadIdx.x, opre);
   // state, page table and query rows are independent loads
   if (threadIdx.x < a.pages_per_slot) pts[threadIdx.x] = a.page_table[slot * a.pages_per_slot + threadIdx.x];
   const int pos0 = st[ST_POS0], nv = st[ST_NV];
@@ -1016,7 +1077,12 @@ __global__ void __launch_bounds__(kSxThreads) k_attn_self_mx(AttnArgs a) {
       }
       o /= L;
     }
-    put_op<bf16>(a.out, a.nsplit, a.R9, slot * kRows + r, head * kHeadDim + dim, o);
+    if (fused) Ob[r][dim] = o;
+    else put_op<bf16>(a.out, a.nsplit, a.R9, slot * kRows + r, head * kHeadDim + dim, o);
+  }
+  if (fused) {
+    __syncthreads();
+    op_apply(a.op, head, g, threadIdx.x, opre, Ob, slot * kRows);
   }
 }
 
@@ -1114,7 +1180,7 @@ static inline unsigned row_blocks(int H) { return (unsigned)(8 * ((H + 7) / 8) *
 
 template <typename S>
 void Ops<S>::attn_self(const AttnArgs& a, int n, hipStream_t st) {
-  if constexpr (sizeof(S) == 2) k_attn_self_mx<<<dim3(a.n_head, n), kSxThreads, 0, st>>>(a);
+  if constexpr (sizeof(S) == 2) k_attn_self_mx<<<dim3(a.n_head, n, a.op.w ? kOpGroups : 1), kSxThreads, 0, st>>>(a);
   else k_attn_self<S><<<dim3(row_blocks(a.n_head), n), kSelfThreads, 0, st>>>(a);
 }
 template <typename S>
@@ -1135,7 +1201,8 @@ void Ops<S>::attn_cross(const CrossArgs& a, int n, hipStream_t st) {
     }
     k_attn_cross_rows<S><<<dim3(a.n_head, n, a.nchunk), kXrThreads, xr_lds_bytes(a.chunk), st>>>(a);
   }
-  if (a.nchunk > 1) k_attn_cross_merge<S><<<dim3(a.n_head, n), kXmThreads, 0, st>>>(a);
+  if (a.nchunk > 1 || a.op.w != nullptr)
+    k_attn_cross_merge<S><<<dim3(a.n_head, n, a.op.w ? kOpGroups : 1), kXmThreads, 0, st>>>(a);
 }
 
 template void Ops<float>::attn_self(const AttnArgs&, int, hipStream_t);

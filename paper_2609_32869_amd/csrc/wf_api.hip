@@ -351,6 +351,15 @@ struct Runner {
   // (three split terms) with rows short enough to stage in LDS.
   bool fold_ln() const { return frag() && L.nsplit_op == 3 && c.d_model <= kLnFoldMaxK; }
 
+  // Batch 1 with bf16 storage: the attention output products are fused into the
+  // attention kernels (h += O W + b through atomic adds); 2 d / kOpGroups items
+  // must fit the merge kernel's block.
+  bool fuse_oproj() const { return frag() && L.nsplit_op == 3 && c.d_model / 2 <= 640; }
+  OprojArgs oproj(size_t w, size_t b) {
+    if (!fuse_oproj()) return OprojArgs{};
+    return OprojArgs{W(w), W(b), F32(L.h), (int)c.d_model, (int)c.d_model, (int)c.d_model};
+  }
+
   // Make LayerNorm(rows x; gain g, bias b) the operand of product a: folded into
   // the product, or a separate launch that writes operand `op`.
   // The fold repeats the normalisation in every block, so products with many
@@ -385,8 +394,9 @@ struct Runner {
            });
   }
 
-  void cross(int slot0, int n, int layer) {
+  void cross(int slot0, int n, int layer, const OprojArgs& op) {
     CrossArgs a{};
+    a.op = op;
     a.q = F32(L.qkv);
     a.ldq = 3 * c.d_model;
     a.kv = xkv_layer(layer);
@@ -405,7 +415,8 @@ struct Runner {
       cross_chunks(n * c.n_head, c.n_frames, a.nchunk, a.chunk);
     }
     a.part = F32(L.xpart);
-    launch("attn_cross", 2.0 * c.n_head * c.n_frames * kHeadDim * eb() * n, [&](unsigned long long* sp) {
+    const double wbytes = op.w ? (double)c.d_model * c.d_model * eb() : 0.0;  // fused output product
+    launch("attn_cross", 2.0 * c.n_head * c.n_frames * kHeadDim * eb() * n + wbytes, [&](unsigned long long* sp) {
       a.stamp = sp;
       Ops<S>::attn_cross(a, n, st);
     });
@@ -427,8 +438,9 @@ struct Runner {
     const int d = c.d_model;
     float *h_ = F32(L.h), *qkv = F32(L.qkv);
     gemv_ln("gemv_q2", EPI_STORE, slot0, n, h_, b.ln2_g, b.ln2_b, Ad16(), b.w_q2, b.b_q2, d, d, qkv, 3 * d);
-    cross(slot0, n, xlayer);
-    gemv("gemv_o", EPI_RESID, slot0, n, Ad16(), b.w_o2, b.b_o2, d, d, h_, d);
+    const OprojArgs op2 = oproj(b.w_o2, b.b_o2);
+    cross(slot0, n, xlayer, op2);
+    if (op2.w == nullptr) gemv("gemv_o", EPI_RESID, slot0, n, Ad16(), b.w_o2, b.b_o2, d, d, h_, d);
     gemv_ln("gemv_fc1", EPI_GELU, slot0, n, h_, b.ln3_g, b.ln3_b, Ad32(), b.w_fc1, b.b_fc1, d, c.d_ff, nullptr, 0,
             Af16());
     const int ksplit = L.fc2_split > 0 ? L.fc2_split : fc2_split_batch(slot0, n);
@@ -475,11 +487,14 @@ struct Runner {
       at.state = I32(L.state); at.page_table = I32(L.page_table); at.rope = F32(L.rope); at.out = Ad16();
       at.slot0 = slot0; at.d = d; at.n_head = c.n_head; at.n_ctx = c.n_ctx; at.pages_per_slot = L.pages_per_slot;
       at.nsplit = L.nsplit_op; at.R9 = R9();
-      launch("attn_self", 0, [&](unsigned long long* sp) {
+      at.op = oproj(b.w_o, b.b_o);
+      // bytes: the fused output product's weights (the cache reads depend on the
+      // device-side lengths and are not counted)
+      launch("attn_self", at.op.w ? (double)d * d * eb() : 0.0, [&](unsigned long long* sp) {
         at.stamp = sp;
         Ops<S>::attn_self(at, n, st);
       });
-      gemv("gemv_o", EPI_RESID, slot0, n, Ad16(), b.w_o, b.b_o, d, d, h_, d);
+      if (at.op.w == nullptr) gemv("gemv_o", EPI_RESID, slot0, n, Ad16(), b.w_o, b.b_o, d, d, h_, d);
       const LnNext nx = l + 1 < c.n_layer ? LnNext{L.tb[l + 1].ln1_g, L.tb[l + 1].ln1_b, false}
                                           : LnNext{L.lnf_g, L.lnf_b, true};
       block_tail(slot0, n, b, l, tap, nx);

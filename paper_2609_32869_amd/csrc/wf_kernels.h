@@ -75,6 +75,19 @@ struct GemvArgs {
   unsigned long long* stamp;  // launch timing slot (profiled calls), or null
 };
 
+// Attention output product fused into the attention kernel (bf16, one slot):
+// h[row][c] += sum over the head's 64 dims of O[row][k] W[k][c] (+ b[c], added
+// once), W in 16-column fragment order with K = d.  Each block takes one of
+// kOpGroups column groups of its head; the partial sums of the heads reach h
+// through fp32 atomic adds (their order varies from run to run).
+constexpr int kOpGroups = 8;
+struct OprojArgs {
+  const void* w;     // null: no fused product (the operand rows are written instead)
+  const void* bias;  // [N]
+  float* h;          // residual rows [rows][ldh]
+  int ldh, N, K;
+};
+
 struct AttnArgs {
   const float* q;  // q at column head*64 of row slot*9+i (stride ldq); drafter: q | k | v
   int ldq;
@@ -85,6 +98,7 @@ struct AttnArgs {
   const float* rope;  // [pos][32][cos, sin]
   Operand out;        // operand rows of the following product
   int slot0, d, n_head, n_ctx, pages_per_slot, nsplit, R9;
+  OprojArgs op;
   unsigned long long* stamp;  // launch timing slot (profiled calls), or null
 };
 
@@ -97,7 +111,8 @@ struct CrossArgs {
   int slot0, d, n_head, n_frames, nsplit, R9;
   int vt_frames;  // padded frame count of the transposed values (bf16), else 0
   int nchunk, chunk;  // frame chunks per (head, slot) and frames per chunk (multiple of 8)
-  float* part;        // [pair][nchunk][kXrPart] chunk partials (nchunk > 1)
+  float* part;        // [pair][nchunk][kXrPart] chunk partials (nchunk > 1 or op.w)
+  OprojArgs op;       // fused output product (taken by the merge kernel)
   unsigned long long* stamp;  // launch timing slot (profiled calls), or null
 };
 // Chunk partial record: max [9] at 0, sum [9] at 16, acc [9][64] at 32.
