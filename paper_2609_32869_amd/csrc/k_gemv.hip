@@ -137,6 +137,8 @@ __device__ __forceinline__ void epi_one(const GemvArgs& a, int row, int n, float
     if (a.tap >= 0) put_op<S>(a.aout, a.nsplit, a.R9, row, a.tap * a.N + n, hn);
   } else if constexpr (EPI == EPI_PART) {
     a.y[blockIdx.y * a.pstride + (size_t)row * a.ldy + n] = v;
+  } else if constexpr (EPI == EPI_ACC) {
+    atomicAdd(a.y + (size_t)row * a.ldy + n, v);
   }
 }
 
@@ -185,7 +187,8 @@ __device__ __forceinline__ void finish_tile(const GemvArgs& a, float (*sv)[TC + 
       if (idx >= kRows * TC) break;
       const int ml = idx / TC, c = idx % TC, n = nb + c, row = R + ml;
       const bool act = n < a.N;
-      float v = ((sv[ml][c] + sv[ml + 9][c]) + sv[ml + 18][c]) + pre.bias(a, it);
+      const float bb = EPI == EPI_ACC && blockIdx.y != 0 ? 0.f : pre.bias(a, it);  // the bias once
+      float v = ((sv[ml][c] + sv[ml + 9][c]) + sv[ml + 18][c]) + bb;
       if constexpr (EPI == EPI_ARGMAX) {
         if (a.suppress != nullptr && pre.sup[it]) v = -INFINITY;
         head_score(a, row, n, act, v, &ov[ml][c], &oz[ml][c], pre.s0);
@@ -922,6 +925,13 @@ static void launch_ln(const GemvArgs& a, hipStream_t st) {
 
 template <typename S, int EPI>
 static void launch_epi(const GemvArgs& a, hipStream_t st) {
+  if constexpr (EPI == EPI_ACC) {  // batch 1, bf16: 64-column blocks, k split over grid y
+    if constexpr (sizeof(S) == 2) {
+      const int ntile = (a.N + 15) / 16, ks = a.ksplit > 1 ? a.ksplit : 1;
+      k_gemv16w<EPI, 8, 4><<<dim3((ntile + 3) / 4, ks), 512, 0, st>>>(a);
+    }
+    return;
+  } else {
   if constexpr (sizeof(S) == 2) {
     if (a.lnx != nullptr) {
       launch_ln<EPI>(a, st);
@@ -952,6 +962,7 @@ static void launch_epi(const GemvArgs& a, hipStream_t st) {
     else if (steps <= 8 * kU) launch_bf16<EPI, 8>(a, st);
     else launch_bf16<EPI, 16>(a, st);
   }
+  }
 }
 
 template <typename S>
@@ -963,6 +974,7 @@ void Ops<S>::gemv(int epi, const GemvArgs& a, hipStream_t st) {
     case EPI_QKV: launch_epi<S, EPI_QKV>(a, st); break;
     case EPI_ARGMAX: launch_epi<S, EPI_ARGMAX>(a, st); break;
     case EPI_PART: launch_epi<S, EPI_PART>(a, st); break;
+    case EPI_ACC: launch_epi<S, EPI_ACC>(a, st); break;
   }
 }
 

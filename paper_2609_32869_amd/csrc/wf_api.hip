@@ -444,7 +444,16 @@ struct Runner {
     gemv_ln("gemv_fc1", EPI_GELU, slot0, n, h_, b.ln3_g, b.ln3_b, Ad32(), b.w_fc1, b.b_fc1, d, c.d_ff, nullptr, 0,
             Af16());
     const int ksplit = L.fc2_split > 0 ? L.fc2_split : fc2_split_batch(slot0, n);
-    if (ksplit > 0) {
+    if (fuse_oproj() && L.fc2_split > 0 && tap < 0) {
+      // batch 1 (bf16), no tap after this block: the k-splits add their partial
+      // sums and the bias straight to the residual rows; the next product folds
+      // its LayerNorm in (or the head's LayerNorm runs on its own)
+      GemvArgs a = gemv_args(slot0, n, Af16(), b.w_fc2, b.b_fc2, c.d_ff, d, h_, d, Operand{nullptr, 0, OP_ROW, 0}, -1);
+      a.ct = 4;
+      a.ksplit = L.fc2_split;
+      run_gemv("gemv_fc2", EPI_ACC, n, a);
+      ln_ready = false;
+    } else if (ksplit > 0) {
       // k-split partial sums, then h += sum + bias, the tap, and the next LayerNorm
       GemvArgs a = gemv_args(slot0, n, Af16(), b.w_fc2, b.b_fc2, c.d_ff, d, F32(L.part), d, Operand{nullptr, 0, OP_ROW, 0}, -1);
       a.bias = nullptr;

@@ -6,9 +6,11 @@
 
 namespace wf {
 
-enum { EPI_STORE = 0, EPI_GELU = 1, EPI_RESID = 2, EPI_QKV = 3, EPI_ARGMAX = 4, EPI_PART = 5 };
+enum { EPI_STORE = 0, EPI_GELU = 1, EPI_RESID = 2, EPI_QKV = 3, EPI_ARGMAX = 4, EPI_PART = 5, EPI_ACC = 6 };
 // EPI_PART: split-K partial sums (no bias) of k-split blockIdx.y stored to
 // y + blockIdx.y * pstride, row-major [rows][ldy].
+// EPI_ACC (bf16, one slot, split-K): each k-split adds its partial sums to y
+// (the residual rows) with fp32 atomic adds, the bias by k-split 0.
 
 // Matrix-operand rows: the activation rows of a pass are stored once per split
 // term, row m = s * R9 + slot * 9 + i, s < nsplit (R9 = 9 * max_batch).  With
