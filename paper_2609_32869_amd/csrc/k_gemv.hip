@@ -447,7 +447,16 @@ __global__ void __launch_bounds__(NW * 64) k_gemv16w(GemvArgs a) {
 // multiply.  Grid y splits the k-steps (EPI_PART stores each split's partial
 // sums).  Block b runs on XCD b % 8; the row blocks of one column block are
 // numbered so they share an XCD and its L2 serves them the weight tile.
+typedef __attribute__((address_space(3))) void lds_void;
 constexpr int kGemmU = 2;
+// From this many 64-row blocks (two-plane operand over ~2 MB) the XCDs split the
+// rows in two halves and the columns in four quarters, so each XCD's L2 keeps its
+// half of the operand while the weight tiles stream (weights are then read by two
+// XCDs, the operand no longer cycles through all eight L2s).
+constexpr int kGemmSplitRows = 6;
+__host__ __device__ __forceinline__ unsigned gemm_grid(int nmb, int nnb) {
+  return nmb >= kGemmSplitRows ? 8u * ((nmb + 1) / 2) * ((nnb + 3) / 4) : 8u * ((nnb + 7) / 8) * nmb;
+}
 template <int EPI>
 __global__ void __launch_bounds__(256) k_gemm16(GemvArgs a, int mb0, int nmb, int nnb) {
   StampScope stamp_scope(a.stamp, 256);
@@ -455,8 +464,17 @@ __global__ void __launch_bounds__(256) k_gemm16(GemvArgs a, int mb0, int nmb, in
   __shared__ float ov[EPI == EPI_ARGMAX ? 64 : 1][64];
   __shared__ float oz[EPI == EPI_ARGMAX ? 64 : 1][64];
   const int x = blockIdx.x & 7, i = blockIdx.x >> 3;
-  const int nbk = x + 8 * (i / nmb), mbk = i % nmb;
-  if (nbk >= nnb) return;
+  int nbk, mbk;
+  if (nmb >= kGemmSplitRows) {  // XCD x: row half x & 1, column quarter x >> 1 (row blocks fastest)
+    const int nrh = (nmb + 1) / 2, ncq = (nnb + 3) / 4, rb0 = (x & 1) * nrh;
+    mbk = rb0 + i % nrh;
+    nbk = (x >> 1) * ncq + i / nrh;
+    if (mbk >= nmb || i / nrh >= ncq || nbk >= nnb) return;
+  } else {  // XCD x: column blocks x, x + 8, ..., each with every row block
+    nbk = x + 8 * (i / nmb);
+    mbk = i % nmb;
+    if (nbk >= nnb) return;
+  }
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
   const int wm = wv >> 1, wn = wv & 1;
   const int KS = a.K / 32, MT = a.a.mt, ntile = (a.N + 15) / 16;
@@ -522,6 +540,116 @@ __global__ void __launch_bounds__(256) k_gemm16(GemvArgs a, int mb0, int nmb, in
         sv[wm * 32 + p * 16 + 4 * (lane >> 4) + v][wn * 32 + q * 16 + (lane & 15)] = acc[p][q][v];
   __syncthreads();
   EpiPre<64, 256> pre;  // batch-1 prefetch, unused here
+  finish_tile<bf16, EPI, 64, 64, 256, true>(a, sv, ov, oz, (mb0 + mbk) * 64, nbk * 64, pre, rp);
+}
+
+// The same GEMM with the fragments staged through LDS: each k-step's twelve
+// distinct 1 KB fragments (four 16-row operand tiles x two planes, four 16-column
+// weight tiles) are copied once per block straight from memory into one of four
+// 12 KB LDS stages (global_load_lds_dwordx4, three per wave), three k-steps ahead,
+// and every wave reads its six fragments from LDS.  The loads through each CU's
+// address units halve (24 KB per k-step became 12 KB), the kernel's limit.  The
+// stages are separate LDS objects and the loop is unrolled over them, so the
+// compiler sees that a copy into one stage cannot alias reads of another and keeps
+// the copies in flight; each step waits for its own stage's copies (vmcnt) and its
+// earlier LDS reads (lgkmcnt) before a plain barrier.
+__shared__ uint4 g_stage0[12][64], g_stage1[12][64], g_stage2[12][64], g_stage3[12][64];
+constexpr unsigned kGemmStagedBlocks = 256;
+constexpr int kStageWait = (6 & 15) | (7 << 4) | (0 << 8);  // vmcnt <= 6 (two later k-steps' copies), lgkmcnt 0
+
+template <int EPI>
+__global__ void __launch_bounds__(256) k_gemm16s(GemvArgs a, int mb0, int nmb, int nnb) {
+  StampScope stamp_scope(a.stamp, 256);
+  __shared__ float sv[64][65];
+  const int x = blockIdx.x & 7, i = blockIdx.x >> 3;
+  int nbk, mbk;
+  if (nmb >= kGemmSplitRows) {
+    const int nrh = (nmb + 1) / 2, ncq = (nnb + 3) / 4, rb0 = (x & 1) * nrh;
+    mbk = rb0 + i % nrh;
+    nbk = (x >> 1) * ncq + i / nrh;
+    if (mbk >= nmb || i / nrh >= ncq || nbk >= nnb) return;
+  } else {
+    nbk = x + 8 * (i / nmb);
+    mbk = i % nmb;
+    if (nbk >= nnb) return;
+  }
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const int wm = wv >> 1, wn = wv & 1;
+  const int KS = a.K / 32, MT = a.a.mt, ntile = (a.N + 15) / 16;
+  const int kper = KS / gridDim.y, ks0 = blockIdx.y * kper, ks1 = ks0 + kper;
+  RowsPre<64, 64, 256> rp;
+  rp.template load<bf16, EPI>(a, (mb0 + mbk) * 64, nbk * 64);
+  // this wave's three fragments of every k-step: f < 8 operand tile f >> 1, plane
+  // f & 1; f >= 8 weight tile f - 8 (tiles past the data re-read the last one)
+  const bf16x8* src[3];
+  size_t sstride[3];
+  const size_t plane = (size_t)MT * KS * 64;
+#pragma unroll
+  for (int j = 0; j < 3; ++j) {
+    const int f = 3 * wv + j;
+    if (f < 8) {
+      const int mt = min((mb0 + mbk) * 4 + (f >> 1), MT - 1);
+      src[j] = reinterpret_cast<const bf16x8*>(a.a.p) + (f & 1) * plane + (size_t)mt * 64 + lane;
+      sstride[j] = (size_t)MT * 64;
+    } else {
+      const int nt = min(nbk * 4 + f - 8, ntile - 1);
+      src[j] = reinterpret_cast<const bf16x8*>(a.w) + (size_t)nt * KS * 64 + lane;
+      sstride[j] = 64;
+    }
+  }
+  auto copy = [&](int st, uint4 (*stg)[64]) {  // k-step st (past the range: the last one)
+    const size_t ss = (size_t)min(st, ks1 - 1);
+#pragma unroll
+    for (int j = 0; j < 3; ++j)
+      __builtin_amdgcn_global_load_lds((const void*)(src[j] + ss * sstride[j]), (lds_void*)&stg[3 * wv + j][0], 16, 0, 0);
+  };
+  floatx4 acc[2][2];
+#pragma unroll
+  for (int p = 0; p < 2; ++p)
+#pragma unroll
+    for (int q = 0; q < 2; ++q) acc[p][q] = floatx4{0.f, 0.f, 0.f, 0.f};
+  auto step = [&](int st, uint4 (*cur)[64], uint4 (*nxt)[64]) {
+    __builtin_amdgcn_s_waitcnt(kStageWait);
+    __builtin_amdgcn_s_barrier();
+    copy(st + 3, nxt);  // every step issues three copies, so the wait count stays exact
+    if (st < ks1) {
+      bf16x8 af[2][2], wf[2];
+#pragma unroll
+      for (int p = 0; p < 2; ++p)
+#pragma unroll
+        for (int h = 0; h < 2; ++h) af[p][h] = __builtin_bit_cast(bf16x8, cur[2 * (2 * wm + p) + h][lane]);
+#pragma unroll
+      for (int q = 0; q < 2; ++q) wf[q] = __builtin_bit_cast(bf16x8, cur[8 + 2 * wn + q][lane]);
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+#pragma unroll
+        for (int p = 0; p < 2; ++p)
+#pragma unroll
+          for (int q = 0; q < 2; ++q)
+            acc[p][q] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[p][h], wf[q], acc[p][q], 0, 0, 0);
+    }
+  };
+  copy(ks0, g_stage0);
+  copy(ks0 + 1, g_stage1);
+  copy(ks0 + 2, g_stage2);
+  for (int st = ks0; st < ks1; st += 4) {
+    step(st, g_stage0, g_stage3);
+    step(st + 1, g_stage1, g_stage0);
+    step(st + 2, g_stage2, g_stage1);
+    step(st + 3, g_stage3, g_stage2);
+  }
+  // no copy may land in LDS after the block has left
+  __builtin_amdgcn_s_waitcnt((0 & 15) | (7 << 4) | (15 << 8));
+#pragma unroll
+  for (int p = 0; p < 2; ++p)
+#pragma unroll
+    for (int q = 0; q < 2; ++q)
+#pragma unroll
+      for (int v = 0; v < 4; ++v)
+        sv[wm * 32 + p * 16 + 4 * (lane >> 4) + v][wn * 32 + q * 16 + (lane & 15)] = acc[p][q][v];
+  __syncthreads();
+  EpiPre<64, 256> pre;  // batch-1 prefetch, unused here
+  float ov[1][64], oz[1][64];  // (no argmax here)
   finish_tile<bf16, EPI, 64, 64, 256, true>(a, sv, ov, oz, (mb0 + mbk) * 64, nbk * 64, pre, rp);
 }
 
@@ -941,7 +1069,18 @@ static void launch_epi(const GemvArgs& a, hipStream_t st) {
     if (a.nsplit == 2 && a.wkind == W_F16) {  // several slots: 64 x 64 GEMM tiles (k split over grid y)
       const int mb0 = a.slot0 * kRows / 64, mb1 = ((a.slot0 + a.nslots) * kRows + 63) / 64;
       const int nmb = mb1 - mb0, nnb = (a.N + 63) / 64;
-      k_gemm16<EPI><<<dim3((unsigned)(8 * ((nnb + 7) / 8) * nmb), ks), 256, 0, st>>>(a, mb0, nmb, nnb);
+      // LDS-staged fragments once the launch has enough blocks to cover the
+      // chip; with fewer, the per-k-step barrier costs more than the halved loads
+      // save (measured: 72-240 blocks at 16 slots 12-15% slower, 280+ at 96
+      // slots 6-32% faster)
+      const unsigned nb = gemm_grid(nmb, nnb);
+      if constexpr (EPI != EPI_ARGMAX) {
+        if (nb * (unsigned)ks >= kGemmStagedBlocks) {
+          k_gemm16s<EPI><<<dim3(nb, ks), 256, 0, st>>>(a, mb0, nmb, nnb);
+          return;
+        }
+      }
+      k_gemm16<EPI><<<dim3(nb, ks), 256, 0, st>>>(a, mb0, nmb, nnb);
       return;
     }
     if constexpr (EPI == EPI_PART) {  // batch 1: 64-column blocks, k split over grid y
