@@ -26,18 +26,19 @@ constexpr int kU = 10;  // k-steps whose loads a wave issues together (16-wave b
 // columns), loaded at kernel start so the epilogue does not wait on a global
 // read.  Element it of a thread is tile entry threadIdx.x + it * NT, as in the
 // epilogue loop.  The loads are unconditional (indexes clamped into the buffers,
-// unused values discarded) so no load waits for another.
-template <int TC, int NT>
+// unused values discarded; also with several slots, whose epilogue does not use
+// them) so no load waits for another and no branch joins a loaded value.
+template <int TC, int NT, bool LN = false>
 struct EpiPre {
   static constexpr int P = (kRows * TC + NT - 1) / NT;
   uint32_t bb[P];    // bf16 bias bits (converted when used, so nothing waits here)
   float r[P];
+  float lc[LN ? P : 1], le[LN ? P : 1];  // LN folded in: the column sums c and e
   uint8_t sup[P];    // ARGMAX: suppressed
   int s0, s1, s2, s3;  // QKV: valid rows, first position, its page, the next page; ARGMAX: step
 
   template <typename S, int EPI>
   __device__ __forceinline__ void load(const GemvArgs& a, int nb) {
-    if (a.nsplit != 3) return;
     const bool has_bias = a.bias != nullptr;  // without one, read the weights and discard
     const uint16_t* bias = reinterpret_cast<const uint16_t*>(has_bias ? a.bias : a.w);
     const int* st = a.state != nullptr ? a.state + a.slot0 * kStateInts : reinterpret_cast<const int*>(a.w);
@@ -46,6 +47,10 @@ struct EpiPre {
       const int idx = threadIdx.x + it * NT, ml = min(idx / TC, kRows - 1), n = min(nb + idx % TC, a.N - 1);
       bb[it] = bias[n];
       r[it] = EPI == EPI_RESID ? a.y[(size_t)(a.slot0 * kRows + ml) * a.ldy + n] : 0.f;
+      if constexpr (LN) {
+        lc[it] = a.lnc[n];
+        le[it] = a.lne[n];
+      }
       if constexpr (EPI == EPI_ARGMAX) {
         const uint8_t* sp = a.suppress != nullptr ? a.suppress : reinterpret_cast<const uint8_t*>(a.w);
         sup[it] = sp[n];
@@ -63,19 +68,28 @@ struct EpiPre {
   __device__ __forceinline__ float bias(const GemvArgs& a, int it) const {
     return a.bias != nullptr ? __uint_as_float(bb[it] << 16) : 0.f;
   }
-  // Called where the epilogue starts: an empty asm redefines every prefetched
-  // value here, so no arithmetic on them (and no wait for their loads) can be
-  // scheduled before the main loop.
-  __device__ __forceinline__ void arrive() {
+  // Called where the epilogue starts: returns a copy in which an empty asm
+  // redefines every prefetched value, so no arithmetic on them (and no wait for
+  // their loads) can be scheduled before the main loop.  The prefetched values
+  // themselves stay unchanged: redefining them in place would carry them around a
+  // tile loop, and the register copy at the loop entry would wait for the loads
+  // before the first weight load is issued.
+  __device__ __forceinline__ EpiPre arrived() const {
+    EpiPre o = *this;
 #pragma unroll
     for (int it = 0; it < P; ++it) {
-      __asm__ volatile("" : "+v"(bb[it]));
-      __asm__ volatile("" : "+v"(r[it]));
-      uint32_t sp = sup[it];
+      __asm__ volatile("" : "+v"(o.bb[it]));
+      __asm__ volatile("" : "+v"(o.r[it]));
+      if constexpr (LN) {
+        __asm__ volatile("" : "+v"(o.lc[it]));
+        __asm__ volatile("" : "+v"(o.le[it]));
+      }
+      uint32_t sp = o.sup[it];
       __asm__ volatile("" : "+v"(sp));
-      sup[it] = (uint8_t)sp;
+      o.sup[it] = (uint8_t)sp;
     }
-    __asm__ volatile("" : "+v"(s0), "+v"(s1), "+v"(s2), "+v"(s3));
+    __asm__ volatile("" : "+v"(o.s0), "+v"(o.s1), "+v"(o.s2), "+v"(o.s3));
+    return o;
   }
 };
 
@@ -172,14 +186,16 @@ __device__ __forceinline__ void head_score(const GemvArgs& a, int row, int n, bo
 // oz are the head's score and z buffers (EPI_ARGMAX).
 // RP: rp holds the bias / residual of a multi-slot tile prefetched at kernel start
 // (bf16); otherwise the epilogue loads them.
-template <typename S, int EPI, int TM, int TC, int NT, bool RP = false>
+// LN: batch 1 with the LayerNorm folded in; sv holds (x*g) W^T and lnst the rows'
+// means (lnst[r]) and 1/sqrt(var + eps) (lnst[9 + r]).
+template <typename S, int EPI, int TM, int TC, int NT, bool RP = false, bool LN = false>
 __device__ __forceinline__ void finish_tile(const GemvArgs& a, float (*sv)[TC + 1], float (*ov)[TC], float (*oz)[TC], int m0, int nb,
-                            EpiPre<TC, NT>& pre, RowsPre<TM, TC, NT>& rp) {
+                            const EpiPre<TC, NT, LN>& pre, RowsPre<TM, TC, NT>& rp, const float* lnst = nullptr) {
   const bool split3 = a.nsplit == 3;
   const int R = a.slot0 * kRows, Rend = (a.slot0 + a.nslots) * kRows;
   const int nrows = split3 ? kRows : TM;
   if (split3) {
-    pre.arrive();
+    const EpiPre<TC, NT, LN> pv = pre.arrived();
     // rows r, r + 9, r + 18 hold the three split terms of row r
 #pragma unroll
     for (int it = 0; it < EpiPre<TC, NT>::P; ++it) {
@@ -187,21 +203,23 @@ __device__ __forceinline__ void finish_tile(const GemvArgs& a, float (*sv)[TC + 
       if (idx >= kRows * TC) break;
       const int ml = idx / TC, c = idx % TC, n = nb + c, row = R + ml;
       const bool act = n < a.N;
-      const float bb = EPI == EPI_ACC && blockIdx.y != 0 ? 0.f : pre.bias(a, it);  // the bias once
-      float v = ((sv[ml][c] + sv[ml + 9][c]) + sv[ml + 18][c]) + bb;
+      const float bb = EPI == EPI_ACC && blockIdx.y != 0 ? 0.f : pv.bias(a, it);  // the bias once
+      float v = (sv[ml][c] + sv[ml + 9][c]) + sv[ml + 18][c];
+      if constexpr (LN) v = lnst[kRows + ml] * (v - lnst[ml] * pv.lc[it]) + pv.le[it];
+      v += bb;
       if constexpr (EPI == EPI_ARGMAX) {
-        if (a.suppress != nullptr && pre.sup[it]) v = -INFINITY;
-        head_score(a, row, n, act, v, &ov[ml][c], &oz[ml][c], pre.s0);
+        if (a.suppress != nullptr && pv.sup[it]) v = -INFINITY;
+        head_score(a, row, n, act, v, &ov[ml][c], &oz[ml][c], pv.s0);
         if (act && a.y != nullptr) a.y[(size_t)row * a.ldy + n] = v;
       } else if constexpr (EPI == EPI_QKV) {
         if (act) {
-          const int pos = pre.s1 + ml;
+          const int pos = pv.s1 + ml;
           if (n < a.d) a.y[(size_t)row * a.ldy + n] = v;
-          else if (ml < pre.s0 && pos < a.n_ctx)
-            qkv_append<S>(a, n, v, ((pre.s1 & 15) + ml >= 16) ? pre.s3 : pre.s2, pos);
+          else if (ml < pv.s0 && pos < a.n_ctx)
+            qkv_append<S>(a, n, v, ((pv.s1 & 15) + ml >= 16) ? pv.s3 : pv.s2, pos);
         }
       } else {
-        if (act) epi_one<S, EPI>(a, row, n, v, pre.r[it]);
+        if (act) epi_one<S, EPI>(a, row, n, v, pv.r[it]);
       }
     }
   } else {
@@ -433,6 +451,76 @@ __global__ void __launch_bounds__(NW * 64) k_gemv16w(GemvArgs a) {
       finish_tile<bf16, EPI, 32, TC, NW * 64>(a, sv, ov, oz, tile0 * 16, blockIdx.x * TC, pre, none);
     }
     if (a.nsplit == 3) break;
+  }
+}
+
+// Batch 1 (three split terms in row tiles mt0 and mt0 + 1), CT 16-column tiles,
+// split-K as k_gemv16w, when every wave's k-steps fit one batch of U: the wave's
+// loads are issued together and unconditionally (tiles and steps past the data
+// re-read the last valid one and are not multiplied), with no loop or branch
+// around them, so nothing waits before the last of them is in flight.
+template <int EPI, int NW, int CT, int U>
+__global__ void __launch_bounds__(NW * 64) k_gemv16k(GemvArgs a) {
+  StampScope stamp_scope(a.stamp, NW * 64);
+  constexpr int TC = 16 * CT;
+  static_assert(EPI == EPI_ACC || EPI == EPI_PART, "split-K epilogues only");
+  __shared__ float red[NW][32][TC + 1];
+  __shared__ float sv[32][TC + 1];
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  EpiPre<TC, NW * 64> pre;
+  pre.template load<bf16, EPI>(a, blockIdx.x * TC);
+  const int col = lane & 15, kg = lane >> 4;
+  const int KS = a.K / 32;
+  const int ntile = (a.N + 15) / 16;
+  const int kss = (KS + gridDim.y - 1) / gridDim.y;
+  const int k0 = min(KS, (int)blockIdx.y * kss), k1 = min(KS, k0 + kss);
+  const int spw = (k1 - k0 + NW - 1) / NW;
+  const int s0 = min(k1, k0 + wv * spw), s1 = min(k1, s0 + spw);
+  const int cmax = min(CT, ntile - (int)blockIdx.x * CT) - 1;  // last tile of this block inside N
+  const bf16x8* Wt = reinterpret_cast<const bf16x8*>(a.w) + (size_t)blockIdx.x * CT * KS * 64 + lane;
+  const bf16x8* Ab = reinterpret_cast<const bf16x8*>(a.a.p) + lane;
+  const int MT = a.a.mt;
+  bf16x8 bw[U][CT], a0[U], a1[U];
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    const int ss = min(s0 + u, KS - 1);
+#pragma unroll
+    for (int c = 0; c < CT; ++c) bw[u][c] = Wt[((size_t)min(c, cmax) * KS + ss) * 64];
+    a0[u] = Ab[((size_t)ss * MT + a.mt0) * 64];
+    a1[u] = Ab[((size_t)ss * MT + a.mt0 + 1) * 64];
+  }
+  __builtin_amdgcn_sched_barrier(0);  // every load issued before the first wait
+  floatx4 acc0[CT], acc1[CT];
+#pragma unroll
+  for (int c = 0; c < CT; ++c) acc0[c] = acc1[c] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int u = 0; u < U; ++u)
+    if (s0 + u < s1) {
+#pragma unroll
+      for (int c = 0; c < CT; ++c) {
+        acc0[c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0[u], bw[u][c], acc0[c], 0, 0, 0);
+        acc1[c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1[u], bw[u][c], acc1[c], 0, 0, 0);
+      }
+    }
+#pragma unroll
+  for (int c = 0; c < CT; ++c)
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      red[wv][kg * 4 + v][16 * c + col] = acc0[c][v];
+      red[wv][16 + kg * 4 + v][16 * c + col] = acc1[c][v];
+    }
+  __syncthreads();
+  for (int idx = threadIdx.x; idx < 32 * TC; idx += NW * 64) {
+    const int ml = idx / TC, c = idx % TC;
+    float s = 0.f;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) s += red[w][ml][c];
+    sv[ml][c] = s;
+  }
+  __syncthreads();
+  {
+    RowsPre<32, TC, NW * 64> none;
+    finish_tile<bf16, EPI, 32, TC, NW * 64>(a, sv, nullptr, nullptr, a.mt0 * 16, blockIdx.x * TC, pre, none);
   }
 }
 
@@ -730,94 +818,103 @@ __device__ __forceinline__ int lds_frag(int m, int k) {
   else return lds_swz((k >> 4) * 64 + (m & 31) + 32 * ((k & 15) >> 3));
 }
 
-// The rows, gains and biases a wave needs, loaded before the weights so the
-// normalisation only waits for them.
+// Operand of a batch-1 product with its LayerNorm folded in.  For a row x with
+// mean m and r = 1/sqrt(var + eps), LN(x) W^T = r ((x*g) W^T - m (g W^T)) + b W^T,
+// so the block stages x*g alone (three split terms, no statistics needed) and
+// the epilogue applies m and r with the column sums c = g W^T and e = b W^T
+// precomputed per matrix.  The 9 x K/8 items (row, 8 consecutive columns) are
+// spread over all the block's lanes, and every item leaves its sum and its sum of
+// squared deviations from its own mean; after the staging barrier wave r merges
+// row r's items (the pairwise update of Chan, Golub and LeVeque) in a fixed order
+// while the weight loads are still in flight.
 template <int NW>
-struct LnRows {
-  static constexpr int RPW = (kRows + NW - 1) / NW;
-  static constexpr int J = (kLnFoldMaxK / 8 + 63) / 64;
-  float x[RPW][J][8];
-  uint4 gr[J], br[J];
+struct LnFold {
+  static constexpr int NT = NW * 64;
+  static constexpr int I = (kRows * (kLnFoldMaxK / 8) + NT - 1) / NT;  // items per lane
+  static_assert(NW >= kRows, "one wave per row merges the statistics");
+  float x[I][8];
+  uint4 g[I];
 
+  // Unconditional loads (the index is clamped; items past the last are not used).
   __device__ __forceinline__ void load(const GemvArgs& a) {
-    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
-    const int nch = a.K >> 3;
+    const int nch = a.K >> 3, ni = kRows * nch;
     const uint4* G = reinterpret_cast<const uint4*>(a.lng);
-    const uint4* B = reinterpret_cast<const uint4*>(a.lnb);
 #pragma unroll
-    for (int j = 0; j < J; ++j) {
-      const int c = lane + 64 * j;
-      const bool ok = c < nch;
-#pragma unroll
-      for (int i = 0; i < RPW; ++i) {
-        const int r = wv + NW * i;
-        if (ok && r < kRows) {
-          ld8(a.lnx + (size_t)r * a.K + 8 * c, x[i][j]);
-        } else {
-#pragma unroll
-          for (int e = 0; e < 8; ++e) x[i][j][e] = 0.f;
-        }
-      }
-      gr[j] = ok ? G[c] : make_uint4(0u, 0u, 0u, 0u);
-      br[j] = ok ? B[c] : make_uint4(0u, 0u, 0u, 0u);
+    for (int i = 0; i < I; ++i) {
+      const int t = min((int)threadIdx.x + i * NT, ni - 1), r = t / nch, c = t - r * nch;
+      ld8(a.lnx + (size_t)r * a.K + 8 * c, x[i]);
+      g[i] = G[c];
     }
   }
 
+  // Writes the operand x*g into aop (rows r, 9 + r and 18 + r hold the three split
+  // terms of row r; rows 27..31 are zero) and the item statistics of row r into
+  // ps + r * pstride: sums at [c], squared deviations at [K/8 + c].
   template <int TILE>
-  __device__ __forceinline__ void stage(const GemvArgs& a, uint4* aop) {
-    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
-    const int K = a.K, nch = K >> 3;
-    // statistics of all the wave's rows as independent chains (rows past the
-    // last are zeros and are not written)
-    float mean[RPW], inv[RPW];
+  __device__ __forceinline__ void stage(const GemvArgs& a, uint4* aop, float* ps, int pstride) const {
+    const int nch = a.K >> 3, ni = kRows * nch;
 #pragma unroll
-    for (int i = 0; i < RPW; ++i) {
-      float s = 0.f;
-#pragma unroll
-      for (int j = 0; j < J; ++j)
-#pragma unroll
-        for (int e = 0; e < 8; ++e) s += x[i][j][e];
-      mean[i] = wave_sum(s) / (float)K;
-    }
-#pragma unroll
-    for (int i = 0; i < RPW; ++i) {
-      float q = 0.f;
-#pragma unroll
-      for (int j = 0; j < J; ++j) {
-        if (lane + 64 * j < nch) {
-#pragma unroll
-          for (int e = 0; e < 8; ++e) {
-            const float cdev = x[i][j][e] - mean[i];
-            q += cdev * cdev;
-          }
-        }
-      }
-      inv[i] = 1.0f / sqrtf(wave_sum(q) / (float)K + 1e-5f);
-    }
-#pragma unroll
-    for (int i = 0; i < RPW; ++i) {
-      const int r = wv + NW * i;
-      if (r >= kRows) break;
-#pragma unroll
-      for (int j = 0; j < J; ++j) {
-        const int c = lane + 64 * j;
-        if (c >= nch) continue;
-        const uint32_t gw[4] = {gr[j].x, gr[j].y, gr[j].z, gr[j].w};
-        const uint32_t bw[4] = {br[j].x, br[j].y, br[j].z, br[j].w};
+    for (int i = 0; i < I; ++i) {
+      const int t = (int)threadIdx.x + i * NT;
+      if (t < ni) {
+        const int r = t / nch, c = t - r * nch;
+        const uint32_t gw[4] = {g[i].x, g[i].y, g[i].z, g[i].w};
         uint32_t th[8], tm[8], tl[8];
+        float sum = 0.f;
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
-          const float g = __uint_as_float(e & 1 ? gw[e >> 1] & 0xffff0000u : gw[e >> 1] << 16);
-          const float b = __uint_as_float(e & 1 ? bw[e >> 1] & 0xffff0000u : bw[e >> 1] << 16);
-          split3_bits((x[i][j][e] - mean[i]) * inv[i] * g + b, th[e], tm[e], tl[e]);
+          const float gv = __uint_as_float(e & 1 ? gw[e >> 1] & 0xffff0000u : gw[e >> 1] << 16);
+          split3_bits(x[i][e] * gv, th[e], tm[e], tl[e]);
+          sum += x[i][e];
+        }
+        const float m = sum * 0.125f;
+        float dev = 0.f;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const float dx = x[i][e] - m;
+          dev = fmaf(dx, dx, dev);
         }
         aop[lds_frag<TILE>(r, 8 * c)] = pack8(th);
         aop[lds_frag<TILE>(kRows + r, 8 * c)] = pack8(tm);
         aop[lds_frag<TILE>(2 * kRows + r, 8 * c)] = pack8(tl);
+        ps[r * pstride + c] = sum;
+        ps[r * pstride + nch + c] = dev;
       }
     }
-    for (int t = threadIdx.x; t < (32 - 3 * kRows) * nch; t += NW * 64)
+    for (int t = threadIdx.x; t < (32 - 3 * kRows) * nch; t += NT)
       aop[lds_frag<TILE>(3 * kRows + t / nch, 8 * (t % nch))] = make_uint4(0u, 0u, 0u, 0u);
+  }
+
+  // Wave r < 9: merges row r's items into st[r] = mean and st[9 + r] = 1/sqrt(var + eps).
+  __device__ __forceinline__ static void row_stats(const GemvArgs& a, const float* ps, int pstride, float* st) {
+    const int lane = threadIdx.x & 63, r = threadIdx.x >> 6;
+    if (r >= kRows) return;
+    constexpr int J = (kLnFoldMaxK / 8 + 63) / 64;
+    const int nch = a.K >> 3;
+    const float* p = ps + r * pstride;
+    float sm[J], dv[J];
+    float sum = 0.f;
+#pragma unroll
+    for (int j = 0; j < J; ++j) {
+      const int c = lane + 64 * j;
+      sm[j] = c < nch ? p[c] : 0.f;
+      dv[j] = c < nch ? p[nch + c] : 0.f;
+      sum += sm[j];
+    }
+    const float mean = wave_sum(sum) / (float)a.K;
+    float m2 = 0.f;
+#pragma unroll
+    for (int j = 0; j < J; ++j) {
+      if (lane + 64 * j < nch) {
+        const float dm = sm[j] * 0.125f - mean;
+        m2 += fmaf(8.f * dm, dm, dv[j]);
+      }
+    }
+    const float var = wave_sum(m2) / (float)a.K;
+    if (lane == 0) {
+      st[r] = mean;
+      st[kRows + r] = 1.0f / sqrtf(var + 1e-5f);
+    }
   }
 };
 
@@ -830,22 +927,32 @@ __global__ void __launch_bounds__(NW * 64) k_gemv16_ln(GemvArgs a) {
   __shared__ float sv[32][17];
   __shared__ float ov[EPI == EPI_ARGMAX ? 32 : 1][16];
   __shared__ float oz[EPI == EPI_ARGMAX ? 32 : 1][16];
+  __shared__ float lnst[2 * kRows];
+  static_assert(2 * (kLnFoldMaxK / 8) <= 32 * 17, "item statistics of a row fit its wave's reduction slot");
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
-  EpiPre<16, NW * 64> pre;
+  EpiPre<16, NW * 64, true> pre;
   pre.template load<bf16, EPI>(a, blockIdx.x * 16);
   const int col = lane & 15, kg = lane >> 4;
   const int KS = a.K / 32;
   const int spw = (KS + NW - 1) / NW;
   const int s0 = min(KS, wv * spw), s1 = min(KS, s0 + spw);
   const bf16x8* Wt = reinterpret_cast<const bf16x8*>(a.w) + (size_t)blockIdx.x * KS * 64 + lane;
-  LnRows<NW> rows;
+  LnFold<NW> rows;
   rows.load(a);
+  // The weight loads are unconditional (steps past the wave's range re-read the
+  // last one and are not multiplied) and kept after the rows' loads (scheduling
+  // barriers), so the staging waits only for the rows, not for the weights.
+  __builtin_amdgcn_sched_barrier(0);
   bf16x8 bw[U];
 #pragma unroll
   for (int u = 0; u < U; ++u)
-    if (s0 + u < s1) bw[u] = Wt[(size_t)(s0 + u) * 64];
-  rows.template stage<16>(a, aop);
+    bw[u] = Wt[(size_t)min(s0 + u, KS - 1) * 64];
+  __builtin_amdgcn_sched_barrier(0);
+  // the item statistics of row r go to wave r's reduction slot, which that wave
+  // reads back before it writes its products there
+  rows.template stage<16>(a, aop, &red[0][0][0], 32 * 17);
   __syncthreads();
+  LnFold<NW>::row_stats(a, &red[0][0][0], 32 * 17, lnst);
   floatx4 acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
   for (int u = 0; u < U; ++u)
@@ -871,7 +978,7 @@ __global__ void __launch_bounds__(NW * 64) k_gemv16_ln(GemvArgs a) {
   __syncthreads();
   {
       RowsPre<32, 16, NW * 64> none;
-      finish_tile<bf16, EPI, 32, 16, NW * 64>(a, sv, ov, oz, 0, blockIdx.x * 16, pre, none);
+      finish_tile<bf16, EPI, 32, 16, NW * 64, false, true>(a, sv, ov, oz, 0, blockIdx.x * 16, pre, none, lnst);
     }
 }
 
@@ -884,22 +991,30 @@ __global__ void __launch_bounds__(NW * 64) k_gemv32_ln(GemvArgs a) {
   __shared__ float sv[32][33];
   __shared__ float ov[EPI == EPI_ARGMAX ? 32 : 1][32];
   __shared__ float oz[EPI == EPI_ARGMAX ? 32 : 1][32];
+  __shared__ float lnst[2 * kRows];
+  static_assert(2 * (kLnFoldMaxK / 8) <= 32 * 33, "item statistics of a row fit its wave's reduction slot");
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
-  EpiPre<32, NW * 64> pre;
+  EpiPre<32, NW * 64, true> pre;
   pre.template load<bf16, EPI>(a, blockIdx.x * 32);
   const int col = lane & 31, kg = lane >> 5;
   const int KS = a.K / 16;
   const int spw = (KS + NW - 1) / NW;
   const int s0 = min(KS, wv * spw), s1 = min(KS, s0 + spw);
   const bf16x8* Wt = reinterpret_cast<const bf16x8*>(a.w) + (size_t)blockIdx.x * KS * 64 + lane;
-  LnRows<NW> rows;
+  LnFold<NW> rows;
   rows.load(a);
+  // The weight loads are unconditional (steps past the wave's range re-read the
+  // last one and are not multiplied) and kept after the rows' loads (scheduling
+  // barriers), so the staging waits only for the rows, not for the weights.
+  __builtin_amdgcn_sched_barrier(0);
   bf16x8 bw[U];
 #pragma unroll
   for (int u = 0; u < U; ++u)
-    if (s0 + u < s1) bw[u] = Wt[(size_t)(s0 + u) * 64];
-  rows.template stage<32>(a, aop);
+    bw[u] = Wt[(size_t)min(s0 + u, KS - 1) * 64];
+  __builtin_amdgcn_sched_barrier(0);
+  rows.template stage<32>(a, aop, &red[0][0][0], 32 * 33);
   __syncthreads();
+  LnFold<NW>::row_stats(a, &red[0][0][0], 32 * 33, lnst);
   floatx16 acc = {};
 #pragma unroll
   for (int u = 0; u < U; ++u)
@@ -921,7 +1036,7 @@ __global__ void __launch_bounds__(NW * 64) k_gemv32_ln(GemvArgs a) {
   __syncthreads();
   {
       RowsPre<32, 32, NW * 64> none;
-      finish_tile<bf16, EPI, 32, 32, NW * 64>(a, sv, ov, oz, 0, blockIdx.x * 32, pre, none);
+      finish_tile<bf16, EPI, 32, 32, NW * 64, false, true>(a, sv, ov, oz, 0, blockIdx.x * 32, pre, none, lnst);
     }
 }
 
@@ -1024,6 +1139,34 @@ __global__ void __launch_bounds__(256) k_repack(const bf16* __restrict__ src, bf
   *reinterpret_cast<uint4*>(dst + c * 8) = v;
 }
 
+// ---------------------------------------------------------------- LayerNorm column sums
+// One wave per row n of w: c[n] = sum_k g[k] w[n][k], e[n] = sum_k b[k] w[n][k] in fp64.
+__global__ void __launch_bounds__(256) k_ln_fold_cols(const bf16* __restrict__ w, const bf16* __restrict__ g,
+                                                      const bf16* __restrict__ b, int N, int K, float* __restrict__ c,
+                                                      float* __restrict__ e) {
+  const int lane = threadIdx.x & 63, n = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (n >= N) return;
+  double sc = 0.0, se = 0.0;
+  for (int k = lane; k < K; k += 64) {
+    const double wv = (double)to_f(w[(size_t)n * K + k]);
+    sc += (double)to_f(g[k]) * wv;
+    se += (double)to_f(b[k]) * wv;
+  }
+  for (int o = 32; o > 0; o >>= 1) {
+    sc += __shfl_xor(sc, o);
+    se += __shfl_xor(se, o);
+  }
+  if (lane == 0) {
+    c[n] = (float)sc;
+    e[n] = (float)se;
+  }
+}
+
+void ln_fold_cols(const void* w, const void* g, const void* b, int N, int K, float* c, float* e, hipStream_t st) {
+  k_ln_fold_cols<<<(N + 3) / 4, 256, 0, st>>>(reinterpret_cast<const bf16*>(w), reinterpret_cast<const bf16*>(g),
+                                              reinterpret_cast<const bf16*>(b), N, K, c, e);
+}
+
 // ---------------------------------------------------------------- launchers
 template <int EPI, int NW>
 static void launch_bf16(const GemvArgs& a, hipStream_t st) {
@@ -1041,23 +1184,36 @@ static void launch_f32(const GemvArgs& a, hipStream_t st) {
 // 16 waves: one row of the LayerNorm per wave; K <= kLnFoldMaxK gives at most
 // kLnFoldMaxK / 16 / 16 = 5 k-steps per wave.
 constexpr int kLnWaves = 16;
-constexpr int kLnSteps = kLnFoldMaxK / 16 / kLnWaves;
+constexpr int kLnSteps = kLnFoldMaxK / 16 / kLnWaves;      // 32-column tiles: k-steps of 16 per wave
+constexpr int kLnSteps16 = (kLnFoldMaxK / 32 + kLnWaves - 1) / kLnWaves;  // 16-column tiles: k-steps of 32
 template <int EPI>
 static void launch_ln(const GemvArgs& a, hipStream_t st) {
   if (a.wkind == W_F32) {
     k_gemv32_ln<EPI, kLnWaves, kLnSteps><<<(a.N + 31) / 32, kLnWaves * 64, 0, st>>>(a);
   } else {
-    k_gemv16_ln<EPI, kLnWaves, kLnSteps><<<(a.N + 15) / 16, kLnWaves * 64, 0, st>>>(a);
+    k_gemv16_ln<EPI, kLnWaves, kLnSteps16><<<(a.N + 15) / 16, kLnWaves * 64, 0, st>>>(a);
   }
+}
+
+// Batch 1, bf16, split-K (EPI_ACC or EPI_PART): 64-column blocks, k split over
+// grid y; the straight-line kernel when each wave's k-steps fit one batch.
+template <int EPI>
+static void launch_splitk(const GemvArgs& a, hipStream_t st) {
+  const int ntile = (a.N + 15) / 16, ks = a.ksplit > 1 ? a.ksplit : 1;
+  const dim3 grid((ntile + 3) / 4, ks);
+  const int KS = a.K / 32, kss = (KS + ks - 1) / ks, spw = (kss + 7) / 8;
+  if (a.nsplit == 3 && a.mt1 - a.mt0 == 2) {
+    if (spw <= 1) { k_gemv16k<EPI, 8, 4, 1><<<grid, 512, 0, st>>>(a); return; }
+    if (spw <= 2) { k_gemv16k<EPI, 8, 4, 2><<<grid, 512, 0, st>>>(a); return; }
+    if (spw <= 4) { k_gemv16k<EPI, 8, 4, 4><<<grid, 512, 0, st>>>(a); return; }
+  }
+  k_gemv16w<EPI, 8, 4><<<grid, 512, 0, st>>>(a);
 }
 
 template <typename S, int EPI>
 static void launch_epi(const GemvArgs& a, hipStream_t st) {
-  if constexpr (EPI == EPI_ACC) {  // batch 1, bf16: 64-column blocks, k split over grid y
-    if constexpr (sizeof(S) == 2) {
-      const int ntile = (a.N + 15) / 16, ks = a.ksplit > 1 ? a.ksplit : 1;
-      k_gemv16w<EPI, 8, 4><<<dim3((ntile + 3) / 4, ks), 512, 0, st>>>(a);
-    }
+  if constexpr (EPI == EPI_ACC) {  // batch 1, bf16
+    if constexpr (sizeof(S) == 2) launch_splitk<EPI_ACC>(a, st);
     return;
   } else {
   if constexpr (sizeof(S) == 2) {
@@ -1083,9 +1239,8 @@ static void launch_epi(const GemvArgs& a, hipStream_t st) {
       k_gemm16<EPI><<<dim3(nb, ks), 256, 0, st>>>(a, mb0, nmb, nnb);
       return;
     }
-    if constexpr (EPI == EPI_PART) {  // batch 1: 64-column blocks, k split over grid y
-      const int ntile = (a.N + 15) / 16;
-      k_gemv16w<EPI, 8, 4><<<dim3((ntile + 3) / 4, ks), 512, 0, st>>>(a);
+    if constexpr (EPI == EPI_PART) {  // batch 1
+      launch_splitk<EPI_PART>(a, st);
       return;
     }
   }

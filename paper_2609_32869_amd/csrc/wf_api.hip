@@ -70,7 +70,11 @@ struct ManEntry {
 struct Mat {
   size_t dst;
   int N, K, kind;
+  // a product with this LayerNorm folded in (batch 1): gain and bias offsets in the
+  // weight region and the fp32 offset of its column sums c, e; lng == kNoLn otherwise
+  size_t lng, lnb, cols;
 };
+constexpr size_t kNoLn = ~(size_t)0;
 
 std::vector<ManEntry> manifest(const wf_config& c, const Layout& L, std::vector<Mat>* mats = nullptr) {
   const size_t d = c.d_model, F = c.d_ff;
@@ -78,9 +82,9 @@ std::vector<ManEntry> manifest(const wf_config& c, const Layout& L, std::vector<
   std::vector<ManEntry> m;
   std::vector<Mat> mm;
   // start a streamed matrix (bf16 storage only); returns its index for the entries
-  auto mat = [&](size_t dst, size_t N, size_t K, int kind) {
+  auto mat = [&](size_t dst, size_t N, size_t K, int kind, size_t lng = kNoLn, size_t lnb = 0, size_t cols = 0) {
     if (!frag) return -1;
-    mm.push_back({dst, (int)N, (int)K, kind});
+    mm.push_back({dst, (int)N, (int)K, kind, L.nsplit_op == 3 ? lng : kNoLn, lnb, cols});
     return (int)mm.size() - 1;
   };
   // 32-column tiles (W_1, head) only at batch 1; with several slots every matrix
@@ -91,18 +95,18 @@ std::vector<ManEntry> manifest(const wf_config& c, const Layout& L, std::vector<
   m.push_back({(size_t)c.n_ctx * d, L.pos_emb, -1});
   auto block = [&](const BlockW& b) {
     m.push_back({d, b.ln1_g, -1}); m.push_back({d, b.ln1_b, -1});
-    const int qkv = mat(b.w_qkv, 3 * d, d, W_F16);
+    const int qkv = mat(b.w_qkv, 3 * d, d, W_F16, b.ln1_g, b.ln1_b, b.c_qkv);
     m.push_back({d * d, b.w_qkv, qkv}); m.push_back({d, b.b_qkv, -1});
     m.push_back({d * d, b.w_qkv + d * d, qkv});
     m.push_back({d * d, b.w_qkv + 2 * d * d, qkv}); m.push_back({d, b.b_qkv + 2 * d, -1});
     m.push_back({d * d, b.w_o, mat(b.w_o, d, d, W_F16)}); m.push_back({d, b.b_o, -1});
     m.push_back({d, b.ln2_g, -1}); m.push_back({d, b.ln2_b, -1});
-    m.push_back({d * d, b.w_q2, mat(b.w_q2, d, d, W_F16)}); m.push_back({d, b.b_q2, -1});
+    m.push_back({d * d, b.w_q2, mat(b.w_q2, d, d, W_F16, b.ln2_g, b.ln2_b, b.c_q2)}); m.push_back({d, b.b_q2, -1});
     m.push_back({d * d, b.w_kv2, -1});  // encode-time product: row-major
     m.push_back({d * d, b.w_kv2 + d * d, -1}); m.push_back({d, b.b_kv2 + d, -1});
     m.push_back({d * d, b.w_o2, mat(b.w_o2, d, d, W_F16)}); m.push_back({d, b.b_o2, -1});
     m.push_back({d, b.ln3_g, -1}); m.push_back({d, b.ln3_b, -1});
-    m.push_back({F * d, b.w_fc1, mat(b.w_fc1, F, d, wide)}); m.push_back({F, b.b_fc1, -1});
+    m.push_back({F * d, b.w_fc1, mat(b.w_fc1, F, d, wide, b.ln3_g, b.ln3_b, b.c_fc1)}); m.push_back({F, b.b_fc1, -1});
     m.push_back({d * F, b.w_fc2, mat(b.w_fc2, d, F, W_F16)}); m.push_back({d, b.b_fc2, -1});
   };
   for (auto& b : L.tb) block(b);
@@ -126,6 +130,8 @@ int compute_layout(const wf_config& c, Layout& L) {
   // weight region (element offsets, 128-element aligned)
   size_t w = 0;
   auto take = [&](size_t n) { size_t o = w; w = align_up(w + n, 128); return o; };
+  size_t cw = 0;  // fp32 LayerNorm column sums (c then e) of the folded products
+  auto takec = [&](size_t n) { size_t o = cw; cw += 2 * n; return o; };
   L.tok_emb = take(align_up(V, 32) * d);  // padded to whole 32-column tiles
   L.pos_emb = take((size_t)c.n_ctx * d);
   auto block = [&]() {
@@ -140,6 +146,7 @@ int compute_layout(const wf_config& c, Layout& L) {
     b.ln3_g = take(d); b.ln3_b = take(d);
     b.w_fc1 = take(F * d); b.b_fc1 = take(F);
     b.w_fc2 = take(d * F); b.b_fc2 = take(d);
+    b.c_qkv = takec(3 * d); b.c_q2 = takec(d); b.c_fc1 = takec(F);
     return b;
   };
   L.tb.clear();
@@ -216,6 +223,7 @@ int compute_layout(const wf_config& c, Layout& L) {
   L.part = region((size_t)nparts * R9 * d * 4);
   const size_t xrec = c.dtype == WF_BF16 ? B * H * (size_t)cross_mx_chunks(1, c.n_frames) : 0;  // 1 slot: the smallest chunks
   L.xpart = region(std::max((size_t)kXrMaxPartials, xrec) * kXrPart * 4);
+  L.lncd = region(L.nsplit_op == 3 ? cw * 4 : 0);
   L.stamps = region((size_t)kStampSlots * kStampWords * 8);
   L.total = o;
   return WF_OK;
@@ -364,11 +372,16 @@ struct Runner {
   // the product, or a separate launch that writes operand `op`.
   // The fold repeats the normalisation in every block, so products with many
   // column blocks (the vocabulary head) take the separate launch.
-  void ln_operand(GemvArgs& a, int slot0, int n, const float* x, size_t g, size_t b, Operand op, bool fold = true) {
+  // cols: fp32 offset of the matrix's column sums c (e follows after N values),
+  // row0: first output column of the product within that matrix
+  void ln_operand(GemvArgs& a, int slot0, int n, const float* x, size_t g, size_t b, Operand op, bool fold = true,
+                  size_t cols = 0, size_t ncols = 0, size_t row0 = 0) {
     if (fold && fold_ln()) {
       a.lnx = x + (size_t)slot0 * kRows * c.d_model;
       a.lng = W(g);
       a.lnb = W(b);
+      a.lnc = F32(L.lncd) + cols + row0;
+      a.lne = F32(L.lncd) + cols + ncols + row0;
     } else {
       ln(slot0, n, x, g, b, op);
       a.a = op;
@@ -376,10 +389,12 @@ struct Runner {
   }
 
   // y = LN(x) W^T + bias with the LayerNorm operand in `op` when not folded
-  void gemv_ln(const char* tag, int epi, int slot0, int n, const float* x, size_t g, size_t gb, Operand op, size_t w,
-               size_t b, int K, int N, float* y, int ldy, Operand aout = Operand{nullptr, 0, OP_ROW, 0}) {
+  // cols / ncols / row0: the LayerNorm column sums of the matrix w belongs to (see ln_operand)
+  void gemv_ln(const char* tag, int epi, int slot0, int n, const float* x, size_t g, size_t gb, size_t cols, size_t ncols,
+               size_t row0, Operand op, size_t w, size_t b, int K, int N, float* y, int ldy,
+               Operand aout = Operand{nullptr, 0, OP_ROW, 0}) {
     GemvArgs a = gemv_args(slot0, n, op, w, b, K, N, y, ldy, aout, -1);
-    ln_operand(a, slot0, n, x, g, gb, op);
+    ln_operand(a, slot0, n, x, g, gb, op, true, cols, ncols, row0);
     run_gemv(tag, epi, n, a);
   }
 
@@ -437,12 +452,12 @@ struct Runner {
   void block_tail(int slot0, int n, const BlockW& b, int xlayer, int tap, const LnNext& nx) {
     const int d = c.d_model;
     float *h_ = F32(L.h), *qkv = F32(L.qkv);
-    gemv_ln("gemv_q2", EPI_STORE, slot0, n, h_, b.ln2_g, b.ln2_b, Ad16(), b.w_q2, b.b_q2, d, d, qkv, 3 * d);
+    gemv_ln("gemv_q2", EPI_STORE, slot0, n, h_, b.ln2_g, b.ln2_b, b.c_q2, d, 0, Ad16(), b.w_q2, b.b_q2, d, d, qkv, 3 * d);
     const OprojArgs op2 = oproj(b.w_o2, b.b_o2);
     cross(slot0, n, xlayer, op2);
     if (op2.w == nullptr) gemv("gemv_o", EPI_RESID, slot0, n, Ad16(), b.w_o2, b.b_o2, d, d, h_, d);
-    gemv_ln("gemv_fc1", EPI_GELU, slot0, n, h_, b.ln3_g, b.ln3_b, Ad32(), b.w_fc1, b.b_fc1, d, c.d_ff, nullptr, 0,
-            Af16());
+    gemv_ln("gemv_fc1", EPI_GELU, slot0, n, h_, b.ln3_g, b.ln3_b, b.c_fc1, c.d_ff, 0, Ad32(), b.w_fc1, b.b_fc1, d, c.d_ff,
+            nullptr, 0, Af16());
     const int ksplit = L.fc2_split > 0 ? L.fc2_split : fc2_split_batch(slot0, n);
     if (fuse_oproj() && L.fc2_split > 0 && tap < 0) {
       // batch 1 (bf16), no tap after this block: the k-splits add their partial
@@ -488,7 +503,7 @@ struct Runner {
       a.w = W(b.w_qkv); a.bias = W(b.b_qkv); a.K = d; a.N = 3 * d;
       a.y = qkv; a.ldy = 3 * d; a.cache = skv_layer(l); a.kv_stride = kv_stride();
       if (ln_ready) a.a = Ad16();
-      else ln_operand(a, slot0, n, h_, b.ln1_g, b.ln1_b, Ad16());
+      else ln_operand(a, slot0, n, h_, b.ln1_g, b.ln1_b, Ad16(), true, b.c_qkv, 3 * d);
       ln_ready = false;
       run_gemv("gemv_qkv", EPI_QKV, n, a);
       AttnArgs at{};
@@ -549,8 +564,8 @@ struct Runner {
     for (int dl = 0; dl < c.n_draft_layer; ++dl) {
       const BlockW& b = L.db[dl];
       // rows d..3d of the concatenated q|k|v matrix start d*d elements in, in either order
-      gemv_ln("gemv_hist_kv", EPI_STORE, slot0, n, hp, b.ln1_g, b.ln1_b, Ad16(), b.w_qkv + (size_t)d * d, b.b_qkv + d, d,
-              2 * d, kvh, 2 * d);
+      gemv_ln("gemv_hist_kv", EPI_STORE, slot0, n, hp, b.ln1_g, b.ln1_b, b.c_qkv, 3 * d, d, Ad16(), b.w_qkv + (size_t)d * d,
+              b.b_qkv + d, d, 2 * d, kvh, 2 * d);
       HistArgs ha{};
       ha.kv = kvh; ha.kcache = hkv(dl, 0); ha.vcache = hkv(dl, 1); ha.state = I32(L.state); ha.rope = F32(L.rope);
       ha.slot0 = slot0; ha.d = d; ha.n_head = c.n_head; ha.n_ctx = c.n_ctx;
@@ -569,8 +584,8 @@ struct Runner {
     for (int dl = 0; dl < c.n_draft_layer; ++dl) {
       const BlockW& b = L.db[dl];
       if (ln_ready) gemv("gemv_draft_qkv", EPI_STORE, slot0, n, Ad16(), b.w_qkv, b.b_qkv, d, 3 * d, qkv, 3 * d);
-      else gemv_ln("gemv_draft_qkv", EPI_STORE, slot0, n, h_, b.ln1_g, b.ln1_b, Ad16(), b.w_qkv, b.b_qkv, d, 3 * d, qkv,
-                   3 * d);
+      else gemv_ln("gemv_draft_qkv", EPI_STORE, slot0, n, h_, b.ln1_g, b.ln1_b, b.c_qkv, 3 * d, 0, Ad16(), b.w_qkv, b.b_qkv,
+                   d, 3 * d, qkv, 3 * d);
       ln_ready = false;
       AttnArgs at{};
       at.q = qkv; at.ldq = 3 * d; at.kcache = hkv(dl, 0); at.vcache = hkv(dl, 1);
@@ -831,6 +846,10 @@ int wf_init_weights(wf_handle** out, const wf_config* cfg, const void* const* we
     if (mi >= 0 && last[mi] == i) {
       // the whole matrix is staged: reorder it into its place
       const Mat& m = mats[mi];
+      if (m.lng != kNoLn) {
+        float* cols = h->at<float>(L.lncd) + m.cols;
+        ln_fold_cols(stage, wbase + m.lng * eb, wbase + m.lnb * eb, m.N, m.K, cols, cols + m.N, st);
+      }
       repack<bf16>(stage, wbase + m.dst * eb, m.N, m.K, m.kind, st);
       e = hipGetLastError();
       if (e != hipSuccess) return cleanup(WF_EHIP, std::string("repack: ") + hipGetErrorString(e));

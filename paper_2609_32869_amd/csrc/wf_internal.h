@@ -20,6 +20,9 @@ struct BlockW {
   size_t ln1_g, ln1_b, w_qkv, b_qkv, w_o, b_o;
   size_t ln2_g, ln2_b, w_q2, b_q2, w_kv2, b_kv2, w_o2, b_o2;
   size_t ln3_g, ln3_b, w_fc1, b_fc1, w_fc2, b_fc2;
+  // fp32 offsets (in the LayerNorm column-sum region) of c then e for the products
+  // with a LayerNorm folded in: q|k|v (3 d each), W'_q (d), W_1 (d_ff)
+  size_t c_qkv, c_q2, c_fc1;
 };
 
 struct Layout {
@@ -28,6 +31,7 @@ struct Layout {
   size_t a_d16, a_d32, a_f16, a_tap16, h, qkv, hp, kvh, hv, hi, tok, g, gmax, draft, lasth, logits, dlogits, part;
   size_t hm, hs, tmax, tsum, dmax, dsum, sst, spart;  // sampling: normalisers and draw partials
   size_t xpart;   // chunked cross-attention: partial records
+  size_t lncd;    // LayerNorm column sums of the folded products (batch 1, bf16)
   size_t stamps;  // launch timing slots (profiling)
   size_t total;
   // element offsets inside the weight region

@@ -46,6 +46,10 @@ struct GemvArgs {
   const float* lnx;  // [9][K] fp32 rows, or null
   const void* lng;
   const void* lnb;
+  // column sums of the weights scaled by the gain and by the bias of that
+  // LayerNorm, c[n] = sum_k g[k] W[n][k] and e[n] = sum_k b[k] W[n][k] ([N] fp32)
+  const float* lnc;
+  const float* lne;
   // split-K (EPI_PART): number of k-splits (grid y) and the element stride between
   // their partial buffers
   int ksplit;
@@ -238,6 +242,11 @@ struct Ops {
 
 template <typename S>
 void repack(const void* src, void* dst, int N, int K, int wkind, hipStream_t st);
+
+// c[n] = sum_k g[k] w[n][k] and e[n] = sum_k b[k] w[n][k] of a row-major bf16
+// matrix w [N][K] and a LayerNorm's gain g and bias b [K] (fp64 sums rounded to
+// fp32): what a product with that LayerNorm folded in adds after its matrix pass.
+void ln_fold_cols(const void* w, const void* g, const void* b, int N, int K, float* c, float* e, hipStream_t st);
 
 constexpr int kRlnMaxPartsHost = 16;
 constexpr int kSampleBlocks = 64;     // vocabulary slices of a sampling draw per slot  // most split-K partials a reduction sums
