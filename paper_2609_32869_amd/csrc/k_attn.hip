@@ -837,14 +837,15 @@ __global__ void __launch_bounds__(NW * 64) k_attn_cross_mx(CrossArgs a) {
 // the merged rows go to LDS and the block adds their product to h.
 constexpr int kXmThreads = 640;  // >= kRows * 64 and >= the fused product's 2C items
 constexpr int kXmGroup = 16;
-template <typename S>
+template <typename S, bool FUSED>
 __global__ void __launch_bounds__(kXmThreads) k_attn_cross_merge(CrossArgs a) {
   StampScope stamp_scope(a.stamp, kXmThreads);
   __shared__ float Ob[kRows][64];
   const int head = blockIdx.x, slot = a.slot0 + blockIdx.y, g = blockIdx.z;
-  const bool fused = a.op.w != nullptr;
+  // FUSED: the output product's weights are loaded unconditionally (a branch around
+  // them would make the record loads below wait for them)
   OpPre opre;
-  if (fused) op_load(a.op, head, g, threadIdx.x, opre);
+  if constexpr (FUSED) op_load(a.op, head, g, threadIdx.x, opre);
   const int t = threadIdx.x, r = t >> 6, dim = t & 63;
   if (t < kRows * 64) {
     const float* part = a.part + (size_t)(blockIdx.y * a.n_head + head) * a.nchunk * kXrPart;
@@ -872,10 +873,10 @@ __global__ void __launch_bounds__(kXmThreads) k_attn_cross_merge(CrossArgs a) {
       }
       M = Mg;
     }
-    if (fused) Ob[r][dim] = o / L;
+    if constexpr (FUSED) Ob[r][dim] = o / L;
     else put_op<S>(a.out, a.nsplit, a.R9, slot * kRows + r, head * kHeadDim + dim, o / L);
   }
-  if (fused) {
+  if constexpr (FUSED) {
     __syncthreads();
     op_apply(a.op, head, g, t, opre, Ob, slot * kRows);
   }
@@ -937,21 +938,22 @@ __global__ void __launch_bounds__(kSelfThreads) k_attn_self(AttnArgs a) {
 // LDS.  Rows i >= nv are padding and get zeros.
 constexpr int kSxWaves = kMaxCtx / 32;
 constexpr int kSxThreads = kSxWaves * 64;
+template <bool FUSED>
 __global__ void __launch_bounds__(kSxThreads) k_attn_self_mx(AttnArgs a) {
   StampScope stamp_scope(a.stamp, kSxThreads);
   __shared__ float wmax[kSxWaves][16];
   __shared__ float wsum[kSxWaves][16];
   __shared__ float wo[kSxWaves][kRows][64];
-  __shared__ int pts[kMaxCtx / kPage];
   __shared__ float Ob[kRows][64];
   const int head = blockIdx.x, slot = a.slot0 + blockIdx.y, g = blockIdx.z;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, n = lane & 15, kg = lane >> 4;
   const int* st = a.state + slot * kStateInts;
-  const bool fused = a.op.w != nullptr;
-  OpPre opre;
-  if (fused) op_load(a.op, head, g, threadIdx.x, opre);
-  // state, page table and query rows are independent loads
-  if (threadIdx.x < a.pages_per_slot) pts[threadIdx.x] = a.page_table[slot * a.pages_per_slot + threadIdx.x];
+  // The wave's two page-table entries, the slot state and the query rows are
+  // independent loads, issued first; the fused output product's weights (FUSED,
+  // unconditional) follow, so the key and value loads wait for the page entries
+  // alone (loads complete in issue order).
+  const int* ptab = a.page_table + (size_t)slot * a.pages_per_slot;
+  const int pe0 = ptab[min(2 * w, a.pages_per_slot - 1)], pe1 = ptab[min(2 * w + 1, a.pages_per_slot - 1)];
   const int pos0 = st[ST_POS0], nv = st[ST_NV];
   float4 qx[2][2];
   {
@@ -962,13 +964,16 @@ __global__ void __launch_bounds__(kSxThreads) k_attn_self_mx(AttnArgs a) {
       qx[h][1] = *reinterpret_cast<const float4*>(qr + 32 * h + 4);
     }
   }
-  __syncthreads();
+  __builtin_amdgcn_sched_barrier(0);
+  OpPre opre;
+  if constexpr (FUSED) op_load(a.op, head, g, threadIdx.x, opre);
+  __builtin_amdgcn_sched_barrier(0);
   float mrow = -INFINITY, lrow = 0.f;
   floatx4 oacc[4];
 #pragma unroll
   for (int dt = 0; dt < 4; ++dt) oacc[dt] = floatx4{0.f, 0.f, 0.f, 0.f};
   if (32 * w < pos0 + nv) {  // this wave holds keys (uniform)
-    const int pg0 = pts[min(2 * w, a.pages_per_slot - 1)], pg1 = pts[min(2 * w + 1, a.pages_per_slot - 1)];
+    const int pg0 = pe0, pg1 = pe1;
     const bf16* Kc = reinterpret_cast<const bf16*>(a.kcache);
     const bf16* Vc = reinterpret_cast<const bf16*>(a.vcache);
     const int H = a.n_head;
@@ -1077,10 +1082,10 @@ __global__ void __launch_bounds__(kSxThreads) k_attn_self_mx(AttnArgs a) {
       }
       o /= L;
     }
-    if (fused) Ob[r][dim] = o;
+    if constexpr (FUSED) Ob[r][dim] = o;
     else put_op<bf16>(a.out, a.nsplit, a.R9, slot * kRows + r, head * kHeadDim + dim, o);
   }
-  if (fused) {
+  if constexpr (FUSED) {
     __syncthreads();
     op_apply(a.op, head, g, threadIdx.x, opre, Ob, slot * kRows);
   }
@@ -1180,7 +1185,10 @@ static inline unsigned row_blocks(int H) { return (unsigned)(8 * ((H + 7) / 8) *
 
 template <typename S>
 void Ops<S>::attn_self(const AttnArgs& a, int n, hipStream_t st) {
-  if constexpr (sizeof(S) == 2) k_attn_self_mx<<<dim3(a.n_head, n, a.op.w ? kOpGroups : 1), kSxThreads, 0, st>>>(a);
+  if constexpr (sizeof(S) == 2) {
+    if (a.op.w != nullptr) k_attn_self_mx<true><<<dim3(a.n_head, n, kOpGroups), kSxThreads, 0, st>>>(a);
+    else k_attn_self_mx<false><<<dim3(a.n_head, n, 1), kSxThreads, 0, st>>>(a);
+  }
   else k_attn_self<S><<<dim3(row_blocks(a.n_head), n), kSelfThreads, 0, st>>>(a);
 }
 template <typename S>
@@ -1201,8 +1209,10 @@ void Ops<S>::attn_cross(const CrossArgs& a, int n, hipStream_t st) {
     }
     k_attn_cross_rows<S><<<dim3(a.n_head, n, a.nchunk), kXrThreads, xr_lds_bytes(a.chunk), st>>>(a);
   }
-  if (a.nchunk > 1 || a.op.w != nullptr)
-    k_attn_cross_merge<S><<<dim3(a.n_head, n, a.op.w ? kOpGroups : 1), kXmThreads, 0, st>>>(a);
+  if (a.nchunk > 1 || a.op.w != nullptr) {
+    if (a.op.w != nullptr) k_attn_cross_merge<S, true><<<dim3(a.n_head, n, kOpGroups), kXmThreads, 0, st>>>(a);
+    else k_attn_cross_merge<S, false><<<dim3(a.n_head, n, 1), kXmThreads, 0, st>>>(a);
+  }
 }
 
 template void Ops<float>::attn_self(const AttnArgs&, int, hipStream_t);
