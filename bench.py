@@ -34,13 +34,13 @@ HBM_PEAK_GBS = 8000.0
 
 # profile role -> kernel symbol as a kernel trace names it (batch-1 bf16 path)
 SYMBOL_OF_ROLE = {  # kernels (rocprofv3 names) that one launch of the role dispatches
-    "attn_cross": ("void wf::k_attn_cross_mx<1, 4>(wf::CrossArgs)", "void wf::k_attn_cross_merge<wf::bf16>(wf::CrossArgs)"),
-    "attn_self": ("void wf::k_attn_self<wf::bf16>(wf::AttnArgs)",),
+    "attn_cross": ("void wf::k_attn_cross_mx<1, 4>(wf::CrossArgs)", "void wf::k_attn_cross_merge<wf::bf16, true>(wf::CrossArgs)"),
+    "attn_self": ("void wf::k_attn_self_mx<true>(wf::AttnArgs)",),
     "gemv_o": ("void wf::k_gemv16<2, 4>(wf::GemvArgs)",),
-    "gemv_qkv": ("void wf::k_gemv16_ln<3, 16, 5>(wf::GemvArgs)",),  # k_gemv16<3, 4> after the tap blocks
-    "gemv_q2": ("void wf::k_gemv16_ln<0, 16, 5>(wf::GemvArgs)",),
+    "gemv_qkv": ("void wf::k_gemv16_ln<3, 16, 3>(wf::GemvArgs)",),  # k_gemv16<3, 4> after the tap blocks
+    "gemv_q2": ("void wf::k_gemv16_ln<0, 16, 3>(wf::GemvArgs)",),
     "gemv_fc1": ("void wf::k_gemv32_ln<1, 16, 5>(wf::GemvArgs)",),
-    "gemv_fc2": ("void wf::k_gemv16w<6, 8, 4>(wf::GemvArgs)",),  # k_gemv16w<5, 8, 4> in the tap blocks
+    "gemv_fc2": ("void wf::k_gemv16k<6, 8, 4, 2>(wf::GemvArgs)",),  # k_gemv16k<5, 8, 4, 2> in the tap blocks
     "reduce_ln": ("void wf::k_reduce_ln<wf::bf16>(wf::RlnArgs)",),
     "head": ("void wf::k_gemv32<4, 8>(wf::GemvArgs)",),
 }
@@ -80,13 +80,13 @@ def measured_traffic(role):
 
 # profile role -> kernel symbol of the batch-1 bf16 path (the roofline names the kernel)
 KERNEL_OF_ROLE = {
-    "attn_cross": "wf::k_attn_cross_mx<1, 4> + wf::k_attn_cross_merge<wf::bf16>",
-    "attn_self": "wf::k_attn_self<wf::bf16>",
+    "attn_cross": "wf::k_attn_cross_mx<1, 4> + wf::k_attn_cross_merge<wf::bf16, true>",
+    "attn_self": "wf::k_attn_self_mx<true> (W_o fused)",
     "gemv_o": "wf::k_gemv16<2, 4> (EPI_RESID)",
-    "gemv_qkv": "wf::k_gemv16_ln<3, 16, 5> (EPI_QKV, LayerNorm folded; k_gemv16<3, 4> after the tap blocks)",
-    "gemv_q2": "wf::k_gemv16_ln<0, 16, 5> (EPI_STORE, LayerNorm folded)",
+    "gemv_qkv": "wf::k_gemv16_ln<3, 16, 3> (EPI_QKV, LayerNorm folded; k_gemv16<3, 4> after the tap blocks)",
+    "gemv_q2": "wf::k_gemv16_ln<0, 16, 3> (EPI_STORE, LayerNorm folded)",
     "gemv_fc1": "wf::k_gemv32_ln<1, 16, 5> (EPI_GELU, LayerNorm folded)",
-    "gemv_fc2": "wf::k_gemv16w<6, 8, 4> (EPI_ACC, split-K into the residual; EPI_PART in the tap blocks)",
+    "gemv_fc2": "wf::k_gemv16k<6, 8, 4, 2> (EPI_ACC, split-K into the residual; EPI_PART in the tap blocks)",
     "reduce_ln": "wf::k_reduce_ln<wf::bf16>",
     "head": "wf::k_gemv32<4, 8> (EPI_ARGMAX)",
 }
