@@ -620,14 +620,18 @@ __device__ __forceinline__ void op_load(const OprojArgs& op, int head, int g, in
   for (int kq = 0; kq < 4; ++kq) pre.w[kq] = wp[16 * kq];
   pre.b = reinterpret_cast<const uint16_t*>(op.bias)[c];
 }
+// Every thread of the block calls it (it holds a barrier).  Thread t < 2C owns
+// column c and half hs of the head's 64 dims; the two halves meet in LDS (half)
+// so each (row, column) of the residual takes one atomic add per head.
 __device__ __forceinline__ void op_apply(const OprojArgs& op, int head, int g, int t, const OpPre& pre,
-                                         const float (*Ob)[64], int row0) {
+                                         const float (*Ob)[64], int row0, float (*half)[kOpMaxCols]) {
   const int C = op.N / kOpGroups;
-  if (t >= 2 * C) return;
+  const bool act = t < 2 * C;
   const int c = g * C + t % C, hs = t / C;
   float acc[kRows];
 #pragma unroll
   for (int r = 0; r < kRows; ++r) acc[r] = 0.f;
+  if (act) {
 #pragma unroll
   for (int kq = 0; kq < 4; ++kq) {
     const uint4 v = pre.w[kq];
@@ -639,9 +643,17 @@ __device__ __forceinline__ void op_apply(const OprojArgs& op, int head, int g, i
 #pragma unroll
       for (int r = 0; r < kRows; ++r) acc[r] = fmaf(Ob[r][32 * hs + 8 * kq + j], w8[j], acc[r]);
   }
-  const float b = head == 0 && hs == 0 ? __uint_as_float(pre.b << 16) : 0.f;
+  }
+  if (act && hs == 1) {
 #pragma unroll
-  for (int r = 0; r < kRows; ++r) atomicAdd(op.h + (size_t)(row0 + r) * op.ldh + c, acc[r] + b);
+    for (int r = 0; r < kRows; ++r) half[r][t - C] = acc[r];
+  }
+  __syncthreads();
+  if (act && hs == 0) {
+    const float b = head == 0 ? __uint_as_float(pre.b << 16) : 0.f;
+#pragma unroll
+    for (int r = 0; r < kRows; ++r) atomicAdd(op.h + (size_t)(row0 + r) * op.ldh + c, (acc[r] + half[r][t]) + b);
+  }
 }
 
 // ---------------------------------------------------------------- cross-attention, bf16, matrix cores
@@ -841,6 +853,7 @@ template <typename S, bool FUSED>
 __global__ void __launch_bounds__(kXmThreads) k_attn_cross_merge(CrossArgs a) {
   StampScope stamp_scope(a.stamp, kXmThreads);
   __shared__ float Ob[kRows][64];
+  __shared__ float ophalf[FUSED ? kRows : 1][kOpMaxCols];  // fused output product: second halves
   const int head = blockIdx.x, slot = a.slot0 + blockIdx.y, g = blockIdx.z;
   // FUSED: the output product's weights are loaded unconditionally (a branch around
   // them would make the record loads below wait for them)
@@ -878,7 +891,7 @@ __global__ void __launch_bounds__(kXmThreads) k_attn_cross_merge(CrossArgs a) {
   }
   if constexpr (FUSED) {
     __syncthreads();
-    op_apply(a.op, head, g, t, opre, Ob, slot * kRows);
+    op_apply(a.op, head, g, t, opre, Ob, slot * kRows, ophalf);
   }
 }
 
@@ -945,6 +958,7 @@ __global__ void __launch_bounds__(kSxThreads) k_attn_self_mx(AttnArgs a) {
   __shared__ float wsum[kSxWaves][16];
   __shared__ float wo[kSxWaves][kRows][64];
   __shared__ float Ob[kRows][64];
+  __shared__ float ophalf[FUSED ? kRows : 1][kOpMaxCols];  // fused output product: second halves
   const int head = blockIdx.x, slot = a.slot0 + blockIdx.y, g = blockIdx.z;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, n = lane & 15, kg = lane >> 4;
   const int* st = a.state + slot * kStateInts;
@@ -1087,7 +1101,7 @@ __global__ void __launch_bounds__(kSxThreads) k_attn_self_mx(AttnArgs a) {
   }
   if constexpr (FUSED) {
     __syncthreads();
-    op_apply(a.op, head, g, threadIdx.x, opre, Ob, slot * kRows);
+    op_apply(a.op, head, g, threadIdx.x, opre, Ob, slot * kRows, ophalf);
   }
 }
 

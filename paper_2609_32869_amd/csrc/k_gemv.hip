@@ -797,11 +797,9 @@ __global__ void __launch_bounds__(NW * 64) k_gemv32(GemvArgs a) {
 }
 
 // ---------------------------------------------------------------- LayerNorm folded in (bf16, batch 1)
-// The block normalises the 9 rows of the pass itself (two-pass mean and variance
-// over K, then gain and bias, as a separate LayerNorm would) and writes their
-// three bf16 split terms (rows r, 9 + r, 18 + r; rows 27..31 zero) into LDS in
-// the fragment order of its tile shape.  Each wave handles rows wv, wv + NW, ...
-// with every load of its rows in flight at once.
+// The block stages its operand in LDS itself (LnFold below): three bf16 split
+// terms per value (rows r, 9 + r, 18 + r; rows 27..31 zero) in the fragment order
+// of its tile shape.
 __device__ __forceinline__ uint4 pack8(const uint32_t* h) {
   return make_uint4(h[0] | ((uint32_t)h[1] << 16), h[2] | ((uint32_t)h[3] << 16), h[4] | ((uint32_t)h[5] << 16),
                     h[6] | ((uint32_t)h[7] << 16));

@@ -87,6 +87,7 @@ struct GemvArgs {
 // kOpGroups column groups of its head; the partial sums of the heads reach h
 // through fp32 atomic adds (their order varies from run to run).
 constexpr int kOpGroups = 8;
+constexpr int kOpMaxCols = 160;  // columns of one group of a fused output product (d_model <= 1280)
 struct OprojArgs {
   const void* w;     // null: no fused product (the operand rows are written instead)
   const void* bias;  // [N]
