@@ -286,27 +286,42 @@ __device__ __forceinline__ void finish_tile(const GemvArgs& a, float (*sv)[TC + 
     }
   }
   if constexpr (EPI == EPI_ARGMAX) {
+    // A row's TC scores are reduced by a group of TC consecutive lanes with
+    // butterflies (ties to the lower column, as better() orders them; columns past
+    // N hold -inf scores and add nothing to the normaliser).
+    static_assert(TC <= 64 && (TC & (TC - 1)) == 0, "a tile row fits one lane group");
+    constexpr int GPB = NT / TC;
+    const int j = threadIdx.x % TC, grp = threadIdx.x / TC;
     __syncthreads();
-    for (int ml = threadIdx.x; ml < nrows; ml += NT) {
+    for (int ml0 = 0; ml0 < nrows; ml0 += GPB) {
+      const int ml = ml0 + grp, mc = min(ml, nrows - 1);
       const int row = split3 ? R + ml : m0 + ml;
-      if (row < R || row >= Rend) continue;
-      float bv = ov[ml][0];
-      int bi = nb;
-      float zm = oz[ml][0];
-      for (int j = 1; j < TC; ++j) {
-        if (nb + j >= a.N) break;
-        if (better(ov[ml][j], nb + j, bv, bi)) { bv = ov[ml][j]; bi = nb + j; }
-        zm = fmaxf(zm, oz[ml][j]);
+      float bv = ov[mc][j], zm = oz[mc][j];
+      int bi = nb + j;
+#pragma unroll
+      for (int o = TC / 2; o > 0; o >>= 1) {
+        const float v2 = __shfl_xor(bv, o, TC);
+        const int i2 = __shfl_xor(bi, o, TC);
+        if (better(v2, i2, bv, bi)) {
+          bv = v2;
+          bi = i2;
+        }
+        zm = fmaxf(zm, __shfl_xor(zm, o, TC));
       }
-      const size_t o = (size_t)row * a.nblk + nb / TC;  // column block of this tile
-      a.hv[o] = bv;
-      a.hi[o] = bi;
+      float zs = 0.f;
       if (a.hm != nullptr) {
-        float zs = 0.f;
-        if (zm > -INFINITY)
-          for (int j = 0; j < TC && nb + j < a.N; ++j) zs += expf(oz[ml][j] - zm);
-        a.hm[o] = zm;
-        a.hs[o] = zs;
+        zs = zm > -INFINITY ? expf(oz[mc][j] - zm) : 0.f;
+#pragma unroll
+        for (int o = TC / 2; o > 0; o >>= 1) zs += __shfl_xor(zs, o, TC);
+      }
+      if (j == 0 && ml < nrows && row >= R && row < Rend) {
+        const size_t o = (size_t)row * a.nblk + nb / TC;  // column block of this tile
+        a.hv[o] = bv;
+        a.hi[o] = bi;
+        if (a.hm != nullptr) {
+          a.hm[o] = zm;
+          a.hs[o] = zs;
+        }
       }
     }
   }
@@ -796,6 +811,79 @@ __global__ void __launch_bounds__(NW * 64) k_gemv32(GemvArgs a) {
   }
 }
 
+// ---------------------------------------------------------------- batch-1 head, persistent
+// Batch 1 (three split terms in one 32-row tile), 32-column tiles: a block walks
+// the column tiles tile = blockIdx.x + i gridDim.x.  The operand fragments of a
+// wave's k-steps are the same for every tile and stay in registers; the next
+// tile's weight fragments and epilogue prefetch are in flight while the current
+// tile is multiplied, reduced and finished.  The two sets of registers alternate
+// (a copy from one to the other would wait for its loads); past the last tile a
+// block re-reads its current one (from L2) instead of branching around the loads.
+constexpr int kHeadBlocks = 256;
+template <int EPI, int NW, int U>
+__global__ void __launch_bounds__(NW * 64) k_gemv32p(GemvArgs a) {
+  StampScope stamp_scope(a.stamp, NW * 64);
+  __shared__ float red[NW][32][33];
+  __shared__ float sv[32][33];
+  __shared__ float ov[EPI == EPI_ARGMAX ? 32 : 1][32];
+  __shared__ float oz[EPI == EPI_ARGMAX ? 32 : 1][32];
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const int col = lane & 31, kg = lane >> 5;
+  const int KS = a.K / 16, ntile = (a.N + 31) / 32;
+  const int spw = (KS + NW - 1) / NW;
+  const int s0 = min(KS, wv * spw), s1 = min(KS, s0 + spw);
+  const bf16x8* W0 = reinterpret_cast<const bf16x8*>(a.w) + lane;
+  const bf16x8* Ab = reinterpret_cast<const bf16x8*>(a.a.p) + lane;
+  typedef EpiPre<32, NW * 64> Pre;
+  auto fetch = [&](int tile, bf16x8* w, Pre& p) {
+    p.template load<bf16, EPI>(a, tile * 32);
+    const bf16x8* Wt = W0 + (size_t)tile * KS * 64;
+#pragma unroll
+    for (int u = 0; u < U; ++u) w[u] = Wt[(size_t)min(s0 + u, KS - 1) * 64];
+  };
+  bf16x8 av[U], wa[U], wb[U];
+  Pre pa, pb;
+  auto finish = [&](int tile, const bf16x8* w, const Pre& p) {
+    floatx16 acc = {};
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+      if (s0 + u < s1) acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[u], w[u], acc, 0, 0, 0);
+    __syncthreads();  // the previous tile's epilogue is done with red, sv, ov and oz
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) red[wv][8 * i + 4 * kg + j][col] = acc[4 * i + j];
+    __syncthreads();
+    for (int idx = threadIdx.x; idx < 32 * 32; idx += NW * 64) {
+      const int ml = idx >> 5, c = idx & 31;
+      float sum = 0.f;
+#pragma unroll
+      for (int w8 = 0; w8 < NW; ++w8) sum += red[w8][ml][c];
+      sv[ml][c] = sum;
+    }
+    __syncthreads();
+    RowsPre<32, 32, NW * 64> none;
+    finish_tile<bf16, EPI, 32, 32, NW * 64>(a, sv, ov, oz, a.mt0 * 32, tile * 32, p, none);
+  };
+  const int G = gridDim.x;
+  int tile = blockIdx.x;
+  fetch(tile, wa, pa);
+#pragma unroll
+  for (int u = 0; u < U; ++u) av[u] = Ab[((size_t)min(s0 + u, KS - 1) * a.a.mt + a.mt0) * 64];
+  for (;;) {
+    fetch(tile + G < ntile ? tile + G : tile, wb, pb);
+    __builtin_amdgcn_sched_barrier(0);
+    finish(tile, wa, pa);
+    tile += G;
+    if (tile >= ntile) break;
+    fetch(tile + G < ntile ? tile + G : tile, wa, pa);
+    __builtin_amdgcn_sched_barrier(0);
+    finish(tile, wb, pb);
+    tile += G;
+    if (tile >= ntile) break;
+  }
+}
+
 // ---------------------------------------------------------------- LayerNorm folded in (bf16, batch 1)
 // The block stages its operand in LDS itself (LnFold below): three bf16 split
 // terms per value (rows r, 9 + r, 18 + r; rows 27..31 zero) in the fragment order
@@ -1218,6 +1306,13 @@ static void launch_epi(const GemvArgs& a, hipStream_t st) {
     if (a.lnx != nullptr) {
       launch_ln<EPI>(a, st);
       return;
+    }
+    if constexpr (EPI == EPI_ARGMAX) {  // batch-1 vocabulary head: persistent blocks
+      if (a.nsplit == 3 && a.wkind == W_F32 && a.mt1 - a.mt0 == 1 && (a.K / 16 + 7) / 8 <= kU) {
+        const int ntile = (a.N + 31) / 32, per = (ntile + kHeadBlocks - 1) / kHeadBlocks;
+        k_gemv32p<EPI, 8, kU><<<(ntile + per - 1) / per, 512, 0, st>>>(a);
+        return;
+      }
     }
     const int ks = a.ksplit > 1 ? a.ksplit : 1;
     if (a.nsplit == 2 && a.wkind == W_F16) {  // several slots: 64 x 64 GEMM tiles (k split over grid y)
