@@ -916,20 +916,24 @@ __device__ __forceinline__ int lds_frag(int m, int k) {
 template <int NW>
 struct LnFold {
   static constexpr int NT = NW * 64;
-  static constexpr int I = (kRows * (kLnFoldMaxK / 8) + NT - 1) / NT;  // items per lane
+  // Item t = lane + i S for i < I, with the stride S = NT - NT % (K/8) a multiple of
+  // K/8: a lane's items share their 8 columns (one load of the gains) and lanes
+  // >= S hold none.  K <= kLnFoldMaxK gives at most I items per lane.
+  static constexpr int I = (kRows + NT / (kLnFoldMaxK / 8) - 1) / (NT / (kLnFoldMaxK / 8));
   static_assert(NW >= kRows, "one wave per row merges the statistics");
   float x[I][8];
-  uint4 g[I];
+  uint4 g;
 
-  // Unconditional loads (the index is clamped; items past the last are not used).
+  // Only the items that exist are loaded; these loads are all issued before the
+  // weights', so waiting for them never waits for the weights.
   __device__ __forceinline__ void load(const GemvArgs& a) {
-    const int nch = a.K >> 3, ni = kRows * nch;
-    const uint4* G = reinterpret_cast<const uint4*>(a.lng);
+    const int nch = a.K >> 3, ni = kRows * nch, S = NT - NT % nch;
+    const int c = (int)threadIdx.x % nch;
+    if ((int)threadIdx.x < S) g = reinterpret_cast<const uint4*>(a.lng)[c];
 #pragma unroll
     for (int i = 0; i < I; ++i) {
-      const int t = min((int)threadIdx.x + i * NT, ni - 1), r = t / nch, c = t - r * nch;
-      ld8(a.lnx + (size_t)r * a.K + 8 * c, x[i]);
-      g[i] = G[c];
+      const int t = (int)threadIdx.x + i * S;
+      if ((int)threadIdx.x < S && t < ni) ld8(a.lnx + (size_t)(t / nch) * a.K + 8 * c, x[i]);
     }
   }
 
@@ -938,13 +942,14 @@ struct LnFold {
   // ps + r * pstride: sums at [c], squared deviations at [K/8 + c].
   template <int TILE>
   __device__ __forceinline__ void stage(const GemvArgs& a, uint4* aop, float* ps, int pstride) const {
-    const int nch = a.K >> 3, ni = kRows * nch;
+    const int nch = a.K >> 3, ni = kRows * nch, S = NT - NT % nch;
+    const int c = (int)threadIdx.x % nch;
 #pragma unroll
     for (int i = 0; i < I; ++i) {
-      const int t = (int)threadIdx.x + i * NT;
-      if (t < ni) {
-        const int r = t / nch, c = t - r * nch;
-        const uint32_t gw[4] = {g[i].x, g[i].y, g[i].z, g[i].w};
+      const int t = (int)threadIdx.x + i * S;
+      if ((int)threadIdx.x < S && t < ni) {
+        const int r = t / nch;
+        const uint32_t gw[4] = {g.x, g.y, g.z, g.w};
         uint32_t th[8], tm[8], tl[8];
         float sum = 0.f;
 #pragma unroll
