@@ -970,6 +970,18 @@ struct LnFold {
         aop[lds_frag<TILE>(2 * kRows + r, 8 * c)] = pack8(tl);
         ps[r * pstride + c] = sum;
         ps[r * pstride + nch + c] = dev;
+        if (a.tap >= 0 && t % (int)gridDim.x == (int)blockIdx.x) {
+          // the drafter tap of the rows (the previous block's output, 16-row
+          // fragment order, three split terms): each item written by one block
+          uint32_t xh[8], xm[8], xl[8];
+#pragma unroll
+          for (int e = 0; e < 8; ++e) split3_bits(x[i][e], xh[e], xm[e], xl[e]);
+          uint4* T = reinterpret_cast<uint4*>(a.aout.p);
+          const int row = a.slot0 * kRows + r, col = a.tap * a.K + 8 * c;
+          T[afrag16_index(row, col, a.aout.mt) / 8] = pack8(xh);
+          T[afrag16_index(a.R9 + row, col, a.aout.mt) / 8] = pack8(xm);
+          T[afrag16_index(2 * a.R9 + row, col, a.aout.mt) / 8] = pack8(xl);
+        }
       }
     }
     for (int t = threadIdx.x; t < (32 - 3 * kRows) * nch; t += NT)

@@ -244,6 +244,7 @@ struct Runner {
   // The LayerNorm operand of the next product was already written by the
   // residual reduction (Ad16 for a block's first product, Ad32 for the head).
   bool ln_ready = false;
+  int tap_next = -1;  // drafter tap the next folded q|k|v product writes from its rows (-1: none)
 
   // The LayerNorm that follows a block: the next block's first one, or the final
   // one before the vocabulary head (wide: its operand feeds 32-column tiles).
@@ -459,15 +460,19 @@ struct Runner {
     gemv_ln("gemv_fc1", EPI_GELU, slot0, n, h_, b.ln3_g, b.ln3_b, b.c_fc1, c.d_ff, 0, Ad32(), b.w_fc1, b.b_fc1, d, c.d_ff,
             nullptr, 0, Af16());
     const int ksplit = L.fc2_split > 0 ? L.fc2_split : fc2_split_batch(slot0, n);
-    if (fuse_oproj() && L.fc2_split > 0 && tap < 0) {
-      // batch 1 (bf16), no tap after this block: the k-splits add their partial
-      // sums and the bias straight to the residual rows; the next product folds
-      // its LayerNorm in (or the head's LayerNorm runs on its own)
+    // a tap block followed by a target block: that block's q|k|v product, which
+    // folds its LayerNorm and so reads the rows anyway, writes the tap
+    const bool tap_later = tap >= 0 && !nx.wide && fold_ln() && Atap16().kind == OP_F16;
+    if (fuse_oproj() && L.fc2_split > 0 && (tap < 0 || tap_later)) {
+      // batch 1 (bf16): the k-splits add their partial sums and the bias straight
+      // to the residual rows; the next product folds its LayerNorm in (or the
+      // head's LayerNorm runs on its own)
       GemvArgs a = gemv_args(slot0, n, Af16(), b.w_fc2, b.b_fc2, c.d_ff, d, h_, d, Operand{nullptr, 0, OP_ROW, 0}, -1);
       a.ct = 4;
       a.ksplit = L.fc2_split;
       run_gemv("gemv_fc2", EPI_ACC, n, a);
       ln_ready = false;
+      tap_next = tap;
     } else if (ksplit > 0) {
       // k-split partial sums, then h += sum + bias, the tap, and the next LayerNorm
       GemvArgs a = gemv_args(slot0, n, Af16(), b.w_fc2, b.b_fc2, c.d_ff, d, F32(L.part), d, Operand{nullptr, 0, OP_ROW, 0}, -1);
@@ -494,6 +499,7 @@ struct Runner {
     const int d = c.d_model;
     float *h_ = F32(L.h), *qkv = F32(L.qkv);
     ln_ready = false;
+    tap_next = -1;
     for (int l = 0; l < c.n_layer; ++l) {
       const BlockW& b = L.tb[l];
       int tap = -1;
@@ -504,6 +510,11 @@ struct Runner {
       a.y = qkv; a.ldy = 3 * d; a.cache = skv_layer(l); a.kv_stride = kv_stride();
       if (ln_ready) a.a = Ad16();
       else ln_operand(a, slot0, n, h_, b.ln1_g, b.ln1_b, Ad16(), true, b.c_qkv, 3 * d);
+      if (tap_next >= 0) {
+        a.aout = Atap16();
+        a.tap = tap_next;
+        tap_next = -1;
+      }
       ln_ready = false;
       run_gemv("gemv_qkv", EPI_QKV, n, a);
       AttnArgs at{};

@@ -57,7 +57,8 @@ struct GemvArgs {
   int ct;  // 16-column tiles per block (4: wide kernel, with split-K), else 1
   float* y;          // STORE: out; RESID: residual stream; QKV: q; ARGMAX: optional logits
   int ldy;
-  Operand aout;      // GELU: operand of the next product; RESID: tap operand (column offset tap * N)
+  Operand aout;      // GELU: operand of the next product; RESID: tap operand (column offset tap * N);
+                     // LayerNorm folded in (batch 1): tap operand of the rows lnx (column offset tap * K)
   int tap;
   // QKV cache append
   const int* state;
