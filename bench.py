@@ -42,7 +42,7 @@ SYMBOL_OF_ROLE = {  # kernels (rocprofv3 names) that one launch of the role disp
     "gemv_fc1": ("void wf::k_gemv32_ln<1, 16, 5>(wf::GemvArgs)",),
     "gemv_fc2": ("void wf::k_gemv16k<6, 8, 4, 2>(wf::GemvArgs)",),  # k_gemv16k<5, 8, 4, 2> in the tap blocks
     "reduce_ln": ("void wf::k_reduce_ln<wf::bf16>(wf::RlnArgs)",),
-    "head": ("void wf::k_gemv32<4, 8>(wf::GemvArgs)",),
+    "head": ("void wf::k_gemv32p<4, 8, 10>(wf::GemvArgs)",),
 }
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic_large-v3_b1_pmc.md")
 
@@ -88,7 +88,7 @@ KERNEL_OF_ROLE = {
     "gemv_fc1": "wf::k_gemv32_ln<1, 16, 5> (EPI_GELU, LayerNorm folded)",
     "gemv_fc2": "wf::k_gemv16k<6, 8, 4, 2> (EPI_ACC, split-K into the residual; EPI_PART in the tap blocks)",
     "reduce_ln": "wf::k_reduce_ln<wf::bf16>",
-    "head": "wf::k_gemv32<4, 8> (EPI_ARGMAX)",
+    "head": "wf::k_gemv32p<4, 8, 10> (EPI_ARGMAX, persistent blocks)",
 }
 
 
