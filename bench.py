@@ -34,7 +34,7 @@ HBM_PEAK_GBS = 8000.0
 
 # profile role -> kernel symbol as a kernel trace names it (batch-1 bf16 path)
 SYMBOL_OF_ROLE = {  # kernels (rocprofv3 names) that one launch of the role dispatches
-    "attn_cross": ("void wf::k_attn_cross_mx<1, 4>(wf::CrossArgs)", "void wf::k_attn_cross_merge<wf::bf16, true>(wf::CrossArgs)"),
+    "attn_cross": ("void wf::k_attn_cross_mx<1, 4>(wf::CrossArgs)", "void wf::k_attn_cross_merge<wf::bf16, true, 12>(wf::CrossArgs)"),
     "attn_self": ("void wf::k_attn_self_mx<true>(wf::AttnArgs)",),
     "gemv_o": ("void wf::k_gemv16<2, 4>(wf::GemvArgs)",),
     "gemv_qkv": ("void wf::k_gemv16_ln<3, 16, 3>(wf::GemvArgs)",),  # k_gemv16<3, 4> after the tap blocks
@@ -80,7 +80,7 @@ def measured_traffic(role):
 
 # profile role -> kernel symbol of the batch-1 bf16 path (the roofline names the kernel)
 KERNEL_OF_ROLE = {
-    "attn_cross": "wf::k_attn_cross_mx<1, 4> + wf::k_attn_cross_merge<wf::bf16, true>",
+    "attn_cross": "wf::k_attn_cross_mx<1, 4> + wf::k_attn_cross_merge<wf::bf16, true, 12>",
     "attn_self": "wf::k_attn_self_mx<true> (W_o fused)",
     "gemv_o": "wf::k_gemv16<2, 4> (EPI_RESID)",
     "gemv_qkv": "wf::k_gemv16_ln<3, 16, 3> (EPI_QKV, LayerNorm folded; k_gemv16<3, 4> after the tap blocks)",

@@ -842,14 +842,13 @@ __global__ void __launch_bounds__(NW * 64) k_attn_cross_mx(CrossArgs a) {
   }
 }
 
-// Merge of the chunk records of one (head, slot): one thread per (row, dim).  The
-// records are read kXmGroup chunks at a time with every load of a group issued
+// Merge of the chunk records of one (head, slot): one thread per (row, 4 dims).
+// The records are read G chunks at a time with every load of a group issued
 // together (indices clamped, chunks past the end weighted 0); groups combine with
 // the same max-shifted rule.  With a fused output product (grid z = column group)
 // the merged rows go to LDS and the block adds their product to h.
-constexpr int kXmThreads = 640;  // >= kRows * 64 and >= the fused product's 2C items
-constexpr int kXmGroup = 16;
-template <typename S, bool FUSED>
+constexpr int kXmThreads = 640;  // >= the fused product's 2C items
+template <typename S, bool FUSED, int G>
 __global__ void __launch_bounds__(kXmThreads) k_attn_cross_merge(CrossArgs a) {
   StampScope stamp_scope(a.stamp, kXmThreads);
   __shared__ float Ob[kRows][64];
@@ -859,40 +858,64 @@ __global__ void __launch_bounds__(kXmThreads) k_attn_cross_merge(CrossArgs a) {
   // them would make the record loads below wait for them)
   OpPre opre;
   if constexpr (FUSED) op_load(a.op, head, g, threadIdx.x, opre);
-  const int t = threadIdx.x, r = t >> 6, dim = t & 63;
-  if (t < kRows * 64) {
+  const int t = threadIdx.x;
+  // thread t < 9 * 16 merges row t / 16, dims 4 (t % 16) .. + 3 (one float4 of each
+  // record), all the chunks of a group of G loaded before the first is used
+  if (t < kRows * 16) {
+    const int r = t >> 4, d4 = 4 * (t & 15);
     const float* part = a.part + (size_t)(blockIdx.y * a.n_head + head) * a.nchunk * kXrPart;
-    float M = -INFINITY, L = 0.f, o = 0.f;
-    for (int c0 = 0; c0 < a.nchunk; c0 += kXmGroup) {
-      float m[kXmGroup], l[kXmGroup], v[kXmGroup];
+    float M = -INFINITY, L = 0.f;
+    float4 o = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int c0 = 0; c0 < a.nchunk; c0 += G) {
+      float m[G], l[G];
+      float4 v[G];
 #pragma unroll
-      for (int j = 0; j < kXmGroup; ++j) {
+      for (int j = 0; j < G; ++j) {
         const float* pc = part + (size_t)min(c0 + j, a.nchunk - 1) * kXrPart;
         m[j] = pc[r];
         l[j] = pc[16 + r];
-        v[j] = pc[32 + t];
+        v[j] = *reinterpret_cast<const float4*>(pc + 32 + r * 64 + d4);
       }
       float Mg = M;
 #pragma unroll
-      for (int j = 0; j < kXmGroup; ++j) Mg = fmaxf(Mg, m[j]);
+      for (int j = 0; j < G; ++j) Mg = fmaxf(Mg, m[j]);
       const float f0 = __expf(M - Mg);  // 0 before the first group
       L *= f0;
-      o *= f0;
+      o.x *= f0;
+      o.y *= f0;
+      o.z *= f0;
+      o.w *= f0;
 #pragma unroll
-      for (int j = 0; j < kXmGroup; ++j) {
+      for (int j = 0; j < G; ++j) {
         const float f = c0 + j < a.nchunk ? __expf(m[j] - Mg) : 0.f;
         L = fmaf(f, l[j], L);
-        o = fmaf(f, v[j], o);
+        o.x = fmaf(f, v[j].x, o.x);
+        o.y = fmaf(f, v[j].y, o.y);
+        o.z = fmaf(f, v[j].z, o.z);
+        o.w = fmaf(f, v[j].w, o.w);
       }
       M = Mg;
     }
-    if constexpr (FUSED) Ob[r][dim] = o / L;
-    else put_op<S>(a.out, a.nsplit, a.R9, slot * kRows + r, head * kHeadDim + dim, o / L);
+    const float ov[4] = {o.x / L, o.y / L, o.z / L, o.w / L};
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      if constexpr (FUSED) Ob[r][d4 + k] = ov[k];
+      else put_op<S>(a.out, a.nsplit, a.R9, slot * kRows + r, head * kHeadDim + d4 + k, ov[k]);
+    }
   }
   if constexpr (FUSED) {
     __syncthreads();
     op_apply(a.op, head, g, t, opre, Ob, slot * kRows, ophalf);
   }
+}
+
+// Merge launch with a chunk group that covers the usual chunk counts in one pass.
+template <typename S, bool FUSED>
+static void launch_merge(const CrossArgs& a, int n, hipStream_t st) {
+  const dim3 grid(a.n_head, n, FUSED ? kOpGroups : 1);
+  if (a.nchunk <= 4) k_attn_cross_merge<S, FUSED, 4><<<grid, kXmThreads, 0, st>>>(a);
+  else if (a.nchunk <= 12) k_attn_cross_merge<S, FUSED, 12><<<grid, kXmThreads, 0, st>>>(a);
+  else k_attn_cross_merge<S, FUSED, 16><<<grid, kXmThreads, 0, st>>>(a);
 }
 
 // ---------------------------------------------------------------- causal self-attention
@@ -1224,8 +1247,8 @@ void Ops<S>::attn_cross(const CrossArgs& a, int n, hipStream_t st) {
     k_attn_cross_rows<S><<<dim3(a.n_head, n, a.nchunk), kXrThreads, xr_lds_bytes(a.chunk), st>>>(a);
   }
   if (a.nchunk > 1 || a.op.w != nullptr) {
-    if (a.op.w != nullptr) k_attn_cross_merge<S, true><<<dim3(a.n_head, n, kOpGroups), kXmThreads, 0, st>>>(a);
-    else k_attn_cross_merge<S, false><<<dim3(a.n_head, n, 1), kXmThreads, 0, st>>>(a);
+    if (a.op.w != nullptr) launch_merge<S, true>(a, n, st);
+    else launch_merge<S, false>(a, n, st);
   }
 }
 
