@@ -119,6 +119,31 @@ def test_micro_bf16_b1_split_operands():
     ls.close()
 
 
+def test_micro_bf16_b1_offset_residual():
+    """Batch 1, bf16, with a residual stream whose mean (about 4, from a shifted
+    output bias of the first block) is tens of times its spread.  At batch 1 a
+    LayerNorm feeding a product is applied after it, r((x*g)W^T - m gW^T) + bW^T,
+    and the two terms nearly cancel for such rows; the logits must still agree
+    with the fp32 oracle to the bf16 tolerance (LayerNorm itself is shift
+    invariant, so the oracle's rows are well conditioned)."""
+    from lockstep import Lockstep
+    from wf_fixtures.gen import _round_inplace
+    cfg = MICRO_BF16
+    W = make_weights(cfg)
+    b = W.values["t0.attn.o.b"]
+    b += 4.0
+    _round_inplace(b.reshape(-1))
+    prompts = [make_prefix(cfg, 0, 11)]
+    ls = Lockstep(cfg, W, prompts, [40], TOL_MICRO_BF16)
+    opts = OracleOpts(dtype=np.float32, kv_bf16=True)
+    T = Target(cfg, W.values, opts)
+    refs = [plain_greedy(T, make_memory(cfg, 0), prompts[0], 40)]
+    _run_planted(ls, refs, np.random.default_rng(6), 8)
+    print(f"micro-bf16 b1 offset: max |dlogit| draft {ls.max_dlogit:.3e} target {ls.max_tlogit:.3e}, near ties {ls.near_ties}")
+    assert ls.steps == 8
+    ls.close()
+
+
 def test_micro_bf16_b3_two_plane_operands():
     """Batch 3, bf16: each operand value as two bf16 planes (hi + lo), products
     accurate to fp32 rounding; compared with the plain fp32 oracle."""
