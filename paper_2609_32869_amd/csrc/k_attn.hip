@@ -611,14 +611,26 @@ struct OpPre {
   uint4 w[4];
   uint32_t b;
 };
+// OWNED: threads t >= 2C load nothing (their registers get defined values from an
+// empty asm, so no copy at the join waits for the other threads' loads); only for a
+// kernel whose next waits also cover younger loads, since the compiler counts
+// outstanding loads on the path without these.  Otherwise every thread loads (index
+// clamped), which keeps the count of younger loads exact.
+template <bool OWNED>
 __device__ __forceinline__ void op_load(const OprojArgs& op, int head, int g, int t, OpPre& pre) {
   const int C = op.N / kOpGroups, KS = op.K / 32;
-  const int tt = min(t, 2 * C - 1);
-  const int c = g * C + tt % C, hs = tt / C;
-  const uint4* wp = reinterpret_cast<const uint4*>(op.w) + ((size_t)(c >> 4) * KS + 2 * head + hs) * 64 + (c & 15);
+  if (!OWNED) t = min(t, 2 * C - 1);
+  if (!OWNED || t < 2 * C) {
+    const int c = g * C + t % C, hs = t / C;
+    const uint4* wp = reinterpret_cast<const uint4*>(op.w) + ((size_t)(c >> 4) * KS + 2 * head + hs) * 64 + (c & 15);
 #pragma unroll
-  for (int kq = 0; kq < 4; ++kq) pre.w[kq] = wp[16 * kq];
-  pre.b = reinterpret_cast<const uint16_t*>(op.bias)[c];
+    for (int kq = 0; kq < 4; ++kq) pre.w[kq] = wp[16 * kq];
+    pre.b = reinterpret_cast<const uint16_t*>(op.bias)[c];
+  } else {
+#pragma unroll
+    for (int kq = 0; kq < 4; ++kq) __asm__ volatile("" : "=v"(pre.w[kq]));
+    __asm__ volatile("" : "=v"(pre.b));
+  }
 }
 // Every thread of the block calls it (it holds a barrier).  Thread t < 2C owns
 // column c and half hs of the head's 64 dims; the two halves meet in LDS (half)
@@ -857,7 +869,7 @@ __global__ void __launch_bounds__(kXmThreads) k_attn_cross_merge(CrossArgs a) {
   // FUSED: the output product's weights are loaded unconditionally (a branch around
   // them would make the record loads below wait for them)
   OpPre opre;
-  if constexpr (FUSED) op_load(a.op, head, g, threadIdx.x, opre);
+  if constexpr (FUSED) op_load<true>(a.op, head, g, threadIdx.x, opre);
   const int t = threadIdx.x;
   // thread t < 9 * 16 merges row t / 16, dims 4 (t % 16) .. + 3 (one float4 of each
   // record), all the chunks of a group of G loaded before the first is used
@@ -1003,7 +1015,7 @@ __global__ void __launch_bounds__(kSxThreads) k_attn_self_mx(AttnArgs a) {
   }
   __builtin_amdgcn_sched_barrier(0);
   OpPre opre;
-  if constexpr (FUSED) op_load(a.op, head, g, threadIdx.x, opre);
+  if constexpr (FUSED) op_load<false>(a.op, head, g, threadIdx.x, opre);
   __builtin_amdgcn_sched_barrier(0);
   float mrow = -INFINITY, lrow = 0.f;
   floatx4 oacc[4];
