@@ -14,47 +14,54 @@ namespace wf {
 // ---------------------------------------------------------------- LayerNorm -> operand
 // y = g * (x - mean) / sqrt(var + 1e-5) + b over the d columns of a row (Whisper's
 // pre-LN blocks and final LN), written as the operand of the next product.  One
-// block of 256 threads per row; the row stays in registers (d <= 2048).
+// wave per row, four rows per block: a lane holds 8 consecutive columns of each of
+// its chunks (lane, lane + 64, ...; d <= 2048), loaded and written 16 bytes at a
+// time, and the statistics are wave sums (no barrier).
+constexpr int kLnRowsPerBlock = 4;
 template <typename S>
-__global__ void __launch_bounds__(256) k_ln_operand(LnArgs a) {
-  StampScope stamp_scope(a.stamp, 256);
-  __shared__ float red[8];
-  const int row = a.row0 + blockIdx.x;
+__global__ void __launch_bounds__(64 * kLnRowsPerBlock) k_ln_operand(LnArgs a) {
+  StampScope stamp_scope(a.stamp, 64 * kLnRowsPerBlock);
+  constexpr int J = 2048 / 8 / 64;
+  const int lane = threadIdx.x & 63;
+  const int row = a.row0 + blockIdx.x * kLnRowsPerBlock + (int)(threadIdx.x >> 6);
+  if (row >= a.row0 + a.rows) return;
+  const int nch = a.d >> 3;
   const float* xr = a.x + (size_t)row * a.d;
-  // every load first and unconditionally (columns past d re-read the last one)
-  float v[8];
-  uint32_t gv[8], bv[8];
+  // every load first and unconditionally (chunks past the row re-read the last one)
+  float v[J][8], gv[J][8], bv[J][8];
 #pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    const int i = min(threadIdx.x + j * 256, a.d - 1);
-    v[j] = xr[i];
-    gv[j] = ld_bits<S>(a.g, i);
-    bv[j] = ld_bits<S>(a.b, i);
+  for (int j = 0; j < J; ++j) {
+    const int c = min(lane + 64 * j, nch - 1);
+    ld8(xr + 8 * c, v[j]);
+    ld8(reinterpret_cast<const S*>(a.g) + 8 * c, gv[j]);
+    ld8(reinterpret_cast<const S*>(a.b) + 8 * c, bv[j]);
   }
   float s = 0.f;
 #pragma unroll
-  for (int j = 0; j < 8; ++j) s += threadIdx.x + j * 256 < a.d ? v[j] : 0.f;
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  s = wave_sum(s);
-  if (lane == 0) red[w] = s;
-  __syncthreads();
-  const float mean = ((red[0] + red[1]) + (red[2] + red[3])) / (float)a.d;
+  for (int j = 0; j < J; ++j)
+    if (lane + 64 * j < nch)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) s += v[j][e];
+  const float mean = wave_sum(s) / (float)a.d;
   float q = 0.f;
 #pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    const int i = threadIdx.x + j * 256;
-    const float c = v[j] - mean;
-    q += i < a.d ? c * c : 0.f;
-  }
-  q = wave_sum(q);
-  if (lane == 0) red[4 + w] = q;
-  __syncthreads();
-  const float var = ((red[4] + red[5]) + (red[6] + red[7])) / (float)a.d;
-  const float inv = 1.0f / sqrtf(var + 1e-5f);
+  for (int j = 0; j < J; ++j)
+    if (lane + 64 * j < nch)
 #pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    const int i = threadIdx.x + j * 256;
-    if (i < a.d) put_op<S>(a.out, a.nsplit, a.R9, row, i, (v[j] - mean) * inv * from_bits<S>(gv[j]) + from_bits<S>(bv[j]));
+      for (int e = 0; e < 8; ++e) {
+        const float c = v[j][e] - mean;
+        q += c * c;
+      }
+  const float inv = 1.0f / sqrtf(wave_sum(q) / (float)a.d + 1e-5f);
+#pragma unroll
+  for (int j = 0; j < J; ++j) {
+    const int c = lane + 64 * j;
+    if (c < nch) {
+      float y[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) y[e] = (v[j][e] - mean) * inv * gv[j][e] + bv[j][e];
+      put_op8<S>(a.out, a.nsplit, a.R9, row, 8 * c, y);
+    }
   }
 }
 
@@ -739,7 +746,9 @@ __global__ void __launch_bounds__(kRlnThreads) k_reduce_ln(RlnArgs a) {
 // ---------------------------------------------------------------- launchers
 template <typename S>
 void Ops<S>::ln_operand(const LnArgs& a, int rows, hipStream_t st) {
-  k_ln_operand<S><<<rows, 256, 0, st>>>(a);
+  LnArgs b = a;
+  b.rows = rows;
+  k_ln_operand<S><<<(rows + kLnRowsPerBlock - 1) / kLnRowsPerBlock, 64 * kLnRowsPerBlock, 0, st>>>(b);
 }
 template <typename S>
 void Ops<S>::reduce_ln(const RlnArgs& a, int rows, hipStream_t st) {

@@ -165,6 +165,7 @@ struct LnArgs {
   const void* b;
   Operand out;
   int d, row0, nsplit, R9;
+  int rows;  // rows row0 .. row0 + rows - 1 (set by the launcher)
   unsigned long long* stamp;  // launch timing slot (profiled calls), or null
 };
 

@@ -46,4 +46,44 @@ __device__ __forceinline__ void put_op(const Operand& o, int nsplit, int R9, int
   put_operand(o, nsplit, R9, row, col, v, S{});
 }
 
+// The same for the 8 values of row `row`, columns col .. col + 7 (col a multiple of
+// 8): they are contiguous in every operand order, so each term is one 16-byte store.
+__device__ __forceinline__ uint4 pack8_bits(const uint32_t* h) {
+  return make_uint4(h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16), h[6] | (h[7] << 16));
+}
+__device__ __forceinline__ void put_operand8(const Operand& o, int, int, int row, int col, const float* v, float) {
+  float* p = reinterpret_cast<float*>(o.p) + op_index(o, row, col);
+  *reinterpret_cast<float4*>(p) = make_float4(v[0], v[1], v[2], v[3]);
+  *reinterpret_cast<float4*>(p + 4) = make_float4(v[4], v[5], v[6], v[7]);
+}
+__device__ __forceinline__ void put_operand8(const Operand& o, int nsplit, int R9, int row, int col, const float* v, bf16) {
+  uint4* A = reinterpret_cast<uint4*>(o.p);
+  uint32_t h[8], m[8], l[8];
+  if (nsplit == 3) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) split3_bits(v[e], h[e], m[e], l[e]);
+    A[op_index(o, row, col) / 8] = pack8_bits(h);
+    A[op_index(o, R9 + row, col) / 8] = pack8_bits(m);
+    A[op_index(o, 2 * R9 + row, col) / 8] = pack8_bits(l);
+  } else if (nsplit == 2) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const uint32_t hb = __float_as_uint(v[e]) & 0xffff0000u;
+      h[e] = hb >> 16;
+      l[e] = bf16_bits_rne(v[e] - __uint_as_float(hb));
+    }
+    const size_t i = op_index(o, row, col);
+    A[i / 8] = pack8_bits(h);
+    A[(i + (size_t)o.mt * 16 * o.ld) / 8] = pack8_bits(l);
+  } else {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) h[e] = bf16_bits_rne(v[e]);
+    A[op_index(o, row, col) / 8] = pack8_bits(h);
+  }
+}
+template <typename S>
+__device__ __forceinline__ void put_op8(const Operand& o, int nsplit, int R9, int row, int col, const float* v) {
+  put_operand8(o, nsplit, R9, row, col, v, S{});
+}
+
 }  // namespace wf
