@@ -228,7 +228,9 @@ __device__ __forceinline__ void finish_tile(const GemvArgs& a, float (*sv)[TC + 
     // so their latencies overlap instead of adding up element by element.
     constexpr int P = (TM * TC + NT - 1) / NT;
     if constexpr (RP) rp.arrive();
-    const bool has_bias = a.bias != nullptr;  // without one, read the weights and discard
+    // without one, read the weights and discard; split-K partial sums added to y
+    // (EPI_ACC) take the bias from the first k-split only
+    const bool has_bias = a.bias != nullptr && !(EPI == EPI_ACC && blockIdx.y != 0);
     const S* bias = reinterpret_cast<const S*>(has_bias ? a.bias : a.w);
     const int rmax = a.R9 - 1, nmax = a.N - 1;
     float bv[P], rv[P];
@@ -1315,8 +1317,18 @@ static void launch_splitk(const GemvArgs& a, hipStream_t st) {
 
 template <typename S, int EPI>
 static void launch_epi(const GemvArgs& a, hipStream_t st) {
-  if constexpr (EPI == EPI_ACC) {  // batch 1, bf16
-    if constexpr (sizeof(S) == 2) launch_splitk<EPI_ACC>(a, st);
+  if constexpr (EPI == EPI_ACC) {  // bf16: split-K partial sums added to y
+    if constexpr (sizeof(S) == 2) {
+      if (a.nsplit == 2 && a.wkind == W_F16) {  // several slots: GEMM tiles, k split over grid y
+        const int mb0 = a.slot0 * kRows / 64, mb1 = ((a.slot0 + a.nslots) * kRows + 63) / 64;
+        const int nmb = mb1 - mb0, nnb = (a.N + 63) / 64, ks = a.ksplit > 1 ? a.ksplit : 1;
+        const unsigned nb = gemm_grid(nmb, nnb);
+        if (nb * (unsigned)ks >= kGemmStagedBlocks) k_gemm16s<EPI><<<dim3(nb, ks), 256, 0, st>>>(a, mb0, nmb, nnb);
+        else k_gemm16<EPI><<<dim3(nb, ks), 256, 0, st>>>(a, mb0, nmb, nnb);
+      } else {
+        launch_splitk<EPI_ACC>(a, st);  // batch 1
+      }
+    }
     return;
   } else {
   if constexpr (sizeof(S) == 2) {

@@ -342,6 +342,23 @@ struct Runner {
     a.tap = tap;
     return a;
   }
+  // h += x W^T + b.  With several slots whose 64 x 64 tiles cover fewer than 160
+  // blocks, the k-steps are split kResidSplit ways and every split adds its
+  // partial sums to h (the bias from the first), so the launch fills the chip.
+  void resid(const char* tag, int slot0, int n, Operand x, size_t w, size_t b, int K, int N) {
+    GemvArgs a = gemv_args(slot0, n, x, w, b, K, N, F32(L.h), c.d_model, Operand{nullptr, 0, OP_ROW, 0}, -1);
+    if (L.nsplit_op == 2) {
+      const int mb0 = slot0 * kRows / 64, mb1 = ((slot0 + n) * kRows + 63) / 64;
+      const int tiles = (mb1 - mb0) * ((N + 63) / 64);
+      if (tiles < 160 && (K / 32) % kResidSplit == 0) {
+        a.ksplit = kResidSplit;
+        run_gemv(tag, EPI_ACC, n, a);
+        return;
+      }
+    }
+    run_gemv(tag, EPI_RESID, n, a);
+  }
+
   // tag: the product's role in the step, for the eager profile
   void run_gemv(const char* tag, int epi, int n, const GemvArgs& a) {
     launch(tag, gemv_bytes(n, a.K, a.N, epi), [&](unsigned long long* sp) {
@@ -456,7 +473,7 @@ struct Runner {
     gemv_ln("gemv_q2", EPI_STORE, slot0, n, h_, b.ln2_g, b.ln2_b, b.c_q2, d, 0, Ad16(), b.w_q2, b.b_q2, d, d, qkv, 3 * d);
     const OprojArgs op2 = oproj(b.w_o2, b.b_o2);
     cross(slot0, n, xlayer, op2);
-    if (op2.w == nullptr) gemv("gemv_o", EPI_RESID, slot0, n, Ad16(), b.w_o2, b.b_o2, d, d, h_, d);
+    if (op2.w == nullptr) resid("gemv_o", slot0, n, Ad16(), b.w_o2, b.b_o2, d, d);
     gemv_ln("gemv_fc1", EPI_GELU, slot0, n, h_, b.ln3_g, b.ln3_b, b.c_fc1, c.d_ff, 0, Ad32(), b.w_fc1, b.b_fc1, d, c.d_ff,
             nullptr, 0, Af16());
     const int ksplit = L.fc2_split > 0 ? L.fc2_split : fc2_split_batch(slot0, n);
@@ -529,7 +546,7 @@ struct Runner {
         at.stamp = sp;
         Ops<S>::attn_self(at, n, st);
       });
-      if (at.op.w == nullptr) gemv("gemv_o", EPI_RESID, slot0, n, Ad16(), b.w_o, b.b_o, d, d, h_, d);
+      if (at.op.w == nullptr) resid("gemv_o", slot0, n, Ad16(), b.w_o, b.b_o, d, d);
       const LnNext nx = l + 1 < c.n_layer ? LnNext{L.tb[l + 1].ln1_g, L.tb[l + 1].ln1_b, false}
                                           : LnNext{L.lnf_g, L.lnf_b, true};
       block_tail(slot0, n, b, l, tap, nx);
@@ -607,7 +624,7 @@ struct Runner {
         at.stamp = sp;
         Ops<S>::attn_draft(at, n, st);
       });
-      gemv("gemv_o", EPI_RESID, slot0, n, Ad16(), b.w_o, b.b_o, d, d, h_, d);
+      resid("gemv_o", slot0, n, Ad16(), b.w_o, b.b_o, d, d);
       const LnNext nx = dl + 1 < c.n_draft_layer ? LnNext{L.db[dl + 1].ln1_g, L.db[dl + 1].ln1_b, false}
                                                  : LnNext{L.dlnf_g, L.dlnf_b, true};
       block_tail(slot0, n, b, c.n_layer + dl, -1, nx);

@@ -48,6 +48,7 @@ struct Layout {
 struct Handle;
 
 constexpr int kFc2SplitBatch = 4;  // k-splits of the second MLP product for small multi-slot batches
+constexpr int kResidSplit = 4;     // k-splits of the attention output products for small multi-slot batches
 
 struct GraphKey {
   int slot0, n, k_max;
