@@ -146,6 +146,21 @@ def test_micro_sampling_with_suppression():
     assert decisions > 20
 
 
+@pytest.mark.parametrize("temperature", [0.75, 1.0])
+def test_micro_bf16_b1_sampling(temperature):
+    """bf16 storage at batch 1 (ragged vocabulary 501, 45 frames), sampling: the
+    batch-1 kernels (folded LayerNorms, fused attention output products, split-K
+    second MLP product, persistent head with the Gumbel scores and softmax
+    normalisers) against the oracle; decisions compared where the oracle's margins
+    exceed the bf16 bar."""
+    cfg = MICRO.with_(name="micro-bf16", dtype="bf16", n_vocab=501, n_frames=45)
+    opts = OracleOpts(dtype=np.float32, kv_bf16=True)
+    decisions, ties = _sampling_lockstep(cfg, temperature, prompts=[make_prefix(cfg, 0, 11)], opts=opts,
+                                         gap_tol=2e-3, margin_tol=2e-3)
+    print(f"micro-bf16 b1 T={temperature}: {decisions} verified rows compared, near ties {ties}")
+    assert decisions > 20
+
+
 # ---------------------------------------------------------------- distribution on V = 64
 def _exact_next(cfg, W, mem, seq, temperature):
     T64 = Target(cfg, W.values, OracleOpts(dtype=np.float64))
