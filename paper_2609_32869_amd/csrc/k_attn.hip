@@ -1115,6 +1115,10 @@ __global__ void __launch_bounds__(kSxThreads) k_attn_self_mx(AttnArgs a) {
       for (int i = 0; i < 4; ++i) wo[w][n][16 * dt + 4 * kg + i] = oacc[dt][i];
   }
   __syncthreads();
+  if (a.clear_q) {  // every wave that multiplies has used its query values by now
+    for (int t = threadIdx.x; t < kRows * 64; t += kSxThreads)
+      const_cast<float*>(a.q)[(size_t)(slot * kRows + (t >> 6)) * a.ldq + head * kHeadDim + (t & 63)] = 0.f;
+  }
   for (int t = threadIdx.x; t < kRows * 64; t += kSxThreads) {
     const int r = t >> 6, dim = t & 63;
     float o = 0.f;

@@ -342,19 +342,23 @@ struct Runner {
     a.tap = tap;
     return a;
   }
+  // Several slots whose 64 x 64 tiles of an N-column product cover fewer than 160
+  // blocks: the product is split over k in kResidSplit (partial sums added).
+  bool split_small(int slot0, int n, int K, int N) const {
+    if (L.nsplit_op != 2) return false;
+    const int mb0 = slot0 * kRows / 64, mb1 = ((slot0 + n) * kRows + 63) / 64;
+    return (mb1 - mb0) * ((N + 63) / 64) < 160 && (K / 32) % kResidSplit == 0;
+  }
+
   // h += x W^T + b.  With several slots whose 64 x 64 tiles cover fewer than 160
   // blocks, the k-steps are split kResidSplit ways and every split adds its
   // partial sums to h (the bias from the first), so the launch fills the chip.
   void resid(const char* tag, int slot0, int n, Operand x, size_t w, size_t b, int K, int N) {
     GemvArgs a = gemv_args(slot0, n, x, w, b, K, N, F32(L.h), c.d_model, Operand{nullptr, 0, OP_ROW, 0}, -1);
-    if (L.nsplit_op == 2) {
-      const int mb0 = slot0 * kRows / 64, mb1 = ((slot0 + n) * kRows + 63) / 64;
-      const int tiles = (mb1 - mb0) * ((N + 63) / 64);
-      if (tiles < 160 && (K / 32) % kResidSplit == 0) {
-        a.ksplit = kResidSplit;
-        run_gemv(tag, EPI_ACC, n, a);
-        return;
-      }
+    if (split_small(slot0, n, K, N)) {
+      a.ksplit = kResidSplit;
+      run_gemv(tag, EPI_ACC, n, a);
+      return;
     }
     run_gemv(tag, EPI_RESID, n, a);
   }
@@ -467,10 +471,19 @@ struct Runner {
   }
 
   // second half of a decoder block shared by target and drafter: cross-attention and MLP
-  void block_tail(int slot0, int n, const BlockW& b, int xlayer, int tap, const LnNext& nx) {
+  // q_clear: the self-attention before left the query places at zero, so a
+  // split W'_q product may add its partial sums into them
+  void block_tail(int slot0, int n, const BlockW& b, int xlayer, int tap, const LnNext& nx, bool q_clear = false) {
     const int d = c.d_model;
     float *h_ = F32(L.h), *qkv = F32(L.qkv);
-    gemv_ln("gemv_q2", EPI_STORE, slot0, n, h_, b.ln2_g, b.ln2_b, b.c_q2, d, 0, Ad16(), b.w_q2, b.b_q2, d, d, qkv, 3 * d);
+    if (q_clear) {
+      GemvArgs a = gemv_args(slot0, n, Ad16(), b.w_q2, b.b_q2, d, d, qkv, 3 * d, Operand{nullptr, 0, OP_ROW, 0}, -1);
+      ln_operand(a, slot0, n, h_, b.ln2_g, b.ln2_b, Ad16(), true, b.c_q2, d, 0);
+      a.ksplit = kResidSplit;
+      run_gemv("gemv_q2", EPI_ACC, n, a);
+    } else {
+      gemv_ln("gemv_q2", EPI_STORE, slot0, n, h_, b.ln2_g, b.ln2_b, b.c_q2, d, 0, Ad16(), b.w_q2, b.b_q2, d, d, qkv, 3 * d);
+    }
     const OprojArgs op2 = oproj(b.w_o2, b.b_o2);
     cross(slot0, n, xlayer, op2);
     if (op2.w == nullptr) resid("gemv_o", slot0, n, Ad16(), b.w_o2, b.b_o2, d, d);
@@ -540,6 +553,11 @@ struct Runner {
       at.slot0 = slot0; at.d = d; at.n_head = c.n_head; at.n_ctx = c.n_ctx; at.pages_per_slot = L.pages_per_slot;
       at.nsplit = L.nsplit_op; at.R9 = R9();
       at.op = oproj(b.w_o, b.b_o);
+      // several slots with a small W'_q product: the attention clears the query
+      // rows it read and W'_q is split over k into them (never with the fused
+      // output product, whose column groups all read the same query rows)
+      const bool q_clear = at.op.w == nullptr && split_small(slot0, n, d, d);
+      at.clear_q = q_clear ? 1 : 0;
       // bytes: the fused output product's weights (the cache reads depend on the
       // device-side lengths and are not counted)
       launch("attn_self", at.op.w ? (double)d * d * eb() : 0.0, [&](unsigned long long* sp) {
@@ -549,7 +567,7 @@ struct Runner {
       if (at.op.w == nullptr) resid("gemv_o", slot0, n, Ad16(), b.w_o, b.b_o, d, d);
       const LnNext nx = l + 1 < c.n_layer ? LnNext{L.tb[l + 1].ln1_g, L.tb[l + 1].ln1_b, false}
                                           : LnNext{L.lnf_g, L.lnf_b, true};
-      block_tail(slot0, n, b, l, tap, nx);
+      block_tail(slot0, n, b, l, tap, nx, q_clear);
     }
   }
 

@@ -107,6 +107,10 @@ struct AttnArgs {
   Operand out;        // operand rows of the following product
   int slot0, d, n_head, n_ctx, pages_per_slot, nsplit, R9;
   OprojArgs op;
+  // nonzero: the block clears the query values it read (its head's 64 columns of
+  // the slot's nine rows) once every wave has used them, so that the next product
+  // can add split-K partial sums into those places
+  int clear_q;
   unsigned long long* stamp;  // launch timing slot (profiled calls), or null
 };
 
