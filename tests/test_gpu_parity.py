@@ -233,6 +233,22 @@ def test_large_v3_bf16_lockstep_b1():
     ls.close()
 
 
+def test_large_v3_bf16_lockstep_b1_long_prefix():
+    """One slot with a 430-token prefix: two steps verify positions up to 447, the
+    last of the 448-position context, so every 32-key wave of the fused causal
+    self-attention holds keys and its pages run to the end of the slot's table."""
+    from lockstep import Lockstep
+    cfg = LARGE_V3
+    W = make_weights(cfg)
+    prompt = make_prefix(cfg, 0, 430)
+    ls = Lockstep(cfg, W, [prompt], [448], TOL_BF16)
+    for _ in range(2):
+        ls.step()
+    print(f"large-v3 long prefix: max |dlogit| draft {ls.max_dlogit:.3e} target {ls.max_tlogit:.3e}, "
+          f"near ties {ls.near_ties}")
+    ls.close()
+
+
 # ---------------------------------------------------------------- large batches (sampled slots)
 # At batch >= 2 operands are two bf16 planes (products accurate to fp32
 # rounding), compared with the plain fp32 oracle; the oracle follows a sample of
