@@ -357,7 +357,7 @@ def main():
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build runs the step on one GPU only; --gpus {args.gpus} is not supported "
-              "(sequences shard across GPUs with no communication; see the design notes)", file=sys.stderr)
+              "(sequences are independent, so several GPUs would each run their own share of the slots)", file=sys.stderr)
         sys.exit(2)
 
     if args.pmc_run:

@@ -104,3 +104,15 @@ def test_init_rejects_bad_arguments_before_touching_the_device():
     # calls on a null handle
     assert lib.wf_draft(None, 0, 1, None, None) == -1
     assert lib.wf_release(None) == -1
+
+
+def test_bench_refuses_several_gpus_without_touching_a_device():
+    """bench.py measures one GPU; asking for more exits with status 2 and a message
+    before any device or library is touched (so it also runs here, with no GPU)."""
+    import subprocess
+    import sys
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    r = subprocess.run([sys.executable, os.path.join(root, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, timeout=120)
+    assert r.returncode == 2
+    assert "one GPU only" in r.stderr and r.stdout == ""
