@@ -30,12 +30,17 @@ Because history keys/values of a position never change once written, they
 are cached per drafter block (``HistoryCache``).
 
 Pin status.  The target block is pinned to torch's pre-LN decoder layer and
-the decoding loop to plain greedy decoding.  The drafter is pinned only by
-properties: history at or beyond the anchor is never read, RoPE scores are
-relative, history written round by round equals a teacher-forced pass, and
-its parameter count matches the paper's 60.7M / 47.5M / 52.5M.  Beyond those
-properties the drafter forward is parity unpinned (no values are printed
-for it), and the GPU drafter is compared with this definition directly.
+the decoding loop to plain greedy decoding.  The drafter is pinned by
+properties (history at or beyond the anchor is never read, RoPE scores are
+relative, history written round by round equals a teacher-forced pass, the
+parameter count matches the paper's 60.7M / 47.5M / 52.5M) and by closed
+forms under constructed weights (tests/test_oracle_drafter_pins.py): with
+zero output projections every mask row's logits are LN_df(m) E^T; a zero
+query makes each row the mean of the values of history < t (through the
+block's pre-LN) and of the whole block; a zero cross-attention query gives
+the mean of the drafter's own acoustic values; a constant pre-RoPE key and
+a query rotated by -D omega make mask row j copy the history row at
+position t + j - D.
 """
 import numpy as np
 
