@@ -49,7 +49,10 @@ extern "C" {
 
 /* Device status word bits (wf_status). */
 #define WF_STATUS_NONFINITE_LOGITS 0x1u  /* a verified row's logits had NaN/Inf */
-#define WF_STATUS_POSITION_OVERFLOW 0x2u /* a write at or beyond n_ctx was refused */
+#define WF_STATUS_POSITION_OVERFLOW 0x2u /* a pass or history write at or beyond n_ctx was refused:
+                                            a live, unfinished slot whose cache length reached n_ctx
+                                            (the budget rule of Appendix A.1 never produces one; the
+                                            bit reports a state corrupted from outside) */
 
 #define WF_MAX_TAPS 8
 
@@ -145,10 +148,10 @@ int wf_set_sampling(wf_handle* h, float temperature, uint64_t seed, const uint8_
 
 /*
  * Draft (Section 3.2): run the drafter for slots [slot0, slot0+n) from each
- * slot's anchor, history and acoustic memory.  Before drafting, the history
- * receives the verified rows of the previous round (their target taps are
- * projected and written at their positions).
+ * slot's anchor, history and acoustic memory.  The history already holds
+ * every position before the anchor (prefill and each verify write it).
  * draft: device int32 [n, block_k] (greedy argmax or Gumbel-max samples).
+ * Errors: WF_EINVAL (slot range), WF_ESTATE (a slot not prefilled), WF_EHIP.
  */
 int wf_draft(wf_handle* h, int slot0, int n, int32_t* draft, void* stream);
 
@@ -158,7 +161,10 @@ int wf_draft(wf_handle* h, int slot0, int n, int32_t* draft, void* stream);
  * k = min(block_k, k_max, max_new - emitted - 1, n_ctx - L - 1), then greedy
  * longest-prefix acceptance (or the rejection rule), then the state update
  * (L += 1 + a, anchor = last emitted token, emitted += a + 1, done on EOS,
- * budget or context end).  Finished slots are left unchanged and report
+ * budget or context end), then the drafter history of the verified rows
+ * (Appendix A.2: the target taps of rows L..L+k projected and written at their
+ * positions; rows at or beyond the new length are never read and are
+ * overwritten later).  Finished slots are left unchanged and report
  * n_out = 0.  k_max in [0, block_k]; k_max = 0 is plain decoding.
  * draft: device int32 [n, block_k]. out: device int32 [n, block_k + 1];
  * n_out, n_acc, done: device int32 [n] (any may be NULL).
@@ -170,6 +176,8 @@ int wf_verify_accept(wf_handle* h, int slot0, int n, const int32_t* draft, int k
  * One full step: wf_draft followed by wf_verify_accept.  If draft_override
  * (device int32 [n, block_k]) is not NULL the drafter still runs but its
  * proposals are replaced by draft_override (planted drafts for benchmarks).
+ * With k_max = 0 no proposal is verified and the drafter does not run (plain
+ * decoding: one target pass per token).
  * use_graph != 0 captures the step into a HIP graph on first use (per
  * argument tuple) and replays it afterwards.
  */

@@ -223,6 +223,10 @@ __global__ void __launch_bounds__(256) k_verify_begin(BeginArgs a) {
   const int L = st[ST_L], left = st[ST_MAX_NEW] - st[ST_EMITTED], anchor = st[ST_ANCHOR];
   const bool go = st[ST_LIVE] && !st[ST_DONE] && left > 0 && L < a.n_ctx;
   const int nv = go ? min(min(a.block_k, a.k_max), min(left - 1, a.n_ctx - L - 1)) + 1 : 0;
+  // the acceptance marks a slot finished once its cache reaches n_ctx, so a live,
+  // unfinished slot at or beyond it has an inconsistent state: its pass is refused
+  if (threadIdx.x == 0 && a.status && st[ST_LIVE] && !st[ST_DONE] && left > 0 && L >= a.n_ctx)
+    atomicOr(a.status, WF_STATUS_POSITION_OVERFLOW);
   if (threadIdx.x < kRows) {
     const int i = threadIdx.x;
     int t = (i == 0 || i >= nv) ? anchor : a.draft[(size_t)blockIdx.x * a.block_k + i - 1];
@@ -240,8 +244,8 @@ __global__ void __launch_bounds__(256) k_verify_begin(BeginArgs a) {
   fill_rows<S>(a, slot, toks, poss, false);
 }
 
-// Draft block X_t = [Emb(y_t), m, ..., m] (Eq. 2).  The drafter history is up to
-// date at this point, so its pending-row count is cleared here.
+// Draft block X_t = [Emb(y_t), m, ..., m] (Eq. 2).  The drafter history already
+// holds every verified position (it is written at the end of each verify).
 template <typename S>
 __global__ void __launch_bounds__(256) k_draft_begin(BeginArgs a) {
   __shared__ int toks[kRows];
@@ -249,7 +253,6 @@ __global__ void __launch_bounds__(256) k_draft_begin(BeginArgs a) {
   int* st = a.state + slot * kStateInts;
   if (threadIdx.x < kRows) toks[threadIdx.x] = min(max(st[ST_ANCHOR], 0), a.n_vocab - 1);
   __syncthreads();
-  if (threadIdx.x == 0) st[ST_HN] = 0;
   fill_rows<S>(a, slot, toks, nullptr, true);
 }
 
@@ -319,7 +322,11 @@ __global__ void __launch_bounds__(256) k_hist_write(HistArgs a) {
   const int slot = a.slot0 + blockIdx.y, r = blockIdx.x;
   const int* st = a.state + slot * kStateInts;
   const int hn = st[ST_HN], pos = st[ST_HPOS] + r;
-  if (r >= hn || pos >= a.n_ctx) return;
+  if (r >= hn) return;
+  if (pos >= a.n_ctx) {  // never reached by a consistent state (the budget keeps passes below n_ctx)
+    if (threadIdx.x == 0 && a.status) atomicOr(a.status, WF_STATUS_POSITION_OVERFLOW);
+    return;
+  }
   const float* kr = a.kv + (size_t)(slot * kRows + r) * 2 * a.d;
   const float* vr = kr + a.d;
   S* Kh = reinterpret_cast<S*>(a.kcache);
@@ -360,6 +367,7 @@ __global__ void k_accept_greedy(AcceptArgs a) {
     if (a.n_acc) a.n_acc[s] = 0;
     if (a.done) a.done[s] = live ? 1 : 0;
     if (live) st[ST_DONE] = 1;
+    st[ST_HN] = 0;
     return;
   }
   const int k = nv - 1;
@@ -532,6 +540,7 @@ __global__ void k_sample_final(SampleArgs a) {
     if (a.n_acc) a.n_acc[s] = 0;
     if (a.done) a.done[s] = st[ST_LIVE] ? 1 : 0;
     if (st[ST_LIVE]) st[ST_DONE] = 1;
+    st[ST_HN] = 0;
     return;
   }
   const int mode = o[0], acc = o[2];

@@ -615,6 +615,7 @@ struct Runner {
       HistArgs ha{};
       ha.kv = kvh; ha.kcache = hkv(dl, 0); ha.vcache = hkv(dl, 1); ha.state = I32(L.state); ha.rope = F32(L.rope);
       ha.slot0 = slot0; ha.d = d; ha.n_head = c.n_head; ha.n_ctx = c.n_ctx;
+      ha.status = h->at<unsigned>(L.status);
       launch("hist_write", 0, [&](unsigned long long*) { Ops<S>::hist_write(ha, n, st); });
     }
   }
@@ -657,6 +658,7 @@ struct Runner {
     ba.h = F32(L.h); ba.slot0 = slot0; ba.d = c.d_model; ba.n_vocab = c.n_vocab; ba.n_ctx = c.n_ctx;
     ba.block_k = c.block_k; ba.k_max = k_max;
     ba.page_table = I32(L.page_table); ba.pages_per_slot = L.pages_per_slot;
+    ba.status = h->at<unsigned>(L.status);
     launch("begin", 0, [&](unsigned long long*) { Ops<S>::verify_begin(ba, n, st); });
     target_forward(slot0, n);
     head(slot0, n, F32(L.h), L.lnf_g, L.lnf_b, h->debug || sampling() ? F32(L.logits) : nullptr, nullptr, nullptr, 0,
@@ -670,18 +672,20 @@ struct Runner {
       sa.slot0 = slot0; sa.n = n; sa.block_k = c.block_k; sa.eos = c.eos_id; sa.n_ctx = c.n_ctx; sa.V = c.n_vocab;
       sa.inv_t = h->inv_t; sa.seed = h->seed;
       launch("accept", 0, [&](unsigned long long*) { accept_sample(sa, st); });
+      history_apply(slot0, n);
       return;
     }
     AcceptArgs aa{};
     aa.state = I32(L.state); aa.tok = I32(L.tok); aa.g = I32(L.g); aa.out = out; aa.n_out = n_out; aa.n_acc = n_acc;
     aa.done = done; aa.slot0 = slot0; aa.n = n; aa.block_k = c.block_k; aa.eos = c.eos_id; aa.n_ctx = c.n_ctx;
     launch("accept", 0, [&](unsigned long long*) { accept_greedy(aa, st); });
+    history_apply(slot0, n);
   }
 
-  void draft(int slot0, int n, int* dst) {
-    history_apply(slot0, n);  // the drafter's set-up then clears the pending rows
-    drafter_forward(slot0, n, dst);
-  }
+  // The history already holds every verified position: each verify writes the
+  // drafter history of its rows after the acceptance (Appendix A.2), so any
+  // sequence of verify and draft calls sees a complete history.
+  void draft(int slot0, int n, int* dst) { drafter_forward(slot0, n, dst); }
 
   void encode(int slot0, int n, const void* mem) {
     const size_t per = (size_t)c.n_frames * c.d_model;
@@ -1006,7 +1010,9 @@ static int step_enqueue(Handle* h, int slot0, int n, int k_max, const int32_t* o
   return dispatch(h, st, [&](auto* tag) {
     using S = std::remove_pointer_t<decltype(tag)>;
     Runner<S> R(h, st);
-    R.draft(slot0, n, nullptr);
+    // k_max = 0 verifies the anchor alone (plain decoding): no proposal is used,
+    // so the drafter does not run
+    if (k_max > 0) R.draft(slot0, n, nullptr);
     const int* d = ovr ? ovr : h->at<int>(h->lay.draft) + (size_t)slot0 * h->cfg.block_k;
     R.verify(slot0, n, d, k_max, out, n_out, n_acc, done);
   });

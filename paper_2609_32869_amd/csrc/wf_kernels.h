@@ -201,6 +201,7 @@ struct BeginArgs {
   const int* page_table;  // [slot][pages_per_slot] (target passes: sets ST_PG0 / ST_PG1)
   int pages_per_slot;
   int slot0, d, n_vocab, n_ctx, block_k, k_max, chunk, pmax;
+  unsigned* status;  // sticky device status word (verify: position overflow), or null
 };
 
 struct HistArgs {
@@ -210,6 +211,7 @@ struct HistArgs {
   const int* state;
   const float* rope;
   int slot0, d, n_head, n_ctx;
+  unsigned* status;  // sticky device status word (position overflow), or null
 };
 
 struct AcceptArgs {

@@ -121,5 +121,77 @@ class Lockstep:
         self.steps += 1
         return out, n_out, n_acc, done
 
+    def verify_only(self, k_max=0, override=None):
+        """One wf_verify_accept with no draft call before it (the oracle likewise):
+        the drafter history must still receive the verified rows."""
+        cfg, tol, n = self.cfg, self.tol, self.n
+        eng = self.eng
+        eng.set_debug(True)
+        used = np.zeros((n, cfg.block_k), np.int32) if override is None else np.asarray(override, np.int32).copy()
+        out, n_out, n_acc, done = eng.verify_accept(0, torch.from_numpy(used).cuda(), k_max)
+        torch.cuda.synchronize()
+        out, n_out, n_acc, done = (t.cpu().numpy() for t in (out, n_out, n_acc, done))
+        tlog = eng.target_logits()[:n].cpu().numpy()
+        for i, s in enumerate(self.sess):
+            if not self.live[i] or s.done:
+                continue
+            rec = s.verify_accept(used[i], k_max)
+            k = rec["k"]
+            d = float(np.abs(s.last_logits - tlog[i, :k + 1]).max())
+            self.max_tlogit = max(self.max_tlogit, d)
+            assert d <= tol, f"slot {i}: target logits differ by {d}"
+            if list(out[i, :n_out[i]]) != rec["tokens"]:
+                m = margin(s.last_logits[0])
+                assert m <= tol, f"slot {i}: tokens {list(out[i, :n_out[i]])} vs {rec['tokens']} (margin {m})"
+                self.near_ties.append((i, f"verify {self.steps}", m))
+                self.live[i] = False
+        self.steps += 1
+
+    def graph_step(self, override, outs, ovr_dev, k_max=8):
+        """One graph-replayed wf_step (the path the benchmark times) with planted
+        drafts; the drafter runs inside the step and its logits are compared too."""
+        cfg, tol, n = self.cfg, self.tol, self.n
+        eng = self.eng
+        ovr_dev.copy_(torch.from_numpy(np.asarray(override, np.int32)))
+        eng.step(0, n, k_max, draft_override=ovr_dev, outs=outs, use_graph=True)
+        torch.cuda.synchronize()
+        out, n_out, n_acc, done = (t.cpu().numpy() for t in outs)
+        dg = eng.last_draft()[:n].cpu().numpy()
+        dlog = eng.draft_logits()[:n, 1:].cpu().numpy()
+        tlog = eng.target_logits()[:n].cpu().numpy()
+        for i, s in enumerate(self.sess):
+            if not self.live[i]:
+                continue
+            if s.done:
+                assert n_out[i] == 0 and done[i] == 1
+                continue
+            ol = s.draft_logits()
+            dd = float(np.abs(ol - dlog[i]).max())
+            self.max_dlogit = max(self.max_dlogit, dd)
+            assert dd <= tol, f"slot {i}: draft logits differ by {dd}"
+            for j in range(cfg.block_k):
+                oj = int(np.argmax(ol[j]))
+                if oj != dg[i, j]:
+                    m = margin(ol[j])
+                    assert m <= tol, f"slot {i}: draft token {j}: {dg[i, j]} vs {oj} (margin {m})"
+            rec = s.verify_accept(override[i], k_max)
+            k = rec["k"]
+            d = float(np.abs(s.last_logits - tlog[i, :k + 1]).max())
+            self.max_tlogit = max(self.max_tlogit, d)
+            assert d <= tol, f"slot {i}: target logits differ by {d}"
+            gpu_tokens = list(out[i, :n_out[i]])
+            if gpu_tokens != rec["tokens"] or n_acc[i] != rec["a"]:
+                rows = [r for r in range(k + 1) if int(np.argmax(s.last_logits[r])) != int(np.argmax(tlog[i, r]))]
+                assert rows, f"slot {i}: tokens differ without an argmax difference"
+                m = margin(s.last_logits[rows[0]])
+                assert m <= tol, f"slot {i}: tokens {gpu_tokens} vs {rec['tokens']} (margin {m})"
+                self.near_ties.append((i, f"step {self.steps} row {rows[0]}", m))
+                self.live[i] = False
+                continue
+            assert bool(done[i]) == s.done
+            self.accepted.append(int(n_acc[i]))
+        self.steps += 1
+        return out, n_out, n_acc, done
+
     def close(self):
         self.eng.close()

@@ -234,9 +234,11 @@ def test_large_v3_bf16_lockstep_b1():
 
 
 def test_large_v3_bf16_lockstep_b1_long_prefix():
-    """One slot with a 430-token prefix: two steps verify positions up to 447, the
-    last of the 448-position context, so every 32-key wave of the fused causal
-    self-attention holds keys and its pages run to the end of the slot's table."""
+    """One slot with a 430-token prefix and the random drafter's own proposals: two
+    steps verify nine rows each from positions 430 and 431 (rows up to 439 carry
+    keys of 14 32-key waves of the fused causal self-attention, and pages to the
+    slot's 28th); the last context position is reached by
+    test_large_v3_b1_verify_reaches_last_context_position."""
     from lockstep import Lockstep
     cfg = LARGE_V3
     W = make_weights(cfg)
