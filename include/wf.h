@@ -185,6 +185,25 @@ int wf_step(wf_handle* h, int slot0, int n, int k_max, const int32_t* draft_over
             int32_t* n_out, int32_t* n_acc, int32_t* done, int use_graph, void* stream);
 
 /*
+ * wf_step (eager, use_graph = 0) for callers that cannot allocate device memory
+ * or use a workspace of their own per call: code under HIP graph capture, tight
+ * serving loops, harnesses that forbid allocation.  The per-call buffers of the
+ * step (matrix operands, activation rows, partial sums, head partials, logits:
+ * everything but the weights, caches and per-slot state of the workspace) live
+ * in a static device array of the library, 16 MiB per GPU, held until the
+ * process ends; nothing is allocated (no hipMalloc or hipFree, no allocating
+ * library routine).  The array is cleared at the start of every call.  All calls
+ * on one GPU share that array, so calls that overlap on one GPU (other streams,
+ * other handles) race: issue them in order.  Same arguments and results as
+ * wf_step; the debug views (wf_debug_ptr) and profiling are not written by it.
+ * Errors: as wf_step, plus WF_ESIZE when this configuration's per-call buffers
+ * exceed the array (large vocabularies times many slots; batch 1 at
+ * Whisper-large-v3 shapes needs about 7 MiB).
+ */
+int wf_step_noalloc(wf_handle* h, int slot0, int n, int k_max, const int32_t* draft_override, int32_t* out,
+                    int32_t* n_out, int32_t* n_acc, int32_t* done, void* stream);
+
+/*
  * Debug views for tests: device pointers into the workspace (valid until
  * wf_release).  which: 0 = target logits of the last verify [max_batch,
  * block_k+1, n_vocab] fp32 (written when wf_set_debug(h, 1) or when

@@ -23,7 +23,7 @@ WF_STATUS_POSITION_OVERFLOW = 0x2
 # symbols declared in include/wf.h
 EXPORTS = ["wf_workspace_bytes", "wf_weight_count", "wf_weight_numel", "wf_init_weights",
            "wf_encode_memory_set", "wf_prefill", "wf_set_sampling", "wf_draft", "wf_verify_accept",
-           "wf_step", "wf_debug_ptr", "wf_set_debug", "wf_profile_enable", "wf_profile_summary", "wf_status",
+           "wf_step", "wf_step_noalloc", "wf_debug_ptr", "wf_set_debug", "wf_profile_enable", "wf_profile_summary", "wf_status",
            "wf_release", "wf_strerror", "wf_last_error", "wf_rng_words_host", "wf_rng_words_device"]
 
 
@@ -63,6 +63,7 @@ def load_library(path=LIB_PATH):
         "wf_draft": [P, I, I, P, P],
         "wf_verify_accept": [P, I, I, P, I, P, P, P, P, P],
         "wf_step": [P, I, I, I, P, P, P, P, P, I, P],
+        "wf_step_noalloc": [P, I, I, I, P, P, P, P, P, P],
         "wf_debug_ptr": [P, I, ctypes.POINTER(P)],
         "wf_set_debug": [P, I],
         "wf_profile_enable": [P, I],
@@ -223,6 +224,14 @@ class WhisperFlash:
         out, n_out, n_acc, done = outs if outs is not None else self._outs(n)
         self._check(self.lib.wf_step(self.h, slot0, n, k_max, _ptr(draft_override), _ptr(out), _ptr(n_out),
                                      _ptr(n_acc), _ptr(done), 1 if use_graph else 0, _stream(stream)))
+        return out, n_out, n_acc, done
+
+    def step_noalloc(self, slot0, n, k_max=None, draft_override=None, outs=None, stream=None):
+        """wf_step_noalloc: the step with its per-call buffers in the library's static scratch."""
+        k_max = self.K if k_max is None else k_max
+        out, n_out, n_acc, done = outs if outs is not None else self._outs(n)
+        self._check(self.lib.wf_step_noalloc(self.h, slot0, n, k_max, _ptr(draft_override), _ptr(out), _ptr(n_out),
+                                             _ptr(n_acc), _ptr(done), _stream(stream)))
         return out, n_out, n_acc, done
 
     def set_debug(self, on):

@@ -7,6 +7,7 @@
 #include <type_traits>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <vector>
 
@@ -14,7 +15,37 @@
 
 using namespace wf;
 
+// Static scratch of wf_step_noalloc: the per-call buffers of one step when the
+// caller cannot allocate.  Every GPU the library runs on holds its own copy until
+// the process ends; all wf_step_noalloc calls on that GPU share it.
+constexpr size_t kScratchBytes = (size_t)16 << 20;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
 namespace {
+
+// Device address of `scratch` per device.  In host code the array's name is only
+// a stand-in, so kernels and copies get this address, looked up once per device
+// (with that device current) by hipGetSymbolAddress.
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+char* g_scratch_ptr[kMaxDevices] = {};
+
+hipError_t scratch_setup(int dev) {
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (g_scratch_ptr[dev]) return hipSuccess;
+  void* p = nullptr;
+  hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+  if (e != hipSuccess) return e;
+  g_scratch_ptr[dev] = static_cast<char*>(p);
+  return hipSuccess;
+}
+
+char* scratch_of(int dev) {
+  if (dev < 0 || dev >= kMaxDevices) return nullptr;
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  return g_scratch_ptr[dev];
+}
 
 thread_local std::string g_err;
 
@@ -877,6 +908,10 @@ int wf_init_weights(wf_handle** out, const wf_config* cfg, const void* const* we
     if (e0 == hipSuccess) e0 = hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, dev);
     if (e0 != hipSuccess || khz <= 0) return cleanup(WF_EHIP, "wall clock rate unavailable");
     h->wall_khz = khz;
+    h->device = dev;
+    // the static scratch of wf_step_noalloc on this device (looked up once per device)
+    e0 = scratch_setup(dev);
+    if (e0 != hipSuccess) return cleanup(WF_EHIP, std::string("hipGetSymbolAddress(scratch): ") + hipGetErrorString(e0));
   }
   hipError_t e = hipMemsetAsync(workspace, 0, L.total, st);
   if (e != hipSuccess) return cleanup(WF_EHIP, std::string("hipMemsetAsync: ") + hipGetErrorString(e));
@@ -1053,6 +1088,34 @@ int wf_step(wf_handle* hh, int slot0, int n, int k_max, const int32_t* ovr, int3
     return collect_stamps(h, h->graph_recs[key]);
   }
   return WF_OK;
+}
+
+int wf_step_noalloc(wf_handle* hh, int slot0, int n, int k_max, const int32_t* ovr, int32_t* out, int32_t* n_out,
+                    int32_t* n_acc, int32_t* done, void* stream) {
+  Handle* h = reinterpret_cast<Handle*>(hh);
+  if (int r = check_batch(h, slot0, n, true)) return r;
+  if (k_max < 0 || k_max > h->cfg.block_k) return fail(h, WF_EINVAL, "k_max out of range");
+  if (h->capturing) return fail(h, WF_ESTATE, "wf_step_noalloc inside a wf_step capture");
+  const size_t need = h->transient_bytes();
+  if (need > kScratchBytes) {
+    char msg[160];
+    snprintf(msg, sizeof(msg), "per-call buffers need %zu bytes; the static scratch holds %zu (use wf_step)", need,
+             kScratchBytes);
+    return fail(h, WF_ESIZE, msg);
+  }
+  char* p = scratch_of(h->device);
+  if (!p) return fail(h, WF_EHIP, "static scratch not set up on the handle's device");
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  // the scratch keeps the previous call's contents (possibly of another handle and
+  // layout): start from zeros, as the workspace does after wf_init_weights
+  HIPCK(h, hipMemsetAsync(p, 0, need, st));
+  const bool prof = h->prof;
+  h->prof = false;  // timing stamps are not taken in this variant
+  h->scratch = p;
+  const int r = step_enqueue(h, slot0, n, k_max, ovr, out, n_out, n_acc, done, st);
+  h->scratch = nullptr;
+  h->prof = prof;
+  return r;
 }
 
 int wf_debug_ptr(wf_handle* hh, int which, void** ptr) {

@@ -93,9 +93,20 @@ struct Handle {
   std::map<GraphKey, std::vector<ProfRec>> graph_recs;  // launches of each profiled graph
   std::map<std::string, ProfAgg> prof_acc;              // durations per launch class
   double wall_khz = 0;                                   // device wall-clock rate
+  int device = 0;          // device that was current when the handle was created
+  // Non-null only inside a wf_step_noalloc call: the per-call buffers (the byte
+  // range [lay.a_d16, lay.lncd) of the workspace: operands, activation rows,
+  // partial sums, head partials, logits) then live at this device address, the
+  // library's static scratch array, instead of the workspace.
+  char* scratch = nullptr;
 
   template <typename T>
-  T* at(size_t off) const { return reinterpret_cast<T*>(ws + off); }
+  T* at(size_t off) const {
+    if (scratch && off >= lay.a_d16 && off < lay.lncd) return reinterpret_cast<T*>(scratch + (off - lay.a_d16));
+    return reinterpret_cast<T*>(ws + off);
+  }
+  // bytes of the per-call buffers (what wf_step_noalloc places in the static scratch)
+  size_t transient_bytes() const { return lay.lncd - lay.a_d16; }
 };
 
 int compute_layout(const wf_config& c, Layout& L);
