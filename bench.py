@@ -430,15 +430,13 @@ def run_kmax_sweep(args):
                                  "prefix_len": L0}, "rows": rows}), flush=True)
 
 
-def run_request(args):
-    """Request set-up around the step loop: the acoustic K/V projection of every
-    target and drafter block for one 30 s memory, and the prompt prefill."""
+def request_times(cfg, eng, mem, reps=5):
+    """Request set-up around the step loop (batch 1): the acoustic K/V of every target
+    and drafter block for one 1500-frame memory (Appendix A.5) and the prefill of
+    prompts of 32 / 128 / 400 tokens (Appendix A.1)."""
     import torch
     from wf_fixtures import make_prefix
-    log = lambda *a: print(*a, file=sys.stderr, flush=True)
-    cfg, eng, mem, L0, toks = _b1_engine(log)
     ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
-    reps = 5
 
     def timed(fn):
         fn()
@@ -453,11 +451,20 @@ def run_request(args):
     enc_ms = timed(lambda: eng.encode_memory_set(0, mem))
     nblk = cfg.n_layer + cfg.n_draft_layer
     enc_flops = nblk * 2.0 * cfg.n_frames * cfg.d_model * 2 * cfg.d_model
-    out = {"measure": "request set-up", "encode_memory_set_ms": round(enc_ms, 3),
-           "encode_tflops": round(enc_flops / (enc_ms / 1e3) / 1e12, 1), "prefill_ms": {}}
+    out = {"encode_memory_set_ms": round(enc_ms, 3), "encode_tflops": round(enc_flops / (enc_ms / 1e3) / 1e12, 1),
+           "encode_frac_of_bf16_peak": round(enc_flops / (enc_ms / 1e3) / 1e12 / MFMA_PEAK_TFLOPS, 4),
+           "prefill_ms": {}}
     for P in (32, 128, 400):
         t = torch.from_numpy(make_prefix(cfg, 0, P)[None].copy()).cuda()
         out["prefill_ms"][str(P)] = round(timed(lambda: eng.prefill(0, t, [P], [cfg.n_ctx])), 3)
+    return out
+
+
+def run_request(args):
+    """--request: request set-up timing alone, as one JSON line."""
+    log = lambda *a: print(*a, file=sys.stderr, flush=True)
+    cfg, eng, mem, L0, toks = _b1_engine(log)
+    out = {"measure": "request set-up", **request_times(cfg, eng, mem)}
     out["config"] = {"workload": "whisper-large-v3-shaped encode of one 1500-frame memory (32 target + 2 drafter "
                                  "blocks) and prefill of one prompt", "storage": "bf16"}
     log(f"[bench] {out}")
@@ -546,10 +553,11 @@ def b1_workload(args, W, log):
             eng.profile(False)
             first_draw = (mem, prompt, plans[:args.warmup + seg[0]])
         log(f"[bench] b1 draw {i}: prefix {lens[i]}, {seg[i]} timed steps")
+    request = request_times(cfg, eng, to_device_storage(make_memory(cfg, 0), cfg.dtype)[None])
     del eng
     torch.cuda.empty_cache()
     return dict(lens=lens, seg=seg, step_ms=np.array(step_ms), tokens=tokens, planted_ok=planted_ok,
-                Lmid=Lmid, nat=nat, prof=prof, first_draw=first_draw)
+                Lmid=Lmid, nat=nat, prof=prof, first_draw=first_draw, request=request)
 
 
 def main():
@@ -665,6 +673,7 @@ def main():
                               "bytes_per_launch": round(v["bytes"] / v["launches"], 1) if v["launches"] else 0,
                               "GBs": round(v["bytes"] / (v["ms"] / 1e3) / 1e9, 1) if v["bytes"] else None}
                           for k, v in prof.items()},
+        "request": b1["request"],
         "paper_context": PAPER_CONTEXT,
     }
     if not args.no_cpu_baseline:

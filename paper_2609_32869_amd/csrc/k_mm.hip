@@ -1,0 +1,245 @@
+// Matrix-core GEMM for the request-time products (bf16 operands, fp32
+// accumulation): C[m, n] = sum_k A[m, k] B[n, k] (+ bias[n]), A [M, K] and
+// B [N, K] row-major bf16 (a weight matrix [out, in] is B as stored), with one
+// of several epilogues.  It computes the acoustic keys and values of every
+// decoder block for a new request (Appendix A.5) and the products of the
+// audio encoder.
+//
+// Tiling: 128 x 128 output tiles, k in steps of 64, 256 threads = 4 waves of
+// 64 x 64 (2 x 2 tiles of v_mfma_f32_32x32x16_bf16).  A and B tiles are staged
+// through LDS in two buffers (16-byte chunks, chunk q of row r stored at q ^ (r & 7)
+// so that the eight rows a wave's lane group reads fall in different banks); the
+// next k-step's global loads are in flight while the current one is multiplied.
+// The finished tile goes through LDS again so that every epilogue writes 16-byte
+// runs of consecutive elements.
+#include <algorithm>
+
+#include "wf_common.h"
+#include "wf_kernels.h"
+#include "wf_operand.h"
+
+namespace wf {
+
+namespace {
+
+constexpr int BM = kMmTile, BN = kMmTile, BK = kMmK, NT = 256;
+constexpr int kChunks = BM * BK / 8;  // 16-byte chunks of one operand tile (1024)
+constexpr int kCt = BN + 1;           // row stride of the staged output tile (floats)
+
+
+__device__ __forceinline__ uint4 pack8(const float* v) {
+  uint4 r;
+  r.x = bf16_bits_rne(v[0]) | (bf16_bits_rne(v[1]) << 16);
+  r.y = bf16_bits_rne(v[2]) | (bf16_bits_rne(v[3]) << 16);
+  r.z = bf16_bits_rne(v[4]) | (bf16_bits_rne(v[5]) << 16);
+  r.w = bf16_bits_rne(v[6]) | (bf16_bits_rne(v[7]) << 16);
+  return r;
+}
+
+}  // namespace
+
+template <int EP>
+__global__ void __launch_bounds__(NT) k_mm(MmArgs a) {
+  // pipeline: [buffer][A | B][chunk]; afterwards the output tile [BM][kCt] fp32
+  __shared__ __align__(16) unsigned char smem[(2 * 2 * kChunks * 16 > BM * kCt * 4) ? 2 * 2 * kChunks * 16 : BM * kCt * 4];
+  uint4* lds = reinterpret_cast<uint4*>(smem);
+  const int z = blockIdx.z;
+  const bf16* A = a.A + (size_t)z * a.sA;
+  const bf16* B = a.B + (size_t)z * a.sB;
+  const int m0 = blockIdx.x * BM, n0 = blockIdx.y * BN;
+  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+  const int wm = w >> 1, wn = w & 1;
+
+  // global chunk c = t + 256 j of a tile: row c / 8 = t / 8 + 32 j, 16-byte chunk
+  // q = t % 8 along k; rows past the matrix re-read its last row (their results
+  // are not written).  Offsets in 16-byte units from the thread's chunk column.
+  const int q = t & 7, r0 = t >> 3;
+  const uint4* pa = reinterpret_cast<const uint4*>(A) + q;
+  const uint4* pb = reinterpret_cast<const uint4*>(B) + q;
+  int oa[4], ob[4], so[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int row = r0 + 32 * j;
+    oa[j] = min(m0 + row, a.M - 1) * (int)(a.lda >> 3);
+    ob[j] = min(n0 + row, a.N - 1) * (int)(a.ldb >> 3);
+    so[j] = row * 8 + (q ^ (row & 7));
+  }
+  const int nk = a.K / BK;
+  uint4 ra[4], rb[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    ra[j] = pa[oa[j]];
+    rb[j] = pb[ob[j]];
+  }
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    lds[so[j]] = ra[j];
+    lds[kChunks + so[j]] = rb[j];
+  }
+  __syncthreads();
+
+  floatx16 acc[2][2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int jj = 0; jj < 2; ++jj)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[i][jj][v] = 0.f;
+
+  // fragment rows of this lane: row (lane % 32) of each 32-row tile, k chunk
+  // 2 s + lane / 32 of k-substep s
+  const int lr = lane & 31, lk = lane >> 5;
+  for (int kt = 0; kt < nk; ++kt) {
+    const int cur = kt & 1;
+    // the next k-step's chunks (the last step re-reads itself: loads and LDS stores
+    // stay unconditional, so no branch makes the compiler wait for them early)
+    {
+      const int off = min(kt + 1, nk - 1) * (BK / 8);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        ra[j] = pa[oa[j] + off];
+        rb[j] = pb[ob[j] + off];
+      }
+    }
+    const uint4* la = lds + cur * 2 * kChunks;
+    const uint4* lb = la + kChunks;
+#pragma unroll
+    for (int s = 0; s < BK / 16; ++s) {
+      const int q = 2 * s + lk;
+      bf16x8 af[2], bf[2];
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        const int row = wm * 64 + i * 32 + lr;
+        af[i] = __builtin_bit_cast(bf16x8, la[row * 8 + (q ^ (row & 7))]);
+      }
+#pragma unroll
+      for (int jj = 0; jj < 2; ++jj) {
+        const int row = wn * 64 + jj * 32 + lr;
+        bf[jj] = __builtin_bit_cast(bf16x8, lb[row * 8 + (q ^ (row & 7))]);
+      }
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int jj = 0; jj < 2; ++jj)
+          acc[i][jj] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bf[jj], acc[i][jj], 0, 0, 0);
+    }
+    {
+      // the other buffer was last read in step kt - 1, before the barrier that ended it
+      uint4* na = lds + (cur ^ 1) * 2 * kChunks;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        na[so[j]] = ra[j];
+        na[kChunks + so[j]] = rb[j];
+      }
+    }
+    __syncthreads();
+  }
+
+  // stage the tile (+ bias, activation) in LDS: acc element v of a 32 x 32 tile is
+  // row 8 (v / 4) + 4 (lane / 32) + v % 4, column lane % 32
+  float* ct = reinterpret_cast<float*>(smem);
+  const bf16* bias = a.bias ? a.bias + (size_t)z * a.sBias : nullptr;
+#pragma unroll
+  for (int jj = 0; jj < 2; ++jj) {
+    const int cl = wn * 64 + jj * 32 + lr;
+    const float bv = bias ? to_f(bias[min(n0 + cl, a.N - 1)]) : 0.f;
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int rl = wm * 64 + i * 32 + 8 * (v >> 2) + 4 * lk + (v & 3);
+        float x = acc[i][jj][v] * a.scale + bv;
+        if (EP == MM_BF16_GELU) x = gelu_erf(x);
+        ct[rl * kCt + cl] = x;
+      }
+  }
+  __syncthreads();
+
+  if (EP == MM_XKV || EP == MM_QKV_ENC) {
+    // columns [0, nrow) row-major bf16 (keys, or queries | keys), columns
+    // [nrow, N) values transposed per head: MM_XKV in 256-frame pieces
+    // [head][frame / 256][dim][256] after the keys [head][frame][64]; MM_QKV_ENC as
+    // [head][dim][ldv] in out2.  Frames from M to the padded count are zeros.
+    const int nrow = EP == MM_XKV ? a.d : 2 * a.d;
+    bf16* out = reinterpret_cast<bf16*>(a.out) + (size_t)z * a.sO;
+    // row-major part: items (row, 8 columns)
+    for (int it = t; it < BM * (BN / 8); it += NT) {
+      const int rl = it / (BN / 8), c8 = (it % (BN / 8)) * 8, f = m0 + rl, n = n0 + c8;
+      if (f >= a.M || n >= nrow) continue;
+      const uint4 pk = pack8(ct + rl * kCt + c8);
+      if (EP == MM_XKV) {
+        const int head = n >> 6, dim = n & 63;
+        *reinterpret_cast<uint4*>(out + ((size_t)head * a.M + f) * kHeadDim + dim) = pk;
+      } else {
+        *reinterpret_cast<uint4*>(out + (size_t)f * a.ldo + n) = pk;
+      }
+    }
+    // transposed part: items (column, 8 frames)
+    for (int it = t; it < BN * (BM / 8); it += NT) {
+      const int cl = it / (BM / 8), r8 = (it % (BM / 8)) * 8, n = n0 + cl, f = m0 + r8;
+      if (n < nrow || n >= a.N || f >= a.vt_frames) continue;
+      const int col = n - nrow, head = col >> 6, dim = col & 63;
+      float v[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[e] = f + e < a.M ? ct[(r8 + e) * kCt + cl] : 0.f;
+      const uint4 pk = pack8(v);
+      if (EP == MM_XKV) {
+        bf16* vt = out + (size_t)a.n_head * a.M * kHeadDim + (size_t)head * kHeadDim * a.vt_frames;
+        *reinterpret_cast<uint4*>(vt + vt_index(dim, f)) = pk;
+      } else {
+        bf16* vt = reinterpret_cast<bf16*>(a.out2) + (size_t)z * a.sO2;
+        *reinterpret_cast<uint4*>(vt + ((size_t)head * kHeadDim + dim) * a.vt_frames + f) = pk;
+      }
+    }
+    return;
+  }
+  // row-major outputs: items (row, 8 columns)
+  for (int it = t; it < BM * (BN / 8); it += NT) {
+    const int rl = it / (BN / 8), c8 = (it % (BN / 8)) * 8, f = m0 + rl, n = n0 + c8;
+    if (f >= a.M || n >= a.N) continue;
+    const float* src = ct + rl * kCt + c8;
+    if (EP == MM_BF16 || EP == MM_BF16_GELU) {
+      bf16* out = reinterpret_cast<bf16*>(a.out) + (size_t)z * a.sO;
+      *reinterpret_cast<uint4*>(out + (size_t)f * a.ldo + n) = pack8(src);
+    } else {
+      float* out = reinterpret_cast<float*>(a.out) + (size_t)z * a.sO + (size_t)f * a.ldo + n;
+      float4 lo = make_float4(src[0], src[1], src[2], src[3]), hi = make_float4(src[4], src[5], src[6], src[7]);
+      if (EP == MM_RESID) {  // residual rows: each element has exactly one writer
+        const float4 o0 = *reinterpret_cast<const float4*>(out), o1 = *reinterpret_cast<const float4*>(out + 4);
+        lo.x += o0.x; lo.y += o0.y; lo.z += o0.z; lo.w += o0.w;
+        hi.x += o1.x; hi.y += o1.y; hi.z += o1.z; hi.w += o1.w;
+      }
+      *reinterpret_cast<float4*>(out) = lo;
+      *reinterpret_cast<float4*>(out + 4) = hi;
+    }
+  }
+}
+
+// Shapes the kernel assumes: K a multiple of 64, N a multiple of 8, 16-byte
+// aligned rows (lda, ldb, ldo multiples of 8), and for the transposed epilogues
+// head width 64 with the value columns after the row-major ones.
+int mm_check(const MmArgs& a, int ep) {
+  if (a.M < 1 || a.N < 1 || a.K < kMmK || a.K % kMmK) return -1;
+  if (a.N % 8 || a.lda % 8 || a.ldb % 8 || a.lda < a.K || a.ldb < a.K) return -1;
+  if ((ep == MM_BF16 || ep == MM_BF16_GELU || ep == MM_F32 || ep == MM_RESID) && (a.ldo % 8 || a.ldo < a.N)) return -1;
+  if (ep == MM_XKV && (a.N != 2 * a.d || a.d % kHeadDim || a.vt_frames < a.M || a.vt_frames % kVtPiece)) return -1;
+  if (ep == MM_QKV_ENC && (a.N != 3 * a.d || a.d % kHeadDim || a.vt_frames < a.M || a.vt_frames % 8 || a.ldo % 8 ||
+                           a.ldo < 2 * a.d))
+    return -1;
+  return 0;
+}
+
+void mm(const MmArgs& a, int ep, int batch, hipStream_t st) {
+  const dim3 grid((std::max(a.M, (ep == MM_XKV || ep == MM_QKV_ENC) ? a.vt_frames : a.M) + BM - 1) / BM,
+                  (a.N + BN - 1) / BN, batch);
+  switch (ep) {
+    case MM_F32: k_mm<MM_F32><<<grid, NT, 0, st>>>(a); break;
+    case MM_BF16: k_mm<MM_BF16><<<grid, NT, 0, st>>>(a); break;
+    case MM_BF16_GELU: k_mm<MM_BF16_GELU><<<grid, NT, 0, st>>>(a); break;
+    case MM_RESID: k_mm<MM_RESID><<<grid, NT, 0, st>>>(a); break;
+    case MM_XKV: k_mm<MM_XKV><<<grid, NT, 0, st>>>(a); break;
+    case MM_QKV_ENC: k_mm<MM_QKV_ENC><<<grid, NT, 0, st>>>(a); break;
+  }
+}
+
+}  // namespace wf

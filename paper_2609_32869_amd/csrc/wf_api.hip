@@ -720,6 +720,37 @@ struct Runner {
 
   void encode(int slot0, int n, const void* mem) {
     const size_t per = (size_t)c.n_frames * c.d_model;
+    if (std::is_same<S, bf16>::value) {
+      // bf16 storage: the keys and values of all blocks on the matrix cores, one
+      // launch per slot for the target blocks (grid z = block) and one for the
+      // drafter's (their weights sit at a fixed stride within each group)
+      for (int s = 0; s < n; ++s) {
+        const int slot = slot0 + s;
+        auto group = [&](int first, int count, const std::vector<BlockW>& bw) {
+          MmArgs a{};
+          a.A = reinterpret_cast<const bf16*>(mem) + s * per;
+          a.lda = c.d_model;
+          a.B = reinterpret_cast<const bf16*>(W(bw[0].w_kv2));
+          a.ldb = c.d_model;
+          a.sB = count > 1 ? (long long)(bw[1].w_kv2 - bw[0].w_kv2) : 0;
+          a.bias = reinterpret_cast<const bf16*>(W(bw[0].b_kv2));
+          a.sBias = count > 1 ? (long long)(bw[1].b_kv2 - bw[0].b_kv2) : 0;
+          a.M = c.n_frames;
+          a.N = 2 * c.d_model;
+          a.K = c.d_model;
+          a.out = xkv_layer(first) + (size_t)slot * xkv_slot();
+          a.sO = (long long)c.max_batch * xkv_slot();
+          a.d = c.d_model;
+          a.n_head = c.n_head;
+          a.vt_frames = vt_frames();
+          a.scale = 1.f;
+          mm(a, MM_XKV, count, st);
+        };
+        group(0, c.n_layer, L.tb);
+        group(c.n_layer, c.n_draft_layer, L.db);
+      }
+      return;
+    }
     for (int s = 0; s < n; ++s) {
       const int slot = slot0 + s;
       for (int l = 0; l < c.n_layer + c.n_draft_layer; ++l) {
@@ -961,6 +992,13 @@ int wf_encode_memory_set(wf_handle* hh, int slot0, int n, const void* mem, void*
   Handle* h = reinterpret_cast<Handle*>(hh);
   if (int r = check_batch(h, slot0, n, false)) return r;
   if (!mem) return fail(h, WF_EINVAL, "null memory");
+  if (h->cfg.dtype == WF_BF16) {
+    if (reinterpret_cast<uintptr_t>(mem) & 15) return fail(h, WF_EINVAL, "acoustic memory must be 16-byte aligned");
+    MmArgs a{};
+    a.M = h->cfg.n_frames; a.N = 2 * h->cfg.d_model; a.K = a.lda = a.ldb = h->cfg.d_model;
+    a.d = h->cfg.d_model; a.vt_frames = xkv_vt_frames(h->cfg.n_frames);
+    if (mm_check(a, MM_XKV)) return fail(h, WF_EINVAL, "acoustic K/V product: unsupported shape");
+  }
   hipStream_t st = static_cast<hipStream_t>(stream);
   return dispatch(h, st, [&](auto* tag) {
     using S = std::remove_pointer_t<decltype(tag)>;

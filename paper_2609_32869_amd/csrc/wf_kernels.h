@@ -234,6 +234,37 @@ struct XkvArgs {
   int vt_frames;    // > 0: values stored transposed [head][dim][vt_frames], padding zero
 };
 
+// Request-time matrix-core GEMM (k_mm.hip): C = A B^T (+ bias) for bf16 A [M, K] and
+// B [N, K] (row-major, k contiguous), fp32 accumulation, 128 x 128 tiles, k in steps
+// of kMmK; grid z runs over `batch` independent products (element strides sA, sB,
+// sBias, sO, sO2).
+constexpr int kMmTile = 128, kMmK = 64;
+enum {
+  MM_F32 = 0,        // out fp32 [M][ldo] = scale * C + bias
+  MM_BF16 = 1,       // out bf16 [M][ldo]
+  MM_BF16_GELU = 2,  // out bf16 [M][ldo] = GELU(scale * C + bias)
+  MM_RESID = 3,      // out fp32 [M][ldo] += scale * C + bias
+  MM_XKV = 4,        // acoustic keys [head][frame][64] then values [head][frame / 256][dim][256]
+  MM_QKV_ENC = 5,    // columns < 2d: out bf16 [M][ldo]; the rest: out2 bf16 [head][dim][vt_frames]
+};
+struct MmArgs {
+  const bf16* A;
+  long long lda, sA;
+  const bf16* B;
+  long long ldb, sB;
+  const bf16* bias;
+  long long sBias;
+  int M, N, K;
+  void* out;
+  long long ldo, sO;
+  void* out2;
+  long long sO2;
+  int d, n_head, vt_frames;  // transposed epilogues: model width, heads, padded frame count
+  float scale;
+};
+int mm_check(const MmArgs& a, int ep);
+void mm(const MmArgs& a, int ep, int batch, hipStream_t st);
+
 template <typename S>
 struct Ops {
   static void ln_operand(const LnArgs& a, int rows, hipStream_t st);
