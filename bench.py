@@ -560,6 +560,65 @@ def b1_workload(args, W, log):
                 Lmid=Lmid, nat=nat, prof=prof, first_draw=first_draw, request=request)
 
 
+DRAFT_VARIANTS = {
+    "no-audio": dict(draft_audio=False),
+    "no-history": dict(draft_history=False),
+    "abs-pos": dict(draft_pos="abs"),
+    "five-layers": dict(n_draft_layer=5),
+}
+
+
+def draft_variant_times(args, log, steps=10, warmup=3):
+    """Batch-1 step latency of each drafter ablation variant (Section 5.4 Table 3;
+    Table A4) on the first batch-1 request, planted drafts as in the main line."""
+    import torch
+    from wf_fixtures import LARGE_V3, make_weights, make_memory, make_prefix, make_prefix_lengths
+    from paper_2609_32869_amd import WhisperFlash, to_device_storage
+    out = {}
+    L0 = int(make_prefix_lengths(1, 20, 200)[0])
+    for name, kw in DRAFT_VARIANTS.items():
+        cfg = LARGE_V3.with_(name=f"large-v3-{name}", **kw)
+        K = cfg.block_k
+        W = make_weights(cfg)
+        eng = WhisperFlash.from_host(cfg, 1, [W.values[n] for n, _ in W.order])
+        del W
+        eng.encode_memory_set(0, to_device_storage(make_memory(cfg, 0), cfg.dtype)[None])
+        toks = torch.from_numpy(make_prefix(cfg, 0, L0)[None].copy()).cuda()
+        outs = eng._outs(1)
+        zero = torch.zeros((1, K), dtype=torch.int32, device="cuda")
+        first = eng.prefill(0, toks, [L0], [cfg.n_ctx])
+        n_traj = (K + 1) * (steps + warmup + 1) + K
+        traj_t = torch.empty(n_traj, dtype=torch.int32, device="cuda")
+        traj_t[0] = first[0]
+        for t in range(1, n_traj):
+            eng.step(0, 1, 0, draft_override=zero, outs=outs, use_graph=True)
+            traj_t[t].copy_(outs[0][0, 0])
+        plans, accs = plan_planted(traj_t.cpu().numpy(), L0, 1, steps + warmup, cfg, np.random.default_rng(400))
+        plan_t = torch.from_numpy(plans[:, None, :].copy()).cuda()
+        eng.prefill(0, toks, [L0], [cfg.n_ctx])
+        ovr = torch.empty((1, K), dtype=torch.int32, device="cuda")
+        res = torch.zeros(steps + warmup, dtype=torch.int32, device="cuda")
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        for j in range(steps + warmup):
+            if j == warmup:
+                ev[0].record()
+            ovr.copy_(plan_t[j])
+            eng.step(0, 1, K, draft_override=ovr, outs=outs, use_graph=True)
+            res[j].copy_(outs[1][0])
+        ev[1].record()
+        torch.cuda.synchronize()
+        ms = ev[0].elapsed_time(ev[1]) / steps
+        r = res.cpu().numpy()
+        out[name] = {"ms_per_step": round(ms, 4), "verified_tokens_per_s": round(float(r[warmup:].sum()) / (ms * steps / 1e3), 1),
+                     "planted_acceptance_exact": bool(np.array_equal(r, accs + 1))}
+        log(f"[bench] draft variant {name}: {out[name]}")
+        del eng
+        torch.cuda.empty_cache()
+    out["config"] = {"workload": "whisper-large-v3-shaped draft+verify step, batch 1, planted drafts r~U{0..8}",
+                     "prefix_len": L0, "steps": steps, "warmup": warmup}
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -570,6 +629,7 @@ def main():
                     help="batch-1 prompt lengths drawn from U[20,200]; the timed steps are split over them")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-batch96", action="store_true", help="skip the batch-96 object of the default line")
+    ap.add_argument("--no-variants", action="store_true", help="skip the drafter-variant latencies of the default line")
     ap.add_argument("--kmax-sweep", action="store_true",
                     help="batch-1 step latency and verified tokens/s for verification budgets k_max in {0,1,2,4,8} "
                          "(k_max = 0 is plain decoding: the drafter does not run); prints one JSON line")
@@ -684,6 +744,9 @@ def main():
     if not args.no_batch96 and not args.pmc_run:
         log("[bench] batch 96")
         result["batch96"] = batch_workload(args, W, 96, 5, 2, 2, log, cpu_sample=not args.no_cpu_baseline)
+    if not args.no_variants and not args.pmc_run:
+        del W
+        result["draft_variants"] = draft_variant_times(args, log)
     print(json.dumps(result), flush=True)
     if args.pmc_run:
         calibration_copy(log)

@@ -56,6 +56,16 @@ extern "C" {
 
 #define WF_MAX_TAPS 8
 
+/* Drafter variants of the paper's ablations (wf_config.draft_flags; Section 5.4
+ * Table 3 and Appendix Table A4).  0 is the paper's drafter. */
+#define WF_DRAFT_NO_AUDIO 0x1u   /* blocks without the cross-attention sub-layer (and its
+                                    LayerNorm): the manifest omits those eight tensors */
+#define WF_DRAFT_NO_HISTORY 0x2u /* no target history: the manifest omits hproj.w/b and
+                                    the block attends to its own nine rows only */
+#define WF_DRAFT_ABS_POS 0x4u    /* absolute positions: no RoPE; the target's position
+                                    table (shared, like the embedding) is added to the
+                                    block rows at positions t..t+8 */
+
 /*
  * Model and batch shape.  The target is a Whisper decoder (Section 4: Whisper
  * large-v3 has n_layer 32, d_model 1280, n_head 20, d_ff 5120, n_vocab 51866,
@@ -79,6 +89,8 @@ typedef struct wf_config {
   int32_t eos_id;           /* end-of-transcript id, or -1 for none */
   int32_t dtype;            /* WF_F32 or WF_BF16 */
   int32_t max_batch;        /* number of slots */
+  int32_t draft_flags;      /* WF_DRAFT_* bits (0: the paper's drafter); n_draft_layer
+                               sets the depth (2 in the paper, 5 in Table A4) */
 } wf_config;
 
 typedef struct wf_handle wf_handle;
@@ -104,8 +116,9 @@ int wf_weight_numel(const wf_config* cfg, int i, int64_t* numel);
  *     xattn_ln.g/b; xattn.q.w/b; xattn.k.w; xattn.v.w/b; xattn.o.w/b;
  *     mlp_ln.g/b; mlp.fc1.w [F,d] mlp.fc1.b [F]; mlp.fc2.w [d,F] mlp.fc2.b [d]
  *   ln_f.g/b
- *   drafter: hproj.w [d, n_tap*d] hproj.b [d]; mask [d]; then n_draft_layer
- *     blocks with the target block layout; ln_f.g/b
+ *   drafter: hproj.w [d, n_tap*d] hproj.b [d] (absent with WF_DRAFT_NO_HISTORY);
+ *     mask [d]; then n_draft_layer blocks with the target block layout (without
+ *     the xattn_ln / xattn entries with WF_DRAFT_NO_AUDIO); ln_f.g/b
  * The caller's tensors are only read by work enqueued on `stream`; they may be
  * freed once that stream has synchronised.  Slots start empty.
  * Errors: WF_EINVAL (config, null, n_weights), WF_ESIZE, WF_EHIP.

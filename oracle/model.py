@@ -152,16 +152,30 @@ class Target:
 
 
 class Drafter:
+    """The block drafter.  Ablation variants (Section 5.4 Table 3, Table A4) follow
+    ``cfg.draft_audio`` (False: the blocks have no cross-attention sub-layer),
+    ``cfg.draft_history`` (False: no history projection; the block attends to its
+    own nine rows only) and ``cfg.draft_pos`` ("abs": no RoPE; the target's learned
+    position table, shared and frozen like the token embedding, is added to the
+    block rows at positions t..t+K)."""
+
     def __init__(self, cfg, W, opts):
         self.cfg, self.opts = cfg, opts
         dt = opts.dtype
+        self.audio = getattr(cfg, "draft_audio", True)
+        self.hist = getattr(cfg, "draft_history", True)
+        self.use_rope = getattr(cfg, "draft_pos", "rope") == "rope"
         self.E = W["tok_emb"].astype(dt)          # shared embedding / output head
-        self.Wh, self.bh = W["d.hproj.w"], W["d.hproj.b"]
+        self.P = W["pos_emb"].astype(dt)          # shared position table (absolute-position variant)
+        if self.hist:
+            self.Wh, self.bh = W["d.hproj.w"], W["d.hproj.b"]
         self.m = W["d.mask"].astype(dt)
         self.blocks = [_blk(W, f"d{l}") for l in range(cfg.n_draft_layer)]
         self.lnf = (W["d.ln_f.g"], W["d.ln_f.b"])
 
     def cross_kv(self, mem):
+        if not self.audio:
+            return None
         return _cross_kv(self.blocks, mem, "xattn", self.opts)
 
     def new_cache(self):
@@ -175,13 +189,16 @@ class Drafter:
     def _block_kv(self, b, a, positions):
         H, d = self.cfg.n_head, self.cfg.d_model
         hd = d // H
-        k = linear(a, b["attn.k.w"], None, self.opts).reshape(-1, H, hd)
-        k = rope(k, positions, self.opts.dtype).reshape(-1, d)
+        k = linear(a, b["attn.k.w"], None, self.opts)
+        if self.use_rope:
+            k = rope(k.reshape(-1, H, hd), positions, self.opts.dtype).reshape(-1, d)
         v = linear(a, b["attn.v.w"], b["attn.v.b"], self.opts)
         return k, v
 
     def history_update(self, hcache, taps, pos0):
         """Write history K/V of rows at positions pos0.. from their target taps."""
+        if not self.hist:
+            return
         dt = self.opts.dtype
         hp = self.history_proj(taps)
         pos = np.arange(pos0, pos0 + hp.shape[0])
@@ -201,17 +218,22 @@ class Drafter:
         hd = d // H
         x = np.concatenate([self.E[[int(anchor)]], np.repeat(self.m[None, :], K, axis=0)]).astype(dt)
         pos = np.arange(t, t + K + 1)
+        if not self.use_rope:
+            x = x + self.P[np.minimum(pos, cfg.n_ctx - 1)]
+        nh = t if self.hist else 0
         for l, b in enumerate(self.blocks):
             a = layer_norm(x, b["attn_ln.g"], b["attn_ln.b"], dt)
             q = linear(a, b["attn.q.w"], b["attn.q.b"], opts).reshape(-1, H, hd)
-            q = rope(q, pos, dt)
+            if self.use_rope:
+                q = rope(q, pos, dt)
             kb, vb = self._block_kv(b, a, pos)
-            Kall = np.concatenate([hcache.K[l, :t], kb]).reshape(-1, H, hd)
-            Vall = np.concatenate([hcache.V[l, :t], vb]).reshape(-1, H, hd)
-            allowed = np.ones((K + 1, t + K + 1), bool)
+            Kall = np.concatenate([hcache.K[l, :nh], kb]).reshape(-1, H, hd)
+            Vall = np.concatenate([hcache.V[l, :nh], vb]).reshape(-1, H, hd)
+            allowed = np.ones((K + 1, nh + K + 1), bool)
             o = attention(q, Kall, Vall, allowed, dt)
             x = x + linear(o, b["attn.o.w"], b["attn.o.b"], opts)
-            x = x + _cross_attend(b, x, dxkv[l], H, opts)
+            if self.audio:
+                x = x + _cross_attend(b, x, dxkv[l], H, opts)
             x = x + _mlp(b, x, opts)
         hf = layer_norm(x[1:], self.lnf[0], self.lnf[1], dt)
         logits = linear(hf, self.E, None, opts).astype(np.float32)

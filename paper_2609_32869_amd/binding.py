@@ -32,7 +32,7 @@ class WfConfig(ctypes.Structure):
                 ("d_ff", ctypes.c_int32), ("n_vocab", ctypes.c_int32), ("n_ctx", ctypes.c_int32),
                 ("n_frames", ctypes.c_int32), ("n_draft_layer", ctypes.c_int32), ("block_k", ctypes.c_int32),
                 ("n_tap", ctypes.c_int32), ("taps", ctypes.c_int32 * WF_MAX_TAPS), ("eos_id", ctypes.c_int32),
-                ("dtype", ctypes.c_int32), ("max_batch", ctypes.c_int32)]
+                ("dtype", ctypes.c_int32), ("max_batch", ctypes.c_int32), ("draft_flags", ctypes.c_int32)]
 
 
 class WfError(RuntimeError):
@@ -114,6 +114,7 @@ def make_config(cfg, max_batch):
     c.eos_id = cfg.eos_id
     c.dtype = WF_BF16 if cfg.dtype == "bf16" else WF_F32
     c.max_batch = max_batch
+    c.draft_flags = getattr(cfg, "draft_flags", 0)
     return c
 
 

@@ -1149,7 +1149,8 @@ __global__ void __launch_bounds__(kSxThreads) k_attn_self_mx(AttnArgs a) {
 // history keys at positions 0..t-1 and to all nine block keys (Section 3.2:
 // bidirectional inside the block).  The query and the block keys get RoPE here
 // (rotate-half, pairs (j, j+32)); history keys were stored with RoPE at their own
-// positions.
+// positions.  Ablation variants: without history the nine block keys are all the
+// keys; with absolute positions nothing is rotated.
 template <typename S>
 __global__ void __launch_bounds__(kSelfThreads) k_attn_draft(AttnArgs a) {
   StampScope stamp_scope(a.stamp, kSelfThreads);
@@ -1163,13 +1164,15 @@ __global__ void __launch_bounds__(kSelfThreads) k_attn_draft(AttnArgs a) {
   if (!head_row(blockIdx.x, a.n_head, head, row)) return;
   const int slot = a.slot0 + blockIdx.y;
   const int t0 = a.state[slot * kStateInts + ST_L];
+  const int nh = a.draft_hist ? t0 : 0;  // history keys attended
   const int d = a.d;
   const int lane = threadIdx.x & 63, g = lane & 7;
   // rotated block keys and their values
   for (int t = threadIdx.x; t < kRows * 32; t += NT) {
     const int jb = t >> 5, j = t & 31;
     const int pos = t0 + jb;
-    const float c = a.rope[(pos * 32 + j) * 2], sn = a.rope[(pos * 32 + j) * 2 + 1];
+    const float c = a.draft_rope ? a.rope[(pos * 32 + j) * 2] : 1.f;
+    const float sn = a.draft_rope ? a.rope[(pos * 32 + j) * 2 + 1] : 0.f;
     const float* kr = a.q + (size_t)(slot * kRows + jb) * a.ldq + d + head * kHeadDim;
     const float* vr = kr + d;
     const float k1 = kr[j], k2 = kr[j + 32];
@@ -1186,14 +1189,15 @@ __global__ void __launch_bounds__(kSelfThreads) k_attn_draft(AttnArgs a) {
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
       const int dim = 8 * g + e, j = dim & 31;
-      const float c = a.rope[(pos * 32 + j) * 2], sn = a.rope[(pos * 32 + j) * 2 + 1];
+      const float c = a.draft_rope ? a.rope[(pos * 32 + j) * 2] : 1.f;
+      const float sn = a.draft_rope ? a.rope[(pos * 32 + j) * 2 + 1] : 0.f;
       const float u1 = qr[j], u2 = qr[j + 32];
       q8[e] = (dim < 32 ? u1 * c - u2 * sn : u1 * sn + u2 * c) * 0.125f;
     }
   }
   const S* Kh = reinterpret_cast<const S*>(a.kcache) + ((size_t)slot * a.n_head + head) * a.n_ctx * kHeadDim;
   const S* Vh = reinterpret_cast<const S*>(a.vcache) + ((size_t)slot * a.n_head + head) * a.n_ctx * kHeadDim;
-  score_pass<S, NT, 14>(q8, t0, [&](int j) { return Kh + (size_t)j * kHeadDim; }, sc);
+  score_pass<S, NT, 14>(q8, nh, [&](int j) { return Kh + (size_t)j * kHeadDim; }, sc);
   __syncthreads();
   // the nine block keys: one wave, lane (key kl, dims 8g..), keys 0..7 then key 8
   if (threadIdx.x < 64) {
@@ -1206,21 +1210,21 @@ __global__ void __launch_bounds__(kSelfThreads) k_attn_draft(AttnArgs a) {
         for (int e = 0; e < 8; ++e) s = fmaf(q8[e], kb[jb][8 * g + e], s);
       }
       s = key_sum(s);
-      if (g == 0 && jb < kRows) sc[t0 + jb] = s;
+      if (g == 0 && jb < kRows) sc[nh + jb] = s;
     }
   }
   __syncthreads();
-  const int nk = t0 + kRows;
+  const int nk = nh + kRows;
   const float L = softmax_pass<NT>(sc, nk, red);
   __syncthreads();
   float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-  value_pass<S, NT, 14>(acc, t0, [&](int j) { return Vh + (size_t)j * kHeadDim; }, sc);
+  value_pass<S, NT, 14>(acc, nh, [&](int j) { return Vh + (size_t)j * kHeadDim; }, sc);
   if (threadIdx.x < 64) {
     const int kl = lane >> 3;
     for (int half = 0; half < 2; ++half) {
       const int jb = half * 8 + kl;
       if (jb < kRows) {
-        const float pk = sc[t0 + jb];
+        const float pk = sc[nh + jb];
 #pragma unroll
         for (int e = 0; e < 8; ++e) acc[e] = fmaf(pk, vb[jb][8 * g + e], acc[e]);
       }

@@ -254,6 +254,15 @@ __global__ void __launch_bounds__(256) k_draft_begin(BeginArgs a) {
   if (threadIdx.x < kRows) toks[threadIdx.x] = min(max(st[ST_ANCHOR], 0), a.n_vocab - 1);
   __syncthreads();
   fill_rows<S>(a, slot, toks, nullptr, true);
+  if (a.pos2 != nullptr) {  // absolute-position variant: + P[t + i] on row i
+    __syncthreads();
+    const S* P = reinterpret_cast<const S*>(a.pos2);
+    const int L = st[ST_L];
+    for (int idx = threadIdx.x; idx < kRows * a.d; idx += 256) {
+      const int i = idx / a.d, col = idx - i * a.d;
+      a.h[(size_t)(slot * kRows + i) * a.d + col] += to_f(P[(size_t)min(L + i, a.n_ctx - 1) * a.d + col]);
+    }
+  }
 }
 
 // Prefill chunk c: prompt positions 9c..9c+8 of each slot.
@@ -333,7 +342,7 @@ __global__ void __launch_bounds__(256) k_hist_write(HistArgs a) {
   S* Vh = reinterpret_cast<S*>(a.vcache);
   for (int t = threadIdx.x; t < a.n_head * 32; t += 256) {
     const int head = t >> 5, j = t & 31;
-    const float c = a.rope[(pos * 32 + j) * 2], sn = a.rope[(pos * 32 + j) * 2 + 1];
+    const float c = a.use_rope ? a.rope[(pos * 32 + j) * 2] : 1.f, sn = a.use_rope ? a.rope[(pos * 32 + j) * 2 + 1] : 0.f;
     const float k1 = kr[head * kHeadDim + j], k2 = kr[head * kHeadDim + j + 32];
     const size_t base = (((size_t)slot * a.n_head + head) * a.n_ctx + pos) * kHeadDim;
     Kh[base + j] = from_f<S>(k1 * c - k2 * sn);

@@ -85,6 +85,10 @@ int check_config(const wf_config* c, std::string& why) {
   }
   if (c->max_batch < 1 || c->max_batch > 4096) { why = "max_batch must be in [1, 4096]"; return WF_EINVAL; }
   if (c->eos_id < -1 || c->eos_id >= c->n_vocab) { why = "eos_id out of range"; return WF_EINVAL; }
+  if (c->draft_flags & ~(int32_t)(WF_DRAFT_NO_AUDIO | WF_DRAFT_NO_HISTORY | WF_DRAFT_ABS_POS)) {
+    why = "unknown draft_flags bits";
+    return WF_EINVAL;
+  }
   return WF_OK;
 }
 
@@ -124,27 +128,32 @@ std::vector<ManEntry> manifest(const wf_config& c, const Layout& L, std::vector<
   const int emb = mat(L.tok_emb, c.n_vocab, d, wide);
   m.push_back({(size_t)c.n_vocab * d, L.tok_emb, emb});
   m.push_back({(size_t)c.n_ctx * d, L.pos_emb, -1});
-  auto block = [&](const BlockW& b) {
+  auto block = [&](const BlockW& b, bool cross) {
     m.push_back({d, b.ln1_g, -1}); m.push_back({d, b.ln1_b, -1});
     const int qkv = mat(b.w_qkv, 3 * d, d, W_F16, b.ln1_g, b.ln1_b, b.c_qkv);
     m.push_back({d * d, b.w_qkv, qkv}); m.push_back({d, b.b_qkv, -1});
     m.push_back({d * d, b.w_qkv + d * d, qkv});
     m.push_back({d * d, b.w_qkv + 2 * d * d, qkv}); m.push_back({d, b.b_qkv + 2 * d, -1});
     m.push_back({d * d, b.w_o, mat(b.w_o, d, d, W_F16)}); m.push_back({d, b.b_o, -1});
-    m.push_back({d, b.ln2_g, -1}); m.push_back({d, b.ln2_b, -1});
-    m.push_back({d * d, b.w_q2, mat(b.w_q2, d, d, W_F16, b.ln2_g, b.ln2_b, b.c_q2)}); m.push_back({d, b.b_q2, -1});
-    m.push_back({d * d, b.w_kv2, -1});  // encode-time product: row-major
-    m.push_back({d * d, b.w_kv2 + d * d, -1}); m.push_back({d, b.b_kv2 + d, -1});
-    m.push_back({d * d, b.w_o2, mat(b.w_o2, d, d, W_F16)}); m.push_back({d, b.b_o2, -1});
+    if (cross) {
+      m.push_back({d, b.ln2_g, -1}); m.push_back({d, b.ln2_b, -1});
+      m.push_back({d * d, b.w_q2, mat(b.w_q2, d, d, W_F16, b.ln2_g, b.ln2_b, b.c_q2)}); m.push_back({d, b.b_q2, -1});
+      m.push_back({d * d, b.w_kv2, -1});  // encode-time product: row-major
+      m.push_back({d * d, b.w_kv2 + d * d, -1}); m.push_back({d, b.b_kv2 + d, -1});
+      m.push_back({d * d, b.w_o2, mat(b.w_o2, d, d, W_F16)}); m.push_back({d, b.b_o2, -1});
+    }
     m.push_back({d, b.ln3_g, -1}); m.push_back({d, b.ln3_b, -1});
     m.push_back({F * d, b.w_fc1, mat(b.w_fc1, F, d, wide, b.ln3_g, b.ln3_b, b.c_fc1)}); m.push_back({F, b.b_fc1, -1});
     m.push_back({d * F, b.w_fc2, mat(b.w_fc2, d, F, W_F16)}); m.push_back({d, b.b_fc2, -1});
   };
-  for (auto& b : L.tb) block(b);
+  for (auto& b : L.tb) block(b, true);
   m.push_back({d, L.lnf_g, -1}); m.push_back({d, L.lnf_b, -1});
-  m.push_back({d * c.n_tap * d, L.hproj_w, mat(L.hproj_w, d, c.n_tap * d, W_F16)});
-  m.push_back({d, L.hproj_b, -1}); m.push_back({d, L.mask, -1});
-  for (auto& b : L.db) block(b);
+  if (!(c.draft_flags & WF_DRAFT_NO_HISTORY)) {
+    m.push_back({d * c.n_tap * d, L.hproj_w, mat(L.hproj_w, d, c.n_tap * d, W_F16)});
+    m.push_back({d, L.hproj_b, -1});
+  }
+  m.push_back({d, L.mask, -1});
+  for (auto& b : L.db) block(b, !(c.draft_flags & WF_DRAFT_NO_AUDIO));
   m.push_back({d, L.dlnf_g, -1}); m.push_back({d, L.dlnf_b, -1});
   if (mats) *mats = mm;
   return m;
@@ -504,7 +513,15 @@ struct Runner {
   // second half of a decoder block shared by target and drafter: cross-attention and MLP
   // q_clear: the self-attention before left the query places at zero, so a
   // split W'_q product may add its partial sums into them
-  void block_tail(int slot0, int n, const BlockW& b, int xlayer, int tap, const LnNext& nx, bool q_clear = false) {
+  // cross: the block has its cross-attention sub-layer (every target block; drafter
+  // blocks unless the variant drops it)
+  void block_tail(int slot0, int n, const BlockW& b, int xlayer, int tap, const LnNext& nx, bool q_clear = false,
+                  bool cross = true) {
+    if (cross) cross_sublayer(slot0, n, b, xlayer, q_clear);
+    mlp_sublayer(slot0, n, b, tap, nx);
+  }
+
+  void cross_sublayer(int slot0, int n, const BlockW& b, int xlayer, bool q_clear) {
     const int d = c.d_model;
     float *h_ = F32(L.h), *qkv = F32(L.qkv);
     if (q_clear) {
@@ -518,6 +535,11 @@ struct Runner {
     const OprojArgs op2 = oproj(b.w_o2, b.b_o2);
     cross(slot0, n, xlayer, op2);
     if (op2.w == nullptr) resid("gemv_o", slot0, n, Ad16(), b.w_o2, b.b_o2, d, d);
+  }
+
+  void mlp_sublayer(int slot0, int n, const BlockW& b, int tap, const LnNext& nx) {
+    const int d = c.d_model;
+    float* h_ = F32(L.h);
     gemv_ln("gemv_fc1", EPI_GELU, slot0, n, h_, b.ln3_g, b.ln3_b, b.c_fc1, c.d_ff, 0, Ad32(), b.w_fc1, b.b_fc1, d, c.d_ff,
             nullptr, 0, Af16());
     const int ksplit = L.fc2_split > 0 ? L.fc2_split : fc2_split_batch(slot0, n);
@@ -635,6 +657,7 @@ struct Runner {
 
   // drafter history for pending rows (Appendix A.2): taps -> W_h -> per-block LN, k (RoPE), v
   void history_apply(int slot0, int n) {
+    if (c.draft_flags & WF_DRAFT_NO_HISTORY) return;  // the variant keeps no history
     const int d = c.d_model;
     float *hp = F32(L.hp), *kvh = F32(L.kvh);
     gemv("gemv_hproj", EPI_STORE, slot0, n, Atap16(), L.hproj_w, L.hproj_b, c.n_tap * d, d, hp, d);
@@ -647,6 +670,7 @@ struct Runner {
       ha.kv = kvh; ha.kcache = hkv(dl, 0); ha.vcache = hkv(dl, 1); ha.state = I32(L.state); ha.rope = F32(L.rope);
       ha.slot0 = slot0; ha.d = d; ha.n_head = c.n_head; ha.n_ctx = c.n_ctx;
       ha.status = h->at<unsigned>(L.status);
+      ha.use_rope = !(c.draft_flags & WF_DRAFT_ABS_POS);
       launch("hist_write", 0, [&](unsigned long long*) { Ops<S>::hist_write(ha, n, st); });
     }
   }
@@ -657,6 +681,7 @@ struct Runner {
     BeginArgs ba{};
     ba.state = I32(L.state); ba.emb = W(L.tok_emb); ba.emb_kind = wk(true); ba.pos = W(L.mask); ba.h = h_;
     ba.slot0 = slot0; ba.d = d; ba.n_vocab = c.n_vocab; ba.n_ctx = c.n_ctx; ba.block_k = c.block_k;
+    if (c.draft_flags & WF_DRAFT_ABS_POS) ba.pos2 = W(L.pos_emb);
     launch("begin", 0, [&](unsigned long long*) { Ops<S>::draft_begin(ba, n, st); });
     ln_ready = false;
     for (int dl = 0; dl < c.n_draft_layer; ++dl) {
@@ -670,6 +695,8 @@ struct Runner {
       at.state = I32(L.state); at.rope = F32(L.rope); at.out = Ad16();
       at.slot0 = slot0; at.d = d; at.n_head = c.n_head; at.n_ctx = c.n_ctx;
       at.nsplit = L.nsplit_op; at.R9 = R9();
+      at.draft_hist = !(c.draft_flags & WF_DRAFT_NO_HISTORY);
+      at.draft_rope = !(c.draft_flags & WF_DRAFT_ABS_POS);
       launch("attn_draft", 0, [&](unsigned long long* sp) {
         at.stamp = sp;
         Ops<S>::attn_draft(at, n, st);
@@ -677,7 +704,7 @@ struct Runner {
       resid("gemv_o", slot0, n, Ad16(), b.w_o, b.b_o, d, d);
       const LnNext nx = dl + 1 < c.n_draft_layer ? LnNext{L.db[dl + 1].ln1_g, L.db[dl + 1].ln1_b, false}
                                                  : LnNext{L.dlnf_g, L.dlnf_b, true};
-      block_tail(slot0, n, b, c.n_layer + dl, -1, nx);
+      block_tail(slot0, n, b, c.n_layer + dl, -1, nx, false, !(c.draft_flags & WF_DRAFT_NO_AUDIO));
     }
     head(slot0, n, h_, L.dlnf_g, L.dlnf_b, h->debug || sampling() ? F32(L.dlogits) : nullptr, I32(L.draft), dst,
          RNG_DRAFT, F32(L.dmax), F32(L.dsum));
@@ -747,13 +774,14 @@ struct Runner {
           mm(a, MM_XKV, count, st);
         };
         group(0, c.n_layer, L.tb);
-        group(c.n_layer, c.n_draft_layer, L.db);
+        if (!(c.draft_flags & WF_DRAFT_NO_AUDIO)) group(c.n_layer, c.n_draft_layer, L.db);
       }
       return;
     }
     for (int s = 0; s < n; ++s) {
       const int slot = slot0 + s;
-      for (int l = 0; l < c.n_layer + c.n_draft_layer; ++l) {
+      const int nblk = c.n_layer + ((c.draft_flags & WF_DRAFT_NO_AUDIO) ? 0 : c.n_draft_layer);
+      for (int l = 0; l < nblk; ++l) {
         const BlockW& b = l < c.n_layer ? L.tb[l] : L.db[l - c.n_layer];
         XkvArgs a{};
         a.mem = reinterpret_cast<const S*>(mem) + s * per;

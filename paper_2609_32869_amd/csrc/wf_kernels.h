@@ -111,6 +111,9 @@ struct AttnArgs {
   // the slot's nine rows) once every wave has used them, so that the next product
   // can add split-K partial sums into those places
   int clear_q;
+  // drafter attention: the history before the anchor is attended (else the nine
+  // block rows only), and queries / keys carry RoPE (else no rotation)
+  int draft_hist, draft_rope;
   unsigned long long* stamp;  // launch timing slot (profiled calls), or null
 };
 
@@ -202,6 +205,7 @@ struct BeginArgs {
   int pages_per_slot;
   int slot0, d, n_vocab, n_ctx, block_k, k_max, chunk, pmax;
   unsigned* status;  // sticky device status word (verify: position overflow), or null
+  const void* pos2;  // drafter with absolute positions: position table added to row i at t + i, else null
 };
 
 struct HistArgs {
@@ -212,6 +216,7 @@ struct HistArgs {
   const float* rope;
   int slot0, d, n_head, n_ctx;
   unsigned* status;  // sticky device status word (position overflow), or null
+  int use_rope;      // keys rotated at their positions (RoPE drafter), else stored as projected
 };
 
 struct AcceptArgs {

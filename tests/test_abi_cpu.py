@@ -42,7 +42,11 @@ def test_library_exports_every_declared_symbol():
         assert hasattr(lib, s)
 
 
-@pytest.mark.parametrize("cfg", [MICRO, TINY, LARGE_V3])
+@pytest.mark.parametrize("cfg", [MICRO, TINY, LARGE_V3, LARGE_V3.with_(draft_audio=False),
+                                 LARGE_V3.with_(draft_history=False), LARGE_V3.with_(draft_pos="abs"),
+                                 LARGE_V3.with_(n_draft_layer=5),
+                                 MICRO.with_(draft_audio=False, draft_history=False, draft_pos="abs")],
+                         ids=["micro", "tiny", "large-v3", "no-audio", "no-history", "abs-pos", "five-layers", "micro-all"])
 def test_weight_manifest_matches_fixture_order(cfg):
     binding, lib = _lib()
     c = binding.make_config(cfg, 1)

@@ -29,6 +29,13 @@ class ModelConfig:
     n_draft_layer: int = 2
     block_k: int = 8      # mask positions per draft block
     eos_id: int = 50257   # end-of-transcript token id
+    # drafter variants of the ablations (Section 5.4 Table 3; Table A4): without
+    # its cross-attention to the acoustic memory, without the target history, and
+    # with absolute positions (the target's learned position table added to the
+    # block rows) instead of RoPE
+    draft_audio: bool = True
+    draft_history: bool = True
+    draft_pos: str = "rope"   # "rope" or "abs"
 
     @property
     def head_dim(self) -> int:
@@ -37,6 +44,11 @@ class ModelConfig:
     @property
     def n_tap(self) -> int:
         return len(self.taps)
+
+    @property
+    def draft_flags(self) -> int:
+        """Variant bits of the C ABI (1 no audio, 2 no history, 4 absolute positions)."""
+        return (0 if self.draft_audio else 1) | (0 if self.draft_history else 2) | (4 if self.draft_pos == "abs" else 0)
 
     def with_(self, **kw) -> "ModelConfig":
         return replace(self, **kw)

@@ -49,10 +49,19 @@ def target_manifest(cfg):
 
 
 def drafter_manifest(cfg):
+    """The drafter's parameters; the ablation variants drop the history projection
+    (no target history) or every block's cross-attention sub-layer with its
+    LayerNorm (no direct audio)."""
     d, f = cfg.d_model, cfg.d_ff
-    m = [("d.hproj.w", (d, cfg.n_tap * d)), ("d.hproj.b", (d,)), ("d.mask", (d,))]
+    m = []
+    if getattr(cfg, "draft_history", True):
+        m += [("d.hproj.w", (d, cfg.n_tap * d)), ("d.hproj.b", (d,))]
+    m += [("d.mask", (d,))]
     for l in range(cfg.n_draft_layer):
-        m += _block(f"d{l}", d, f)
+        blk = _block(f"d{l}", d, f)
+        if not getattr(cfg, "draft_audio", True):
+            blk = [(n, s) for n, s in blk if ".xattn" not in n]
+        m += blk
     m += [("d.ln_f.g", (d,)), ("d.ln_f.b", (d,))]
     return m
 
