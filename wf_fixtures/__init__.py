@@ -11,14 +11,16 @@ Workload shapes follow the paper's setup: the target is Whisper large-v3
 (Appendix A.2), the acoustic memory is one 30 s window of 1500 encoder
 frames, and text positions stop at Whisper's 448-token context.
 """
-from .configs import (ModelConfig, TINY, LARGE_V3, MICRO, VOCAB64, PURPOSE, config_by_name)
-from .manifest import target_manifest, drafter_manifest, full_manifest, param_count
+from .configs import (ModelConfig, TINY, LARGE_V3, MICRO, VOCAB64, PURPOSE, config_by_name,
+                      EncoderConfig, LARGE_V3_ENC, MICRO_ENC)
+from .manifest import target_manifest, drafter_manifest, full_manifest, param_count, encoder_manifest
 from .gen import (make_weights, make_memory, make_prefix, make_prefix_lengths,
-                  plant_drafts, bf16_round_bits, bits_to_f32, WeightSet)
+                  plant_drafts, bf16_round_bits, bits_to_f32, WeightSet, make_encoder_weights, make_audio)
 
 __all__ = [
     "ModelConfig", "TINY", "LARGE_V3", "MICRO", "VOCAB64", "PURPOSE", "config_by_name",
     "target_manifest", "drafter_manifest", "full_manifest", "param_count",
     "make_weights", "make_memory", "make_prefix", "make_prefix_lengths", "plant_drafts",
     "bf16_round_bits", "bits_to_f32", "WeightSet",
+    "EncoderConfig", "LARGE_V3_ENC", "MICRO_ENC", "encoder_manifest", "make_encoder_weights", "make_audio",
 ]

@@ -75,6 +75,43 @@ VOCAB64 = ModelConfig(name="vocab64", n_layer=2, d_model=128, n_head=2, d_ff=256
 _BY_NAME = {c.name: c for c in (LARGE_V3, TINY, MICRO, VOCAB64)}
 
 
+@dataclass(frozen=True)
+class EncoderConfig:
+    """Whisper audio encoder shapes (the acoustic memory the drafter and the target
+    read): log-mel frontend of a 16 kHz waveform, two-convolution stem halving the
+    frame rate, n_layer pre-LN blocks, n_ctx output positions (1500 for 30 s)."""
+    name: str
+    n_mels: int
+    n_ctx: int            # output positions (half the mel frames)
+    d_model: int
+    n_head: int
+    n_layer: int
+    d_ff: int
+    n_fft: int = 400
+    hop: int = 160
+    sample_rate: int = 16000
+    dtype: str = "bf16"
+
+    @property
+    def n_samples(self) -> int:
+        return 2 * self.n_ctx * self.hop
+
+    @property
+    def head_dim(self) -> int:
+        return self.d_model // self.n_head
+
+    def with_(self, **kw) -> "EncoderConfig":
+        return replace(self, **kw)
+
+
+# Whisper large-v3 encoder: 128 mel bins, 30 s windows (3000 mel frames, 1500
+# positions), 32 blocks of width 1280 with 20 heads, MLP 5120.
+LARGE_V3_ENC = EncoderConfig(name="large-v3-enc", n_mels=128, n_ctx=1500, d_model=1280, n_head=20, n_layer=32,
+                             d_ff=5120)
+# A small encoder for brute-force tests: 1.54 s of audio, 80 mel bins.
+MICRO_ENC = EncoderConfig(name="micro-enc", n_mels=80, n_ctx=48, d_model=128, n_head=2, n_layer=2, d_ff=256)
+
+
 def config_by_name(name: str) -> ModelConfig:
     return _BY_NAME[name]
 

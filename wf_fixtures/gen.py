@@ -81,6 +81,56 @@ def _round_inplace(flat):
         np.bitwise_and(blk, np.uint32(0xFFFF0000), out=blk)
 
 
+def _draw_manifest(order, seed_of, dtype, threads, std):
+    from concurrent.futures import ThreadPoolExecutor
+
+    sizes = [int(np.prod(shape)) for _, shape in order]
+    flat = np.empty(sum(sizes), dtype=np.float32)
+    views, off = [], 0
+    for (name, shape), n in zip(order, sizes):
+        views.append(flat[off:off + n])
+        off += n
+
+    def work(i):
+        name = order[i][0]
+        _fill(views[i], seed_of(name), i, name, std)
+        if dtype == "bf16":
+            _round_inplace(views[i])
+
+    idx = sorted(range(len(order)), key=lambda i: -sizes[i])
+    with ThreadPoolExecutor(max_workers=threads) as ex:
+        list(ex.map(work, idx))
+    return flat, {name: v.reshape(shape) for (name, shape), v in zip(order, views)}
+
+
+def make_encoder_weights(ecfg, seed=2, threads=8, std=0.02):
+    """Whisper encoder parameters in manifest order, drawn as the decoder's are
+    (N(0, std), LayerNorm gains 1 + N(0, std)), rounded to bf16 for bf16 shapes."""
+    from .manifest import encoder_manifest
+    order = encoder_manifest(ecfg)
+    flat, values = _draw_manifest(order, lambda name: seed, ecfg.dtype, threads, std)
+    ws = WeightSet(ecfg, values, order)
+    ws.flat = flat
+    return ws
+
+
+def make_audio(ecfg, slot, seed_base=600):
+    """Synthetic 16 kHz waveform of one request (n_samples long): a few harmonic
+    tones with random fundamentals, a slow amplitude envelope and a little white
+    noise, peak level about 0.3 (fp32)."""
+    rng = np.random.default_rng(seed_base + slot)
+    n = ecfg.n_samples
+    t = np.arange(n) / ecfg.sample_rate
+    x = np.zeros(n)
+    for _ in range(3):
+        f0 = rng.uniform(90.0, 300.0)
+        env = 0.5 + 0.5 * np.sin(2 * np.pi * rng.uniform(0.5, 3.0) * t + rng.uniform(0, 2 * np.pi))
+        for hmn in range(1, 6):
+            x += (0.05 / hmn) * env * np.sin(2 * np.pi * f0 * hmn * t + rng.uniform(0, 2 * np.pi))
+    x += 0.005 * rng.standard_normal(n)
+    return x.astype(np.float32)
+
+
 def make_weights(cfg, seed_target=0, seed_drafter=1, threads=8, std=0.02):
     """All target and drafter parameters for ``cfg``.
 
@@ -92,27 +142,9 @@ def make_weights(cfg, seed_target=0, seed_drafter=1, threads=8, std=0.02):
     parameters and ``seed_drafter`` for drafter parameters.  The draw does
     not depend on the thread count.
     """
-    from concurrent.futures import ThreadPoolExecutor
-
     order = full_manifest(cfg)
-    sizes = [int(np.prod(shape)) for _, shape in order]
-    flat = np.empty(sum(sizes), dtype=np.float32)
-    views, off = [], 0
-    for (name, shape), n in zip(order, sizes):
-        views.append(flat[off:off + n])
-        off += n
-
-    def work(i):
-        name = order[i][0]
-        seed = seed_drafter if _is_drafter(name) else seed_target
-        _fill(views[i], seed, i, name, std)
-        if cfg.dtype == "bf16":
-            _round_inplace(views[i])
-
-    idx = sorted(range(len(order)), key=lambda i: -sizes[i])
-    with ThreadPoolExecutor(max_workers=threads) as ex:
-        list(ex.map(work, idx))
-    values = {name: v.reshape(shape) for (name, shape), v in zip(order, views)}
+    seed_of = lambda name: seed_drafter if _is_drafter(name) else seed_target
+    flat, values = _draw_manifest(order, seed_of, cfg.dtype, threads, std)
     ws = WeightSet(cfg, values, order)
     ws.flat = flat
     return ws

@@ -80,3 +80,22 @@ def param_count(manifest, exclude_prefixes=()):
             k *= s
         n += k
     return n
+
+
+def encoder_manifest(ecfg):
+    """Whisper encoder parameters: the convolution stem (weights [out, in, 3]),
+    n_layer blocks (self-attention without a key bias, GELU MLP) and ln_post."""
+    d, f, m = ecfg.d_model, ecfg.d_ff, ecfg.n_mels
+    out = [("conv1.w", (d, m, 3)), ("conv1.b", (d,)), ("conv2.w", (d, d, 3)), ("conv2.b", (d,))]
+    for l in range(ecfg.n_layer):
+        p = f"e{l}"
+        out += [(f"{p}.attn_ln.g", (d,)), (f"{p}.attn_ln.b", (d,)),
+                (f"{p}.attn.q.w", (d, d)), (f"{p}.attn.q.b", (d,)),
+                (f"{p}.attn.k.w", (d, d)),
+                (f"{p}.attn.v.w", (d, d)), (f"{p}.attn.v.b", (d,)),
+                (f"{p}.attn.o.w", (d, d)), (f"{p}.attn.o.b", (d,)),
+                (f"{p}.mlp_ln.g", (d,)), (f"{p}.mlp_ln.b", (d,)),
+                (f"{p}.mlp.fc1.w", (f, d)), (f"{p}.mlp.fc1.b", (f,)),
+                (f"{p}.mlp.fc2.w", (d, f)), (f"{p}.mlp.fc2.b", (d,))]
+    out += [("ln_post.g", (d,)), ("ln_post.b", (d,))]
+    return out
