@@ -460,6 +460,52 @@ def request_times(cfg, eng, mem, reps=5):
     return out
 
 
+def encoder_flops(ecfg):
+    """Algorithmic FLOPs of one encoder pass: the two convolutions, and per block the
+    q|k|v, output and MLP products plus the two attention products."""
+    n, d, F, m, T = ecfg.n_ctx, ecfg.d_model, ecfg.d_ff, ecfg.n_mels, 2 * ecfg.n_ctx
+    conv = 2.0 * T * 3 * m * d + 2.0 * n * 3 * d * d
+    blk = 2.0 * n * (3 * d * d + d * d + 2 * d * F) + 2 * 2.0 * n * n * d
+    return conv + ecfg.n_layer * blk
+
+
+def encoder_times(dec, log, reps=3):
+    """One 30 s request through the Whisper-large-v3-shaped encoder (waveform ->
+    log-mel -> 32 blocks -> acoustic memory), then its acoustic K/V for every
+    decoder block: the request set-up on the audio side."""
+    import torch
+    from wf_fixtures import LARGE_V3_ENC, make_encoder_weights, make_audio
+    from paper_2609_32869_amd import WhisperEncoder
+    ecfg = LARGE_V3_ENC
+    W = make_encoder_weights(ecfg)
+    enc = WhisperEncoder.from_host(ecfg, [W.values[n] for n, _ in W.order])
+    del W
+    audio = torch.from_numpy(make_audio(ecfg, 0)[None].copy()).cuda()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+    mem = enc.run(audio)
+    dec.encode_memory_set(0, mem)
+    torch.cuda.synchronize()
+    ev[0].record()
+    for _ in range(reps):
+        mem = enc.run(audio)
+    ev[1].record()
+    for _ in range(reps):
+        dec.encode_memory_set(0, mem)
+    ev[2].record()
+    torch.cuda.synchronize()
+    ms = ev[0].elapsed_time(ev[1]) / reps
+    kv_ms = ev[1].elapsed_time(ev[2]) / reps
+    fl = encoder_flops(ecfg)
+    out = {"workload": "whisper-large-v3-shaped encoder, one 30 s request (480000 samples, 128 mel bins, "
+                       "32 blocks, 1500 positions)",
+           "encoder_ms": round(ms, 3), "algorithmic_tflops": round(fl / (ms / 1e3) / 1e12, 1),
+           "frac_of_bf16_peak": round(fl / (ms / 1e3) / 1e12 / MFMA_PEAK_TFLOPS, 4),
+           "waveform_to_acoustic_kv_ms": round(ms + kv_ms, 3)}
+    log(f"[bench] encoder: {out}")
+    enc.close()
+    return out
+
+
 def run_request(args):
     """--request: request set-up timing alone, as one JSON line."""
     log = lambda *a: print(*a, file=sys.stderr, flush=True)
@@ -554,6 +600,7 @@ def b1_workload(args, W, log):
             first_draw = (mem, prompt, plans[:args.warmup + seg[0]])
         log(f"[bench] b1 draw {i}: prefix {lens[i]}, {seg[i]} timed steps")
     request = request_times(cfg, eng, to_device_storage(make_memory(cfg, 0), cfg.dtype)[None])
+    request["encoder"] = encoder_times(eng, log)
     del eng
     torch.cuda.empty_cache()
     return dict(lens=lens, seg=seg, step_ms=np.array(step_ms), tokens=tokens, planted_ok=planted_ok,

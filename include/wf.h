@@ -270,6 +270,64 @@ int wf_rng_words_host(uint64_t seed, int purpose, int slot, int step, int pos, i
 int wf_rng_words_device(uint64_t seed, int purpose, int slot, int step, int pos, int n, uint64_t* out, void* stream);
 const char* wf_last_error(wf_handle* h);
 
+/*
+ * Whisper audio encoder: waveform -> acoustic memory A = E(x), the frozen
+ * encoder output both the target and the drafter cross-attend to (Section 3.2;
+ * it runs once per request over a 30 s window, Section 1).  The paper names the
+ * model only as Whisper large-v3; these are that model's definitions:
+ *  - log-mel frontend: 16 kHz samples, periodic Hann window of n_fft, hop
+ *    samples apart, signal reflect-padded by n_fft / 2, |STFT|^2 with the last
+ *    frame dropped (2 n_ctx frames), triangular filters on the Slaney mel scale
+ *    normalised to unit area, log10 of max(mel, 1e-10), raised to at least
+ *    (maximum - 8), then (x + 4) / 4;
+ *  - stem: conv(n_mels -> d, kernel 3, padding 1) + GELU, conv(d -> d, kernel 3,
+ *    stride 2, padding 1) + GELU, plus the sinusoid position table;
+ *  - n_layer pre-LN blocks: bidirectional self-attention (no key bias, scores
+ *    scaled by 1/8), GELU MLP; then the final LayerNorm.
+ * Storage bf16 (weights, products' inputs); the residual stream, LayerNorm,
+ * softmax, GELU and accumulation are fp32; the frontend is fp64.
+ * Large-v3: n_mels 128, n_ctx 1500, d_model 1280, n_head 20, n_layer 32,
+ * d_ff 5120, n_fft 400, hop 160, sample_rate 16000.
+ */
+typedef struct wf_encoder_config {
+  int32_t n_mels;
+  int32_t n_ctx;       /* output positions; the waveform holds 2 * n_ctx * hop samples */
+  int32_t d_model;     /* 64 * n_head, <= 2048 */
+  int32_t n_head;
+  int32_t n_layer;
+  int32_t d_ff;        /* multiple of 64 */
+  int32_t n_fft;       /* even, <= 512 */
+  int32_t hop;
+  int32_t sample_rate;
+} wf_encoder_config;
+
+typedef struct wf_encoder wf_encoder;
+
+/* Workspace bytes of an encoder handle (one request's activations). */
+int wf_encoder_workspace_bytes(const wf_encoder_config* cfg, size_t* bytes);
+/* Number of parameter tensors and the element count of tensor i, in manifest
+ * order: conv1.w [d, n_mels, 3] conv1.b [d] conv2.w [d, d, 3] conv2.b [d]; per
+ * block: attn_ln.g/b [d]; attn.q.w [d,d] attn.q.b; attn.k.w; attn.v.w attn.v.b;
+ * attn.o.w attn.o.b; mlp_ln.g/b; mlp.fc1.w [d_ff,d] mlp.fc1.b; mlp.fc2.w [d,d_ff]
+ * mlp.fc2.b; then ln_post.g/b. */
+int wf_encoder_weight_count(const wf_encoder_config* cfg, int* n);
+int wf_encoder_weight_numel(const wf_encoder_config* cfg, int i, int64_t* numel);
+/* Create an encoder over `workspace` (device, 256-byte aligned, >= the bytes
+ * above) and copy the bf16 parameters (device pointers in manifest order) into
+ * it; the caller's tensors may be freed once `stream` has synchronised.
+ * Errors: WF_EINVAL, WF_ESIZE, WF_EHIP. */
+int wf_encoder_init(wf_encoder** e, const wf_encoder_config* cfg, const void* const* weights, int n_weights,
+                    void* workspace, size_t ws_bytes, void* stream);
+/* Encode n waveforms: audio device fp32 [n, 2 * n_ctx * hop]; mem device bf16
+ * [n, n_ctx, d_model] (16-byte aligned), ready for wf_encode_memory_set.
+ * Requests run one after another on `stream`. */
+int wf_encoder_run(wf_encoder* e, int n, const float* audio, void* mem, void* stream);
+/* The frontend alone: scaled log-mel features of one waveform into mel, device
+ * fp32 [n_mels, 2 * n_ctx]. */
+int wf_encoder_logmel(wf_encoder* e, const float* audio, float* mel, void* stream);
+int wf_encoder_release(wf_encoder* e);
+const char* wf_encoder_last_error(wf_encoder* e);
+
 #ifdef __cplusplus
 }
 #endif

@@ -24,7 +24,9 @@ WF_STATUS_POSITION_OVERFLOW = 0x2
 EXPORTS = ["wf_workspace_bytes", "wf_weight_count", "wf_weight_numel", "wf_init_weights",
            "wf_encode_memory_set", "wf_prefill", "wf_set_sampling", "wf_draft", "wf_verify_accept",
            "wf_step", "wf_step_noalloc", "wf_debug_ptr", "wf_set_debug", "wf_profile_enable", "wf_profile_summary", "wf_status",
-           "wf_release", "wf_strerror", "wf_last_error", "wf_rng_words_host", "wf_rng_words_device"]
+           "wf_release", "wf_strerror", "wf_last_error", "wf_rng_words_host", "wf_rng_words_device",
+           "wf_encoder_workspace_bytes", "wf_encoder_weight_count", "wf_encoder_weight_numel", "wf_encoder_init",
+           "wf_encoder_run", "wf_encoder_logmel", "wf_encoder_release", "wf_encoder_last_error"]
 
 
 class WfConfig(ctypes.Structure):
@@ -33,6 +35,12 @@ class WfConfig(ctypes.Structure):
                 ("n_frames", ctypes.c_int32), ("n_draft_layer", ctypes.c_int32), ("block_k", ctypes.c_int32),
                 ("n_tap", ctypes.c_int32), ("taps", ctypes.c_int32 * WF_MAX_TAPS), ("eos_id", ctypes.c_int32),
                 ("dtype", ctypes.c_int32), ("max_batch", ctypes.c_int32), ("draft_flags", ctypes.c_int32)]
+
+
+class WfEncoderConfig(ctypes.Structure):
+    _fields_ = [("n_mels", ctypes.c_int32), ("n_ctx", ctypes.c_int32), ("d_model", ctypes.c_int32),
+                ("n_head", ctypes.c_int32), ("n_layer", ctypes.c_int32), ("d_ff", ctypes.c_int32),
+                ("n_fft", ctypes.c_int32), ("hop", ctypes.c_int32), ("sample_rate", ctypes.c_int32)]
 
 
 class WfError(RuntimeError):
@@ -74,11 +82,19 @@ def load_library(path=LIB_PATH):
         "wf_last_error": [P],
         "wf_rng_words_host": [U64, I, I, I, I, I, ctypes.POINTER(U64)],
         "wf_rng_words_device": [U64, I, I, I, I, I, P, P],
+        "wf_encoder_workspace_bytes": [ctypes.POINTER(WfEncoderConfig), ctypes.POINTER(Z)],
+        "wf_encoder_weight_count": [ctypes.POINTER(WfEncoderConfig), ctypes.POINTER(I)],
+        "wf_encoder_weight_numel": [ctypes.POINTER(WfEncoderConfig), I, ctypes.POINTER(ctypes.c_int64)],
+        "wf_encoder_init": [ctypes.POINTER(P), ctypes.POINTER(WfEncoderConfig), ctypes.POINTER(P), I, P, Z, P],
+        "wf_encoder_run": [P, I, P, P, P],
+        "wf_encoder_logmel": [P, P, P, P],
+        "wf_encoder_release": [P],
+        "wf_encoder_last_error": [P],
     }
     for name, args in sig.items():
         fn = getattr(lib, name)
         fn.argtypes = args
-        fn.restype = ctypes.c_char_p if name in ("wf_strerror", "wf_last_error") else ctypes.c_int
+        fn.restype = ctypes.c_char_p if name in ("wf_strerror", "wf_last_error", "wf_encoder_last_error") else ctypes.c_int
     _lib = lib
     return lib
 
@@ -271,3 +287,70 @@ class WhisperFlash:
         f = ctypes.c_uint32()
         self._check(self.lib.wf_status(self.h, ctypes.byref(f), _stream(stream)))
         return f.value
+
+
+def make_encoder_config(ecfg):
+    """WfEncoderConfig from an encoder-shape object (attributes as in wf_fixtures.EncoderConfig)."""
+    c = WfEncoderConfig()
+    c.n_mels, c.n_ctx, c.d_model, c.n_head = ecfg.n_mels, ecfg.n_ctx, ecfg.d_model, ecfg.n_head
+    c.n_layer, c.d_ff, c.n_fft, c.hop, c.sample_rate = ecfg.n_layer, ecfg.d_ff, ecfg.n_fft, ecfg.hop, ecfg.sample_rate
+    return c
+
+
+class WhisperEncoder:
+    """One libwf encoder handle over a workspace tensor it owns (bf16 weights)."""
+
+    def __init__(self, ecfg, weights, stream=None):
+        self.lib = load_library()
+        self.cfg = ecfg
+        self.ccfg = make_encoder_config(ecfg)
+        nbytes = ctypes.c_size_t()
+        self._check(self.lib.wf_encoder_workspace_bytes(ctypes.byref(self.ccfg), ctypes.byref(nbytes)))
+        self.ws = torch.empty(nbytes.value, dtype=torch.uint8, device="cuda")
+        n = ctypes.c_int()
+        self._check(self.lib.wf_encoder_weight_count(ctypes.byref(self.ccfg), ctypes.byref(n)))
+        if len(weights) != n.value:
+            raise WfError(f"expected {n.value} encoder weight tensors, got {len(weights)}")
+        arr = (ctypes.c_void_p * n.value)(*[w.data_ptr() for w in weights])
+        h = ctypes.c_void_p()
+        self._check(self.lib.wf_encoder_init(ctypes.byref(h), ctypes.byref(self.ccfg), arr, n.value,
+                                             ctypes.c_void_p(self.ws.data_ptr()), nbytes.value, _stream(stream)))
+        self.h = h
+
+    @classmethod
+    def from_host(cls, ecfg, ordered_arrays, stream=None):
+        dev = [to_device_storage(a, "bf16") for a in ordered_arrays]
+        obj = cls(ecfg, dev, stream)
+        torch.cuda.synchronize()
+        del dev
+        return obj
+
+    def _check(self, rc):
+        if rc != 0:
+            h = getattr(self, "h", None)
+            msg = self.lib.wf_encoder_last_error(h if h is not None else None)
+            raise WfError(f"{self.lib.wf_strerror(rc).decode()} ({rc}): {msg.decode() if msg else ''}")
+
+    def run(self, audio, stream=None):
+        """audio: device fp32 [n, n_samples] -> acoustic memory, device bf16 [n, n_ctx, d]."""
+        n = audio.shape[0]
+        mem = torch.empty((n, self.cfg.n_ctx, self.cfg.d_model), dtype=torch.bfloat16, device="cuda")
+        self._check(self.lib.wf_encoder_run(self.h, n, _ptr(audio), _ptr(mem), _stream(stream)))
+        return mem
+
+    def logmel(self, audio, stream=None):
+        """audio: device fp32 [n_samples] -> scaled log-mel features, device fp32 [n_mels, frames]."""
+        mel = torch.empty((self.cfg.n_mels, 2 * self.cfg.n_ctx), dtype=torch.float32, device="cuda")
+        self._check(self.lib.wf_encoder_logmel(self.h, _ptr(audio), _ptr(mel), _stream(stream)))
+        return mel
+
+    def close(self):
+        if getattr(self, "h", None) is not None:
+            self.lib.wf_encoder_release(self.h)
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

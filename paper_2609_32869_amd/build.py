@@ -8,7 +8,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libwf.so")
 OBJDIR = os.path.join(os.path.dirname(HERE), "_build")
-SOURCES = ["k_gemv.hip", "k_attn.hip", "k_misc.hip", "k_mm.hip", "wf_api.hip"]
+SOURCES = ["k_gemv.hip", "k_attn.hip", "k_misc.hip", "k_mm.hip", "k_enc.hip", "wf_api.hip", "enc_api.hip"]
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",
          # packed fp32 arithmetic is kept out of every kernel
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",

@@ -61,7 +61,7 @@ __global__ void __launch_bounds__(NT) k_mm(MmArgs a) {
   for (int j = 0; j < 4; ++j) {
     const int row = r0 + 32 * j;
     oa[j] = min(m0 + row, a.M - 1) * (int)(a.lda >> 3);
-    ob[j] = min(n0 + row, a.N - 1) * (int)(a.ldb >> 3);
+    ob[j] = min(n0 + row, (a.nb > 0 ? a.nb : a.N) - 1) * (int)(a.ldb >> 3);
     so[j] = row * 8 + (q ^ (row & 7));
   }
   const int nk = a.K / BK;
@@ -204,6 +204,13 @@ __global__ void __launch_bounds__(NT) k_mm(MmArgs a) {
     } else {
       float* out = reinterpret_cast<float*>(a.out) + (size_t)z * a.sO + (size_t)f * a.ldo + n;
       float4 lo = make_float4(src[0], src[1], src[2], src[3]), hi = make_float4(src[4], src[5], src[6], src[7]);
+      if (EP == MM_GELU_ADD_F32) {
+        const float* ad = a.add + (size_t)f * a.ldadd + n;
+        lo.x = gelu_erf(lo.x) + ad[0]; lo.y = gelu_erf(lo.y) + ad[1];
+        lo.z = gelu_erf(lo.z) + ad[2]; lo.w = gelu_erf(lo.w) + ad[3];
+        hi.x = gelu_erf(hi.x) + ad[4]; hi.y = gelu_erf(hi.y) + ad[5];
+        hi.z = gelu_erf(hi.z) + ad[6]; hi.w = gelu_erf(hi.w) + ad[7];
+      }
       if (EP == MM_RESID) {  // residual rows: each element has exactly one writer
         const float4 o0 = *reinterpret_cast<const float4*>(out), o1 = *reinterpret_cast<const float4*>(out + 4);
         lo.x += o0.x; lo.y += o0.y; lo.z += o0.z; lo.w += o0.w;
@@ -221,7 +228,10 @@ __global__ void __launch_bounds__(NT) k_mm(MmArgs a) {
 int mm_check(const MmArgs& a, int ep) {
   if (a.M < 1 || a.N < 1 || a.K < kMmK || a.K % kMmK) return -1;
   if (a.N % 8 || a.lda % 8 || a.ldb % 8 || a.lda < a.K || a.ldb < a.K) return -1;
-  if ((ep == MM_BF16 || ep == MM_BF16_GELU || ep == MM_F32 || ep == MM_RESID) && (a.ldo % 8 || a.ldo < a.N)) return -1;
+  if ((ep == MM_BF16 || ep == MM_BF16_GELU || ep == MM_F32 || ep == MM_RESID || ep == MM_GELU_ADD_F32) &&
+      (a.ldo % 8 || a.ldo < a.N))
+    return -1;
+  if (ep == MM_GELU_ADD_F32 && (!a.add || a.ldadd < a.N)) return -1;
   if (ep == MM_XKV && (a.N != 2 * a.d || a.d % kHeadDim || a.vt_frames < a.M || a.vt_frames % kVtPiece)) return -1;
   if (ep == MM_QKV_ENC && (a.N != 3 * a.d || a.d % kHeadDim || a.vt_frames < a.M || a.vt_frames % 8 || a.ldo % 8 ||
                            a.ldo < 2 * a.d))
@@ -239,6 +249,7 @@ void mm(const MmArgs& a, int ep, int batch, hipStream_t st) {
     case MM_RESID: k_mm<MM_RESID><<<grid, NT, 0, st>>>(a); break;
     case MM_XKV: k_mm<MM_XKV><<<grid, NT, 0, st>>>(a); break;
     case MM_QKV_ENC: k_mm<MM_QKV_ENC><<<grid, NT, 0, st>>>(a); break;
+    case MM_GELU_ADD_F32: k_mm<MM_GELU_ADD_F32><<<grid, NT, 0, st>>>(a); break;
   }
 }
 

@@ -251,6 +251,7 @@ enum {
   MM_RESID = 3,      // out fp32 [M][ldo] += scale * C + bias
   MM_XKV = 4,        // acoustic keys [head][frame][64] then values [head][frame / 256][dim][256]
   MM_QKV_ENC = 5,    // columns < 2d: out bf16 [M][ldo]; the rest: out2 bf16 [head][dim][vt_frames]
+  MM_GELU_ADD_F32 = 6,  // out fp32 [M][ldo] = GELU(scale * C + bias) + add[M][ldadd]
 };
 struct MmArgs {
   const bf16* A;
@@ -266,9 +267,33 @@ struct MmArgs {
   long long sO2;
   int d, n_head, vt_frames;  // transposed epilogues: model width, heads, padded frame count
   float scale;
+  const float* add;  // MM_GELU_ADD_F32: fp32 rows added after the activation
+  long long ldadd;
+  int nb;            // rows of B present (0: N); columns past them re-read its last row
 };
 int mm_check(const MmArgs& a, int ep);
 void mm(const MmArgs& a, int ep, int batch, hipStream_t st);
+
+// Audio encoder (k_enc.hip).  Largest frontend window, model width and output
+// positions the kernels hold in registers / LDS.
+constexpr int kMaxFft = 512, kMaxEncD = 2048, kMaxEncCtx = 2048;
+struct LogmelArgs {
+  const float* audio;     // [n_samples] fp32
+  int n_samples, n_fft, hop, n_frames, n_mels;
+  const double* window;   // [n_fft] periodic Hann
+  const double* twiddle;  // [n_fft][2]: cos(2 pi i / n_fft), -sin(2 pi i / n_fft)
+  const double* filters;  // [n_mels][n_fft / 2 + 1] mel filterbank
+  const int* fband;       // [n_mels][2]: first and one-past-last nonzero bin of each filter
+  float* logmel;          // [n_frames][n_mels] log10 values
+  int* gmax;              // the request's largest log10 value (order-preserving int)
+  bf16* rows;             // [n_frames][ld1] first-convolution rows
+  int ld1;
+  float* mel_out;         // [n_mels][n_frames] scaled features, or null
+};
+void logmel(const LogmelArgs& a, hipStream_t st);
+void conv_rows_s2(const bf16* z, bf16* out, int n_in, int n_out, int d, hipStream_t st);
+void ln_rows(const float* x, const bf16* g, const bf16* b, bf16* out, int rows, int d, long long ldo, hipStream_t st);
+void softmax_rows(const float* s, bf16* p, int rows, int n, int ld, hipStream_t st);
 
 template <typename S>
 struct Ops {
