@@ -26,12 +26,12 @@ struct EncLayer {
 };
 
 struct EncLayout {
-  int T, Tp, Np, Kp1, nb;  // mel frames, padded positions, score columns, first-conv row length, FFT bins
+  int T, Tp, Kp1, nb;  // mel frames, positions padded to 64, first-conv row length, FFT bins
   // bf16 weight element offsets
   size_t conv1, conv1_b, conv2, conv2_b, lnp_g, lnp_b, wtotal;
   std::vector<EncLayer> layers;
   // byte offsets
-  size_t weights, pos, window, twiddle, filters, fband, gmax, logmel, rows1, z, rows2, x, a, qk, vt, s, p, o, u, total;
+  size_t weights, pos, window, twiddle, filters, fband, gmax, logmel, rows1, z, rows2, x, a, qk, vt, o, u, total;
 };
 
 struct Enc {
@@ -71,7 +71,6 @@ void layout(const wf_encoder_config& c, EncLayout& L) {
   const size_t d = c.d_model, F = c.d_ff;
   L.T = 2 * c.n_ctx;
   L.Tp = (int)up(c.n_ctx, 64);
-  L.Np = (int)up(c.n_ctx, 8);
   L.Kp1 = (int)up(3 * (size_t)c.n_mels, kMmK);
   L.nb = c.n_fft / 2 + 1;
   size_t w = 0;
@@ -109,8 +108,6 @@ void layout(const wf_encoder_config& c, EncLayout& L) {
   L.a = region(n * d * 2);
   L.qk = region(n * 2 * d * 2);
   L.vt = region(H * kHeadDim * L.Tp * 2);
-  L.s = region(H * n * L.Tp * 4);
-  L.p = region(H * n * L.Tp * 2);
   L.o = region(n * d * 2);
   L.u = region(n * F * 2);
   L.total = o;
@@ -315,8 +312,8 @@ static void enc_forward(Enc& e, const float* audio, bf16* mem, hipStream_t st) {
   const int d = c.d_model, F = c.d_ff, H = c.n_head, n = c.n_ctx;
   enc_frontend(e, audio, nullptr, st);
   bf16 *z = e.at<bf16>(L.z), *rows2 = e.at<bf16>(L.rows2), *a = e.at<bf16>(L.a), *qk = e.at<bf16>(L.qk);
-  bf16 *vt = e.at<bf16>(L.vt), *p = e.at<bf16>(L.p), *o = e.at<bf16>(L.o), *u = e.at<bf16>(L.u);
-  float *x = e.at<float>(L.x), *s = e.at<float>(L.s);
+  bf16 *vt = e.at<bf16>(L.vt), *o = e.at<bf16>(L.o), *u = e.at<bf16>(L.u);
+  float* x = e.at<float>(L.x);
   // stem: conv1 + GELU, conv2 (stride 2) + GELU + positions
   mm(mm_args(e.at<bf16>(L.rows1), L.Kp1, e.W(L.conv1), L.Kp1, e.W(L.conv1_b), L.T, d, L.Kp1, z, d), MM_BF16_GELU, 1, st);
   conv_rows_s2(z, rows2, L.T, n, d, st);
@@ -336,21 +333,10 @@ static void enc_forward(Enc& e, const float* audio, bf16* mem, hipStream_t st) {
       m.vt_frames = L.Tp;
       mm(m, MM_QKV_ENC, 1, st);
     }
-    {  // scores / 8 per head
-      MmArgs m = mm_args(qk, 2 * d, qk + d, 2 * d, nullptr, n, L.Np, kHeadDim, s, L.Tp);
-      m.sA = m.sB = kHeadDim;
-      m.sO = (long long)n * L.Tp;
-      m.nb = n;  // the keys of the n positions (columns n..Np-1 are ignored by the softmax)
-      m.scale = 0.125f;
-      mm(m, MM_F32, H, st);
-    }
-    softmax_rows(s, p, H * n, n, L.Tp, st);
-    {  // probabilities x values per head, into the head's 64 columns
-      MmArgs m = mm_args(p, L.Tp, vt, L.Tp, nullptr, n, kHeadDim, L.Tp, o, d);
-      m.sA = (long long)n * L.Tp;
-      m.sB = (long long)kHeadDim * L.Tp;
-      m.sO = kHeadDim;
-      mm(m, MM_BF16, H, st);
+    {  // softmax(q k^T / 8) v per head, fused (scores stay on chip)
+      EncAttnArgs at{};
+      at.qk = qk; at.ldqk = 2 * d; at.vt = vt; at.Tp = L.Tp; at.o = o; at.ldo = d; at.n = n; at.d = d;
+      enc_attention(at, H, st);
     }
     mm(mm_args(o, d, e.W(w.wo), d, e.W(w.bo), n, d, d, x, d), MM_RESID, 1, st);
     ln_rows(x, e.W(w.ln2_g), e.W(w.ln2_b), a, n, d, d, st);

@@ -293,7 +293,18 @@ struct LogmelArgs {
 void logmel(const LogmelArgs& a, hipStream_t st);
 void conv_rows_s2(const bf16* z, bf16* out, int n_in, int n_out, int d, hipStream_t st);
 void ln_rows(const float* x, const bf16* g, const bf16* b, bf16* out, int rows, int d, long long ldo, hipStream_t st);
-void softmax_rows(const float* s, bf16* p, int rows, int n, int ld, hipStream_t st);
+// fused bidirectional attention of the encoder: q | k rows [n][ldqk] (q at column
+// head * 64, k at d + head * 64), values transposed per head [head][64][Tp] (zero
+// past n), output rows [n][ldo] at column head * 64; Tp a multiple of 64
+struct EncAttnArgs {
+  const bf16* qk;
+  int ldqk;
+  const bf16* vt;
+  int Tp;
+  bf16* o;
+  int ldo, n, d;
+};
+void enc_attention(const EncAttnArgs& a, int n_head, hipStream_t st);
 
 template <typename S>
 struct Ops {
