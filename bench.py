@@ -511,6 +511,7 @@ def run_request(args):
     log = lambda *a: print(*a, file=sys.stderr, flush=True)
     cfg, eng, mem, L0, toks = _b1_engine(log)
     out = {"measure": "request set-up", **request_times(cfg, eng, mem)}
+    out["encoder"] = encoder_times(eng, log)
     out["config"] = {"workload": "whisper-large-v3-shaped encode of one 1500-frame memory (32 target + 2 drafter "
                                  "blocks) and prefill of one prompt", "storage": "bf16"}
     log(f"[bench] {out}")

@@ -222,6 +222,26 @@ __device__ __forceinline__ void finish_tile(const GemvArgs& a, float (*sv)[TC + 
         if (act) epi_one<S, EPI>(a, row, n, v, pv.r[it]);
       }
     }
+  } else if (EPI == EPI_GELU && TC % 8 == 0 && a.N % 8 == 0) {
+    // GELU into the next product's operand: an item is 8 consecutive columns of
+    // one row, contiguous in every operand order, so each split term is one
+    // 16-byte store (scalar stores would write 2 bytes per lane)
+    constexpr int NI = TM * TC / 8, PI = (NI + NT - 1) / NT;
+#pragma unroll
+    for (int it = 0; it < PI; ++it) {
+      const int item = threadIdx.x + it * NT;
+      const int ml = item / (TC / 8), c8 = 8 * (item % (TC / 8)), row = m0 + ml, n = nb + c8;
+      if (item >= NI || row < R || row >= Rend || n >= a.N) continue;
+      float b8[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+      if (a.bias != nullptr) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) b8[e] = to_f(reinterpret_cast<const S*>(a.bias)[n + e]);
+      }
+      float v[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[e] = gelu_erf(sv[ml][c8 + e] + b8[e]);
+      put_op8<S>(a.aout, a.nsplit, a.R9, row, n, v);
+    }
   } else {
     // Every global load of the epilogue is issued before any result is formed, and
     // unconditionally (indexes clamped into the buffers, unused values discarded),
