@@ -778,6 +778,151 @@ __global__ void __launch_bounds__(256) k_gemm16s(GemvArgs a, int mb0, int nmb, i
   finish_tile<bf16, EPI, 64, 64, 256, true>(a, sv, ov, oz, (mb0 + mbk) * 64, nbk * 64, pre, rp);
 }
 
+// ---------------------------------------------------------------- several slots, wide tiles
+// Products of many slots' rows (hundreds of rows) on v_mfma_f32_32x32x16_bf16,
+// which issues twice the work per cycle of the 16x16x32 form here.  The data keep
+// their 16x32 fragment order: the 32x32x16 operand of lane l is row l % 32 of a
+// 32-row tile and k chunk 2 s + l / 32 of k-substep s, i.e. lane (l % 16) + 16 (2 s +
+// l / 32) of 16-row fragment 2 j + (l % 32) / 16, so every load is 16 bytes from a
+// 256-byte run.  Block tile 64 rows x 32 CN columns, four independent waves of 32 x
+// 16 CN (no LDS in the main loop, no barrier): each wave loads its own operand and
+// weight fragments straight into registers kWideD k-steps ahead (about 160 KB in
+// flight per CU; LDS-staged copies behind a barrier per k-step stayed latency-bound
+// at a third of that).  XCD x takes row half x & 1 and column quarter x >> 1, so the
+// blocks sharing an L2 share their operand rows and weight columns.  The finished
+// tile is staged in LDS and written 8 consecutive columns per item (16-byte stores).
+constexpr int kWideD = 4;             // k-steps in flight per wave (the k-step count must be a multiple)
+constexpr int kWideMinRowBlocks = 8;  // 64-row blocks from which the wide kernel is used (about 57 slots)
+constexpr int kWideMaxCN = 10;        // widest tile: 32 kWideMaxCN columns
+
+__host__ __device__ __forceinline__ unsigned wide_grid(int nmb, int nnb) {
+  return 8u * ((nmb + 1) / 2) * ((nnb + 3) / 4);
+}
+
+template <int EPI, int CN>
+__global__ void __launch_bounds__(256) k_gemm32r(GemvArgs a, int mb0, int nmb, int nnb) {
+  static_assert(CN <= kWideMaxCN && CN % 2 == 0, "tile width");
+  StampScope stamp_scope(a.stamp, 256);
+  constexpr int WCT = CN / 2, TC = 32 * CN;
+  __shared__ float sv[64][TC + 1];  // the finished tile
+  int mbk, nbk;
+  {
+    const int x = blockIdx.x & 7, i = blockIdx.x >> 3;
+    const int nrh = (nmb + 1) / 2, ncq = (nnb + 3) / 4;
+    mbk = (x & 1) * nrh + i % nrh;
+    nbk = (x >> 1) * ncq + i / nrh;
+    if (i >= nrh * ncq || mbk >= nmb || nbk >= nnb) return;
+  }
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6, wm = wv >> 1, wn = wv & 1;
+  const int KS = a.K / 32, MT = a.a.mt, ntile = (a.N + 15) / 16;
+  const size_t plane = (size_t)MT * KS * 64;
+  const int r32 = lane & 31, kh = lane >> 5, fsub = r32 >> 4, fl = (r32 & 15) + 16 * kh;
+  // rows and columns past the data re-read the last tile; their results are not written
+  const int mt = min((mb0 + mbk) * 4 + 2 * wm + fsub, MT - 1);
+  const bf16x8* pa = reinterpret_cast<const bf16x8*>(a.a.p) + (size_t)mt * 64 + fl;
+  const bf16x8* pb[WCT];
+#pragma unroll
+  for (int q = 0; q < WCT; ++q)
+    pb[q] = reinterpret_cast<const bf16x8*>(a.w) + (size_t)min(2 * (nbk * CN + wn * WCT + q) + fsub, ntile - 1) * KS * 64 + fl;
+  struct Frag {
+    bf16x8 a[2][2], w[2][WCT];  // [k-substep][plane], [k-substep][column tile]
+  };
+  auto ld = [&](int st, Frag& f) {
+    const size_t ss = (size_t)min(st, KS - 1);
+#pragma unroll
+    for (int sub = 0; sub < 2; ++sub) {
+#pragma unroll
+      for (int h = 0; h < 2; ++h) f.a[sub][h] = pa[h * plane + ss * MT * 64 + 32 * sub];
+#pragma unroll
+      for (int q = 0; q < WCT; ++q) f.w[sub][q] = pb[q][ss * 64 + 32 * sub];
+    }
+  };
+  floatx16 acc[WCT];
+#pragma unroll
+  for (int q = 0; q < WCT; ++q)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) acc[q][v] = 0.f;
+  auto mul = [&](const Frag& f) {
+#pragma unroll
+    for (int sub = 0; sub < 2; ++sub)
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+#pragma unroll
+        for (int q = 0; q < WCT; ++q) acc[q] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a[sub][h], f.w[sub][q], acc[q], 0, 0, 0);
+  };
+  // Each step multiplies the fragments loaded kWideD steps earlier and reloads their
+  // registers kWideD steps ahead (past the end: the last k-step again, unused); the
+  // scheduling barriers keep every load where it is issued (the scheduler otherwise
+  // moves loads next to their use to shorten register lifetimes).
+  Frag fr[kWideD];
+#pragma unroll
+  for (int d = 0; d < kWideD; ++d) ld(d, fr[d]);
+  __builtin_amdgcn_sched_barrier(0);
+  for (int st = 0; st < KS; st += kWideD) {
+#pragma unroll
+    for (int d = 0; d < kWideD; ++d) {
+      mul(fr[d]);
+      __builtin_amdgcn_sched_barrier(0);
+      ld(st + d + kWideD, fr[d]);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  }
+  // accumulator v of 32 x 32 tile q: row 8 (v / 4) + 4 (lane / 32) + v % 4, column lane % 32
+#pragma unroll
+  for (int q = 0; q < WCT; ++q)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) sv[wm * 32 + 8 * (v >> 2) + 4 * kh + (v & 3)][(wn * WCT + q) * 32 + r32] = acc[q][v];
+  __syncthreads();
+  // epilogue items: 8 consecutive columns of one row
+  const int m0 = (mb0 + mbk) * 64, n0 = nbk * TC;
+  const int R = a.slot0 * kRows, Rend = (a.slot0 + a.nslots) * kRows;
+  const uint4* bias8 = reinterpret_cast<const uint4*>(a.bias);
+  for (int item = threadIdx.x; item < 64 * (TC / 8); item += 256) {
+    const int ml = item / (TC / 8), c8 = 8 * (item % (TC / 8)), row = m0 + ml, n = n0 + c8;
+    if (row < R || row >= Rend || n >= a.N) continue;
+    float v[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[e] = sv[ml][c8 + e];
+    if (bias8 != nullptr) {
+      const uint4 bb = bias8[n / 8];
+      const uint32_t bw[4] = {bb.x, bb.y, bb.z, bb.w};
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[e] += __uint_as_float(e & 1 ? bw[e >> 1] & 0xffff0000u : bw[e >> 1] << 16);
+    }
+    if constexpr (EPI == EPI_GELU) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[e] = gelu_erf(v[e]);
+      put_op8<bf16>(a.aout, a.nsplit, a.R9, row, n, v);
+    } else if constexpr (EPI == EPI_STORE) {
+      float4* y = reinterpret_cast<float4*>(a.y + (size_t)row * a.ldy + n);
+      y[0] = make_float4(v[0], v[1], v[2], v[3]);
+      y[1] = make_float4(v[4], v[5], v[6], v[7]);
+    } else if constexpr (EPI == EPI_RESID) {
+      float4* y = reinterpret_cast<float4*>(a.y + (size_t)row * a.ldy + n);
+      const float4 r0 = y[0], r1 = y[1];
+      v[0] += r0.x; v[1] += r0.y; v[2] += r0.z; v[3] += r0.w;
+      v[4] += r1.x; v[5] += r1.y; v[6] += r1.z; v[7] += r1.w;
+      y[0] = make_float4(v[0], v[1], v[2], v[3]);
+      y[1] = make_float4(v[4], v[5], v[6], v[7]);
+      if (a.tap >= 0) put_op8<bf16>(a.aout, a.nsplit, a.R9, row, a.tap * a.N + n, v);
+    } else if constexpr (EPI == EPI_QKV) {
+      if (n < a.d) {
+        float4* y = reinterpret_cast<float4*>(a.y + (size_t)row * a.ldy + n);
+        y[0] = make_float4(v[0], v[1], v[2], v[3]);
+        y[1] = make_float4(v[4], v[5], v[6], v[7]);
+      } else {
+        const int* st = a.state + (row / kRows) * kStateInts;
+        const int r = row - (row / kRows) * kRows, pos0 = st[ST_POS0];
+        const int page = (pos0 & 15) + r >= 16 ? st[ST_PG1] : st[ST_PG0];
+        if (r < st[ST_NV] && pos0 + r < a.n_ctx) {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) qkv_append<bf16>(a, n + e, v[e], page, pos0 + r);
+        }
+      }
+    }
+  }
+}
+
 // ---------------------------------------------------------------- bf16, 32-column tiles
 template <int EPI, int NW>
 __global__ void __launch_bounds__(NW * 64) k_gemv32(GemvArgs a) {
@@ -1367,6 +1512,21 @@ static void launch_epi(const GemvArgs& a, hipStream_t st) {
     if (a.nsplit == 2 && a.wkind == W_F16) {  // several slots: 64 x 64 GEMM tiles (k split over grid y)
       const int mb0 = a.slot0 * kRows / 64, mb1 = ((a.slot0 + a.nslots) * kRows + 63) / 64;
       const int nmb = mb1 - mb0, nnb = (a.N + 63) / 64;
+      if constexpr (EPI == EPI_STORE || EPI == EPI_GELU || EPI == EPI_RESID || EPI == EPI_QKV) {
+        // many rows: wide tiles on the 32x32x16 matrix instruction
+        if (ks == 1 && nmb >= kWideMinRowBlocks && (a.K / 32) % kWideD == 0 && a.N % 8 == 0 && a.a.kind == OP_F16) {
+          if (a.N % 320 == 0 && a.N / 320 >= 16) {
+            k_gemm32r<EPI, 10><<<wide_grid(nmb, a.N / 320), 256, 0, st>>>(a, mb0, nmb, a.N / 320);
+            return;
+          }
+          if (a.N % 256 == 0 && a.N >= 2560) {
+            k_gemm32r<EPI, 8><<<wide_grid(nmb, a.N / 256), 256, 0, st>>>(a, mb0, nmb, a.N / 256);
+            return;
+          }
+          // narrower products (1280 columns at 96 slots) measured slower in this kernel
+          // (128-column tiles: 33 against 17.5 us per launch) and keep the 64 x 64 tiles
+        }
+      }
       // LDS-staged fragments once the launch has enough blocks to cover the
       // chip; with fewer, the per-k-step barrier costs more than the halved loads
       // save (measured: 72-240 blocks at 16 slots 12-15% slower, 280+ at 96

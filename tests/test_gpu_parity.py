@@ -162,6 +162,32 @@ def test_micro_bf16_b3_two_plane_operands():
 
 
 @pytest.mark.timeout(900)
+def test_micro_bf16_b64_wide_tiles():
+    """64 slots (576 rows, nine 64-row blocks), bf16, d 1024 (16 heads), FFN 2560:
+    the q|k|v (3072 columns, k/v appended to the paged cache), first MLP (2560
+    columns, GELU into the next operand) and drafter q|k|v products take the
+    wide-tile kernel on the 32x32x16 matrix instruction (operand rows read from
+    16x32 fragment order); ragged prompts, planted drafts on six followed slots."""
+    from lockstep import Lockstep
+    cfg = MICRO_BF16.with_(name="micro-wide", d_model=1024, n_head=16, d_ff=2560)
+    W = make_weights(cfg)
+    n = 64
+    lens = [int(x) for x in make_prefix_lengths(n, 1, 40, seed=301)]
+    prompts = [make_prefix(cfg, s, lens[s]) for s in range(n)]
+    check = [0, 9, 31, 32, 50, 63]
+    opts = OracleOpts(dtype=np.float32, kv_bf16=True)
+    ls = Lockstep(cfg, W, prompts, [30] * n, TOL_MICRO_BF16, opts=opts, check=check)
+    refs = {i: plain_greedy(ls.T, make_memory(cfg, i), prompts[i], 30) for i in check}
+    rng = np.random.default_rng(7)
+    for _ in range(5):
+        ls.step(override=_planted_subset(ls, refs, rng))
+    print(f"micro-wide b64: max |dlogit| draft {ls.max_dlogit:.3e} target {ls.max_tlogit:.3e}, "
+          f"accepted {ls.accepted}, near ties {ls.near_ties}")
+    assert ls.steps == 5 and max(ls.accepted) > 0
+    ls.close()
+
+
+@pytest.mark.timeout(900)
 # Several slots over many frames: bf16 cross-attention splits the frames into
 # chunks of 256 (997 = 3 x 256 + 229: the last chunk ends inside a 16-frame
 # score tile and inside an 8-frame value group, read from the zero padding of
