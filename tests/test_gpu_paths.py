@@ -9,6 +9,8 @@ C ABI) against the oracle.
     batch 1 (the step the benchmark times), compared with the oracle on every
     step: draft and target logits, drafted tokens, emitted tokens, accepted
     counts and the done flag;
+  * verification budgets k_max below K (micro shapes, and the graph-replayed step
+    at large-v3 shapes);
   * a verify pass reaching the last context position at large-v3 shapes;
   * GPU speculative greedy decoding equals GPU plain greedy decoding over 200
     tokens at large-v3 shapes (Section 3.1: speculation keeps greedy's output).
@@ -170,6 +172,63 @@ def test_large_v3_b1_graph_step_planted_matches_oracle(side_stream):
     print(f"large-v3 graph step: accepted {accepted}; max |dlogit| draft {ls.max_dlogit:.2e} "
           f"target {ls.max_tlogit:.2e}; near ties {ls.near_ties}", flush=True)
     assert len(accepted) >= 16 and max(accepted) == cfg.block_k
+    ls.close()
+
+
+@pytest.mark.parametrize("cfg,tol", [(MICRO, TOL_F32), (MICRO_BF16, 2e-3)], ids=["f32", "bf16"])
+def test_verification_budget_sweep(cfg, tol):
+    """The verification budget (Appendix A.1; Table A5 varies it): k_max = 1, 2, 4,
+    5 and 7 on three slots whose planted drafts are the target's own greedy
+    continuation (so a step accepts min(k_max, remaining budget) candidates unless
+    EOS ends it), and the same budgets with the first rejection at r ~ U{0..8};
+    drafts, target logits, emitted tokens, accepted counts and done against the
+    oracle every step."""
+    from lockstep import Lockstep
+    W = make_weights(cfg)
+    prompts = [make_prefix(cfg, 0, 5), make_prefix(cfg, 1, 17), make_prefix(cfg, 2, 30)]
+    max_new = [60, 25, 60]
+    ls = Lockstep(cfg, W, prompts, max_new, tol)
+    refs = [plain_greedy(ls.T, make_memory(cfg, i), prompts[i], max_new[i]) for i in range(3)]
+    rng = np.random.default_rng(12)
+    K = cfg.block_k
+    for rep in range(2):
+        for k_max in (1, 2, 4, 5, 7):
+            ov = np.stack([_plan(refs[i], ls.sess[i].emitted, K, K if rep == 0 else int(rng.integers(0, K + 1)),
+                                 cfg.n_vocab, rng) for i in range(3)])
+            ls.step(k_max=k_max, override=ov)
+    print(f"budget sweep {cfg.name}: accepted {ls.accepted}; max |dlogit| draft {ls.max_dlogit:.2e} "
+          f"target {ls.max_tlogit:.2e}; near ties {ls.near_ties}")
+    assert ls.steps == 10 and max(ls.accepted) == 7
+    ls.close()
+
+
+@pytest.mark.timeout(900)
+def test_large_v3_b1_graph_step_budgets(side_stream):
+    """The timed path at budgets below K (Table A5's knob) at large-v3 shapes,
+    batch 1: graph-replayed wf_step with k_max = 1, 2, 4 and 7 and the whole
+    greedy continuation planted, so each step accepts exactly k_max candidates;
+    logits, tokens and accepted counts against the oracle."""
+    from lockstep import Lockstep
+    cfg = LARGE_V3
+    W = make_weights(cfg)
+    prompt = make_prefix(cfg, 0, 60)
+    ls = Lockstep(cfg, W, [prompt], [cfg.n_ctx], TOL_BF16)
+    ls.eng.set_debug(True)
+    budgets = (1, 2, 4, 7, 4, 1)
+    ref = plain_greedy(ls.T, make_memory(cfg, 0), prompt, sum(budgets) + len(budgets) + 2)
+    rng = np.random.default_rng(13)
+    outs = ls.eng._outs(1)
+    ovr = torch.zeros((1, cfg.block_k), dtype=torch.int32, device="cuda")
+    accepted = []
+    for k_max in budgets:
+        ov = _plan(ref, ls.sess[0].emitted, cfg.block_k, cfg.block_k, cfg.n_vocab, rng)[None]
+        _, _, n_acc, _ = ls.graph_step(ov, outs, ovr, k_max=k_max)
+        if not ls.live[0]:
+            break
+        accepted.append(int(n_acc[0]))
+    print(f"large-v3 budgets {budgets}: accepted {accepted}; max |dlogit| draft {ls.max_dlogit:.2e} "
+          f"target {ls.max_tlogit:.2e}; near ties {ls.near_ties}", flush=True)
+    assert accepted == list(budgets[:len(accepted)]) and len(accepted) >= 4
     ls.close()
 
 
