@@ -1237,6 +1237,132 @@ __global__ void __launch_bounds__(kSelfThreads) k_attn_draft(AttnArgs a) {
   }
 }
 
+// Drafter attention (Section 3.2, Eq. 2; Appendix A.2) with all nine block rows of
+// a (head, slot) in one block: one softmax over the history positions before the
+// anchor and the nine block rows (bidirectional inside the block), RoPE on the
+// queries and the block keys (the history keys were stored rotated), scores / 8.
+// Each history key and value is read once per block for all nine rows (a block per
+// (head, row) read the slot's history nine times: 183 us per launch at 96 slots).
+// Scores: thread t takes keys t, t + 256 (loaded together, both at once) and forms
+// the nine rows' dot products against the rotated queries in LDS; softmax per row
+// by one wave; values: wave w sums keys w, w + 4, ... for all rows and its lane's
+// dim, eight keys' values in flight, and the four waves' partial sums are added in
+// a fixed order.
+constexpr int kDrThreads = 256;
+constexpr int kDrKeys = (kMaxCtx + kRows + kDrThreads - 1) / kDrThreads;  // keys per thread in the score pass
+constexpr int kDrSc = kMaxCtx + kRows + 3;                                // score row stride (floats)
+constexpr int kDrMinBlocks = 160;  // (head, slot) blocks from which the all-rows kernel is used
+
+template <typename S>
+__global__ void __launch_bounds__(kDrThreads) k_attn_draft_rows(AttnArgs a) {
+  StampScope stamp_scope(a.stamp, kDrThreads);
+  constexpr int NW = kDrThreads / 64;
+  static_assert(NW == 4, "the partial sums of four waves are added below");
+  __shared__ float qs[kRows][kHeadDim];
+  __shared__ float kb[kRows][kHeadDim];
+  __shared__ float vb[kRows][kHeadDim];
+  __shared__ float sc[kRows][kDrSc];
+  __shared__ float part[NW][kRows][kHeadDim];
+  __shared__ float rsum[kRows];
+  const int head = blockIdx.x, slot = a.slot0 + blockIdx.y;
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const int t0 = a.state[slot * kStateInts + ST_L];
+  const int nh = a.draft_hist ? min(t0, a.n_ctx) : 0;  // history keys attended
+  const int nk = nh + kRows;
+  const int d = a.d;
+  const S* Kh = reinterpret_cast<const S*>(a.kcache) + ((size_t)slot * a.n_head + head) * a.n_ctx * kHeadDim;
+  const S* Vh = reinterpret_cast<const S*>(a.vcache) + ((size_t)slot * a.n_head + head) * a.n_ctx * kHeadDim;
+  // this thread's history keys (clamped into the cache; keys past nh are not used),
+  // issued before the block rows are staged
+  float kv[kDrKeys][kHeadDim];
+#pragma unroll
+  for (int u = 0; u < kDrKeys; ++u) {
+    const int j = min((int)threadIdx.x + u * kDrThreads, max(nh - 1, 0));
+#pragma unroll
+    for (int c = 0; c < kHeadDim; c += 8) ld8(Kh + (size_t)j * kHeadDim + c, &kv[u][c]);
+  }
+  // rotated, scaled queries; rotated block keys; block values
+  for (int t = threadIdx.x; t < kRows * 32; t += kDrThreads) {
+    const int r = t >> 5, j = t & 31, pos = t0 + r;
+    const float c = a.draft_rope ? a.rope[(pos * 32 + j) * 2] : 1.f;
+    const float sn = a.draft_rope ? a.rope[(pos * 32 + j) * 2 + 1] : 0.f;
+    const float* qr = a.q + (size_t)(slot * kRows + r) * a.ldq + head * kHeadDim;
+    const float* kr = qr + d;
+    const float* vr = qr + 2 * d;
+    const float q1 = qr[j], q2 = qr[j + 32], k1 = kr[j], k2 = kr[j + 32];
+    qs[r][j] = (q1 * c - q2 * sn) * 0.125f;
+    qs[r][j + 32] = (q1 * sn + q2 * c) * 0.125f;
+    kb[r][j] = k1 * c - k2 * sn;
+    kb[r][j + 32] = k1 * sn + k2 * c;
+    vb[r][j] = vr[j];
+    vb[r][j + 32] = vr[j + 32];
+  }
+  __syncthreads();
+  // scores of keys t, t + 256: history keys from registers, block keys from LDS
+#pragma unroll
+  for (int u = 0; u < kDrKeys; ++u) {
+    const int j = (int)threadIdx.x + u * kDrThreads;
+    if (j >= nk) continue;
+    if (j >= nh) {
+#pragma unroll
+      for (int e = 0; e < kHeadDim; ++e) kv[u][e] = kb[j - nh][e];
+    }
+#pragma unroll
+    for (int r = 0; r < kRows; ++r) {
+      float s = 0.f;
+#pragma unroll
+      for (int e = 0; e < kHeadDim; ++e) s = fmaf(qs[r][e], kv[u][e], s);
+      sc[r][j] = s;
+    }
+  }
+  __syncthreads();
+  // softmax numerators per row (max subtracted) and their sums
+  for (int r = wv; r < kRows; r += NW) {
+    float m = -INFINITY;
+    for (int j = lane; j < nk; j += 64) m = fmaxf(m, sc[r][j]);
+    m = wave_max(m);
+    float sum = 0.f;
+    for (int j = lane; j < nk; j += 64) {
+      const float p = expf(sc[r][j] - m);
+      sc[r][j] = p;
+      sum += p;
+    }
+    sum = wave_sum(sum);
+    if (lane == 0) rsum[r] = sum;
+  }
+  __syncthreads();
+  // values: wave wv sums keys wv, wv + 4, ... (eight in flight) for its lane's dim
+  float acc[kRows];
+#pragma unroll
+  for (int r = 0; r < kRows; ++r) acc[r] = 0.f;
+  for (int j0 = wv; j0 < nh; j0 += 8 * NW) {
+    float v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) v[u] = to_f(Vh[(size_t)min(j0 + u * NW, nh - 1) * kHeadDim + lane]);
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int j = j0 + u * NW;
+      if (j < nh) {
+#pragma unroll
+        for (int r = 0; r < kRows; ++r) acc[r] = fmaf(sc[r][j], v[u], acc[r]);
+      }
+    }
+  }
+  for (int jb = wv; jb < kRows; jb += NW) {
+    const float v = vb[jb][lane];
+#pragma unroll
+    for (int r = 0; r < kRows; ++r) acc[r] = fmaf(sc[r][nh + jb], v, acc[r]);
+  }
+#pragma unroll
+  for (int r = 0; r < kRows; ++r) part[wv][r][lane] = acc[r];
+  __syncthreads();
+  for (int t = threadIdx.x; t < kRows * kHeadDim; t += kDrThreads) {
+    const int r = t / kHeadDim, dim = t % kHeadDim;
+    const float o = (part[0][r][dim] + part[1][r][dim]) + (part[2][r][dim] + part[3][r][dim]);
+    put_op<S>(a.out, a.nsplit, a.R9, slot * kRows + r, head * kHeadDim + dim, o / rsum[r]);
+  }
+}
+
 // ---------------------------------------------------------------- launchers
 static inline unsigned row_blocks(int H) { return (unsigned)(8 * ((H + 7) / 8) * kRows); }
 
@@ -1250,7 +1376,11 @@ void Ops<S>::attn_self(const AttnArgs& a, int n, hipStream_t st) {
 }
 template <typename S>
 void Ops<S>::attn_draft(const AttnArgs& a, int n, hipStream_t st) {
-  k_attn_draft<S><<<dim3(row_blocks(a.n_head), n), kSelfThreads, 0, st>>>(a);
+  // a few slots: a block per (head, row) fills more of the chip (20 all-rows blocks
+  // at one slot took 13.3 us per launch against 8.6); with more slots the history is
+  // read once per (head, slot)
+  if (n * a.n_head >= kDrMinBlocks) k_attn_draft_rows<S><<<dim3(a.n_head, n), kDrThreads, 0, st>>>(a);
+  else k_attn_draft<S><<<dim3(row_blocks(a.n_head), n), kSelfThreads, 0, st>>>(a);
 }
 // enough slots to fill the chip with (head, slot) blocks: all rows per block;
 // otherwise one block per (head, row)

@@ -6,7 +6,8 @@ Each variant runs the lockstep comparison of the parity tests: draft and target
 logits within tolerance, drafted and emitted tokens, accepted counts and done
 flags identical wherever the deciding row's top-2 margin exceeds the tolerance,
 with natural and planted drafts; at fp32 storage with two slots, at bf16
-storage with one slot (the batch-1 kernels), and at large-v3 shapes.
+storage with one slot (the batch-1 kernels), at bf16 storage with ten slots of
+a wider micro model (the several-slot kernels), and at large-v3 shapes.
 """
 import numpy as np
 import pytest
@@ -41,13 +42,19 @@ def _planted(ls, refs, rng):
     return ov
 
 
+# d 1024 (16 heads) at 10 slots: 160 (head, slot) blocks, so the drafter attention
+# takes its all-rows kernel (one block per (head, slot) for the nine block rows)
+MICRO_WIDE = MICRO_BF16.with_(name="micro-wide", d_model=1024, n_head=16, d_ff=2560)
+
+
 @pytest.mark.parametrize("variant", list(VARIANTS))
-@pytest.mark.parametrize("base,tol,nslots", [(MICRO, 1e-3, 2), (MICRO_BF16, 2e-3, 1)], ids=["f32-b2", "bf16-b1"])
+@pytest.mark.parametrize("base,tol,nslots", [(MICRO, 1e-3, 2), (MICRO_BF16, 2e-3, 1), (MICRO_WIDE, 2e-3, 10)],
+                         ids=["f32-b2", "bf16-b1", "wide-b10"])
 def test_micro_variant_lockstep(variant, base, tol, nslots):
     from lockstep import Lockstep
     cfg = base.with_(name=f"{base.name}-{variant}", **VARIANTS[variant])
     W = make_weights(cfg)
-    prompts = [make_prefix(cfg, s, 7 + 9 * s) for s in range(nslots)]
+    prompts = [make_prefix(cfg, s, 7 + (9 * s) % 40) for s in range(nslots)]
     max_new = [40] * nslots
     opts = OracleOpts(dtype=np.float32, kv_bf16=cfg.dtype == "bf16")
     ls = Lockstep(cfg, W, prompts, max_new, tol, opts=opts)
