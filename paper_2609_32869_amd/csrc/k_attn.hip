@@ -702,55 +702,69 @@ __device__ __forceinline__ void split_planes(const float* v, bf16x8& hi, bf16x8&
   lo = pack_bf16x8(lb);
 }
 
+// The loads of one (head, slot, chunk) item: query row n (rows >= 9 re-read row 8,
+// zeroed below), key tiles (frames past the end re-read the last one, masked
+// below), value fragments (inside the padded rows).
+template <int KS>
+struct XItem {
+  float4 qx[2][2];
+  bf16x8 kt[2 * KS][2];
+  bf16x8 vt[KS][4];
+};
+
 template <int KS, int NW>
-__global__ void __launch_bounds__(NW * 64) k_attn_cross_mx(CrossArgs a) {
-  StampScope stamp_scope(a.stamp, NW * 64);
-  constexpr int NT = 2 * KS;  // 16-frame score tiles per wave
-  __shared__ float wmax[NW][16];
-  __shared__ float wsum[NW][16];
-  __shared__ float wo[NW][kRows][64];
-  const int head = blockIdx.x, slot = a.slot0 + blockIdx.y, c = blockIdx.z;
+__device__ __forceinline__ void xitem_load(const CrossArgs& a, int head, int slot, int c, XItem<KS>& it) {
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, n = lane & 15, kg = lane >> 4;
   const int F = a.n_frames, Fp = a.vt_frames;
   const int f0w = c * a.chunk + w * 32 * KS;  // first frame of this wave
   const bf16* base = reinterpret_cast<const bf16*>(a.kv) + (size_t)slot * a.d * (F + Fp);
   const bf16* Kh = base + (size_t)head * F * kHeadDim;
   const bf16* Vt = base + (size_t)a.n_head * F * kHeadDim + (size_t)head * kHeadDim * Fp;
-  // loads: query row n (rows >= 9 re-read row 8, zeroed below), key tiles (frames
-  // past the end re-read the last one, masked below), value fragments (inside the
-  // padded rows)
-  float4 qx[2][2];
-  {
-    const float* qr = a.q + (size_t)(slot * kRows + min(n, kRows - 1)) * a.ldq + head * kHeadDim + 8 * kg;
+  const float* qr = a.q + (size_t)(slot * kRows + min(n, kRows - 1)) * a.ldq + head * kHeadDim + 8 * kg;
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      qx[h][0] = *reinterpret_cast<const float4*>(qr + 32 * h);
-      qx[h][1] = *reinterpret_cast<const float4*>(qr + 32 * h + 4);
-    }
+  for (int h = 0; h < 2; ++h) {
+    it.qx[h][0] = *reinterpret_cast<const float4*>(qr + 32 * h);
+    it.qx[h][1] = *reinterpret_cast<const float4*>(qr + 32 * h + 4);
   }
-  bf16x8 kt[NT][2];
 #pragma unroll
-  for (int t = 0; t < NT; ++t) {
+  for (int t = 0; t < 2 * KS; ++t) {
     const int f = min(f0w + 16 * t + n, F - 1);
     const bf16x8* kp = reinterpret_cast<const bf16x8*>(Kh + (size_t)f * kHeadDim) + kg;
-    kt[t][0] = kp[0];
-    kt[t][1] = kp[4];
+    it.kt[t][0] = kp[0];
+    it.kt[t][1] = kp[4];
   }
-  bf16x8 vt[KS][4];
 #pragma unroll
   for (int st = 0; st < KS; ++st)
 #pragma unroll
     for (int dt = 0; dt < 4; ++dt)
-      vt[st][dt] = *reinterpret_cast<const bf16x8*>(Vt + vt_index(16 * dt + n, f0w + 32 * st + 8 * kg));
-  __builtin_amdgcn_sched_barrier(0);  // every load above is issued before any use below
+      it.vt[st][dt] = *reinterpret_cast<const bf16x8*>(Vt + vt_index(16 * dt + n, f0w + 32 * st + 8 * kg));
+}
+
+// Block-wide barrier for LDS only: waits for this wave's LDS operations, not for
+// its global loads in flight (a __syncthreads would wait for those too).
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_s_waitcnt((63 & 15) | ((63 >> 4) << 14) | (7 << 4) | (0 << 8));  // lgkmcnt(0), vmcnt any
+  __builtin_amdgcn_s_barrier();
+}
+
+// Scores, chunk softmax and values of one item whose loads are in `it`; writes the
+// chunk record (pair = slot index within the launch * H + head), or the output rows
+// when the chunk is the only one and no output product is fused.
+template <int KS, int NW>
+__device__ __forceinline__ void xitem_compute(const CrossArgs& a, int head, int slot, int pair, int c, const XItem<KS>& it,
+                                              float (*wmax)[16], float (*wsum)[16], float (*wo)[kRows][64]) {
+  constexpr int NT = 2 * KS;  // 16-frame score tiles per wave
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, n = lane & 15, kg = lane >> 4;
+  const int F = a.n_frames;
+  const int f0w = c * a.chunk + w * 32 * KS;
   // query planes of the scaled rows
   bf16x8 qh[2], ql[2];
   {
     const float scale = n < kRows ? 0.125f : 0.f;
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
-      const float v[8] = {qx[h][0].x * scale, qx[h][0].y * scale, qx[h][0].z * scale, qx[h][0].w * scale,
-                          qx[h][1].x * scale, qx[h][1].y * scale, qx[h][1].z * scale, qx[h][1].w * scale};
+      const float v[8] = {it.qx[h][0].x * scale, it.qx[h][0].y * scale, it.qx[h][0].z * scale, it.qx[h][0].w * scale,
+                          it.qx[h][1].x * scale, it.qx[h][1].y * scale, it.qx[h][1].z * scale, it.qx[h][1].w * scale};
       split_planes(v, qh[h], ql[h]);
     }
   }
@@ -760,10 +774,10 @@ __global__ void __launch_bounds__(NW * 64) k_attn_cross_mx(CrossArgs a) {
 #pragma unroll
   for (int t = 0; t < NT; ++t) {
     floatx4 acc = {0.f, 0.f, 0.f, 0.f};
-    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kt[t][0], qh[0], acc, 0, 0, 0);
-    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kt[t][0], ql[0], acc, 0, 0, 0);
-    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kt[t][1], qh[1], acc, 0, 0, 0);
-    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kt[t][1], ql[1], acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(it.kt[t][0], qh[0], acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(it.kt[t][0], ql[0], acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(it.kt[t][1], qh[1], acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(it.kt[t][1], ql[1], acc, 0, 0, 0);
     sct[t] = acc;
 #pragma unroll
     for (int i = 0; i < 4; ++i)
@@ -776,7 +790,7 @@ __global__ void __launch_bounds__(NW * 64) k_attn_cross_mx(CrossArgs a) {
     mx = fmaxf(__uint_as_float(y[0]), __uint_as_float(y[1]));
     if (lane < 16) wmax[w][lane] = mx;
   }
-  __syncthreads();
+  lds_barrier();
   float M = wmax[0][n];
 #pragma unroll
   for (int i = 1; i < NW; ++i) M = fmaxf(M, wmax[i][n]);  // finite: frame c * chunk is present
@@ -810,8 +824,8 @@ __global__ void __launch_bounds__(NW * 64) k_attn_cross_mx(CrossArgs a) {
     split_planes(pb, ph, pl);
 #pragma unroll
     for (int dt = 0; dt < 4; ++dt) {
-      oacc[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vt[st][dt], ph, oacc[dt], 0, 0, 0);
-      oacc[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vt[st][dt], pl, oacc[dt], 0, 0, 0);
+      oacc[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(it.vt[st][dt], ph, oacc[dt], 0, 0, 0);
+      oacc[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(it.vt[st][dt], pl, oacc[dt], 0, 0, 0);
     }
   }
   // this wave's row sums (over the four frame groups) and outputs to LDS
@@ -828,8 +842,7 @@ __global__ void __launch_bounds__(NW * 64) k_attn_cross_mx(CrossArgs a) {
 #pragma unroll
       for (int i = 0; i < 4; ++i) wo[w][n][16 * dt + 4 * kg + i] = oacc[dt][i];
   }
-  __syncthreads();
-  const int pair = blockIdx.y * a.n_head + head;
+  lds_barrier();
   float* part = a.part + ((size_t)pair * a.nchunk + c) * kXrPart;
   for (int t = threadIdx.x; t < kRows * 64; t += NW * 64) {
     const int r = t >> 6, dim = t & 63;
@@ -852,6 +865,19 @@ __global__ void __launch_bounds__(NW * 64) k_attn_cross_mx(CrossArgs a) {
       }
     }
   }
+}
+
+template <int KS, int NW>
+__global__ void __launch_bounds__(NW * 64) k_attn_cross_mx(CrossArgs a) {
+  StampScope stamp_scope(a.stamp, NW * 64);
+  __shared__ float wmax[NW][16];
+  __shared__ float wsum[NW][16];
+  __shared__ float wo[NW][kRows][64];
+  const int head = blockIdx.x, slot = a.slot0 + blockIdx.y, c = blockIdx.z;
+  XItem<KS> it;
+  xitem_load<KS, NW>(a, head, slot, c, it);
+  __builtin_amdgcn_sched_barrier(0);  // every load above is issued before any use below
+  xitem_compute<KS, NW>(a, head, slot, blockIdx.y * a.n_head + head, c, it, wmax, wsum, wo);
 }
 
 // Merge of the chunk records of one (head, slot): one thread per (row, 4 dims).
