@@ -686,6 +686,10 @@ template <int EPI>
 __global__ void __launch_bounds__(256) k_gemm16s(GemvArgs a, int mb0, int nmb, int nnb) {
   StampScope stamp_scope(a.stamp, 256);
   __shared__ float sv[64][65];
+  if (a.pf.blocks > 0 && blockIdx.x >= gridDim.x - a.pf.blocks) {  // appended blocks: a later product's weights
+    if (blockIdx.y == 0) touch_range(a.pf, blockIdx.x - (gridDim.x - a.pf.blocks));
+    return;
+  }
   const int x = blockIdx.x & 7, i = blockIdx.x >> 3;
   int nbk, mbk;
   if (nmb >= kGemmSplitRows) {
@@ -1480,6 +1484,9 @@ static void launch_splitk(const GemvArgs& a, hipStream_t st) {
   k_gemv16w<EPI, 8, 4><<<grid, 512, 0, st>>>(a);
 }
 
+// blocks appended to a staged several-slot GEMM launch for the weights it reads ahead
+static unsigned pf_blocks(const GemvArgs& a) { return (unsigned)a.pf.blocks; }
+
 template <typename S, int EPI>
 static void launch_epi(const GemvArgs& a, hipStream_t st) {
   if constexpr (EPI == EPI_ACC) {  // bf16: split-K partial sums added to y
@@ -1488,7 +1495,7 @@ static void launch_epi(const GemvArgs& a, hipStream_t st) {
         const int mb0 = a.slot0 * kRows / 64, mb1 = ((a.slot0 + a.nslots) * kRows + 63) / 64;
         const int nmb = mb1 - mb0, nnb = (a.N + 63) / 64, ks = a.ksplit > 1 ? a.ksplit : 1;
         const unsigned nb = gemm_grid(nmb, nnb);
-        if (nb * (unsigned)ks >= kGemmStagedBlocks) k_gemm16s<EPI><<<dim3(nb, ks), 256, 0, st>>>(a, mb0, nmb, nnb);
+        if (nb * (unsigned)ks >= kGemmStagedBlocks) k_gemm16s<EPI><<<dim3(nb + pf_blocks(a), ks), 256, 0, st>>>(a, mb0, nmb, nnb);
         else k_gemm16<EPI><<<dim3(nb, ks), 256, 0, st>>>(a, mb0, nmb, nnb);
       } else {
         launch_splitk<EPI_ACC>(a, st);  // batch 1
@@ -1534,7 +1541,7 @@ static void launch_epi(const GemvArgs& a, hipStream_t st) {
       const unsigned nb = gemm_grid(nmb, nnb);
       if constexpr (EPI != EPI_ARGMAX) {
         if (nb * (unsigned)ks >= kGemmStagedBlocks) {
-          k_gemm16s<EPI><<<dim3(nb, ks), 256, 0, st>>>(a, mb0, nmb, nnb);
+          k_gemm16s<EPI><<<dim3(nb + pf_blocks(a), ks), 256, 0, st>>>(a, mb0, nmb, nnb);
           return;
         }
       }
@@ -1562,7 +1569,11 @@ static void launch_epi(const GemvArgs& a, hipStream_t st) {
 }
 
 template <typename S>
-void Ops<S>::gemv(int epi, const GemvArgs& a, hipStream_t st) {
+void Ops<S>::gemv(int epi, const GemvArgs& a0, hipStream_t st) {
+  // the staged GEMM takes the last pf.blocks blocks of grid x as reading blocks
+  // (other kernels ignore the request): a request with nothing to read appends none
+  GemvArgs a = a0;
+  if (a.pf.p == nullptr || a.pf.bytes < 16 || a.pf.blocks <= 0) a.pf = Touch{nullptr, 0, 0};
   switch (epi) {
     case EPI_STORE: launch_epi<S, EPI_STORE>(a, st); break;
     case EPI_GELU: launch_epi<S, EPI_GELU>(a, st); break;

@@ -291,7 +291,26 @@ struct Runner {
   struct LnNext {
     size_t g, b;
     bool wide;
+    size_t wq, nq;  // weights of the next block's q|k|v product (offset, elements; 0: none)
   };
+
+  // Several slots (kTouchMinRowBlocks row blocks or more, bf16 operands): the
+  // weights of the wide-tile products (q|k|v, W_1) are read by extra blocks of
+  // the product launched before them (W'_o, W_2 of the previous block), so they
+  // come from the memory-side cache rather than HBM.  The 64 x 64 tile products
+  // stage three k-steps ahead through LDS and gain nothing from it (measured).
+  // touch_ holds the request for the next product launch, which takes it.
+  Touch touch_{nullptr, 0, 0};
+  bool touch_ahead(int slot0, int n) const {
+    if (L.nsplit_op != 2) return false;
+    const int mb0 = slot0 * kRows / 64, mb1 = ((slot0 + n) * kRows + 63) / 64;
+    return mb1 - mb0 >= kTouchMinRowBlocks;
+  }
+  // blocks: extra blocks of the launch (64 beside a 64 x 64 tile product, which
+  // holds two blocks per CU)
+  void touch_next(int slot0, int n, size_t w, size_t elems, int blocks) {
+    touch_ = touch_ahead(slot0, n) && elems > 0 ? Touch{W(w), elems * (size_t)eb(), blocks} : Touch{nullptr, 0, 0};
+  }
 
   // Run one launch.  When profiling, the launch gets a timing slot (kernels that
   // take one record their first-wave start and last-wave end in it).
@@ -405,9 +424,12 @@ struct Runner {
 
   // tag: the product's role in the step, for the eager profile
   void run_gemv(const char* tag, int epi, int n, const GemvArgs& a) {
+    const Touch pf = touch_;
+    touch_ = Touch{nullptr, 0, 0};
     launch(tag, gemv_bytes(n, a.K, a.N, epi), [&](unsigned long long* sp) {
       GemvArgs b = a;
       b.stamp = sp;
+      b.pf = pf;
       Ops<S>::gemv(epi, b, st);
     });
   }
@@ -534,7 +556,10 @@ struct Runner {
     }
     const OprojArgs op2 = oproj(b.w_o2, b.b_o2);
     cross(slot0, n, xlayer, op2);
-    if (op2.w == nullptr) resid("gemv_o", slot0, n, Ad16(), b.w_o2, b.b_o2, d, d);
+    if (op2.w == nullptr) {
+      touch_next(slot0, n, b.w_fc1, (size_t)c.d_ff * d, 64);
+      resid("gemv_o", slot0, n, Ad16(), b.w_o2, b.b_o2, d, d);
+    }
   }
 
   void mlp_sublayer(int slot0, int n, const BlockW& b, int tap, const LnNext& nx) {
@@ -542,6 +567,7 @@ struct Runner {
     float* h_ = F32(L.h);
     gemv_ln("gemv_fc1", EPI_GELU, slot0, n, h_, b.ln3_g, b.ln3_b, b.c_fc1, c.d_ff, 0, Ad32(), b.w_fc1, b.b_fc1, d, c.d_ff,
             nullptr, 0, Af16());
+    touch_next(slot0, n, nx.wq, nx.nq, 64);
     const int ksplit = L.fc2_split > 0 ? L.fc2_split : fc2_split_batch(slot0, n);
     // a tap block followed by a target block: that block's q|k|v product, which
     // folds its LayerNorm and so reads the rows anyway, writes the tap
@@ -583,6 +609,7 @@ struct Runner {
     float *h_ = F32(L.h), *qkv = F32(L.qkv);
     ln_ready = false;
     tap_next = -1;
+    touch_ = Touch{nullptr, 0, 0};
     for (int l = 0; l < c.n_layer; ++l) {
       const BlockW& b = L.tb[l];
       int tap = -1;
@@ -618,8 +645,8 @@ struct Runner {
         Ops<S>::attn_self(at, n, st);
       });
       if (at.op.w == nullptr) resid("gemv_o", slot0, n, Ad16(), b.w_o, b.b_o, d, d);
-      const LnNext nx = l + 1 < c.n_layer ? LnNext{L.tb[l + 1].ln1_g, L.tb[l + 1].ln1_b, false}
-                                          : LnNext{L.lnf_g, L.lnf_b, true};
+      const LnNext nx = l + 1 < c.n_layer ? LnNext{L.tb[l + 1].ln1_g, L.tb[l + 1].ln1_b, false, L.tb[l + 1].w_qkv, (size_t)3 * d * d}
+                                          : LnNext{L.lnf_g, L.lnf_b, true, 0, 0};
       block_tail(slot0, n, b, l, tap, nx, q_clear);
     }
   }
@@ -684,6 +711,8 @@ struct Runner {
     if (c.draft_flags & WF_DRAFT_ABS_POS) ba.pos2 = W(L.pos_emb);
     launch("begin", 0, [&](unsigned long long*) { Ops<S>::draft_begin(ba, n, st); });
     ln_ready = false;
+    touch_ = Touch{nullptr, 0, 0};
+    const bool xattn = !(c.draft_flags & WF_DRAFT_NO_AUDIO);
     for (int dl = 0; dl < c.n_draft_layer; ++dl) {
       const BlockW& b = L.db[dl];
       if (ln_ready) gemv("gemv_draft_qkv", EPI_STORE, slot0, n, Ad16(), b.w_qkv, b.b_qkv, d, 3 * d, qkv, 3 * d);
@@ -701,11 +730,14 @@ struct Runner {
         at.stamp = sp;
         Ops<S>::attn_draft(at, n, st);
       });
+      if (!xattn) touch_next(slot0, n, b.w_fc1, (size_t)c.d_ff * d, 64);  // the MLP follows directly
       resid("gemv_o", slot0, n, Ad16(), b.w_o, b.b_o, d, d);
-      const LnNext nx = dl + 1 < c.n_draft_layer ? LnNext{L.db[dl + 1].ln1_g, L.db[dl + 1].ln1_b, false}
-                                                 : LnNext{L.dlnf_g, L.dlnf_b, true};
-      block_tail(slot0, n, b, c.n_layer + dl, -1, nx, false, !(c.draft_flags & WF_DRAFT_NO_AUDIO));
+      const LnNext nx = dl + 1 < c.n_draft_layer
+                            ? LnNext{L.db[dl + 1].ln1_g, L.db[dl + 1].ln1_b, false, L.db[dl + 1].w_qkv, (size_t)3 * d * d}
+                            : LnNext{L.dlnf_g, L.dlnf_b, true, 0, 0};
+      block_tail(slot0, n, b, c.n_layer + dl, -1, nx, false, xattn);
     }
+    touch_ = Touch{nullptr, 0, 0};
     head(slot0, n, h_, L.dlnf_g, L.dlnf_b, h->debug || sampling() ? F32(L.dlogits) : nullptr, I32(L.draft), dst,
          RNG_DRAFT, F32(L.dmax), F32(L.dsum));
   }

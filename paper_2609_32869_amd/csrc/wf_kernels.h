@@ -33,6 +33,39 @@ void stamp_init(unsigned long long* s, int n, hipStream_t st);
 // Weight orders: row-major [N][K] or bf16 fragment order (16- or 32-column tiles).
 enum { W_ROW = 0, W_F16 = 1, W_F32 = 2 };
 
+// Weights of a later product read ahead by extra blocks of an earlier launch.
+// With many slots every weight product runs from HBM (a step reads far more
+// weights than the memory-side cache holds), and the wide-tile GEMM, which loads
+// its fragments straight into registers four k-steps ahead, stalls on those
+// first reads; read once shortly before, it runs as if warm (864 rows, first MLP
+// product: 41.5 -> 34.0 us standalone).  Non-temporal loads do not allocate in
+// that cache and do not help.
+struct Touch {
+  const void* p;  // null: nothing to read
+  size_t bytes;
+  int blocks;     // extra blocks of the launch that read it
+};
+// Row blocks (64 rows) from which the step reads weights ahead (about 57 slots)
+constexpr int kTouchMinRowBlocks = 8;
+
+// Block b of nb reads bytes [0, bytes) of p, 16 bytes per thread and eight loads
+// in flight, and discards the values (the empty asm keeps the loads).
+__device__ inline void touch_range(const Touch& t, unsigned b) {
+  typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+  const u32x4* q = static_cast<const u32x4*>(t.p);
+  const size_t n16 = t.bytes / 16, stride = (size_t)t.blocks * blockDim.x;
+  for (size_t i = (size_t)b * blockDim.x + threadIdx.x; i < n16; i += 8 * stride) {
+    unsigned x = 0;
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const size_t j = min(i + u * stride, n16 - 1);
+      const u32x4 v = q[j];
+      x ^= v.x ^ v.w;
+    }
+    asm volatile("" ::"v"(x));
+  }
+}
+
 struct GemvArgs {
   Operand a;         // input operand (unused when lnx is set)
   const void* w;     // [N, K] storage type, order wkind
@@ -80,6 +113,9 @@ struct GemvArgs {
   float* hm;
   float* hs;
   unsigned long long* stamp;  // launch timing slot (profiled calls), or null
+  // weights of a later product, read by pf.blocks blocks appended to grid x (grid
+  // y 0 only); the LDS-staged several-slot GEMM takes it, other kernels ignore it
+  Touch pf;
 };
 
 // Attention output product fused into the attention kernel (bf16, one slot):

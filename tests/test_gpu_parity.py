@@ -188,6 +188,29 @@ def test_micro_bf16_b64_wide_tiles():
 
 
 @pytest.mark.timeout(900)
+def test_micro_bf16_b96_width1280_all_slots():
+    """96 slots (864 rows) at width 1280 (20 heads), FFN 5120, two blocks: the
+    1280-column products take the LDS-staged 64 x 64 GEMM with 280 tile blocks,
+    and W'_o and W_2 append blocks that read the next wide-tile product's weights
+    (W_1, the next block's q|k|v) ahead.  Every slot is compared with the oracle,
+    so a tile block lost to the appended ones would show in some slot's logits."""
+    from lockstep import Lockstep
+    cfg = MICRO_BF16.with_(name="micro-1280", d_model=1280, n_head=20, d_ff=5120)
+    W = make_weights(cfg)
+    n = 96
+    lens = [int(x) for x in make_prefix_lengths(n, 1, 40, seed=302)]
+    prompts = [make_prefix(cfg, s, lens[s]) for s in range(n)]
+    opts = OracleOpts(dtype=np.float32, kv_bf16=True)
+    ls = Lockstep(cfg, W, prompts, [30] * n, TOL_MICRO_BF16, opts=opts)
+    for _ in range(3):
+        ls.step()
+    print(f"micro-1280 b96: max |dlogit| draft {ls.max_dlogit:.3e} target {ls.max_tlogit:.3e}, "
+          f"near ties {ls.near_ties}")
+    assert ls.steps == 3 and sum(ls.live) >= n - 4
+    ls.close()
+
+
+@pytest.mark.timeout(900)
 # Several slots over many frames: bf16 cross-attention splits the frames into
 # chunks of 256 (997 = 3 x 256 + 229: the last chunk ends inside a 16-frame
 # score tile and inside an 8-frame value group, read from the zero padding of
