@@ -706,26 +706,34 @@ __device__ __forceinline__ void split_planes(const float* v, bf16x8& hi, bf16x8&
 // zeroed below), key tiles (frames past the end re-read the last one, masked
 // below), value fragments (inside the padded rows).
 template <int KS>
-struct XItem {
-  float4 qx[2][2];
+struct XKv {
   bf16x8 kt[2 * KS][2];
   bf16x8 vt[KS][4];
 };
+template <int KS>
+struct XItem {
+  float4 qx[2][2];
+  XKv<KS> kv;
+};
+
+__device__ __forceinline__ void xq_load(const CrossArgs& a, int head, int slot, float4 (&qx)[2][2]) {
+  const int lane = threadIdx.x & 63, n = lane & 15, kg = lane >> 4;
+  const float* qr = a.q + (size_t)(slot * kRows + min(n, kRows - 1)) * a.ldq + head * kHeadDim + 8 * kg;
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    qx[h][0] = *reinterpret_cast<const float4*>(qr + 32 * h);
+    qx[h][1] = *reinterpret_cast<const float4*>(qr + 32 * h + 4);
+  }
+}
 
 template <int KS, int NW>
-__device__ __forceinline__ void xitem_load(const CrossArgs& a, int head, int slot, int c, XItem<KS>& it) {
+__device__ __forceinline__ void xkv_load(const CrossArgs& a, int head, int slot, int c, XKv<KS>& it) {
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, n = lane & 15, kg = lane >> 4;
   const int F = a.n_frames, Fp = a.vt_frames;
   const int f0w = c * a.chunk + w * 32 * KS;  // first frame of this wave
   const bf16* base = reinterpret_cast<const bf16*>(a.kv) + (size_t)slot * a.d * (F + Fp);
   const bf16* Kh = base + (size_t)head * F * kHeadDim;
   const bf16* Vt = base + (size_t)a.n_head * F * kHeadDim + (size_t)head * kHeadDim * Fp;
-  const float* qr = a.q + (size_t)(slot * kRows + min(n, kRows - 1)) * a.ldq + head * kHeadDim + 8 * kg;
-#pragma unroll
-  for (int h = 0; h < 2; ++h) {
-    it.qx[h][0] = *reinterpret_cast<const float4*>(qr + 32 * h);
-    it.qx[h][1] = *reinterpret_cast<const float4*>(qr + 32 * h + 4);
-  }
 #pragma unroll
   for (int t = 0; t < 2 * KS; ++t) {
     const int f = min(f0w + 16 * t + n, F - 1);
@@ -740,6 +748,24 @@ __device__ __forceinline__ void xitem_load(const CrossArgs& a, int head, int slo
       it.vt[st][dt] = *reinterpret_cast<const bf16x8*>(Vt + vt_index(16 * dt + n, f0w + 32 * st + 8 * kg));
 }
 
+template <int KS, int NW>
+__device__ __forceinline__ void xitem_load(const CrossArgs& a, int head, int slot, int c, XItem<KS>& it) {
+  xq_load(a, head, slot, it.qx);
+  xkv_load<KS, NW>(a, head, slot, c, it.kv);
+}
+
+// The query planes of the nine rows scaled by 1/sqrt(64) (rows >= 9 zero).
+__device__ __forceinline__ void xq_planes(const float4 (&qx)[2][2], bf16x8 (&qh)[2], bf16x8 (&ql)[2]) {
+  const int n = threadIdx.x & 15;
+  const float scale = n < kRows ? 0.125f : 0.f;
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const float v[8] = {qx[h][0].x * scale, qx[h][0].y * scale, qx[h][0].z * scale, qx[h][0].w * scale,
+                        qx[h][1].x * scale, qx[h][1].y * scale, qx[h][1].z * scale, qx[h][1].w * scale};
+    split_planes(v, qh[h], ql[h]);
+  }
+}
+
 // Block-wide barrier for LDS only: waits for this wave's LDS operations, not for
 // its global loads in flight (a __syncthreads would wait for those too).
 __device__ __forceinline__ void lds_barrier() {
@@ -747,27 +773,17 @@ __device__ __forceinline__ void lds_barrier() {
   __builtin_amdgcn_s_barrier();
 }
 
-// Scores, chunk softmax and values of one item whose loads are in `it`; writes the
-// chunk record (pair = slot index within the launch * H + head), or the output rows
-// when the chunk is the only one and no output product is fused.
+// Scores, chunk softmax and values of chunk c whose keys and values are in `it`:
+// leaves each wave's row maxima, row sums and unnormalised output rows in LDS
+// (wmax / wsum / wo), readable by every thread of the block on return.
 template <int KS, int NW>
-__device__ __forceinline__ void xitem_compute(const CrossArgs& a, int head, int slot, int pair, int c, const XItem<KS>& it,
-                                              float (*wmax)[16], float (*wsum)[16], float (*wo)[kRows][64]) {
+__device__ __forceinline__ void xchunk_rows(const CrossArgs& a, int c, const XKv<KS>& it, const bf16x8 (&qh)[2],
+                                            const bf16x8 (&ql)[2], float (*wmax)[16], float (*wsum)[16],
+                                            float (*wo)[kRows][64]) {
   constexpr int NT = 2 * KS;  // 16-frame score tiles per wave
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, n = lane & 15, kg = lane >> 4;
   const int F = a.n_frames;
   const int f0w = c * a.chunk + w * 32 * KS;
-  // query planes of the scaled rows
-  bf16x8 qh[2], ql[2];
-  {
-    const float scale = n < kRows ? 0.125f : 0.f;
-#pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      const float v[8] = {it.qx[h][0].x * scale, it.qx[h][0].y * scale, it.qx[h][0].z * scale, it.qx[h][0].w * scale,
-                          it.qx[h][1].x * scale, it.qx[h][1].y * scale, it.qx[h][1].z * scale, it.qx[h][1].w * scale};
-      split_planes(v, qh[h], ql[h]);
-    }
-  }
   // scores and this wave's row maxima
   floatx4 sct[NT];
   float mx = -INFINITY;
@@ -843,6 +859,17 @@ __device__ __forceinline__ void xitem_compute(const CrossArgs& a, int head, int 
       for (int i = 0; i < 4; ++i) wo[w][n][16 * dt + 4 * kg + i] = oacc[dt][i];
   }
   lds_barrier();
+}
+
+// One (head, slot, chunk) item whose loads are in `it`: writes the chunk record
+// (pair = slot index within the launch * H + head), or the output rows when the
+// chunk is the only one and no output product is fused.
+template <int KS, int NW>
+__device__ __forceinline__ void xitem_compute(const CrossArgs& a, int head, int slot, int pair, int c, const XItem<KS>& it,
+                                              float (*wmax)[16], float (*wsum)[16], float (*wo)[kRows][64]) {
+  bf16x8 qh[2], ql[2];
+  xq_planes(it.qx, qh, ql);
+  xchunk_rows<KS, NW>(a, c, it.kv, qh, ql, wmax, wsum, wo);
   float* part = a.part + ((size_t)pair * a.nchunk + c) * kXrPart;
   for (int t = threadIdx.x; t < kRows * 64; t += NW * 64) {
     const int r = t >> 6, dim = t & 63;
@@ -878,6 +905,77 @@ __global__ void __launch_bounds__(NW * 64) k_attn_cross_mx(CrossArgs a) {
   xitem_load<KS, NW>(a, head, slot, c, it);
   __builtin_amdgcn_sched_barrier(0);  // every load above is issued before any use below
   xitem_compute<KS, NW>(a, head, slot, blockIdx.y * a.n_head + head, c, it, wmax, wsum, wo);
+}
+
+// Many (head, slot) pairs: one block per pair walks all NCH chunks of 32 KS NW
+// frames, the next chunk's keys and values in flight while the current one is
+// computed (two register sets used alternately: the chunk count is a
+// compile-time constant, since a load under a runtime condition makes the
+// compiler wait for every load in flight), and folds each chunk's rows into
+// running maxima, sums and outputs with the merge's max-shifted rule.  The rows
+// go straight into the next product's operand: no chunk records (their writes
+// among the key and value reads cost about a tenth of the launch at 96 slots)
+// and no merge launch.
+template <int KS, int NW, int NCH>
+__global__ void __launch_bounds__(NW * 64) k_attn_cross_pair(CrossArgs a) {
+  constexpr int NI = (kRows * 64 + NW * 64 - 1) / (NW * 64);  // (row, dim) items per thread
+  StampScope stamp_scope(a.stamp, NW * 64);
+  // LDS partials alternate between chunks, so chunk c + 1 writes while slower
+  // threads still fold chunk c
+  __shared__ float wmax[2][NW][16];
+  __shared__ float wsum[2][NW][16];
+  __shared__ float wo[2][NW][kRows][64];
+  const int head = blockIdx.x, slot = a.slot0 + blockIdx.y;
+  float4 qx[2][2];
+  XKv<KS> it[2];
+  xq_load(a, head, slot, qx);
+#pragma unroll
+  for (int c = 0; c < 2 && c < NCH; ++c) xkv_load<KS, NW>(a, head, slot, c, it[c]);
+  __builtin_amdgcn_sched_barrier(0);  // every load above is issued before any use below
+  bf16x8 qh[2], ql[2];
+  xq_planes(qx, qh, ql);
+  float rM[NI], rL[NI], rO[NI];
+#pragma unroll
+  for (int i = 0; i < NI; ++i) {
+    rM[i] = -INFINITY;
+    rL[i] = 0.f;
+    rO[i] = 0.f;
+  }
+#pragma unroll
+  for (int c = 0; c < NCH; ++c) {
+    const int b = c & 1;
+    xchunk_rows<KS, NW>(a, c, it[b], qh, ql, wmax[b], wsum[b], wo[b]);
+    if (c + 2 < NCH) {  // the set just used takes chunk c + 2
+      __builtin_amdgcn_sched_barrier(0);
+      xkv_load<KS, NW>(a, head, slot, c + 2, it[b]);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+      const int t = threadIdx.x + i * NW * 64;
+      if (t < kRows * 64) {
+        const int r = t >> 6, dim = t & 63;
+        float o = 0.f, L = 0.f, m = wmax[b][0][r];
+#pragma unroll
+        for (int j = 0; j < NW; ++j) {
+          o += wo[b][j][r][dim];
+          L += wsum[b][j][r];
+          m = fmaxf(m, wmax[b][j][r]);
+        }
+        const float Mn = fmaxf(rM[i], m);  // finite: every chunk holds a frame
+        const float f0 = __expf(rM[i] - Mn), f1 = __expf(m - Mn);  // f0 = 0 for the first chunk
+        rO[i] = rO[i] * f0 + o * f1;
+        rL[i] = rL[i] * f0 + L * f1;
+        rM[i] = Mn;
+      }
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < NI; ++i) {
+    const int t = threadIdx.x + i * NW * 64;
+    if (t < kRows * 64)
+      put_op<bf16>(a.out, a.nsplit, a.R9, slot * kRows + (t >> 6), head * kHeadDim + (t & 63), rO[i] / rL[i]);
+  }
 }
 
 // Merge of the chunk records of one (head, slot): one thread per (row, 4 dims).
@@ -1413,6 +1511,17 @@ void Ops<S>::attn_draft(const AttnArgs& a, int n, hipStream_t st) {
 template <typename S>
 void Ops<S>::attn_cross(const CrossArgs& a, int n, hipStream_t st) {
   if constexpr (sizeof(S) == 2) {  // transposed values, matrix cores, frame chunks + merge
+    if (a.by_pair) {  // one block per (head, slot) over every chunk: no merge
+      const dim3 grid(a.n_head, n);
+      switch (a.nchunk) {
+#define WF_XPAIR(N) \
+  case N: k_attn_cross_pair<1, 4, N><<<grid, 256, 0, st>>>(a); break;
+        WF_XPAIR(1) WF_XPAIR(2) WF_XPAIR(3) WF_XPAIR(4) WF_XPAIR(5) WF_XPAIR(6)
+        WF_XPAIR(7) WF_XPAIR(8) WF_XPAIR(9) WF_XPAIR(10) WF_XPAIR(11) WF_XPAIR(12)
+#undef WF_XPAIR
+      }
+      return;
+    }
     if (a.chunk == 128) k_attn_cross_mx<1, 4><<<dim3(a.n_head, n, a.nchunk), 256, 0, st>>>(a);
     else k_attn_cross_mx<2, 8><<<dim3(a.n_head, n, a.nchunk), 512, 0, st>>>(a);
   } else {

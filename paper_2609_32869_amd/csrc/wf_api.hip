@@ -507,7 +507,11 @@ struct Runner {
     a.nsplit = L.nsplit_op;
     a.R9 = R9();
     a.vt_frames = vt_frames();
-    if (c.dtype == WF_BF16) {
+    if (c.dtype == WF_BF16 && op.w == nullptr && cross_by_pair(n, c.n_head, c.n_frames)) {
+      a.by_pair = 1;
+      a.chunk = kXpChunk;
+      a.nchunk = (c.n_frames + kXpChunk - 1) / kXpChunk;
+    } else if (c.dtype == WF_BF16) {
       a.chunk = cross_mx_chunk(n);
       a.nchunk = cross_mx_chunks(n, c.n_frames);
     } else {

@@ -188,6 +188,33 @@ def test_micro_bf16_b64_wide_tiles():
 
 
 @pytest.mark.timeout(900)
+def test_micro_bf16_b64_cross_attention_by_pair():
+    """64 slots x 16 heads (1024 (head, slot) pairs), 900 frames: the bf16
+    cross-attention runs one block per pair over eight 128-frame chunks (the next
+    chunk's keys and values loaded during the current one, rows folded into
+    running maxima and sums); in the last chunk (frames 896..1023) only the first
+    wave holds frames, the other three are masked whole.  Planted drafts on six
+    followed slots."""
+    from lockstep import Lockstep
+    cfg = MICRO_BF16.with_(name="micro-wide-900f", d_model=1024, n_head=16, d_ff=2560, n_frames=900)
+    W = make_weights(cfg)
+    n = 64
+    lens = [int(x) for x in make_prefix_lengths(n, 1, 40, seed=303)]
+    prompts = [make_prefix(cfg, s, lens[s]) for s in range(n)]
+    check = [0, 13, 31, 32, 47, 63]
+    opts = OracleOpts(dtype=np.float32, kv_bf16=True)
+    ls = Lockstep(cfg, W, prompts, [30] * n, TOL_MICRO_BF16, opts=opts, check=check)
+    refs = {i: plain_greedy(ls.T, make_memory(cfg, i), prompts[i], 30) for i in check}
+    rng = np.random.default_rng(9)
+    for _ in range(4):
+        ls.step(override=_planted_subset(ls, refs, rng))
+    print(f"micro-wide 900f b64: max |dlogit| draft {ls.max_dlogit:.3e} target {ls.max_tlogit:.3e}, "
+          f"accepted {ls.accepted}, near ties {ls.near_ties}")
+    assert ls.steps == 4 and max(ls.accepted) > 0
+    ls.close()
+
+
+@pytest.mark.timeout(900)
 def test_micro_bf16_b96_width1280_all_slots():
     """96 slots (864 rows) at width 1280 (20 heads), FFN 5120, two blocks: the
     1280-column products take the LDS-staged 64 x 64 GEMM with 280 tile blocks,
