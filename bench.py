@@ -185,6 +185,27 @@ def role_flops(cfg, role, rows):
 
 
 MFMA_FILE = os.path.join(ROOT, "profiles", "mfma_large-v3_b96_pmc.md")
+TRAFFIC96_FILE = os.path.join(ROOT, "profiles", "hbm_traffic_large-v3_b96_pmc.md")
+# batch-96 role -> kernel symbol whose counters the batch object reports
+SYMBOL_OF_ROLE96 = {"attn_cross": "void wf::k_attn_cross_pair<1, 4, 12>(wf::CrossArgs)"}
+
+
+def measured_traffic96(role):
+    """HBM bytes per dispatch of a batch-96 role's kernel from the committed counter
+    summary (copy-calibrated FETCH_SIZE and WRITE_SIZE), with its source, or None
+    when there is none or the kernel sources changed since the passes."""
+    try:
+        with open(TRAFFIC96_FILE) as f:
+            line = next(l for l in f if l.startswith("traffic-json: "))
+        rec = json.loads(line[len("traffic-json: "):])
+    except (OSError, StopIteration, ValueError):
+        return None, "no counter summary"
+    if rec.get("source_sha256") != source_digest():
+        return None, "kernel sources changed since the counter passes"
+    k = rec.get("kernels", {}).get(SYMBOL_OF_ROLE96.get(role, ""))
+    if not k:
+        return None, "kernel not in the counter summary"
+    return k["hbm_bytes_per_dispatch"], TRAFFIC96_FILE[len(ROOT) + 1:]
 
 
 def measured_mfma():
@@ -298,6 +319,12 @@ def batch_workload(args, W, B, steps, warmup, profile_steps, log, cpu_sample=Tru
         if role == "attn_cross":
             per["GBs"] = round(v["bytes"] / (v["ms"] / 1e3) / 1e9, 1)
             per["frac_of_hbm_peak"] = round(per["GBs"] / HBM_PEAK_GBS, 4)
+            alg = v["bytes"] / max(v["launches"], 1)
+            tr, tr_src = measured_traffic96(role)
+            per["bytes_per_launch"] = alg
+            per["traffic"] = round(tr, 1) if tr else None
+            per["traffic_over_algorithmic"] = round(tr / alg, 3) if tr else None
+            per["traffic_source"] = tr_src
         if role == "attn_self":
             # the cache up to each slot's verified rows, keys and values, every block
             kv = float(np.sum(Ls + K + 1)) * 2 * cfg.d_model * 2
@@ -373,6 +400,8 @@ def run_batch(args):
               "config": r.pop("config")}
     result.update({k: v for k, v in r.items() if k not in ("steps", "warmup", "ms_per_step")})
     print(json.dumps(result), flush=True)
+    if args.pmc_run:
+        calibration_copy(log)
 
 
 def _b1_engine(log):
