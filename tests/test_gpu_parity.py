@@ -188,15 +188,18 @@ def test_micro_bf16_b64_wide_tiles():
 
 
 @pytest.mark.timeout(900)
-def test_micro_bf16_b64_cross_attention_by_pair():
-    """64 slots x 16 heads (1024 (head, slot) pairs), 900 frames: the bf16
-    cross-attention runs one block per pair over eight 128-frame chunks (the next
-    chunk's keys and values loaded during the current one, rows folded into
-    running maxima and sums); in the last chunk (frames 896..1023) only the first
-    wave holds frames, the other three are masked whole.  Planted drafts on six
-    followed slots."""
+@pytest.mark.parametrize("frames", [300, 900, 1300])
+def test_micro_bf16_b64_cross_attention_by_pair(frames):
+    """64 slots x 16 heads (1024 (head, slot) pairs): the bf16 cross-attention runs
+    one block per pair over the 128-frame chunks (the next chunk's keys and values
+    loaded during the current one, rows folded into running maxima and sums);
+    300 / 900 / 1300 frames take 3 / 8 / 11 chunks (odd and even counts of the
+    two alternating register sets).  The last chunk is ragged: at 900 frames
+    (896..1023) only its first wave holds frames and the other three are masked
+    whole, at 300 and 1300 (256..383, 1280..1407) the second wave ends inside
+    its frames.  Planted drafts on six followed slots."""
     from lockstep import Lockstep
-    cfg = MICRO_BF16.with_(name="micro-wide-900f", d_model=1024, n_head=16, d_ff=2560, n_frames=900)
+    cfg = MICRO_BF16.with_(name=f"micro-wide-{frames}f", d_model=1024, n_head=16, d_ff=2560, n_frames=frames)
     W = make_weights(cfg)
     n = 64
     lens = [int(x) for x in make_prefix_lengths(n, 1, 40, seed=303)]
@@ -208,7 +211,7 @@ def test_micro_bf16_b64_cross_attention_by_pair():
     rng = np.random.default_rng(9)
     for _ in range(4):
         ls.step(override=_planted_subset(ls, refs, rng))
-    print(f"micro-wide 900f b64: max |dlogit| draft {ls.max_dlogit:.3e} target {ls.max_tlogit:.3e}, "
+    print(f"micro-wide {frames}f b64: max |dlogit| draft {ls.max_dlogit:.3e} target {ls.max_tlogit:.3e}, "
           f"accepted {ls.accepted}, near ties {ls.near_ties}")
     assert ls.steps == 4 and max(ls.accepted) > 0
     ls.close()
