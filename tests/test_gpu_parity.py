@@ -119,6 +119,36 @@ def test_micro_bf16_b1_split_operands():
     ls.close()
 
 
+@pytest.mark.parametrize("d_model,batch", [(512, 1), (768, 1), (512, 3), (768, 3)])
+def test_bf16_other_widths(d_model, batch):
+    """bf16 at Whisper base and small widths (8 and 12 heads), 2003-token
+    vocabulary (a ragged last head tile) and 700 frames.  One slot: the folded
+    LayerNorm over 64 or 96 eight-column items per row, output-product column
+    groups of 64 or 96, sixteen k-splits of the second MLP product (one k-step
+    per wave), a 32-column head, five 128-frame chunks and a ragged 60; every
+    block is tapped, so each block's tap reaches the drafter through the next
+    block's query product and the last block's through the reduction kernel.
+    Three slots: two-plane operands over one 64-row block, the k-split residual
+    products, a 512-frame chunk and a ragged 188 merged.  Weights at std 0.05,
+    under which the greedy continuation varies (35-49 distinct tokens of 60)
+    rather than repeating one token."""
+    from lockstep import Lockstep
+    cfg = MICRO.with_(name=f"w{d_model}-bf16", dtype="bf16", n_layer=3, d_model=d_model, n_head=d_model // 64,
+                      d_ff=4 * d_model, n_vocab=2003, taps=(0, 1, 2), n_ctx=128, n_frames=700)
+    W = make_weights(cfg, std=0.05)
+    lens, max_new = [23, 7, 40][:batch], [60, 20, 45][:batch]
+    prompts = [make_prefix(cfg, i, n) for i, n in enumerate(lens)]
+    ls = Lockstep(cfg, W, prompts, max_new, TOL_BF16)
+    T = Target(cfg, W.values, OracleOpts(dtype=np.float32, kv_bf16=True))
+    refs = [plain_greedy(T, make_memory(cfg, i), prompts[i], max_new[i]) for i in range(batch)]
+    _run_planted(ls, refs, np.random.default_rng(9), 12)
+    print(f"{cfg.name} b{batch}: max |dlogit| draft {ls.max_dlogit:.3e} target {ls.max_tlogit:.3e}, "
+          f"near ties {ls.near_ties}")
+    assert ls.steps == 12
+    assert max(ls.accepted) > 0
+    ls.close()
+
+
 def test_micro_bf16_b1_offset_residual():
     """Batch 1, bf16, with a residual stream whose mean (about 4, from a shifted
     output bias of the first block) is tens of times its spread.  At batch 1 a
