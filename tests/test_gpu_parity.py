@@ -270,6 +270,28 @@ def test_micro_bf16_b96_width1280_all_slots():
     ls.close()
 
 
+def test_bf16_b96_width768_all_slots():
+    """96 slots at width 768 (12 heads), FFN 3072, 700 frames, two blocks: the
+    first MLP product takes the wide-tile kernel with 256-column tiles (3072 is
+    not a multiple of 320), q|k|v (2304 columns) the LDS-staged 64 x 64 GEMM,
+    the read-ahead blocks carry those widths, and the cross-attention runs one
+    block per (head, slot) over six 128-frame chunks, the last one ragged (60
+    frames).  Every slot is compared with the oracle."""
+    from lockstep import Lockstep
+    cfg = MICRO.with_(name="w768-bf16", dtype="bf16", d_model=768, n_head=12, d_ff=3072, n_vocab=2003,
+                      n_ctx=128, n_frames=700)
+    W = make_weights(cfg, std=0.05)
+    n = 96
+    lens = [int(x) for x in make_prefix_lengths(n, 1, 40, seed=303)]
+    prompts = [make_prefix(cfg, s, lens[s]) for s in range(n)]
+    ls = Lockstep(cfg, W, prompts, [30] * n, TOL_BF16)
+    for _ in range(3):
+        ls.step()
+    print(f"w768 b96: max |dlogit| draft {ls.max_dlogit:.3e} target {ls.max_tlogit:.3e}, near ties {ls.near_ties}")
+    assert ls.steps == 3 and sum(ls.live) >= n - 4
+    ls.close()
+
+
 @pytest.mark.timeout(900)
 # Several slots over many frames: bf16 cross-attention splits the frames into
 # chunks of 256 (997 = 3 x 256 + 229: the last chunk ends inside a 16-frame
