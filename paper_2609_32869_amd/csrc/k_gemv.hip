@@ -982,79 +982,6 @@ __global__ void __launch_bounds__(NW * 64) k_gemv32(GemvArgs a) {
   }
 }
 
-// ---------------------------------------------------------------- batch-1 head, persistent
-// Batch 1 (three split terms in one 32-row tile), 32-column tiles: a block walks
-// the column tiles tile = blockIdx.x + i gridDim.x.  The operand fragments of a
-// wave's k-steps are the same for every tile and stay in registers; the next
-// tile's weight fragments and epilogue prefetch are in flight while the current
-// tile is multiplied, reduced and finished.  The two sets of registers alternate
-// (a copy from one to the other would wait for its loads); past the last tile a
-// block re-reads its current one (from L2) instead of branching around the loads.
-constexpr int kHeadBlocks = 256;
-template <int EPI, int NW, int U>
-__global__ void __launch_bounds__(NW * 64) k_gemv32p(GemvArgs a) {
-  StampScope stamp_scope(a.stamp, NW * 64);
-  __shared__ float red[NW][32][33];
-  __shared__ float sv[32][33];
-  __shared__ float ov[EPI == EPI_ARGMAX ? 32 : 1][32];
-  __shared__ float oz[EPI == EPI_ARGMAX ? 32 : 1][32];
-  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
-  const int col = lane & 31, kg = lane >> 5;
-  const int KS = a.K / 16, ntile = (a.N + 31) / 32;
-  const int spw = (KS + NW - 1) / NW;
-  const int s0 = min(KS, wv * spw), s1 = min(KS, s0 + spw);
-  const bf16x8* W0 = reinterpret_cast<const bf16x8*>(a.w) + lane;
-  const bf16x8* Ab = reinterpret_cast<const bf16x8*>(a.a.p) + lane;
-  typedef EpiPre<32, NW * 64> Pre;
-  auto fetch = [&](int tile, bf16x8* w, Pre& p) {
-    p.template load<bf16, EPI>(a, tile * 32);
-    const bf16x8* Wt = W0 + (size_t)tile * KS * 64;
-#pragma unroll
-    for (int u = 0; u < U; ++u) w[u] = Wt[(size_t)min(s0 + u, KS - 1) * 64];
-  };
-  bf16x8 av[U], wa[U], wb[U];
-  Pre pa, pb;
-  auto finish = [&](int tile, const bf16x8* w, const Pre& p) {
-    floatx16 acc = {};
-#pragma unroll
-    for (int u = 0; u < U; ++u)
-      if (s0 + u < s1) acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[u], w[u], acc, 0, 0, 0);
-    __syncthreads();  // the previous tile's epilogue is done with red, sv, ov and oz
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int j = 0; j < 4; ++j) red[wv][8 * i + 4 * kg + j][col] = acc[4 * i + j];
-    __syncthreads();
-    for (int idx = threadIdx.x; idx < 32 * 32; idx += NW * 64) {
-      const int ml = idx >> 5, c = idx & 31;
-      float sum = 0.f;
-#pragma unroll
-      for (int w8 = 0; w8 < NW; ++w8) sum += red[w8][ml][c];
-      sv[ml][c] = sum;
-    }
-    __syncthreads();
-    RowsPre<32, 32, NW * 64> none;
-    finish_tile<bf16, EPI, 32, 32, NW * 64>(a, sv, ov, oz, a.mt0 * 32, tile * 32, p, none);
-  };
-  const int G = gridDim.x;
-  int tile = blockIdx.x;
-  fetch(tile, wa, pa);
-#pragma unroll
-  for (int u = 0; u < U; ++u) av[u] = Ab[((size_t)min(s0 + u, KS - 1) * a.a.mt + a.mt0) * 64];
-  for (;;) {
-    fetch(tile + G < ntile ? tile + G : tile, wb, pb);
-    __builtin_amdgcn_sched_barrier(0);
-    finish(tile, wa, pa);
-    tile += G;
-    if (tile >= ntile) break;
-    fetch(tile + G < ntile ? tile + G : tile, wa, pa);
-    __builtin_amdgcn_sched_barrier(0);
-    finish(tile, wb, pb);
-    tile += G;
-    if (tile >= ntile) break;
-  }
-}
-
 // ---------------------------------------------------------------- LayerNorm folded in (bf16, batch 1)
 // The block stages its operand in LDS itself (LnFold below): three bf16 split
 // terms per value (rows r, 9 + r, 18 + r; rows 27..31 zero) in the fragment order
@@ -1083,7 +1010,8 @@ __device__ __forceinline__ int lds_frag(int m, int k) {
 // spread over all the block's lanes, and every item leaves its sum and its sum of
 // squared deviations from its own mean; after the staging barrier wave r merges
 // row r's items (the pairwise update of Chan, Golub and LeVeque) in a fixed order
-// while the weight loads are still in flight.
+// while the weight loads are still in flight (with fewer than nine waves, wave w
+// merges rows w, w + NW, ...).
 template <int NW>
 struct LnFold {
   static constexpr int NT = NW * 64;
@@ -1091,7 +1019,7 @@ struct LnFold {
   // K/8: a lane's items share their 8 columns (one load of the gains) and lanes
   // >= S hold none.  K <= kLnFoldMaxK gives at most I items per lane.
   static constexpr int I = (kRows + NT / (kLnFoldMaxK / 8) - 1) / (NT / (kLnFoldMaxK / 8));
-  static_assert(NW >= kRows, "one wave per row merges the statistics");
+  static_assert(NT >= kLnFoldMaxK / 8, "a lane per column of the items");
   float x[I][8];
   uint4 g;
 
@@ -1159,13 +1087,15 @@ struct LnFold {
       aop[lds_frag<TILE>(3 * kRows + t / nch, 8 * (t % nch))] = make_uint4(0u, 0u, 0u, 0u);
   }
 
-  // Wave r < 9: merges row r's items into st[r] = mean and st[9 + r] = 1/sqrt(var + eps).
+  // Merges row r's items into st[r] = mean and st[9 + r] = 1/sqrt(var + eps), row r
+  // taken by wave r % NW.
   __device__ __forceinline__ static void row_stats(const GemvArgs& a, const float* ps, int pstride, float* st) {
-    const int lane = threadIdx.x & 63, r = threadIdx.x >> 6;
-    if (r >= kRows) return;
+    for (int r = (int)threadIdx.x >> 6; r < kRows; r += NW) row_stat(a, ps + r * pstride, r, st);
+  }
+  __device__ __forceinline__ static void row_stat(const GemvArgs& a, const float* p, int r, float* st) {
+    const int lane = threadIdx.x & 63;
     constexpr int J = (kLnFoldMaxK / 8 + 63) / 64;
     const int nch = a.K >> 3;
-    const float* p = ps + r * pstride;
     float sm[J], dv[J];
     float sum = 0.f;
 #pragma unroll
@@ -1191,6 +1121,102 @@ struct LnFold {
     }
   }
 };
+
+// ---------------------------------------------------------------- batch-1 head, persistent
+// Batch 1 (three split terms in one 32-row tile), 32-column tiles: a block walks
+// the column tiles tile = blockIdx.x + i gridDim.x.  The operand fragments of a
+// wave's k-steps are the same for every tile and stay in registers; the next
+// tile's weight fragments and epilogue prefetch are in flight while the current
+// tile is multiplied, reduced and finished.  The two sets of registers alternate
+// (a copy from one to the other would wait for its loads); past the last tile a
+// block re-reads its current one (from L2) instead of branching around the loads.
+// LN: the final LayerNorm folded in; each block stages the rows (LnFold) before its
+// first tile, behind its first weight loads, and the epilogue applies the rows'
+// statistics with the column sums of that LayerNorm.
+constexpr int kHeadBlocks = 256;
+template <int EPI, int NW, int U, bool LN>
+__global__ void __launch_bounds__(NW * 64) k_gemv32p(GemvArgs a) {
+  StampScope stamp_scope(a.stamp, NW * 64);
+  __shared__ float red[NW][32][33];
+  __shared__ float sv[32][33];
+  __shared__ float ov[EPI == EPI_ARGMAX ? 32 : 1][32];
+  __shared__ float oz[EPI == EPI_ARGMAX ? 32 : 1][32];
+  __shared__ uint4 aop[LN ? kLnFoldMaxK / 16 * 64 : 1];
+  __shared__ float lnst[LN ? 2 * kRows : 1];
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const int col = lane & 31, kg = lane >> 5;
+  const int KS = a.K / 16, ntile = (a.N + 31) / 32;
+  const int spw = (KS + NW - 1) / NW;
+  const int s0 = min(KS, wv * spw), s1 = min(KS, s0 + spw);
+  const bf16x8* W0 = reinterpret_cast<const bf16x8*>(a.w) + lane;
+  const bf16x8* Ab = reinterpret_cast<const bf16x8*>(a.a.p) + lane;
+  typedef EpiPre<32, NW * 64, LN> Pre;
+  auto fetch = [&](int tile, bf16x8* w, Pre& p) {
+    p.template load<bf16, EPI>(a, tile * 32);
+    const bf16x8* Wt = W0 + (size_t)tile * KS * 64;
+#pragma unroll
+    for (int u = 0; u < U; ++u) w[u] = Wt[(size_t)min(s0 + u, KS - 1) * 64];
+  };
+  bf16x8 av[U], wa[U], wb[U];
+  Pre pa, pb;
+  auto finish = [&](int tile, const bf16x8* w, const Pre& p) {
+    floatx16 acc = {};
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+      if (s0 + u < s1) acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[u], w[u], acc, 0, 0, 0);
+    __syncthreads();  // the previous tile's epilogue is done with red, sv, ov and oz
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) red[wv][8 * i + 4 * kg + j][col] = acc[4 * i + j];
+    __syncthreads();
+    for (int idx = threadIdx.x; idx < 32 * 32; idx += NW * 64) {
+      const int ml = idx >> 5, c = idx & 31;
+      float sum = 0.f;
+#pragma unroll
+      for (int w8 = 0; w8 < NW; ++w8) sum += red[w8][ml][c];
+      sv[ml][c] = sum;
+    }
+    __syncthreads();
+    RowsPre<32, 32, NW * 64> none;
+    finish_tile<bf16, EPI, 32, 32, NW * 64, false, LN>(a, sv, ov, oz, a.mt0 * 32, tile * 32, p, none, lnst);
+  };
+  const int G = gridDim.x;
+  int tile = blockIdx.x;
+  if constexpr (LN) {
+    // rows first, then the first tile's weights, then the staging (which waits for
+    // the rows alone); the item statistics of the nine rows sit packed in the
+    // reduction buffer, which the first tile's epilogue takes only after a barrier
+    constexpr int PS = 2 * (kLnFoldMaxK / 8);
+    static_assert(kRows * PS <= NW * 32 * 33, "item statistics fit the reduction buffer");
+    LnFold<NW> rows;
+    rows.load(a);
+    __builtin_amdgcn_sched_barrier(0);
+    fetch(tile, wa, pa);
+    __builtin_amdgcn_sched_barrier(0);
+    rows.template stage<32>(a, aop, &red[0][0][0], PS);
+    __syncthreads();
+    LnFold<NW>::row_stats(a, &red[0][0][0], PS, lnst);
+#pragma unroll
+    for (int u = 0; u < U; ++u) av[u] = __builtin_bit_cast(bf16x8, aop[lds_swz(min(s0 + u, KS - 1) * 64 + lane)]);
+  } else {
+    fetch(tile, wa, pa);
+#pragma unroll
+    for (int u = 0; u < U; ++u) av[u] = Ab[((size_t)min(s0 + u, KS - 1) * a.a.mt + a.mt0) * 64];
+  }
+  for (;;) {
+    fetch(tile + G < ntile ? tile + G : tile, wb, pb);
+    __builtin_amdgcn_sched_barrier(0);
+    finish(tile, wa, pa);
+    tile += G;
+    if (tile >= ntile) break;
+    fetch(tile + G < ntile ? tile + G : tile, wa, pa);
+    __builtin_amdgcn_sched_barrier(0);
+    finish(tile, wb, pb);
+    tile += G;
+    if (tile >= ntile) break;
+  }
+}
 
 // 16-column tiles; every wave's k-steps fit one batch of loads (K <= kLnFoldMaxK).
 template <int EPI, int NW, int U>
@@ -1504,16 +1530,17 @@ static void launch_epi(const GemvArgs& a, hipStream_t st) {
     return;
   } else {
   if constexpr (sizeof(S) == 2) {
-    if (a.lnx != nullptr) {
-      launch_ln<EPI>(a, st);
-      return;
-    }
     if constexpr (EPI == EPI_ARGMAX) {  // batch-1 vocabulary head: persistent blocks
       if (a.nsplit == 3 && a.wkind == W_F32 && a.mt1 - a.mt0 == 1 && (a.K / 16 + 7) / 8 <= kU) {
         const int ntile = (a.N + 31) / 32, per = (ntile + kHeadBlocks - 1) / kHeadBlocks;
-        k_gemv32p<EPI, 8, kU><<<(ntile + per - 1) / per, 512, 0, st>>>(a);
+        if (a.lnx != nullptr) k_gemv32p<EPI, 8, kU, true><<<(ntile + per - 1) / per, 512, 0, st>>>(a);
+        else k_gemv32p<EPI, 8, kU, false><<<(ntile + per - 1) / per, 512, 0, st>>>(a);
         return;
       }
+    }
+    if (a.lnx != nullptr) {
+      launch_ln<EPI>(a, st);
+      return;
     }
     const int ks = a.ksplit > 1 ? a.ksplit : 1;
     if (a.nsplit == 2 && a.wkind == W_F16) {  // several slots: 64 x 64 GEMM tiles (k split over grid y)

@@ -196,6 +196,7 @@ int compute_layout(const wf_config& c, Layout& L) {
   L.hproj_w = take(d * c.n_tap * d); L.hproj_b = take(d); L.mask = take(d);
   for (int l = 0; l < c.n_draft_layer; ++l) L.db.push_back(block());
   L.dlnf_g = take(d); L.dlnf_b = take(d);
+  L.c_head = takec(V); L.c_dhead = takec(V);
   L.weight_elems = w;
   L.pages_per_slot = c.n_ctx / kPage;
   // column blocks of the vocabulary head: 32-column tiles (bf16, batch 1), 64-column
@@ -677,7 +678,7 @@ struct Runner {
       }
     }
     if (ln_ready) a.a = Ad32();
-    else ln_operand(a, slot0, n, x, g, gb, Ad32(), false);
+    else ln_operand(a, slot0, n, x, g, gb, Ad32(), true, g == L.lnf_g ? L.c_head : L.c_dhead, c.n_vocab, 0);
     ln_ready = false;
     run_gemv("head", EPI_ARGMAX, n, a);
     launch("argmax_final", kRows * n * L.head_blocks * 8.0, [&](unsigned long long*) {
@@ -1038,6 +1039,16 @@ int wf_init_weights(wf_handle** out, const wf_config* cfg, const void* const* we
   if (!mats.empty()) {
     e = hipMemsetAsync(stage, 0, L.stage_bytes, st);
     if (e != hipSuccess) return cleanup(WF_EHIP, std::string("hipMemsetAsync: ") + hipGetErrorString(e));
+  }
+  if (cfg->dtype == WF_BF16 && L.nsplit_op == 3 && (size_t)cfg->d_model <= (size_t)kLnFoldMaxK) {
+    // the heads' column sums, from the caller's row-major embedding (manifest entry
+    // 0), now that both final LayerNorms are in place
+    float* cols = h->at<float>(L.lncd);
+    const int V = cfg->n_vocab, d = cfg->d_model;
+    ln_fold_cols(weights[0], wbase + L.lnf_g * eb, wbase + L.lnf_b * eb, V, d, cols + L.c_head, cols + L.c_head + V, st);
+    ln_fold_cols(weights[0], wbase + L.dlnf_g * eb, wbase + L.dlnf_b * eb, V, d, cols + L.c_dhead, cols + L.c_dhead + V, st);
+    e = hipGetLastError();
+    if (e != hipSuccess) return cleanup(WF_EHIP, std::string("ln_fold_cols: ") + hipGetErrorString(e));
   }
   // page table: logical page j of slot s -> physical page j * max_batch + s
   std::vector<int> pt((size_t)cfg->max_batch * L.pages_per_slot);

@@ -36,6 +36,9 @@ struct Layout {
   size_t total;
   // element offsets inside the weight region
   size_t tok_emb, pos_emb, lnf_g, lnf_b, hproj_w, hproj_b, mask, dlnf_g, dlnf_b;
+  // fp32 offsets (column-sum region) of the heads' c then e: the final LayerNorm of
+  // the target (lnf) and of the drafter (dlnf) folded into the vocabulary product
+  size_t c_head, c_dhead;
   std::vector<BlockW> tb, db;
   size_t weight_elems;
   int pages_per_slot, head_blocks;
