@@ -986,10 +986,6 @@ __global__ void __launch_bounds__(NW * 64) k_gemv32(GemvArgs a) {
 // The block stages its operand in LDS itself (LnFold below): three bf16 split
 // terms per value (rows r, 9 + r, 18 + r; rows 27..31 zero) in the fragment order
 // of its tile shape.
-__device__ __forceinline__ uint4 pack8(const uint32_t* h) {
-  return make_uint4(h[0] | ((uint32_t)h[1] << 16), h[2] | ((uint32_t)h[3] << 16), h[4] | ((uint32_t)h[5] << 16),
-                    h[6] | ((uint32_t)h[7] << 16));
-}
 
 // LDS slot of operand chunk (row m, k..k+7): fragment order with the 16-byte slot
 // inside each 256-byte group XOR-swizzled by the group index, so that both the
@@ -1064,9 +1060,9 @@ struct LnFold {
           const float dx = x[i][e] - m;
           dev = fmaf(dx, dx, dev);
         }
-        aop[lds_frag<TILE>(r, 8 * c)] = pack8(th);
-        aop[lds_frag<TILE>(kRows + r, 8 * c)] = pack8(tm);
-        aop[lds_frag<TILE>(2 * kRows + r, 8 * c)] = pack8(tl);
+        aop[lds_frag<TILE>(r, 8 * c)] = pack8_bits(th);
+        aop[lds_frag<TILE>(kRows + r, 8 * c)] = pack8_bits(tm);
+        aop[lds_frag<TILE>(2 * kRows + r, 8 * c)] = pack8_bits(tl);
         ps[r * pstride + c] = sum;
         ps[r * pstride + nch + c] = dev;
         if (a.tap >= 0 && t % (int)gridDim.x == (int)blockIdx.x) {
@@ -1077,9 +1073,9 @@ struct LnFold {
           for (int e = 0; e < 8; ++e) split3_bits(x[i][e], xh[e], xm[e], xl[e]);
           uint4* T = reinterpret_cast<uint4*>(a.aout.p);
           const int row = a.slot0 * kRows + r, col = a.tap * a.K + 8 * c;
-          T[afrag16_index(row, col, a.aout.mt) / 8] = pack8(xh);
-          T[afrag16_index(a.R9 + row, col, a.aout.mt) / 8] = pack8(xm);
-          T[afrag16_index(2 * a.R9 + row, col, a.aout.mt) / 8] = pack8(xl);
+          T[afrag16_index(row, col, a.aout.mt) / 8] = pack8_bits(xh);
+          T[afrag16_index(a.R9 + row, col, a.aout.mt) / 8] = pack8_bits(xm);
+          T[afrag16_index(2 * a.R9 + row, col, a.aout.mt) / 8] = pack8_bits(xl);
         }
       }
     }

@@ -48,8 +48,9 @@ struct Touch {
 // Row blocks (64 rows) from which the step reads weights ahead (about 57 slots)
 constexpr int kTouchMinRowBlocks = 8;
 
-// Block b of nb reads bytes [0, bytes) of p, 16 bytes per thread and eight loads
-// in flight, and discards the values (the empty asm keeps the loads).
+// Block b of the t.blocks reading blocks reads its share of bytes [0, t.bytes) of
+// t.p, 16 bytes per thread and eight loads in flight, and discards the values (the
+// empty asm keeps the loads).
 __device__ inline void touch_range(const Touch& t, unsigned b) {
   typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
   const u32x4* q = static_cast<const u32x4*>(t.p);
