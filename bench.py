@@ -43,7 +43,7 @@ SYMBOL_OF_ROLE = {  # kernels (rocprofv3 names) that one launch of the role disp
     "gemv_fc1": ("void wf::k_gemv32_ln<1, 16, 5>(wf::GemvArgs)",),
     "gemv_fc2": ("void wf::k_gemv16k<6, 8, 4, 2>(wf::GemvArgs)",),  # k_gemv16k<5, 8, 4, 2> in the tap blocks
     "reduce_ln": ("void wf::k_reduce_ln<wf::bf16>(wf::RlnArgs)",),
-    "head": ("void wf::k_gemv32p<4, 8, 10>(wf::GemvArgs)",),
+    "head": ("void wf::k_gemv32p<4, 8, 10, true>(wf::GemvArgs)",),
 }
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic_large-v3_b1_pmc.md")
 
@@ -89,7 +89,7 @@ KERNEL_OF_ROLE = {
     "gemv_fc1": "wf::k_gemv32_ln<1, 16, 5> (EPI_GELU, LayerNorm folded)",
     "gemv_fc2": "wf::k_gemv16k<6, 8, 4, 2> (EPI_ACC, split-K into the residual; EPI_PART in the tap blocks)",
     "reduce_ln": "wf::k_reduce_ln<wf::bf16>",
-    "head": "wf::k_gemv32p<4, 8, 10> (EPI_ARGMAX, persistent blocks)",
+    "head": "wf::k_gemv32p<4, 8, 10, true> (EPI_ARGMAX, persistent blocks, final LayerNorm folded)",
 }
 
 
@@ -120,14 +120,19 @@ def gemv_flops_per_step(cfg):
 
 
 def plan_planted(traj, L0, e0, n_steps, cfg, rng, k_max=None):
-    """Planted draft blocks and the acceptance each must produce."""
+    """Planted draft blocks and, per step, the tokens it must emit minus one (-1:
+    the slot has finished).  traj is the slot's plain greedy continuation; when it
+    ends with the end-of-transcript token, the step that reaches that token emits
+    up to and including it and the slot finishes (Section 3.1 with Appendix A.1)."""
     from wf_fixtures import plant_drafts
     K, V = cfg.block_k, cfg.n_vocab
     k_max = K if k_max is None else k_max
+    n_traj = len(traj)
+    ends_eos = n_traj > 0 and int(traj[-1]) == cfg.eos_id
     plans, accs = [], []
     e, L = e0, L0
     for _ in range(n_steps):
-        if L >= cfg.n_ctx or e >= cfg.n_ctx:  # finished (context end or budget): nothing emitted
+        if L >= cfg.n_ctx or e >= cfg.n_ctx or (ends_eos and e >= n_traj):  # finished: nothing emitted
             plans.append(np.zeros(K, np.int32))
             accs.append(-1)
             continue
@@ -137,13 +142,28 @@ def plan_planted(traj, L0, e0, n_steps, cfg, rng, k_max=None):
         r = int(rng.integers(0, K + 1))
         dr = plant_drafts(cont, r, V, rng)
         a = 0
-        while a < k and e + a < len(traj) and dr[a] == traj[e + a]:
+        while a < k and e + a < n_traj and dr[a] == traj[e + a]:
             a += 1
+        if ends_eos and e + a >= n_traj - 1:  # the transcript's last token is among this step's
+            a = n_traj - 1 - e
         plans.append(dr)
         accs.append(a)
         e += a + 1
         L += a + 1
     return np.stack(plans).astype(np.int32), np.array(accs)
+
+
+def first_mismatch(emitted, accs, trajs, eos):
+    """The first (slot, step) whose emitted count differs from the plan, with
+    whether that slot's continuation ends in the end-of-transcript token."""
+    want = np.asarray(accs) + 1
+    for s in range(emitted.shape[0]):
+        bad = np.nonzero(emitted[s] != want[s])[0]
+        if len(bad):
+            j = int(bad[0])
+            return {"slot": s, "step": j, "emitted": int(emitted[s][j]), "planned": int(want[s][j]),
+                    "continuation_ends_eos": bool(len(trajs[s]) and int(trajs[s][-1]) == eos)}
+    return None
 
 
 def blas_threads():
@@ -290,6 +310,8 @@ def batch_workload(args, W, B, steps, warmup, profile_steps, log, cpu_sample=Tru
     tokens = int(em[warmup:warmup + steps].sum())
     live_steps = int((em[warmup:warmup + steps] > 0).sum())
     planted_ok = bool(np.array_equal(em[:warmup + steps].T, np.stack(accs)[:, :warmup + steps] + 1))
+    mismatch = None if planted_ok else first_mismatch(em[:warmup + steps].T, np.stack(accs)[:, :warmup + steps],
+                                                       [traj[s][traj[s] >= 0] for s in range(B)], cfg.eos_id)
     Ls = eng.state()[:B, 0].cpu().numpy().astype(np.int64)
 
     # profiled replays (kernel-stamped timeline), the first one discarded
@@ -341,7 +363,7 @@ def batch_workload(args, W, B, steps, warmup, profile_steps, log, cpu_sample=Tru
         "verified_tokens_per_s": round(tokens / (total_ms / 1e3), 2),
         "step": {"median_ms": round(float(np.median(step_ms)), 4), "verified_rows_per_step": rows * B,
                  "tokens_per_live_slot_step": round(tokens / max(live_steps, 1), 3), "live_slot_steps": live_steps,
-                 "planted_acceptance_exact": planted_ok},
+                 "planted_acceptance_exact": planted_ok, "planted_mismatch": mismatch},
         "roofline": {"bound": "mfma", "achieved": round(achieved, 1), "peak": MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
                      "frac": round(achieved / MFMA_PEAK_TFLOPS, 4), "traffic": None,
                      "kernel": role, "flops_per_launch": fl, "avg_launch_us": round(1e3 * v["ms"] / v["launches"], 3),
