@@ -213,12 +213,20 @@ __device__ __forceinline__ void set_pass_pages(const BeginArgs& a, int slot, int
   st[ST_PG1] = pt[min(p + 1, a.pages_per_slot - 1)];
 }
 
+// Zeroes the slot's nine history-projection rows (a.hp; d a multiple of 4).
+__device__ __forceinline__ void clear_hp(const BeginArgs& a, int slot) {
+  if (a.hp == nullptr) return;
+  float4* r = reinterpret_cast<float4*>(a.hp + (size_t)slot * kRows * a.d);
+  for (int t = threadIdx.x; t < kRows * a.d / 4; t += blockDim.x) r[t] = make_float4(0.f, 0.f, 0.f, 0.f);
+}
+
 // Verify rows: [anchor, c_1..c_k] at positions L..L+k with the budget rule
 // k = min(K, k_max, max_new - emitted - 1, n_ctx - L - 1) (Appendix A.1).
 template <typename S>
 __global__ void __launch_bounds__(256) k_verify_begin(BeginArgs a) {
   __shared__ int toks[kRows], poss[kRows];
   const int slot = a.slot0 + blockIdx.x;
+  clear_hp(a, slot);
   int* st = a.state + slot * kStateInts;
   const int L = st[ST_L], left = st[ST_MAX_NEW] - st[ST_EMITTED], anchor = st[ST_ANCHOR];
   const bool go = st[ST_LIVE] && !st[ST_DONE] && left > 0 && L < a.n_ctx;
@@ -270,6 +278,7 @@ template <typename S>
 __global__ void __launch_bounds__(256) k_prefill_begin(BeginArgs a) {
   __shared__ int toks[kRows], poss[kRows];
   const int slot = a.slot0 + blockIdx.x;
+  clear_hp(a, slot);
   int* st = a.state + slot * kStateInts;
   const int len = st[ST_LEN];
   const int pos0 = a.chunk * kRows;

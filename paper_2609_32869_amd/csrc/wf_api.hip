@@ -687,12 +687,29 @@ struct Runner {
     });
   }
 
+  // Batch 1 (bf16): the history projection (K = n_tap d) split over k into about
+  // 240 blocks of 64 columns whose partial sums add into the projection rows,
+  // which the pass's set-up kernel cleared; 0 (one launch storing the rows) otherwise.
+  int hproj_split() const {
+    if (!fuse_oproj() || (c.draft_flags & WF_DRAFT_NO_HISTORY)) return 0;
+    const int tiles64 = (c.d_model + 63) / 64, ksteps = c.n_tap * c.d_model / 32;
+    return std::max(1, std::min(240 / tiles64, ksteps));
+  }
+  float* hp_clear() { return hproj_split() > 0 ? F32(L.hp) : nullptr; }
+
   // drafter history for pending rows (Appendix A.2): taps -> W_h -> per-block LN, k (RoPE), v
   void history_apply(int slot0, int n) {
     if (c.draft_flags & WF_DRAFT_NO_HISTORY) return;  // the variant keeps no history
     const int d = c.d_model;
     float *hp = F32(L.hp), *kvh = F32(L.kvh);
-    gemv("gemv_hproj", EPI_STORE, slot0, n, Atap16(), L.hproj_w, L.hproj_b, c.n_tap * d, d, hp, d);
+    if (const int ks = hproj_split()) {
+      GemvArgs a = gemv_args(slot0, n, Atap16(), L.hproj_w, L.hproj_b, c.n_tap * d, d, hp, d,
+                             Operand{nullptr, 0, OP_ROW, 0}, -1);
+      a.ksplit = ks;
+      run_gemv("gemv_hproj", EPI_ACC, n, a);
+    } else {
+      gemv("gemv_hproj", EPI_STORE, slot0, n, Atap16(), L.hproj_w, L.hproj_b, c.n_tap * d, d, hp, d);
+    }
     for (int dl = 0; dl < c.n_draft_layer; ++dl) {
       const BlockW& b = L.db[dl];
       // rows d..3d of the concatenated q|k|v matrix start d*d elements in, in either order
@@ -754,6 +771,7 @@ struct Runner {
     ba.block_k = c.block_k; ba.k_max = k_max;
     ba.page_table = I32(L.page_table); ba.pages_per_slot = L.pages_per_slot;
     ba.status = h->at<unsigned>(L.status);
+    ba.hp = hp_clear();
     launch("begin", 0, [&](unsigned long long*) { Ops<S>::verify_begin(ba, n, st); });
     target_forward(slot0, n);
     head(slot0, n, F32(L.h), L.lnf_g, L.lnf_b, h->debug || sampling() ? F32(L.logits) : nullptr, nullptr, nullptr, 0,
@@ -841,6 +859,7 @@ struct Runner {
     ba.h = F32(L.h); ba.slot0 = slot0; ba.d = c.d_model; ba.n_vocab = c.n_vocab; ba.n_ctx = c.n_ctx;
     ba.block_k = c.block_k; ba.pmax = pmax;
     ba.page_table = I32(L.page_table); ba.pages_per_slot = L.pages_per_slot;
+    ba.hp = hp_clear();
     for (int ch = 0; ch < nchunks; ++ch) {
       ba.chunk = ch;
       Ops<S>::prefill_begin(ba, n, st);

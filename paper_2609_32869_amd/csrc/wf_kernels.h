@@ -253,6 +253,8 @@ struct BeginArgs {
   int slot0, d, n_vocab, n_ctx, block_k, k_max, chunk, pmax;
   unsigned* status;  // sticky device status word (verify: position overflow), or null
   const void* pos2;  // drafter with absolute positions: position table added to row i at t + i, else null
+  float* hp;  // target passes: history-projection rows [slot][9][d] cleared for the split-K
+              // product at the pass's end (its k-splits add into them), or null
 };
 
 struct HistArgs {
