@@ -601,70 +601,91 @@ __global__ void __launch_bounds__(kXrThreads, 4) k_attn_cross_rows(CrossArgs a) 
 
 
 // ---------------------------------------------------------------- fused attention output product (one slot)
-// Items t < 2C (C = N / kOpGroups columns in group g): column c = gC + t % C and
-// half hs = t / C of the head's two 32-dim k-steps.  op_load fetches the item's
-// weights (four 8-element fragment pieces) and bias at block start; op_apply forms
-// the nine partial sums from the head's output rows in LDS and adds them to h
-// (the bias once, by head 0's first half).  Threads past the items re-read the
-// last one and add nothing.
+// Group g of C = N / kOpGroups columns, C / 16 tiles of 16 on the matrix cores:
+// wave w < C / 16 takes tile T = g C / 16 + w over the head's two 32-dim k-steps.
+// op_load fetches the wave's two weight fragments (lane l: column 16 T + l % 16,
+// k-group l / 16, in the weights' fragment order) and each lane's column bias at
+// block start.  op_apply splits the head's output rows (fp32, in LDS) into three
+// bf16 terms as a 27-row operand (two 16-row tiles, rows 9 e + r holding term e of
+// row r, so the products are exact in fp32), multiplies, adds each row's three
+// terms and adds the nine rows to h with one atomic per (row, column) (the bias
+// once, by head 0).
 struct OpPre {
-  uint4 w[4];
+  bf16x8 w[2];
   uint32_t b;
 };
-// OWNED: threads t >= 2C load nothing (their registers get defined values from an
-// empty asm, so no copy at the join waits for the other threads' loads); only for a
-// kernel whose next waits also cover younger loads, since the compiler counts
-// outstanding loads on the path without these.  Otherwise every thread loads (index
-// clamped), which keeps the count of younger loads exact.
+constexpr int kOpTerms = 3 * kRows;            // operand rows that hold terms
+constexpr int kOpTiles = kOpMaxCols / 16;      // column tiles of a group at most
+// OWNED: waves past the group's tiles load nothing (their registers get defined
+// values from an empty asm, so no copy at the join waits for the other waves'
+// loads); only for a kernel whose next waits also cover younger loads, since the
+// compiler counts outstanding loads on the path without these.  Otherwise every
+// wave loads (tile clamped), which keeps the count of younger loads exact.
 template <bool OWNED>
 __device__ __forceinline__ void op_load(const OprojArgs& op, int head, int g, int t, OpPre& pre) {
-  const int C = op.N / kOpGroups, KS = op.K / 32;
-  if (!OWNED) t = min(t, 2 * C - 1);
-  if (!OWNED || t < 2 * C) {
-    const int c = g * C + t % C, hs = t / C;
-    const uint4* wp = reinterpret_cast<const uint4*>(op.w) + ((size_t)(c >> 4) * KS + 2 * head + hs) * 64 + (c & 15);
-#pragma unroll
-    for (int kq = 0; kq < 4; ++kq) pre.w[kq] = wp[16 * kq];
-    pre.b = reinterpret_cast<const uint16_t*>(op.bias)[c];
+  const int nt = op.N / kOpGroups / 16, KS = op.K / 32, lane = t & 63;
+  int w = t >> 6;
+  if (!OWNED) w = min(w, nt - 1);
+  if (!OWNED || w < nt) {
+    const int T = g * nt + w;
+    const bf16x8* wp = reinterpret_cast<const bf16x8*>(op.w) + ((size_t)T * KS + 2 * head) * 64 + lane;
+    pre.w[0] = wp[0];
+    pre.w[1] = wp[64];
+    pre.b = reinterpret_cast<const uint16_t*>(op.bias)[16 * T + (lane & 15)];
   } else {
 #pragma unroll
-    for (int kq = 0; kq < 4; ++kq) __asm__ volatile("" : "=v"(pre.w[kq]));
+    for (int s = 0; s < 2; ++s) __asm__ volatile("" : "=v"(pre.w[s]));
     __asm__ volatile("" : "=v"(pre.b));
   }
 }
-// Every thread of the block calls it (it holds a barrier).  Thread t < 2C owns
-// column c and half hs of the head's 64 dims; the two halves meet in LDS (half)
-// so each (row, column) of the residual takes one atomic add per head.
+// Every thread of the block (nt threads of 64 at least) calls it; it holds barriers.
+// aop: the operand's 2 x 2 fragments; part: each wave's 27 x 16 products.
 __device__ __forceinline__ void op_apply(const OprojArgs& op, int head, int g, int t, const OpPre& pre,
-                                         const float (*Ob)[64], int row0, float (*half)[kOpMaxCols]) {
-  const int C = op.N / kOpGroups;
-  const bool act = t < 2 * C;
-  const int c = g * C + t % C, hs = t / C;
-  float acc[kRows];
+                                         const float (*Ob)[64], int row0, uint4 (*aop)[64],
+                                         float (*part)[kOpTerms][16]) {
+  const int nt = op.N / kOpGroups / 16, lane = t & 63, w = t >> 6;
+  // fragment (tile mt, k-step s), lane l: operand row 16 mt + l % 16, dims 32 s + 8 (l / 16) .. + 7
+  for (int i = t; i < 4 * 64; i += blockDim.x) {
+    const int mt = i >> 7, st = (i >> 6) & 1, l = i & 63, R = 16 * mt + (l & 15), k0 = 32 * st + 8 * (l >> 4);
+    uint32_t bits[8] = {0u, 0u, 0u, 0u, 0u, 0u, 0u, 0u};
+    if (R < kOpTerms) {
+      const int e = R / kRows, r = R - e * kRows;
 #pragma unroll
-  for (int r = 0; r < kRows; ++r) acc[r] = 0.f;
-  if (act) {
-#pragma unroll
-  for (int kq = 0; kq < 4; ++kq) {
-    const uint4 v = pre.w[kq];
-    const float w8[8] = {__uint_as_float(v.x << 16), __uint_as_float(v.x & 0xffff0000u), __uint_as_float(v.y << 16),
-                         __uint_as_float(v.y & 0xffff0000u), __uint_as_float(v.z << 16), __uint_as_float(v.z & 0xffff0000u),
-                         __uint_as_float(v.w << 16), __uint_as_float(v.w & 0xffff0000u)};
-#pragma unroll
-    for (int j = 0; j < 8; ++j)
-#pragma unroll
-      for (int r = 0; r < kRows; ++r) acc[r] = fmaf(Ob[r][32 * hs + 8 * kq + j], w8[j], acc[r]);
-  }
-  }
-  if (act && hs == 1) {
-#pragma unroll
-    for (int r = 0; r < kRows; ++r) half[r][t - C] = acc[r];
+      for (int j = 0; j < 8; ++j) {
+        uint32_t hi, mid, lo;
+        split3_bits(Ob[r][k0 + j], hi, mid, lo);
+        bits[j] = e == 0 ? hi : e == 1 ? mid : lo;
+      }
+    }
+    aop[2 * mt + st][l] = pack8_bits(bits);
   }
   __syncthreads();
-  if (act && hs == 0) {
-    const float b = head == 0 ? __uint_as_float(pre.b << 16) : 0.f;
+  if (w < nt) {
+    floatx4 acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int r = 0; r < kRows; ++r) atomicAdd(op.h + (size_t)(row0 + r) * op.ldh + c, (acc[r] + half[r][t]) + b);
+    for (int st = 0; st < 2; ++st) {
+      acc0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, aop[st][lane]), pre.w[st], acc0, 0, 0, 0);
+      acc1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, aop[2 + st][lane]), pre.w[st], acc1, 0, 0,
+                                                     0);
+    }
+    // lane l holds column l % 16 of operand rows 4 (l / 16) + v (and 16 + ...)
+    const int col = lane & 15, kg = lane >> 4;
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      part[w][4 * kg + v][col] = acc0[v];
+      if (16 + 4 * kg + v < kOpTerms) part[w][16 + 4 * kg + v][col] = acc1[v];
+    }
+  }
+  __syncthreads();
+  if (w < nt) {
+    // item i = lane + 64 j: row i / 16, column i % 16 (= lane % 16, whose bias the lane holds)
+    const int T = g * nt + w;
+    const float b = head == 0 ? __uint_as_float(pre.b << 16) : 0.f;
+    for (int i = lane; i < kRows * 16; i += 64) {
+      const int r = i >> 4, cc = i & 15;
+      const float v = (part[w][r][cc] + part[w][kRows + r][cc]) + part[w][2 * kRows + r][cc];
+      atomicAdd(op.h + (size_t)(row0 + r) * op.ldh + 16 * T + cc, v + b);
+    }
   }
 }
 
@@ -983,12 +1004,14 @@ __global__ void __launch_bounds__(NW * 64) k_attn_cross_pair(CrossArgs a) {
 // together (indices clamped, chunks past the end weighted 0); groups combine with
 // the same max-shifted rule.  With a fused output product (grid z = column group)
 // the merged rows go to LDS and the block adds their product to h.
-constexpr int kXmThreads = 640;  // >= the fused product's 2C items
+constexpr int kXmThreads = 640;  // a wave per column tile of the fused product's group
+static_assert(kXmThreads / 64 >= kOpTiles, "merge blocks hold a wave per column tile");
 template <typename S, bool FUSED, int G>
 __global__ void __launch_bounds__(kXmThreads) k_attn_cross_merge(CrossArgs a) {
   StampScope stamp_scope(a.stamp, kXmThreads);
   __shared__ float Ob[kRows][64];
-  __shared__ float ophalf[FUSED ? kRows : 1][kOpMaxCols];  // fused output product: second halves
+  __shared__ uint4 opa[FUSED ? 4 : 1][64];                          // fused output product: operand
+  __shared__ float oppart[FUSED ? kOpTiles : 1][kOpTerms][16];     // and its products per wave
   const int head = blockIdx.x, slot = a.slot0 + blockIdx.y, g = blockIdx.z;
   // FUSED: the output product's weights are loaded unconditionally (a branch around
   // them would make the record loads below wait for them)
@@ -1041,7 +1064,7 @@ __global__ void __launch_bounds__(kXmThreads) k_attn_cross_merge(CrossArgs a) {
   }
   if constexpr (FUSED) {
     __syncthreads();
-    op_apply(a.op, head, g, t, opre, Ob, slot * kRows, ophalf);
+    op_apply(a.op, head, g, t, opre, Ob, slot * kRows, opa, oppart);
   }
 }
 
@@ -1110,6 +1133,7 @@ __global__ void __launch_bounds__(kSelfThreads) k_attn_self(AttnArgs a) {
 // LDS.  Rows i >= nv are padding and get zeros.
 constexpr int kSxWaves = kMaxCtx / 32;
 constexpr int kSxThreads = kSxWaves * 64;
+static_assert(kSxWaves >= kOpTiles, "self-attention blocks hold a wave per column tile of the fused product");
 template <bool FUSED>
 __global__ void __launch_bounds__(kSxThreads) k_attn_self_mx(AttnArgs a) {
   StampScope stamp_scope(a.stamp, kSxThreads);
@@ -1117,7 +1141,8 @@ __global__ void __launch_bounds__(kSxThreads) k_attn_self_mx(AttnArgs a) {
   __shared__ float wsum[kSxWaves][16];
   __shared__ float wo[kSxWaves][kRows][64];
   __shared__ float Ob[kRows][64];
-  __shared__ float ophalf[FUSED ? kRows : 1][kOpMaxCols];  // fused output product: second halves
+  __shared__ uint4 opa[FUSED ? 4 : 1][64];                          // fused output product: operand
+  __shared__ float oppart[FUSED ? kOpTiles : 1][kOpTerms][16];     // and its products per wave
   const int head = blockIdx.x, slot = a.slot0 + blockIdx.y, g = blockIdx.z;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, n = lane & 15, kg = lane >> 4;
   const int* st = a.state + slot * kStateInts;
@@ -1264,7 +1289,7 @@ __global__ void __launch_bounds__(kSxThreads) k_attn_self_mx(AttnArgs a) {
   }
   if constexpr (FUSED) {
     __syncthreads();
-    op_apply(a.op, head, g, threadIdx.x, opre, Ob, slot * kRows, ophalf);
+    op_apply(a.op, head, g, threadIdx.x, opre, Ob, slot * kRows, opa, oppart);
   }
 }
 

@@ -447,7 +447,9 @@ struct Runner {
   // Batch 1 with bf16 storage: the attention output products are fused into the
   // attention kernels (h += O W + b through atomic adds); a group's d / kOpGroups
   // columns (two threads each) must fit the merge kernel's block.
-  bool fuse_oproj() const { return frag() && L.nsplit_op == 3 && c.d_model / kOpGroups <= kOpMaxCols; }
+  bool fuse_oproj() const {
+    return frag() && L.nsplit_op == 3 && c.d_model / kOpGroups <= kOpMaxCols && (c.d_model / kOpGroups) % 16 == 0;
+  }
   OprojArgs oproj(size_t w, size_t b) {
     if (!fuse_oproj()) return OprojArgs{};
     return OprojArgs{W(w), W(b), F32(L.h), (int)c.d_model, (int)c.d_model, (int)c.d_model};
