@@ -160,21 +160,33 @@ __global__ void __launch_bounds__(256) k_argmax_final(const float* __restrict__ 
 
 // ---------------------------------------------------------------- pass set-up
 // Rows of a pass: h[slot * 9 + i] = E[toks[i]] + P[pos[i]] (target) or E[anchor] /
-// mask vector (drafter).  Work is split into 8-column chunks, every load of a
-// thread issued before the first add.
-constexpr int kBeginTasks = 9;  // chunk tasks per thread: 9 rows * 2048 / 8 / 256
+// mask vector (drafter).  A slot's rows are split over kBeginGroups blocks by
+// 8-column chunks (block g takes chunks [g nch / G, (g + 1) nch / G)), every
+// load of a thread issued before the first add; each block works out the pass's
+// tokens and positions itself, and block 0 alone writes the slot's state.
+constexpr int kBeginGroups = 8;
+constexpr int kBeginTasks = 2;  // chunk tasks per thread: 9 rows * 2048 / 8 / 8 / 256, rounded up
+struct BeginCols {
+  int cb, ce;  // this block's 8-column chunks
+  __device__ __forceinline__ BeginCols(int d) {
+    const int nch = d >> 3;
+    cb = (int)blockIdx.y * nch / kBeginGroups;
+    ce = ((int)blockIdx.y + 1) * nch / kBeginGroups;
+  }
+};
 template <typename S>
-__device__ __forceinline__ void fill_rows(const BeginArgs& a, int slot, const int* toks, const int* poss, bool mask_rows) {
+__device__ __forceinline__ void fill_rows(const BeginArgs& a, int slot, const int* toks, const int* poss, bool mask_rows,
+                                          BeginCols bc) {
   const S* E = reinterpret_cast<const S*>(a.emb);
   const S* P = reinterpret_cast<const S*>(a.pos);
-  const int nch = a.d >> 3;
+  const int nc = max(bc.ce - bc.cb, 1);
   float e8[kBeginTasks][8], p8[kBeginTasks][8];
   // every load unconditionally (tasks past the nine rows re-read row 8), so all
   // chunks are in flight together; rows that take no embedding / no position
   // read one anyway and zero it below
 #pragma unroll
   for (int j = 0; j < kBeginTasks; ++j) {
-    const int t = threadIdx.x + 256 * j, i = min(t / nch, kRows - 1), c = 8 * (t % nch);
+    const int t = threadIdx.x + 256 * j, i = min(t / nc, kRows - 1), c = 8 * min(bc.cb + t % nc, (a.d >> 3) - 1);
     const int tok = toks[i];
     const size_t ei = a.emb_kind == W_F32   ? wfrag32_index(tok, c, a.d / 16)
                       : a.emb_kind == W_F16 ? wfrag16_index(tok, c, a.d / 32)
@@ -184,7 +196,7 @@ __device__ __forceinline__ void fill_rows(const BeginArgs& a, int slot, const in
   }
 #pragma unroll
   for (int j = 0; j < kBeginTasks; ++j) {
-    const int t = threadIdx.x + 256 * j, i = t / nch;
+    const int t = threadIdx.x + 256 * j, i = t / nc;
     if (mask_rows) {  // draft block: row 0 is the anchor's embedding, rows 1.. the mask vector
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
@@ -195,8 +207,8 @@ __device__ __forceinline__ void fill_rows(const BeginArgs& a, int slot, const in
   }
 #pragma unroll
   for (int j = 0; j < kBeginTasks; ++j) {
-    const int t = threadIdx.x + 256 * j, i = t / nch, c = 8 * (t % nch);
-    if (i < kRows) {
+    const int t = threadIdx.x + 256 * j, i = t / nc, c = 8 * (bc.cb + t % nc);
+    if (i < kRows && bc.ce > bc.cb) {
       float* hr = a.h + (size_t)(slot * kRows + i) * a.d + c;
       *reinterpret_cast<float4*>(hr) = make_float4(e8[j][0] + p8[j][0], e8[j][1] + p8[j][1], e8[j][2] + p8[j][2], e8[j][3] + p8[j][3]);
       *reinterpret_cast<float4*>(hr + 4) =
@@ -213,11 +225,14 @@ __device__ __forceinline__ void set_pass_pages(const BeginArgs& a, int slot, int
   st[ST_PG1] = pt[min(p + 1, a.pages_per_slot - 1)];
 }
 
-// Zeroes the slot's nine history-projection rows (a.hp; d a multiple of 4).
-__device__ __forceinline__ void clear_hp(const BeginArgs& a, int slot) {
+// Zeroes the block's columns of the slot's nine history-projection rows (a.hp).
+__device__ __forceinline__ void clear_hp(const BeginArgs& a, int slot, BeginCols bc) {
   if (a.hp == nullptr) return;
-  float4* r = reinterpret_cast<float4*>(a.hp + (size_t)slot * kRows * a.d);
-  for (int t = threadIdx.x; t < kRows * a.d / 4; t += blockDim.x) r[t] = make_float4(0.f, 0.f, 0.f, 0.f);
+  const int n4 = 2 * (bc.ce - bc.cb);  // float4 per row
+  for (int t = threadIdx.x; t < kRows * n4; t += blockDim.x) {
+    const int i = t / n4, q = t - i * n4;
+    reinterpret_cast<float4*>(a.hp + (size_t)(slot * kRows + i) * a.d + 8 * bc.cb)[q] = make_float4(0.f, 0.f, 0.f, 0.f);
+  }
 }
 
 // Verify rows: [anchor, c_1..c_k] at positions L..L+k with the budget rule
@@ -226,14 +241,16 @@ template <typename S>
 __global__ void __launch_bounds__(256) k_verify_begin(BeginArgs a) {
   __shared__ int toks[kRows], poss[kRows];
   const int slot = a.slot0 + blockIdx.x;
-  clear_hp(a, slot);
+  const BeginCols bc(a.d);
+  const bool lead = blockIdx.y == 0;  // writes the slot's state, tokens and status
+  clear_hp(a, slot, bc);
   int* st = a.state + slot * kStateInts;
   const int L = st[ST_L], left = st[ST_MAX_NEW] - st[ST_EMITTED], anchor = st[ST_ANCHOR];
   const bool go = st[ST_LIVE] && !st[ST_DONE] && left > 0 && L < a.n_ctx;
   const int nv = go ? min(min(a.block_k, a.k_max), min(left - 1, a.n_ctx - L - 1)) + 1 : 0;
   // the acceptance marks a slot finished once its cache reaches n_ctx, so a live,
   // unfinished slot at or beyond it has an inconsistent state: its pass is refused
-  if (threadIdx.x == 0 && a.status && st[ST_LIVE] && !st[ST_DONE] && left > 0 && L >= a.n_ctx)
+  if (lead && threadIdx.x == 0 && a.status && st[ST_LIVE] && !st[ST_DONE] && left > 0 && L >= a.n_ctx)
     atomicOr(a.status, WF_STATUS_POSITION_OVERFLOW);
   if (threadIdx.x < kRows) {
     const int i = threadIdx.x;
@@ -241,15 +258,15 @@ __global__ void __launch_bounds__(256) k_verify_begin(BeginArgs a) {
     t = min(max(t, 0), a.n_vocab - 1);
     toks[i] = t;
     poss[i] = min(L + i, a.n_ctx - 1);
-    a.tok[slot * kRows + i] = t;
+    if (lead) a.tok[slot * kRows + i] = t;
   }
-  if (threadIdx.x == 0) {
+  __syncthreads();  // every read of the slot's state is done before block 0 writes it
+  if (lead && threadIdx.x == 0) {
     st[ST_POS0] = L;
     st[ST_NV] = nv;
     set_pass_pages(a, slot, st, L);
   }
-  __syncthreads();
-  fill_rows<S>(a, slot, toks, poss, false);
+  fill_rows<S>(a, slot, toks, poss, false, bc);
 }
 
 // Draft block X_t = [Emb(y_t), m, ..., m] (Eq. 2).  The drafter history already
@@ -258,16 +275,17 @@ template <typename S>
 __global__ void __launch_bounds__(256) k_draft_begin(BeginArgs a) {
   __shared__ int toks[kRows];
   const int slot = a.slot0 + blockIdx.x;
+  const BeginCols bc(a.d);
   int* st = a.state + slot * kStateInts;
   if (threadIdx.x < kRows) toks[threadIdx.x] = min(max(st[ST_ANCHOR], 0), a.n_vocab - 1);
   __syncthreads();
-  fill_rows<S>(a, slot, toks, nullptr, true);
+  fill_rows<S>(a, slot, toks, nullptr, true, bc);
   if (a.pos2 != nullptr) {  // absolute-position variant: + P[t + i] on row i
     __syncthreads();
     const S* P = reinterpret_cast<const S*>(a.pos2);
-    const int L = st[ST_L];
-    for (int idx = threadIdx.x; idx < kRows * a.d; idx += 256) {
-      const int i = idx / a.d, col = idx - i * a.d;
+    const int L = st[ST_L], w = 8 * (bc.ce - bc.cb);
+    for (int idx = threadIdx.x; idx < kRows * w; idx += 256) {
+      const int i = idx / w, col = 8 * bc.cb + idx - i * w;
       a.h[(size_t)(slot * kRows + i) * a.d + col] += to_f(P[(size_t)min(L + i, a.n_ctx - 1) * a.d + col]);
     }
   }
@@ -278,7 +296,9 @@ template <typename S>
 __global__ void __launch_bounds__(256) k_prefill_begin(BeginArgs a) {
   __shared__ int toks[kRows], poss[kRows];
   const int slot = a.slot0 + blockIdx.x;
-  clear_hp(a, slot);
+  const BeginCols bc(a.d);
+  const bool lead = blockIdx.y == 0;  // writes the slot's state and tokens
+  clear_hp(a, slot, bc);
   int* st = a.state + slot * kStateInts;
   const int len = st[ST_LEN];
   const int pos0 = a.chunk * kRows;
@@ -289,17 +309,17 @@ __global__ void __launch_bounds__(256) k_prefill_begin(BeginArgs a) {
     t = min(max(t, 0), a.n_vocab - 1);
     toks[i] = t;
     poss[i] = min(pos0 + i, a.n_ctx - 1);
-    a.tok[slot * kRows + i] = t;
+    if (lead) a.tok[slot * kRows + i] = t;
   }
-  if (threadIdx.x == 0) {
+  __syncthreads();  // every read of the slot's state is done before block 0 writes it
+  if (lead && threadIdx.x == 0) {
     st[ST_POS0] = pos0;
     st[ST_NV] = nv;
     st[ST_HPOS] = pos0;
     st[ST_HN] = nv;
     set_pass_pages(a, slot, st, pos0);
   }
-  __syncthreads();
-  fill_rows<S>(a, slot, toks, poss, false);
+  fill_rows<S>(a, slot, toks, poss, false, bc);
 }
 
 // keep the final hidden row of each slot's last prompt position (row 0 of lasth)
@@ -782,11 +802,11 @@ void Ops<S>::reduce_ln(const RlnArgs& a, int rows, hipStream_t st) {
   k_reduce_ln<S><<<rows, kRlnThreads, 0, st>>>(a);
 }
 template <typename S>
-void Ops<S>::verify_begin(const BeginArgs& a, int n, hipStream_t st) { k_verify_begin<S><<<n, 256, 0, st>>>(a); }
+void Ops<S>::verify_begin(const BeginArgs& a, int n, hipStream_t st) { k_verify_begin<S><<<dim3(n, kBeginGroups), 256, 0, st>>>(a); }
 template <typename S>
-void Ops<S>::draft_begin(const BeginArgs& a, int n, hipStream_t st) { k_draft_begin<S><<<n, 256, 0, st>>>(a); }
+void Ops<S>::draft_begin(const BeginArgs& a, int n, hipStream_t st) { k_draft_begin<S><<<dim3(n, kBeginGroups), 256, 0, st>>>(a); }
 template <typename S>
-void Ops<S>::prefill_begin(const BeginArgs& a, int n, hipStream_t st) { k_prefill_begin<S><<<n, 256, 0, st>>>(a); }
+void Ops<S>::prefill_begin(const BeginArgs& a, int n, hipStream_t st) { k_prefill_begin<S><<<dim3(n, kBeginGroups), 256, 0, st>>>(a); }
 template <typename S>
 void Ops<S>::hist_write(const HistArgs& a, int n, hipStream_t st) { k_hist_write<S><<<dim3(kRows, n), 256, 0, st>>>(a); }
 template <typename S>
