@@ -365,10 +365,11 @@ __global__ void __launch_bounds__(256) k_hist_write(HistArgs a) {
     if (threadIdx.x == 0 && a.status) atomicOr(a.status, WF_STATUS_POSITION_OVERFLOW);
     return;
   }
-  const float* kr = a.kv + (size_t)(slot * kRows + r) * 2 * a.d;
+  const int layer = blockIdx.z;
+  const float* kr = a.kv + layer * a.kv_stride + (size_t)(slot * kRows + r) * 2 * a.d;
   const float* vr = kr + a.d;
-  S* Kh = reinterpret_cast<S*>(a.kcache);
-  S* Vh = reinterpret_cast<S*>(a.vcache);
+  S* Kh = reinterpret_cast<S*>(a.kcache) + layer * a.cache_stride;
+  S* Vh = reinterpret_cast<S*>(a.vcache) + layer * a.cache_stride;
   for (int t = threadIdx.x; t < a.n_head * 32; t += 256) {
     const int head = t >> 5, j = t & 31;
     const float c = a.use_rope ? a.rope[(pos * 32 + j) * 2] : 1.f, sn = a.use_rope ? a.rope[(pos * 32 + j) * 2 + 1] : 0.f;
@@ -808,7 +809,9 @@ void Ops<S>::draft_begin(const BeginArgs& a, int n, hipStream_t st) { k_draft_be
 template <typename S>
 void Ops<S>::prefill_begin(const BeginArgs& a, int n, hipStream_t st) { k_prefill_begin<S><<<dim3(n, kBeginGroups), 256, 0, st>>>(a); }
 template <typename S>
-void Ops<S>::hist_write(const HistArgs& a, int n, hipStream_t st) { k_hist_write<S><<<dim3(kRows, n), 256, 0, st>>>(a); }
+void Ops<S>::hist_write(const HistArgs& a, int n, hipStream_t st) {
+  k_hist_write<S><<<dim3(kRows, n, a.nlayer > 0 ? a.nlayer : 1), 256, 0, st>>>(a);
+}
 template <typename S>
 void Ops<S>::gemm_xkv(const XkvArgs& a, hipStream_t st) {
   const int frames = a.vt_frames > a.n_frames ? a.vt_frames : a.n_frames;  // blocks past n_frames write value padding

@@ -235,7 +235,7 @@ int compute_layout(const wf_config& c, Layout& L) {
   L.h = region(R9 * d * 4);
   L.qkv = region(R9 * 3 * d * 4);
   L.hp = region(R9 * d * 4);
-  L.kvh = region(R9 * 2 * d * 4);
+  L.kvh = region(R9 * 2 * d * 4 * std::max(c.n_draft_layer, 1));  // k | v rows of each drafter block
   L.hv = region(R9 * L.head_blocks * 4);
   L.hi = region(R9 * L.head_blocks * 4);
   L.hm = region(R9 * L.head_blocks * 4);
@@ -712,13 +712,20 @@ struct Runner {
     } else {
       gemv("gemv_hproj", EPI_STORE, slot0, n, Atap16(), L.hproj_w, L.hproj_b, c.n_tap * d, d, hp, d);
     }
+    // every block's k | v rows first (each block its own rows), then one launch
+    // writes them all into the blocks' history caches
+    const size_t kvs = (size_t)R9() * 2 * d;
     for (int dl = 0; dl < c.n_draft_layer; ++dl) {
       const BlockW& b = L.db[dl];
       // rows d..3d of the concatenated q|k|v matrix start d*d elements in, in either order
       gemv_ln("gemv_hist_kv", EPI_STORE, slot0, n, hp, b.ln1_g, b.ln1_b, b.c_qkv, 3 * d, d, Ad16(), b.w_qkv + (size_t)d * d,
-              b.b_qkv + d, d, 2 * d, kvh, 2 * d);
+              b.b_qkv + d, d, 2 * d, kvh + dl * kvs, 2 * d);
+    }
+    if (c.n_draft_layer > 0) {
       HistArgs ha{};
-      ha.kv = kvh; ha.kcache = hkv(dl, 0); ha.vcache = hkv(dl, 1); ha.state = I32(L.state); ha.rope = F32(L.rope);
+      ha.kv = kvh; ha.kcache = hkv(0, 0); ha.vcache = hkv(0, 1); ha.state = I32(L.state); ha.rope = F32(L.rope);
+      ha.nlayer = c.n_draft_layer; ha.kv_stride = kvs;
+      ha.cache_stride = (size_t)2 * c.max_batch * c.n_head * c.n_ctx * kHeadDim;  // hkv(dl + 1, .) - hkv(dl, .)
       ha.slot0 = slot0; ha.d = d; ha.n_head = c.n_head; ha.n_ctx = c.n_ctx;
       ha.status = h->at<unsigned>(L.status);
       ha.use_rope = !(c.draft_flags & WF_DRAFT_ABS_POS);

@@ -258,9 +258,12 @@ struct BeginArgs {
 };
 
 struct HistArgs {
-  const float* kv;  // [rows][2d]: k (no RoPE yet) | v
-  void* kcache;     // drafter block base [slot][head][n_ctx][64]
+  const float* kv;  // [rows][2d]: k (no RoPE yet) | v, of the first drafter block
+  void* kcache;     // first drafter block base [slot][head][n_ctx][64]
   void* vcache;
+  int nlayer;           // drafter blocks written (grid z), 1 if 0
+  size_t kv_stride;     // floats from one block's kv rows to the next's
+  size_t cache_stride;  // storage elements from one block's caches to the next's
   const int* state;
   const float* rope;
   int slot0, d, n_head, n_ctx;
