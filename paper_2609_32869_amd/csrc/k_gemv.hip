@@ -809,6 +809,10 @@ __global__ void __launch_bounds__(256) k_gemm32r(GemvArgs a, int mb0, int nmb, i
   StampScope stamp_scope(a.stamp, 256);
   constexpr int WCT = CN / 2, TC = 32 * CN;
   __shared__ float sv[64][TC + 1];  // the finished tile
+  if (a.pf.blocks > 0 && blockIdx.x >= gridDim.x - a.pf.blocks) {  // appended blocks: a later product's weights
+    if (blockIdx.y == 0) touch_range(a.pf, blockIdx.x - (gridDim.x - a.pf.blocks));
+    return;
+  }
   int mbk, nbk;
   {
     const int x = blockIdx.x & 7, i = blockIdx.x >> 3;
@@ -858,11 +862,13 @@ __global__ void __launch_bounds__(256) k_gemm32r(GemvArgs a, int mb0, int nmb, i
   // registers kWideD steps ahead (past the end: the last k-step again, unused); the
   // scheduling barriers keep every load where it is issued (the scheduler otherwise
   // moves loads next to their use to shorten register lifetimes).
+  // grid y splits the k-steps (EPI_PART: one partial-sum buffer per split)
+  const int kper = KS / gridDim.y, kb = blockIdx.y * kper, ke = kb + kper;
   Frag fr[kWideD];
 #pragma unroll
-  for (int d = 0; d < kWideD; ++d) ld(d, fr[d]);
+  for (int d = 0; d < kWideD; ++d) ld(kb + d, fr[d]);
   __builtin_amdgcn_sched_barrier(0);
-  for (int st = 0; st < KS; st += kWideD) {
+  for (int st = kb; st < ke; st += kWideD) {
 #pragma unroll
     for (int d = 0; d < kWideD; ++d) {
       mul(fr[d]);
@@ -897,8 +903,9 @@ __global__ void __launch_bounds__(256) k_gemm32r(GemvArgs a, int mb0, int nmb, i
 #pragma unroll
       for (int e = 0; e < 8; ++e) v[e] = gelu_erf(v[e]);
       put_op8<bf16>(a.aout, a.nsplit, a.R9, row, n, v);
-    } else if constexpr (EPI == EPI_STORE) {
-      float4* y = reinterpret_cast<float4*>(a.y + (size_t)row * a.ldy + n);
+    } else if constexpr (EPI == EPI_STORE || EPI == EPI_PART) {
+      float* yb = EPI == EPI_PART ? a.y + blockIdx.y * a.pstride : a.y;
+      float4* y = reinterpret_cast<float4*>(yb + (size_t)row * a.ldy + n);
       y[0] = make_float4(v[0], v[1], v[2], v[3]);
       y[1] = make_float4(v[4], v[5], v[6], v[7]);
     } else if constexpr (EPI == EPI_RESID) {
@@ -1542,15 +1549,25 @@ static void launch_epi(const GemvArgs& a, hipStream_t st) {
     if (a.nsplit == 2 && a.wkind == W_F16) {  // several slots: 64 x 64 GEMM tiles (k split over grid y)
       const int mb0 = a.slot0 * kRows / 64, mb1 = ((a.slot0 + a.nslots) * kRows + 63) / 64;
       const int nmb = mb1 - mb0, nnb = (a.N + 63) / 64;
+      if constexpr (EPI == EPI_PART) {
+        // many rows, k split into partial sums: wide tiles, grid y = the splits
+        const int kss = a.K / 32;
+        if (ks > 1 && nmb >= kWideMinRowBlocks && kss % (ks * kWideD) == 0 && a.N % 320 == 0 && a.a.kind == OP_F16) {
+          k_gemm32r<EPI, 10><<<dim3(wide_grid(nmb, a.N / 320) + pf_blocks(a), ks), 256, 0, st>>>(a, mb0, nmb, a.N / 320);
+          return;
+        }
+      }
       if constexpr (EPI == EPI_STORE || EPI == EPI_GELU || EPI == EPI_RESID || EPI == EPI_QKV) {
         // many rows: wide tiles on the 32x32x16 matrix instruction
         if (ks == 1 && nmb >= kWideMinRowBlocks && (a.K / 32) % kWideD == 0 && a.N % 8 == 0 && a.a.kind == OP_F16) {
+          GemvArgs b = a;
+          b.pf = Touch{nullptr, 0, 0};  // these launches append no reading blocks
           if (a.N % 320 == 0 && a.N / 320 >= 16) {
-            k_gemm32r<EPI, 10><<<wide_grid(nmb, a.N / 320), 256, 0, st>>>(a, mb0, nmb, a.N / 320);
+            k_gemm32r<EPI, 10><<<wide_grid(nmb, a.N / 320), 256, 0, st>>>(b, mb0, nmb, a.N / 320);
             return;
           }
           if (a.N % 256 == 0 && a.N >= 2560) {
-            k_gemm32r<EPI, 8><<<wide_grid(nmb, a.N / 256), 256, 0, st>>>(a, mb0, nmb, a.N / 256);
+            k_gemm32r<EPI, 8><<<wide_grid(nmb, a.N / 256), 256, 0, st>>>(b, mb0, nmb, a.N / 256);
             return;
           }
           // narrower products (1280 columns at 96 slots) measured slower in this kernel

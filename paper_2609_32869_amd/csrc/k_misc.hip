@@ -791,6 +791,77 @@ __global__ void __launch_bounds__(kRlnThreads) k_reduce_ln(RlnArgs a) {
   }
 }
 
+// The same update for several slots' rows with at most kRlnRowParts partial
+// buffers and d <= 8 kRlnColThreads: one block per row, a thread holding 8
+// consecutive columns, loaded and written 16 bytes at a time (h, the tap and the
+// operand), statistics as wave sums merged in LDS.  The sums are formed in the
+// order of k_reduce_ln: h + ((p0 + p1 + ...) + bias).
+constexpr int kRlnRowParts = 4;
+constexpr int kRlnColThreads = 192;
+template <typename S>
+__global__ void __launch_bounds__(kRlnColThreads) k_reduce_ln_rows(RlnArgs a) {
+  StampScope stamp_scope(a.stamp, kRlnColThreads);
+  constexpr int NW = kRlnColThreads / 64;
+  __shared__ float red[2][NW];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int row = a.row0 + blockIdx.x;
+  const int d = a.d, nch = d >> 3, c = threadIdx.x;
+  const int cc = min(c, nch - 1);
+  float* hr = a.h + (size_t)row * d;
+  const bool has_bias = a.bias != nullptr, has_ln = a.g != nullptr, act = c < nch;
+  // every load first and unconditionally (chunks past the row and partials past
+  // nparts re-read valid ones, then discarded)
+  float v[8], pv[kRlnRowParts][8], bv[8], gv[8], lv[8];
+  ld8(hr + 8 * cc, v);
+#pragma unroll
+  for (int p = 0; p < kRlnRowParts; ++p) ld8(a.part + min(p, a.nparts - 1) * a.pstride + (size_t)row * d + 8 * cc, pv[p]);
+  ld8(reinterpret_cast<const S*>(has_bias ? a.bias : a.part) + 8 * cc, bv);
+  ld8(reinterpret_cast<const S*>(has_ln ? a.g : a.part) + 8 * cc, gv);
+  ld8(reinterpret_cast<const S*>(has_ln ? a.b : a.part) + 8 * cc, lv);
+  float s = 0.f;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    float sum = 0.f;
+#pragma unroll
+    for (int p = 0; p < kRlnRowParts; ++p) sum += p < a.nparts ? pv[p][e] : 0.f;
+    v[e] = act ? v[e] + (sum + (has_bias ? bv[e] : 0.f)) : 0.f;
+    s += v[e];
+  }
+  if (act) {
+    float4* y = reinterpret_cast<float4*>(hr + 8 * c);
+    y[0] = make_float4(v[0], v[1], v[2], v[3]);
+    y[1] = make_float4(v[4], v[5], v[6], v[7]);
+    if (a.tapcol >= 0) put_op8<S>(a.tap, a.nsplit, a.R9, row, a.tapcol + 8 * c, v);
+  }
+  if (!has_ln) return;
+  s = wave_sum(s);
+  if (lane == 0) red[0][w] = s;
+  __syncthreads();
+  float tot = 0.f;
+#pragma unroll
+  for (int i = 0; i < NW; ++i) tot += red[0][i];
+  const float mean = tot / (float)d;
+  float q = 0.f;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const float cd = v[e] - mean;
+    q += act ? cd * cd : 0.f;
+  }
+  q = wave_sum(q);
+  if (lane == 0) red[1][w] = q;
+  __syncthreads();
+  float qt = 0.f;
+#pragma unroll
+  for (int i = 0; i < NW; ++i) qt += red[1][i];
+  const float inv = 1.0f / sqrtf(qt / (float)d + 1e-5f);
+  if (act) {
+    float y[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) y[e] = (v[e] - mean) * inv * gv[e] + lv[e];
+    put_op8<S>(a.out, a.nsplit, a.R9, row, 8 * c, y);
+  }
+}
+
 // ---------------------------------------------------------------- launchers
 template <typename S>
 void Ops<S>::ln_operand(const LnArgs& a, int rows, hipStream_t st) {
@@ -800,6 +871,10 @@ void Ops<S>::ln_operand(const LnArgs& a, int rows, hipStream_t st) {
 }
 template <typename S>
 void Ops<S>::reduce_ln(const RlnArgs& a, int rows, hipStream_t st) {
+  if (a.nparts <= kRlnRowParts && a.d <= 8 * kRlnColThreads && a.d % 8 == 0) {
+    k_reduce_ln_rows<S><<<rows, kRlnColThreads, 0, st>>>(a);
+    return;
+  }
   k_reduce_ln<S><<<rows, kRlnThreads, 0, st>>>(a);
 }
 template <typename S>

@@ -536,7 +536,7 @@ struct Runner {
     if (L.nsplit_op != 2) return 0;
     const int mb0 = slot0 * kRows / 64, mb1 = ((slot0 + n) * kRows + 63) / 64;
     const int tiles = (mb1 - mb0) * ((c.d_model + 63) / 64);
-    return tiles < 160 && (c.d_ff / 32) % kFc2SplitBatch == 0 ? kFc2SplitBatch : 0;
+    return (c.d_ff / 32) % kFc2SplitBatch == 0 ? kFc2SplitBatch : 0;
   }
 
   // second half of a decoder block shared by target and drafter: cross-attention and MLP
