@@ -528,14 +528,12 @@ struct Runner {
     });
   }
 
-  // Several slots with bf16 operands: when the 64 x 64 tiles of the second MLP
-  // product cover too few blocks to fill the chip, split its k-steps in
+  // Several slots with bf16 operands: the second MLP product's k-steps split in
   // kFc2SplitBatch (partial sums reduced with the residual update and the next
-  // LayerNorm), else 0.
-  int fc2_split_batch(int slot0, int n) const {
+  // LayerNorm), else 0.  Few slots: its 64 x 64 tiles alone would not fill the
+  // chip; many slots: it runs on the wide tiles, which alone would give too few.
+  int fc2_split_batch() const {
     if (L.nsplit_op != 2) return 0;
-    const int mb0 = slot0 * kRows / 64, mb1 = ((slot0 + n) * kRows + 63) / 64;
-    const int tiles = (mb1 - mb0) * ((c.d_model + 63) / 64);
     return (c.d_ff / 32) % kFc2SplitBatch == 0 ? kFc2SplitBatch : 0;
   }
 
@@ -575,7 +573,7 @@ struct Runner {
     gemv_ln("gemv_fc1", EPI_GELU, slot0, n, h_, b.ln3_g, b.ln3_b, b.c_fc1, c.d_ff, 0, Ad32(), b.w_fc1, b.b_fc1, d, c.d_ff,
             nullptr, 0, Af16());
     touch_next(slot0, n, nx.wq, nx.nq, 64);
-    const int ksplit = L.fc2_split > 0 ? L.fc2_split : fc2_split_batch(slot0, n);
+    const int ksplit = L.fc2_split > 0 ? L.fc2_split : fc2_split_batch();
     // a tap block followed by a target block: that block's q|k|v product, which
     // folds its LayerNorm and so reads the rows anyway, writes the tap
     const bool tap_later = tap >= 0 && !nx.wide && fold_ln() && Atap16().kind == OP_F16;

@@ -50,7 +50,7 @@ struct Layout {
 
 struct Handle;
 
-constexpr int kFc2SplitBatch = 4;  // k-splits of the second MLP product for small multi-slot batches
+constexpr int kFc2SplitBatch = 4;  // k-splits of the second MLP product with several slots
 constexpr int kResidSplit = 4;     // k-splits of the attention output products for small multi-slot batches
 
 struct GraphKey {
