@@ -3,9 +3,11 @@
 // encode-time cross K/V product.
 //
 // Rows: a pass over slot s uses activation rows s*9 + i, i = 0..8 (anchor plus
-// eight candidates, or eight masks for the drafter).  Every kernel computes a
-// row's result the same way however many rows or slots share the launch, so a
-// token's logits never depend on the batch composition.
+// eight candidates, or eight masks for the drafter).  Every kernel here computes a
+// row's result the same way however many rows or slots share the launch, except
+// the LayerNorm operand launch, which sums a row's statistics in another order
+// from kLnColMaxRows rows on (as the products' kernels and k-splits also change
+// with the slot count).
 #include "../../include/wf.h"
 #include "wf_operand.h"
 
@@ -62,6 +64,56 @@ __global__ void __launch_bounds__(64 * kLnRowsPerBlock) k_ln_operand(LnArgs a) {
       for (int e = 0; e < 8; ++e) y[e] = (v[j][e] - mean) * inv * gv[j][e] + bv[j][e];
       put_op8<S>(a.out, a.nsplit, a.R9, row, 8 * c, y);
     }
+  }
+}
+
+// The same LayerNorm with one block of three waves per row (d <= 1536), a thread
+// holding 8 consecutive columns, statistics as wave sums merged in LDS: for
+// launches of fewer than kLnColMaxRows rows, which the wave-per-row kernel
+// spreads over too few CUs (144 rows: 3.7 against 5.0 us; 864 rows: 7.8
+// against 6.9, where the four-row blocks already cover the chip).
+constexpr int kLnColThreads = 192;
+constexpr int kLnColMaxRows = 512;
+template <typename S>
+__global__ void __launch_bounds__(kLnColThreads) k_ln_operand_cols(LnArgs a) {
+  StampScope stamp_scope(a.stamp, kLnColThreads);
+  constexpr int NW = kLnColThreads / 64;
+  __shared__ float red[2][NW];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int row = a.row0 + blockIdx.x, nch = a.d >> 3, c = threadIdx.x, cc = min(c, nch - 1);
+  const bool act = c < nch;
+  float v[8], gv[8], bv[8];
+  ld8(a.x + (size_t)row * a.d + 8 * cc, v);
+  ld8(reinterpret_cast<const S*>(a.g) + 8 * cc, gv);
+  ld8(reinterpret_cast<const S*>(a.b) + 8 * cc, bv);
+  float s = 0.f;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) s += act ? v[e] : 0.f;
+  s = wave_sum(s);
+  if (lane == 0) red[0][w] = s;
+  __syncthreads();
+  float tot = 0.f;
+#pragma unroll
+  for (int i = 0; i < NW; ++i) tot += red[0][i];
+  const float mean = tot / (float)a.d;
+  float q = 0.f;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const float cd = v[e] - mean;
+    q += act ? cd * cd : 0.f;
+  }
+  q = wave_sum(q);
+  if (lane == 0) red[1][w] = q;
+  __syncthreads();
+  float qt = 0.f;
+#pragma unroll
+  for (int i = 0; i < NW; ++i) qt += red[1][i];
+  const float inv = 1.0f / sqrtf(qt / (float)a.d + 1e-5f);
+  if (act) {
+    float y[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) y[e] = (v[e] - mean) * inv * gv[e] + bv[e];
+    put_op8<S>(a.out, a.nsplit, a.R9, row, 8 * c, y);
   }
 }
 
@@ -867,6 +919,10 @@ template <typename S>
 void Ops<S>::ln_operand(const LnArgs& a, int rows, hipStream_t st) {
   LnArgs b = a;
   b.rows = rows;
+  if (rows < kLnColMaxRows && a.d <= 8 * kLnColThreads && a.d % 8 == 0) {
+    k_ln_operand_cols<S><<<rows, kLnColThreads, 0, st>>>(b);
+    return;
+  }
   k_ln_operand<S><<<(rows + kLnRowsPerBlock - 1) / kLnRowsPerBlock, 64 * kLnRowsPerBlock, 0, st>>>(b);
 }
 template <typename S>
